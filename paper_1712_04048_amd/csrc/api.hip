@@ -1,0 +1,375 @@
+// C ABI of libcavs.so: context management, workspace layout and the
+// forward / backward drivers (Algorithm 1: tasks in order for F, popped in
+// reverse for dF; Algorithm 2: level-major dynamic tensors).
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "kernels.h"
+
+#include <map>
+#include <string.h>
+
+namespace cavs {
+
+thread_local cavs_ctx* t_active_ctx = nullptr;
+
+hipEvent_t timing_event(cavs_ctx* c) {
+  if (!c->event_pool.empty()) {
+    hipEvent_t e = c->event_pool.back();
+    c->event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
+cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...) {
+  if (ctx) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    ctx->err = buf;
+  }
+  return st;
+}
+
+namespace {
+
+// Workspace of forward + backward, all level-major (row = position).
+struct WsLayout {
+  size_t P, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, total;
+  size_t part_floats;
+};
+
+WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
+  WsLayout L{};
+  const size_t V = (size_t)(s->V > 0 ? s->V : 1), H = (size_t)p->H;
+  const bool lstm = p->cell == CAVS_TREE_LSTM;
+  const size_t GW = lstm ? (size_t)(3 + p->N) * H : H;
+  const size_t C = p->loss == CAVS_LOSS_CE ? (size_t)p->C : 0;
+  size_t o = 0;
+  auto take = [&](size_t floats) {
+    size_t r = o;
+    o = align_up(o + floats * sizeof(float), 256);
+    return r;
+  };
+  L.P = take(lstm ? V * 4 * H : 0);
+  L.Hs = take(V * H);
+  L.Cs = take(lstm ? V * H : 0);
+  L.Gs = take(lstm ? V * GW : 0);
+  L.dZ = take(V * (C > 0 ? C : 1));
+  L.lossv = take(V);
+  L.dHp = take(V * H);
+  L.dCp = take(lstm ? V * H : 0);
+  L.dA = take(V * GW);
+  L.part_floats = lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
+  L.part = take(L.part_floats);
+  L.total = o;
+  return L;
+}
+
+cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                       const cavs_inputs* in) {
+  if (!ctx) return CAVS_ERR_ARG;
+  if (!p || !s || !in) return fail(ctx, CAVS_ERR_ARG, "null params / sched / inputs");
+  if (p->cell != CAVS_TREE_LSTM && p->cell != CAVS_TREE_FC)
+    return fail(ctx, CAVS_ERR_ARG, "unknown cell %d", p->cell);
+  if (p->loss != CAVS_LOSS_CE && p->loss != CAVS_LOSS_L2)
+    return fail(ctx, CAVS_ERR_ARG, "unknown loss %d", p->loss);
+  if (p->prec != CAVS_FP32 && p->prec != CAVS_BF16)
+    return fail(ctx, CAVS_ERR_ARG, "unknown precision %d", p->prec);
+  if (p->H <= 0 || p->D < 0 || p->N <= 0) return fail(ctx, CAVS_ERR_ARG, "bad D/H/N");
+  if (p->N != s->N) return fail(ctx, CAVS_ERR_ARG, "params N=%d != schedule N=%d", p->N, s->N);
+  if (p->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots (max 2)", p->N);
+  if (p->H % 64 != 0) return fail(ctx, CAVS_ERR_UNSUPPORTED, "H=%d not a multiple of 64", p->H);
+  if (p->prec == CAVS_BF16) return fail(ctx, CAVS_ERR_UNSUPPORTED, "bf16 products not built");
+  if (s->V < 0 || s->T < 0 || (s->V > 0 && s->T <= 0))
+    return fail(ctx, CAVS_ERR_ARG, "schedule not built");
+  if (s->V > 0 && (!s->child_pos || !s->parent_pos || !s->pull_pos || !s->push_pos ||
+                   !s->order || !s->pull_list || !s->level_offsets_host))
+    return fail(ctx, CAVS_ERR_ARG, "schedule arrays missing");
+  if (!p->U || !p->b) return fail(ctx, CAVS_ERR_ARG, "U and b are required");
+  if (p->loss == CAVS_LOSS_CE) {
+    if (p->C <= 0 || p->C > 16) return fail(ctx, CAVS_ERR_UNSUPPORTED, "C=%d (1..16)", p->C);
+    if (s->n_push != p->C) return fail(ctx, CAVS_ERR_ARG, "schedule n_push != C");
+    if (!p->Ws || !p->bs) return fail(ctx, CAVS_ERR_ARG, "Ws and bs are required for CE");
+  } else {
+    if (s->n_push != in->n_y) return fail(ctx, CAVS_ERR_ARG, "schedule n_push != n_y");
+    if (s->n_labelled > 0 && !in->Y) return fail(ctx, CAVS_ERR_ARG, "Y is required for L2");
+  }
+  if (s->n_pull > 0 && !in->X) return fail(ctx, CAVS_ERR_ARG, "X is required");
+  if (p->cell == CAVS_TREE_LSTM) {
+    if (p->D % 4 != 0) return fail(ctx, CAVS_ERR_UNSUPPORTED, "D=%d not a multiple of 4", p->D);
+    if (s->n_pull > 0 && !p->Wx) return fail(ctx, CAVS_ERR_ARG, "Wx is required");
+  } else {
+    if (p->D != p->H) return fail(ctx, CAVS_ERR_ARG, "Tree-FC needs D == H");
+    if (s->n_leaf_noinput != 0 || s->n_inner_input != 0)
+      return fail(ctx, CAVS_ERR_ARG, "Tree-FC: a vertex must pull an input iff it is a leaf");
+  }
+  return CAVS_OK;
+}
+
+Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, void* ws,
+             const WsLayout& L) {
+  Net n{};
+  char* base = (char*)ws;
+  n.V = s->V;
+  n.N = p->N;
+  n.D = p->D;
+  n.H = p->H;
+  n.C = p->C;
+  n.loss = p->loss;
+  n.GW = p->cell == CAVS_TREE_LSTM ? (3 + p->N) * p->H : p->H;
+  n.inv_denom = 1.f / (float)(s->n_labelled > 0 ? s->n_labelled : 1);
+  n.child_pos = s->child_pos;
+  n.parent_pos = s->parent_pos;
+  n.pull_pos = s->pull_pos;
+  n.push_pos = s->push_pos;
+  n.order = s->order;
+  n.pull_list = s->pull_list;
+  n.Wx = p->Wx;
+  n.U = p->U;
+  n.b = p->b;
+  n.Ws = p->Ws;
+  n.bs = p->bs;
+  n.X = in->X;
+  n.Y = in->Y;
+  n.P = (float*)(base + L.P);
+  n.Hs = (float*)(base + L.Hs);
+  n.Cs = (float*)(base + L.Cs);
+  n.Gs = (float*)(base + L.Gs);
+  n.dZ = (float*)(base + L.dZ);
+  n.lossv = (float*)(base + L.lossv);
+  n.dHp = (float*)(base + L.dHp);
+  n.dCp = (float*)(base + L.dCp);
+  n.dA = (float*)(base + L.dA);
+  return n;
+}
+
+}  // namespace
+}  // namespace cavs
+
+using namespace cavs;
+
+extern "C" {
+
+cavs_status cavs_create(cavs_ctx** out, int32_t device, void* hip_stream) {
+  if (!out) return CAVS_ERR_ARG;
+  *out = nullptr;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev)
+    return CAVS_ERR_ARG;
+  cavs_ctx* ctx = new cavs_ctx();
+  ctx->device = device;
+  ctx->stream = (hipStream_t)hip_stream;
+  if (hipSetDevice(device) != hipSuccess ||
+      hipHostMalloc((void**)&ctx->host_stage, sizeof(int32_t) * kHostStageInts,
+                    hipHostMallocDefault) != hipSuccess) {
+    delete ctx;
+    return CAVS_ERR_HIP;
+  }
+  *out = ctx;
+  return CAVS_OK;
+}
+
+cavs_status cavs_set_stream(cavs_ctx* ctx, void* hip_stream) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->stream = (hipStream_t)hip_stream;
+  return CAVS_OK;
+}
+
+void cavs_destroy(cavs_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
+  for (auto& r : ctx->timed) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  for (auto e : ctx->event_pool) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+cavs_status cavs_timing_enable(cavs_ctx* ctx, int32_t on) {
+  if (!ctx) return CAVS_ERR_ARG;
+  for (auto& r : ctx->timed) {
+    ctx->event_pool.push_back(r.start);
+    ctx->event_pool.push_back(r.stop);
+  }
+  ctx->timed.clear();
+  ctx->timing = on != 0;
+  return CAVS_OK;
+}
+
+int32_t cavs_timing_read(cavs_ctx* ctx, cavs_kernel_time* out, int32_t max) {
+  if (!ctx || (max > 0 && !out)) return CAVS_ERR_ARG;
+  if (hipStreamSynchronize(ctx->stream) != hipSuccess)
+    return fail(ctx, CAVS_ERR_HIP, "hipStreamSynchronize failed");
+  std::map<std::string, std::pair<int, double>> agg;
+  std::vector<std::string> first_seen;
+  for (auto& r : ctx->timed) {
+    float ms = 0.f;
+    (void)hipEventElapsedTime(&ms, r.start, r.stop);
+    auto it = agg.find(r.name);
+    if (it == agg.end()) {
+      first_seen.push_back(r.name);
+      agg[r.name] = {1, (double)ms};
+    } else {
+      it->second.first += 1;
+      it->second.second += ms;
+    }
+    ctx->event_pool.push_back(r.start);
+    ctx->event_pool.push_back(r.stop);
+  }
+  ctx->timed.clear();
+  int32_t n = 0;
+  for (auto& name : first_seen) {
+    if (n < max) {
+      memset(out[n].name, 0, sizeof out[n].name);
+      strncpy(out[n].name, name.c_str(), sizeof out[n].name - 1);
+      out[n].launches = agg[name].first;
+      out[n].total_ms = agg[name].second;
+    }
+    ++n;
+  }
+  return n;
+}
+
+const char* cavs_last_error(const cavs_ctx* ctx) {
+  if (!ctx) return "null context";
+  return ctx->err.c_str();
+}
+
+size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x) {
+  return schedule_ws_bytes(V, N, n_x);
+}
+
+cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
+                          size_t ws_bytes) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  if (!g || !s) return fail(ctx, CAVS_ERR_ARG, "null graphs / sched");
+  if (g->V < 0 || g->n_x < 0 || g->n_push < 0) return fail(ctx, CAVS_ERR_ARG, "negative size");
+  if (g->N < 1 || g->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots", g->N);
+  if (g->V > 0 && (!g->child || !g->parent))
+    return fail(ctx, CAVS_ERR_ARG, "child / parent arrays are required");
+  if (g->V > 0 && (!s->level || !s->order || !s->pos || !s->child_pos || !s->parent_pos ||
+                   !s->pull_pos || !s->push_pos || !s->pull_list || !s->level_offsets))
+    return fail(ctx, CAVS_ERR_ARG, "schedule output arrays are required");
+  if (!s->level_offsets_host) return fail(ctx, CAVS_ERR_ARG, "level_offsets_host is required");
+  if (g->V > 0 && !ws) return fail(ctx, CAVS_ERR_ARG, "workspace is required");
+  if (hipSetDevice(ctx->device) != hipSuccess) return fail(ctx, CAVS_ERR_HIP, "hipSetDevice");
+  ActiveCtx active(ctx);
+  return schedule_run(ctx, g, s, ws, ws_bytes);
+}
+
+size_t cavs_workspace_bytes(const cavs_params* p, const cavs_sched* s) {
+  if (!p || !s || p->H <= 0 || p->N <= 0 || s->V < 0) return 0;
+  return ws_layout(p, s).total;
+}
+
+cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                         const cavs_inputs* in, float* h_out, float* c_out, float* loss_out,
+                         void* ws, size_t ws_bytes) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  cavs_status st = check_args(ctx, p, s, in);
+  if (st != CAVS_OK) return st;
+  if (!loss_out || (s->V > 0 && !h_out)) return fail(ctx, CAVS_ERR_ARG, "null output");
+  WsLayout L = ws_layout(p, s);
+  if (!ws || ws_bytes < L.total)
+    return fail(ctx, CAVS_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, L.total);
+  CAVS_HIP_CHECK(ctx, hipSetDevice(ctx->device));
+  ActiveCtx active(ctx);
+  hipStream_t str = ctx->stream;
+  if (s->V == 0) {
+    CAVS_HIP_CHECK(ctx, hipMemsetAsync(loss_out, 0, sizeof(float), str));
+    return CAVS_OK;
+  }
+  Net n = make_net(p, s, in, ws, L);
+  n.h_out = h_out;
+  n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
+  const int* lo = s->level_offsets_host;
+  if (p->cell == CAVS_TREE_LSTM) {
+    pull_gemm(n, s->n_pull, s->n_inner_input > 0, str);
+    lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
+    for (int t = 1; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+  } else {
+    fc_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
+    for (int t = 1; t < s->T; ++t) fc_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+  }
+  loss_fwd(n, loss_out, str);
+  CAVS_LAUNCH_CHECK(ctx);
+  return CAVS_OK;
+}
+
+cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                          const cavs_inputs* in, void* ws, size_t ws_bytes,
+                          const cavs_grads* g) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  cavs_status st = check_args(ctx, p, s, in);
+  if (st != CAVS_OK) return st;
+  if (!g || !g->dU || !g->db) return fail(ctx, CAVS_ERR_ARG, "null gradient output");
+  if (p->cell == CAVS_TREE_LSTM && p->D > 0 && !g->dWx)
+    return fail(ctx, CAVS_ERR_ARG, "dWx is required");
+  if (p->loss == CAVS_LOSS_CE && (!g->dWs || !g->dbs))
+    return fail(ctx, CAVS_ERR_ARG, "dWs / dbs are required for CE");
+  if (s->n_x > 0 && !g->dX) return fail(ctx, CAVS_ERR_ARG, "dX is required");
+  WsLayout L = ws_layout(p, s);
+  if (!ws || ws_bytes < L.total)
+    return fail(ctx, CAVS_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, L.total);
+  CAVS_HIP_CHECK(ctx, hipSetDevice(ctx->device));
+  ActiveCtx active(ctx);
+  hipStream_t str = ctx->stream;
+  const int H = p->H, D = p->D;
+  const bool lstm = p->cell == CAVS_TREE_LSTM;
+  if (s->V == 0) {
+    const size_t nU = lstm ? (size_t)H * 4 * H : (size_t)p->N * H * H;
+    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dU, 0, nU * sizeof(float), str));
+    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->db, 0, (lstm ? 4 * H : H) * sizeof(float), str));
+    if (lstm && D > 0)
+      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dWx, 0, (size_t)D * 4 * H * sizeof(float), str));
+    if (p->loss == CAVS_LOSS_CE) {
+      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dWs, 0, (size_t)H * p->C * sizeof(float), str));
+      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dbs, 0, (size_t)p->C * sizeof(float), str));
+    }
+    if (s->n_x > 0)
+      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
+    return CAVS_OK;
+  }
+  Net n = make_net(p, s, in, ws, L);
+  float* part = (float*)((char*)ws + L.part);
+  const int* lo = s->level_offsets_host;
+  const int T = s->T;
+  const int off1 = T > 1 ? lo[1] : s->V;
+  if (s->n_x > 0 && s->n_pull < s->n_x)
+    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
+  if (lstm) {
+    for (int t = T - 1; t >= 0; --t) {
+      const int M = lo[t + 1] - lo[t];
+      lstm_bwd_gates(n, lo[t], M, str);
+      if (t >= 1) lstm_bwd_level(n, lo[t], M, str);
+    }
+    const bool with_f = s->n_inner_input > 0;
+    lstm_dU(n, off1, g->dU, part, L.part_floats, str);
+    if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part, L.part_floats, str);
+    dx_gemm(n, s->n_pull, with_f, g->dX, str);
+    bias_grad(n, 0, s->V, g->db, part, L.part_floats, str);
+  } else {
+    for (int t = T - 1; t >= 0; --t) {
+      const int M = lo[t + 1] - lo[t];
+      fc_bwd_gates(n, lo[t], M, t == 0, g->dX, str);
+      if (t >= 1) fc_bwd_level(n, lo[t], M, str);
+    }
+    fc_dW(n, off1, g->dU, part, L.part_floats, str);
+    bias_grad(n, off1, s->V, g->db, part, L.part_floats, str);
+  }
+  if (p->loss == CAVS_LOSS_CE) head_grad(n, g->dWs, g->dbs, part, L.part_floats, str);
+  CAVS_LAUNCH_CHECK(ctx);
+  return CAVS_OK;
+}
+
+}  // extern "C"

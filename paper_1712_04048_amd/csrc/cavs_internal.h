@@ -1,0 +1,137 @@
+// Internal declarations shared by the HIP sources of libcavs.so (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "cavs.h"
+
+// One timed launch: events recorded on the context stream around it.
+struct cavs_timed_launch {
+  const char* name;
+  hipEvent_t start, stop;
+};
+
+struct cavs_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  int32_t* host_stage = nullptr;  // pinned, kHostStageInts entries
+  std::string err;
+  bool timing = false;
+  std::vector<cavs_timed_launch> timed;   // pending records
+  std::vector<hipEvent_t> event_pool;     // reusable events
+};
+
+namespace cavs {
+
+constexpr int kHostStageInts = 4096 + 32;
+constexpr int kWave = 64;
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// error plumbing
+// ---------------------------------------------------------------------------
+cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...);
+
+#define CAVS_HIP_CHECK(ctx, call)                                              \
+  do {                                                                         \
+    hipError_t e_ = (call);                                                    \
+    if (e_ != hipSuccess)                                                      \
+      return ::cavs::fail((ctx), CAVS_ERR_HIP, "%s failed: %s (%s:%d)", #call, \
+                          hipGetErrorString(e_), __FILE__, __LINE__);          \
+  } while (0)
+
+#define CAVS_LAUNCH_CHECK(ctx) CAVS_HIP_CHECK(ctx, hipGetLastError())
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+// ---------------------------------------------------------------------------
+// device math (IEEE fp32 through the device math library; no fast-math)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float sigmoidf_(float a) {
+  if (a >= 0.f) return 1.f / (1.f + expf(-a));
+  float e = expf(a);
+  return e / (1.f + e);
+}
+
+__device__ __forceinline__ v4f mfma_f32_16x16x4(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// deterministic wave-wide sum (butterfly over all 64 lanes)
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// optional per-launch timing (cavs_timing_enable): the API entry points make
+// their context current; launchers wrap each kernel in a TimedScope.
+// ---------------------------------------------------------------------------
+extern thread_local cavs_ctx* t_active_ctx;
+
+struct ActiveCtx {
+  explicit ActiveCtx(cavs_ctx* c) { t_active_ctx = c; }
+  ~ActiveCtx() { t_active_ctx = nullptr; }
+};
+
+hipEvent_t timing_event(cavs_ctx* c);
+
+struct TimedScope {
+  cavs_ctx* c;
+  cavs_timed_launch rec;
+  TimedScope(const char* name, hipStream_t s) : c(t_active_ctx) {
+    if (!c || !c->timing) {
+      c = nullptr;
+      return;
+    }
+    rec.name = name;
+    rec.start = timing_event(c);
+    rec.stop = timing_event(c);
+    (void)hipEventRecord(rec.start, s);
+    stream = s;
+  }
+  ~TimedScope() {
+    if (!c) return;
+    (void)hipEventRecord(rec.stop, stream);
+    c->timed.push_back(rec);
+  }
+  hipStream_t stream = nullptr;
+};
+
+}  // namespace cavs
+
+// Launch on `stream`, bracketed by timing events when timing is enabled.
+#define CAVS_LAUNCH(name, kernel, grid, block, shmem, stream, ...)            \
+  do {                                                                      \
+    ::cavs::TimedScope ts_(name, stream);                                   \
+    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);    \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// host entry points implemented in the individual sources
+// ---------------------------------------------------------------------------
+namespace cavs {
+
+struct SchedWs;
+
+// schedule.hip
+size_t schedule_ws_bytes(int32_t V, int32_t N, int32_t n_x);
+cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
+                         size_t ws_bytes);
+
+}  // namespace cavs

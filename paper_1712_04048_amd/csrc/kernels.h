@@ -1,0 +1,147 @@
+// Kernel argument blocks, launchers and the fp32 MFMA tile engine shared by
+// the forward / backward sources.
+#pragma once
+
+#include "cavs_internal.h"
+
+namespace cavs {
+
+// Per-batch device views.  All "by position" arrays use the level-major
+// layout produced by the scheduler: task V_t = positions [off_t, off_{t+1}).
+struct Net {
+  int V, N, D, H, C, loss;
+  int GW;                       // saved-gate / dA row width: (3+N)H (LSTM) or H (FC)
+  float inv_denom;              // 1 / |Lambda|
+  // schedule
+  const int* child_pos;         // [V*N]
+  const int* parent_pos;        // [V]
+  const int* pull_pos;          // [V]
+  const int* push_pos;          // [V]
+  const int* order;             // [V]
+  const int* pull_list;         // [n_pull]
+  // parameters and inputs
+  const float* Wx;              // [D, 4H]
+  const float* U;               // LSTM [H, 4H]; FC [N*H, H]
+  const float* b;
+  const float* Ws;              // [H, C]
+  const float* bs;              // [C]
+  const float* X;               // [n_x, D]
+  const float* Y;               // [n_y, H]
+  // workspace (level-major)
+  float* P;                     // [V, 4H] pull projection x W_x (rows that pull)
+  float* Hs;                    // [V, H]
+  float* Cs;                    // [V, H]
+  float* Gs;                    // [V, GW] saved gates  i | f_0 | o | u | f_1
+  float* dZ;                    // [V, C]  d loss / d logits
+  float* lossv;                 // [V]     per-vertex loss terms
+  float* dHp;                   // [V, H]  dL/dh contributed by the parent
+  float* dCp;                   // [V, H]  dL/dc contributed by the parent
+  float* dA;                    // [V, GW] pre-activation gradients, same layout as Gs
+  // outputs in vertex-id order
+  float* h_out;
+  float* c_out;
+};
+
+// gate column blocks of Wx / U / b (each H wide)
+enum { G_I = 0, G_F = 1, G_O = 2, G_U = 3 };
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+// lstm.hip
+void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
+void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s);
+void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s);
+void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s);
+// fc.hip
+void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
+void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);
+void fc_bwd_gates(const Net& n, int off, int M, int leaf, float* dX, hipStream_t s);
+void fc_bwd_level(const Net& n, int off, int M, hipStream_t s);
+// lazy.hip
+void pull_gemm(const Net& n, int n_pull, bool with_f, hipStream_t s);
+void loss_fwd(const Net& n, float* loss_out, hipStream_t s);
+void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s);
+// Lazy weight-gradient products; `part` is split-K scratch of part_floats floats.
+void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
+void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
+              size_t part_floats, hipStream_t s);
+void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);
+// column sums over positions [row0, row1) of the gate gradients -> db
+void bias_grad(const Net& n, int row0, int row1, float* db, float* part, size_t part_floats,
+               hipStream_t s);
+void head_grad(const Net& n, float* dWs, float* dbs, float* part, size_t part_floats,
+               hipStream_t s);
+size_t lazy_part_floats(int V, int D, int H, int N, int C);
+
+// ---------------------------------------------------------------------------
+// fp32 MFMA tile engine (v_mfma_f32_16x16x4_f32, 64-lane wavefronts)
+//
+// Lane l = 16*g + r of a wavefront supplies A[row r][k_g] and B[k_g][col r]
+// for one 4-deep K step and receives C[row 4g+i][col r], i = 0..3.  Inside a
+// 32-deep LDS chunk the K index is permuted so that lane group g covers
+// k = 8g .. 8g+7: an M-major ("MK", k contiguous) operand tile then serves
+// four K steps per 128-bit LDS read.  A and B use the same permutation, so
+// the sum over k is unchanged.
+// ---------------------------------------------------------------------------
+constexpr int kBK = 32;
+
+template <bool MK, int LD>
+__device__ __forceinline__ void load_frag4(const float* __restrict__ S, int idx, int gq, int half,
+                                           float (&f)[4]) {
+  if constexpr (MK) {
+    const float4 t = *reinterpret_cast<const float4*>(&S[idx * LD + 8 * gq + 4 * half]);
+    f[0] = t.x;
+    f[1] = t.y;
+    f[2] = t.z;
+    f[3] = t.w;
+  } else {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) f[s] = S[(8 * gq + 4 * half + s) * LD + idx];
+  }
+}
+
+// acc[tm][tn] += A[wrow + 16 tm .., :] * B[:, wcol + 16 tn ..] over one chunk.
+template <int TM, int TN, bool A_MK, bool B_MK, int LDA, int LDB>
+__device__ __forceinline__ void mfma_chunk(const float* __restrict__ As,
+                                           const float* __restrict__ Bs, int wrow, int wcol,
+                                           v4f (&acc)[TM][TN]) {
+  const int lane = threadIdx.x & 63, gq = lane >> 4, r = lane & 15;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    float a[TM][4], b[TN][4];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) load_frag4<A_MK, LDA>(As, wrow + 16 * tm + r, gq, half, a[tm]);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) load_frag4<B_MK, LDB>(Bs, wcol + 16 * tn + r, gq, half, b[tn]);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma_f32_16x16x4(a[tm][s], b[tn][s], acc[tm][tn]);
+  }
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void zero_acc(v4f (&acc)[TM][TN]) {
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = v4f{0.f, 0.f, 0.f, 0.f};
+}
+
+__device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ float4 ldg4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void st4_scalar(float* p, float4 v) {
+  p[0] = v.x;
+  p[1] = v.y;
+  p[2] = v.z;
+  p[3] = v.w;
+}
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+}  // namespace cavs

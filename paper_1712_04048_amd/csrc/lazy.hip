@@ -1,0 +1,530 @@
+// Operators that are not on a gather->scatter path of F or dF and therefore
+// run batched over all vertices at once (lazy batching, Section 3.5), plus
+// the eager pull projection:
+//   - pull:   P = X W_x for every vertex that pulls an input (one GEMM);
+//   - push:   the loss head over every labelled vertex (z = h W_s + b_s);
+//   - dF:     dW_x, dU, db, dX, dW_s, db_s as long-K products over all
+//             vertices, with deterministic split-K (fixed-order reduction).
+#include "kernels.h"
+
+namespace cavs {
+namespace {
+
+constexpr int kLossMaxC = 16;
+constexpr int kMaxSplits = 8;
+
+// ------------------------------------------------------------- pull GEMM
+// P[p, n] = X[pull_pos[p], :] W_x[:, n] for p = pull_list[m]; tile 64 x 64.
+// Column tiles cover the gate blocks i,f,o,u (with_f) or i,o,u.
+__global__ void __launch_bounds__(256) k_pull_gemm(Net n, int n_pull, int with_f) {
+  constexpr int BM = 64, BN = 64, LDA = kBK + 4, LDB = BN + 2;
+  __shared__ __attribute__((aligned(16))) float As[BM * LDA];
+  __shared__ float Bs[kBK * LDB];
+  const int H = n.H, H4 = 4 * H, D = n.D;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int m0 = blockIdx.x * BM;
+  const int tpg = H / BN, gsel = blockIdx.y / tpg;
+  const int gate = with_f ? gsel : (gsel == 0 ? G_I : gsel + 1);
+  const int n0 = gate * H + (blockIdx.y % tpg) * BN;
+  const float* asrc[2];
+  int arow[2], aq[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int idx = tid + 256 * a;
+    arow[a] = idx / 8;
+    aq[a] = idx % 8;
+    asrc[a] = nullptr;
+    if (m0 + arow[a] < n_pull) {
+      const int p = n.pull_list[m0 + arow[a]];
+      asrc[a] = n.X + (size_t)n.pull_pos[p] * D;
+    }
+  }
+  float4 ra[2], rb[2];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int k = k0 + 4 * aq[a];
+      ra[a] = (asrc[a] && k < D) ? ldg4(asrc[a] + k) : f4zero();
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
+      rb[b] = k0 + kk < D ? ldg4(n.Wx + (size_t)(k0 + kk) * H4 + n0 + 4 * q) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) st4(&As[arow[a] * LDA + 4 * aq[a]], ra[a]);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
+      st4_scalar(&Bs[kk * LDB + 4 * q], rb[b]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  const int nk = (D + kBK - 1) / kBK;
+  gload(0);
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (kc + 1 < nk) gload((kc + 1) * kBK);
+    mfma_chunk<2, 2, true, false, LDA, LDB>(As, Bs, wrow, wcol, acc);
+  }
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= n_pull) continue;
+      const int p = n.pull_list[m];
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn)
+        n.P[(size_t)p * H4 + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+    }
+}
+
+// --------------------------------------------------------------- dX GEMM
+// dX[pull_pos[p], d] = sum_k dA_x[p, k] W_x[d, k], k over the gate columns
+// (i,f,o,u or i,o,u); the f column of dA_x is delta_f0 + delta_f1.
+__global__ void __launch_bounds__(256) k_dx_gemm(Net n, int n_pull, int with_f, float* dX) {
+  constexpr int BM = 64, BN = 64, LDA = kBK + 4, LDB = kBK + 4;
+  __shared__ __attribute__((aligned(16))) float As[BM * LDA];
+  __shared__ __attribute__((aligned(16))) float Bs[BN * LDB];
+  const int H = n.H, H4 = 4 * H, D = n.D, GW = n.GW, N = n.N;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int m0 = blockIdx.x * BM, d0 = blockIdx.y * BN;
+  const float* asrc[2];
+  int arow[2], aq[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int idx = tid + 256 * a;
+    arow[a] = idx / 8;
+    aq[a] = idx % 8;
+    asrc[a] = m0 + arow[a] < n_pull ? n.dA + (size_t)n.pull_list[m0 + arow[a]] * GW : nullptr;
+  }
+  float4 ra[2], rb[2];
+  auto col_of = [&](int kc) {
+    const int c = kc * kBK;
+    if (with_f) return c;
+    return c < H ? c : c + H;
+  };
+  auto gload = [&](int kc) {
+    const int c0 = col_of(kc);
+    const bool fblock = c0 >= H && c0 < 2 * H;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      float4 v = f4zero();
+      if (asrc[a]) {
+        v = ldg4(asrc[a] + c0 + 4 * aq[a]);
+        if (fblock && N == 2) v = add4(v, ldg4(asrc[a] + 3 * H + c0 + 4 * aq[a]));
+      }
+      ra[a] = v;
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, dr = idx / 8, q = idx % 8;
+      rb[b] = d0 + dr < D ? ldg4(n.Wx + (size_t)(d0 + dr) * H4 + c0 + 4 * q) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) st4(&As[arow[a] * LDA + 4 * aq[a]], ra[a]);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, dr = idx / 8, q = idx % 8;
+      st4(&Bs[dr * LDB + 4 * q], rb[b]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  const int nk = (with_f ? H4 : 3 * H) / kBK;
+  gload(0);
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (kc + 1 < nk) gload(kc + 1);
+    mfma_chunk<2, 2, true, true, LDA, LDB>(As, Bs, wrow, wcol, acc);
+  }
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= n_pull) continue;
+      const int row = n.pull_pos[n.pull_list[m]];
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) {
+        const int d = d0 + wcol + tn * 16 + r;
+        if (d < D) dX[(size_t)row * D + d] = acc[tm][tn][i];
+      }
+    }
+}
+
+// ------------------------------------------------ long-K "A^T B" products
+// out[s][m][n] = sum_{q in split s} A(q, m) B(q, n).  The loader supplies
+// 4 consecutive m (or n) of row q; rows outside [0, Q) are never requested.
+struct LdDUiou {
+  static constexpr const char* kName = "k_tn_gemm<LdDUiou>";  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
+  Net n;
+  int off1;
+  __device__ float4 a4(int q, int m) const {
+    const int p = off1 + q;
+    float4 s = f4zero();
+    for (int k = 0; k < n.N; ++k) {
+      const int cp = n.child_pos[(size_t)p * n.N + k];
+      if (cp >= 0) s = add4(s, ldg4(n.Hs + (size_t)cp * n.H + m));
+    }
+    return s;
+  }
+  __device__ float4 b4(int q, int c) const {
+    const int p = off1 + q;
+    const int col = (n.N == 2 && c >= n.H) ? c + n.H : c;
+    return ldg4(n.dA + (size_t)p * n.GW + col);
+  }
+};
+
+struct LdDUf {
+  static constexpr const char* kName = "k_tn_gemm<LdDUf>";  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
+  Net n;
+  int off1, MI;
+  __device__ float4 a4(int q, int m) const {
+    const int k = q >= MI, p = off1 + q - k * MI;
+    const int cp = n.child_pos[(size_t)p * 2 + k];
+    return cp >= 0 ? ldg4(n.Hs + (size_t)cp * n.H + m) : f4zero();
+  }
+  __device__ float4 b4(int q, int c) const {
+    const int k = q >= MI, p = off1 + q - k * MI;
+    return ldg4(n.dA + (size_t)p * n.GW + (k ? 4 * n.H : n.H) + c);
+  }
+};
+
+struct LdDWx {
+  static constexpr const char* kName = "k_tn_gemm<LdDWx>";  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
+  Net n;
+  int with_f;
+  __device__ float4 a4(int q, int m) const {
+    const int p = n.pull_list[q];
+    return m < n.D ? ldg4(n.X + (size_t)n.pull_pos[p] * n.D + m) : f4zero();
+  }
+  __device__ float4 b4(int q, int c) const {
+    const int p = n.pull_list[q];
+    const int H = n.H;
+    const int col = (with_f || c < H) ? c : c + H;
+    const float* row = n.dA + (size_t)p * n.GW;
+    float4 v = ldg4(row + col);
+    if (n.N == 2 && col >= H && col < 2 * H) v = add4(v, ldg4(row + 3 * H + col));
+    return v;
+  }
+};
+
+struct LdFCdW {
+  static constexpr const char* kName = "k_tn_gemm<LdFCdW>";  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
+  Net n;
+  int off1, slot;
+  __device__ float4 a4(int q, int m) const {
+    const int p = off1 + q;
+    const int cp = n.child_pos[(size_t)p * n.N + slot];
+    return cp >= 0 ? ldg4(n.Hs + (size_t)cp * n.H + m) : f4zero();
+  }
+  __device__ float4 b4(int q, int c) const {
+    return ldg4(n.dA + (size_t)(off1 + q) * n.H + c);
+  }
+};
+
+template <class L>
+__global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo, int No,
+                                                 float* out) {
+  constexpr int BM = 64, BN = 64, LD = 64 + 2;
+  __shared__ float As[kBK * LD];
+  __shared__ float Bs[kBK * LD];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
+  float4 ra[2], rb[2];
+  auto gload = [&](int q0) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+      const int q = q0 + qq;
+      ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(q, m0 + 4 * c4) : f4zero();
+      rb[a] = (q < q_hi) ? ld.b4(q, n0 + 4 * c4) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+      st4_scalar(&As[qq * LD + 4 * c4], ra[a]);
+      st4_scalar(&Bs[qq * LD + 4 * c4], rb[a]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  gload(q_lo);
+  for (int q0 = q_lo; q0 < q_hi; q0 += kBK) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (q0 + kBK < q_hi) gload(q0 + kBK);
+    mfma_chunk<2, 2, false, false, LD, LD>(As, Bs, wrow, wcol, acc);
+  }
+  float* o = out + (size_t)s * Mo * No;
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= Mo) continue;
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+    }
+}
+
+// dst[m, col(n)] = sum_s part[s][m][n] in split order; col(n) = col_off + n
+// (+ gap for n >= gap_start).
+__global__ void k_reduce_splits(const float* __restrict__ part, int S, int Mo, int No,
+                                float* __restrict__ dst, int ldd, int col_off, int gap_start,
+                                int gap) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)Mo * No) return;
+  const int m = (int)(idx / No), nn = (int)(idx % No);
+  float s = 0.f;
+  for (int k = 0; k < S; ++k) s += part[(size_t)k * Mo * No + idx];
+  dst[(size_t)m * ldd + col_off + nn + (nn >= gap_start ? gap : 0)] = s;
+}
+
+template <class L>
+void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col_off,
+                int gap_start, int gap, float* part, size_t part_floats, hipStream_t st) {
+  if (Q <= 0) {
+    // empty contraction: zero output columns
+    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
+                       (const float*)part, 0, Mo, No, dst, ldd, col_off, gap_start, gap);
+    return;
+  }
+  const int tiles = (No / 64) * cdiv(Mo, 64);
+  int S = cdiv(1024, tiles);
+  S = S < 1 ? 1 : S;
+  S = S > kMaxSplits ? kMaxSplits : S;
+  int maxS = cdiv(Q, 256);
+  if (S > maxS) S = maxS;
+  while (S > 1 && (size_t)S * Mo * No > part_floats) --S;
+  int qchunk = cdiv(cdiv(Q, S), kBK) * kBK;
+  S = cdiv(Q, qchunk);
+  CAVS_LAUNCH(L::kName, k_tn_gemm<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld, Q,
+                     qchunk, Mo, No, part);
+  CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
+                     (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
+}
+
+// -------------------------------------------------------------- col sums
+// mode 0: LSTM db (4H columns, f = f_0 + f_1); mode 1: FC db (H columns);
+// mode 2: db_s (C columns of dZ); mode 3: dW_s (H*C columns: h_j dZ_c).
+template <int MODE>
+__global__ void k_colsum_part(Net n, int row0, int row1, int width, int rows_per,
+                              float* part) {
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  if (col >= width) return;
+  const int lo = row0 + blockIdx.y * rows_per, hi = min(row1, lo + rows_per);
+  const int H = n.H;
+  float s = 0.f;
+  for (int p = lo; p < hi; ++p) {
+    if constexpr (MODE == 0) {
+      const float* row = n.dA + (size_t)p * n.GW;
+      float v = row[col];
+      if (n.N == 2 && col >= H && col < 2 * H) v += row[3 * H + col];
+      s += v;
+    } else if constexpr (MODE == 1) {
+      s += n.dA[(size_t)p * H + col];
+    } else if constexpr (MODE == 2) {
+      s += n.dZ[(size_t)p * n.C + col];
+    } else {
+      const int j = col / n.C, c = col % n.C;
+      s += n.Hs[(size_t)p * H + j] * n.dZ[(size_t)p * n.C + c];
+    }
+  }
+  part[(size_t)blockIdx.y * width + col] = s;
+}
+
+__global__ void k_colsum_reduce(const float* __restrict__ part, int nblk, int width,
+                                float* __restrict__ dst) {
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  if (col >= width) return;
+  float s = 0.f;
+  for (int b = 0; b < nblk; ++b) s += part[(size_t)b * width + col];
+  dst[col] = s;
+}
+
+constexpr const char* kColsumName[4] = {"k_colsum_part<0>", "k_colsum_part<1>",
+                                        "k_colsum_part<2>", "k_colsum_part<3>"};
+
+template <int MODE>
+void colsum(const Net& n, int row0, int row1, int width, float* dst, float* part,
+            size_t part_floats, hipStream_t st) {
+  const int rows = row1 - row0;
+  int nblk = rows > 0 ? cdiv(rows, 128) : 1;
+  if (nblk > 256) nblk = 256;
+  while (nblk > 1 && (size_t)nblk * width > part_floats) --nblk;
+  const int rows_per = rows > 0 ? cdiv(rows, nblk) : 0;
+  CAVS_LAUNCH(kColsumName[MODE], k_colsum_part<MODE>, dim3(cdiv(width, 256), nblk), dim3(256), 0, st, n,
+                     row0, row1, width, rows_per, part);
+  CAVS_LAUNCH("k_colsum_reduce", k_colsum_reduce, dim3(cdiv(width, 256)), dim3(256), 0, st,
+                     (const float*)part, nblk, width, dst);
+}
+
+// ---------------------------------------------------------------- loss
+// One wavefront per position: logits (or the L2 residual), the loss term and
+// d loss / d logits = (softmax - onehot) / |Lambda|.
+__global__ void __launch_bounds__(256) k_loss(Net n) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int p = blockIdx.x * 4 + w;
+  if (p >= n.V) return;
+  const int q = n.push_pos[p], H = n.H, C = n.C;
+  const float* h = n.Hs + (size_t)p * H;
+  if (q < 0) {
+    if (lane == 0) n.lossv[p] = 0.f;
+    if (n.loss == CAVS_LOSS_CE && lane < C) n.dZ[(size_t)p * C + lane] = 0.f;
+    return;
+  }
+  if (n.loss == CAVS_LOSS_CE) {
+    float z[kLossMaxC];
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c) z[c] = 0.f;
+    for (int j = lane; j < H; j += 64) {
+      const float hj = h[j];
+      const float* ws = n.Ws + (size_t)j * C;
+#pragma unroll
+      for (int c = 0; c < kLossMaxC; ++c)
+        if (c < C) z[c] += hj * ws[c];
+    }
+    float zmax = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C) {
+        z[c] = wave_sum(z[c]) + n.bs[c];
+        zmax = fmaxf(zmax, z[c]);
+      }
+    float se = 0.f;
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C) se += expf(z[c] - zmax);
+    const float lse = zmax + logf(se);
+    float zq = 0.f;
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c == q) zq = z[c];
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C && lane == c)
+        n.dZ[(size_t)p * C + c] = (expf(z[c] - lse) - (c == q ? 1.f : 0.f)) * n.inv_denom;
+    if (lane == 0) n.lossv[p] = lse - zq;
+  } else {
+    const float* y = n.Y + (size_t)q * H;
+    float s = 0.f;
+    for (int j = lane; j < H; j += 64) {
+      const float d = h[j] - y[j];
+      s += d * d;
+    }
+    s = wave_sum(s);
+    if (lane == 0) n.lossv[p] = 0.5f * s;
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_loss_sum(const float* __restrict__ lossv, int V,
+                                                   float scale, float* out) {
+  __shared__ float red[1024];
+  float s = 0.f;
+  for (int i = threadIdx.x; i < V; i += 1024) s += lossv[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 512; o >= 1; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0] * scale;
+}
+
+}  // namespace
+
+size_t lazy_part_floats(int V, int D, int H, int N, int C) {
+  (void)V;
+  size_t a = (size_t)kMaxSplits * 4 * H * (size_t)H;        // dU / FC dW
+  size_t b = (size_t)kMaxSplits * 4 * H * (size_t)(D + 64);  // dW_x (m tail padding)
+  size_t c = (size_t)256 * (4 * H + (size_t)H * (C > 0 ? C : 1));
+  (void)N;
+  size_t m = a > b ? a : b;
+  return m > c ? m : c;
+}
+
+void pull_gemm(const Net& n, int n_pull, bool with_f, hipStream_t s) {
+  if (n_pull <= 0) return;
+  dim3 grid(cdiv(n_pull, 64), (with_f ? 4 : 3) * (n.H / 64));
+  CAVS_LAUNCH("k_pull_gemm", k_pull_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
+}
+
+void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
+  if (n_pull <= 0) return;
+  dim3 grid(cdiv(n_pull, 64), cdiv(n.D, 64));
+  CAVS_LAUNCH("k_dx_gemm", k_dx_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
+}
+
+void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
+  CAVS_LAUNCH("k_loss", k_loss, dim3(cdiv(n.V, 4)), dim3(256), 0, s, n);
+  CAVS_LAUNCH("k_loss_sum", k_loss_sum, dim3(1), dim3(1024), 0, s, (const float*)n.lossv, n.V,
+                     n.inv_denom, loss_out);
+}
+
+void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
+  const int H = n.H, MI = n.V - off1;
+  if (n.N == 1) {
+    LdDUiou ld{n, off1};
+    tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
+  } else {
+    LdDUiou ld{n, off1};
+    tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s);
+    LdDUf lf{n, off1, MI};
+    tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s);
+  }
+}
+
+void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
+              size_t part_floats, hipStream_t s) {
+  const int H = n.H;
+  LdDWx ld{n, (int)with_f};
+  if (with_f) {
+    tn_product(ld, n_pull, n.D, 4 * H, dWx, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
+  } else {
+    tn_product(ld, n_pull, n.D, 3 * H, dWx, 4 * H, 0, H, H, part, part_floats, s);
+    // the f block of dW_x is exactly zero: no vertex with children pulls
+    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)n.D * H, 256)), dim3(256), 0, s,
+                       (const float*)part, 0, n.D, H, dWx, 4 * H, H, 1 << 30, 0);
+  }
+}
+
+void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s) {
+  const int H = n.H, MI = n.V - off1;
+  for (int k = 0; k < n.N; ++k) {
+    LdFCdW ld{n, off1, k};
+    tn_product(ld, MI, H, H, dW + (size_t)k * H * H, H, 0, 1 << 30, 0, part, part_floats, s);
+  }
+}
+
+void bias_grad(const Net& n, int row0, int row1, float* db, float* part, size_t part_floats,
+               hipStream_t s) {
+  if (n.GW == n.H) colsum<1>(n, row0, row1, n.H, db, part, part_floats, s);
+  else colsum<0>(n, row0, row1, 4 * n.H, db, part, part_floats, s);
+}
+
+void head_grad(const Net& n, float* dWs, float* dbs, float* part, size_t part_floats,
+               hipStream_t s) {
+  colsum<2>(n, 0, n.V, n.C, dbs, part, part_floats, s);
+  colsum<3>(n, 0, n.V, n.H * n.C, dWs, part, part_floats, s);
+}
+
+}  // namespace cavs

@@ -1,0 +1,489 @@
+// GPU scheduler: the batching tasks V_t of Algorithm 1 (Section 3.2) and the
+// level-major "dynamic tensor" layout of Section 3.3 / Algorithm 2.
+//
+// A vertex is activated once all of its children are evaluated, so the task
+// that evaluates v is its level: 0 for a leaf, else 1 + the largest level of
+// its children.  The schedule is built without host round trips:
+//   1. validation counters (range, references per vertex, pull rows, links);
+//   2. level assignment: one thread per leaf walks towards the root; at each
+//      parent it bumps an arrival counter and only the last child to arrive
+//      continues, so every vertex is assigned exactly once, in O(V) total;
+//   3. per-level histogram and exclusive scan -> level_offsets;
+//   4. stable LSD radix sort of vertex ids by level (8-bit digits, ranks from
+//      wavefront ballots), giving ascending ids inside each task;
+//   5. index remap to positions, and a stable compaction of the positions
+//      that pull an input;
+//   6. one device->host copy of T, the counts, the error flags and the
+//      offsets, and the only stream synchronisation.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "cavs_internal.h"
+
+namespace cavs {
+
+namespace {
+
+enum Flag {
+  F_RANGE = 0,
+  F_MULTI = 1,
+  F_DUP = 2,
+  F_MISMATCH = 3,
+  F_CYCLE = 4,
+  F_T = 5,
+  F_LINKS = 6,
+  F_WITHPARENT = 7,
+  F_LABELLED = 8,
+  F_LEAF_NOIN = 9,
+  F_INNER_IN = 10,
+  F_NPULL = 11,
+  F_COUNT = 32
+};
+
+constexpr int kTile = 1024;      // radix tile: 256 threads x 4 rounds
+constexpr int kStageHead = 32;   // stage = flags[32] then offsets
+
+__device__ __forceinline__ int ld_acquire_int(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_relaxed_int(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// -------------------------------------------------------------------------
+// 1. validation counters
+// -------------------------------------------------------------------------
+__global__ void k_scan_edges(int V, int N, int n_x, int n_push, const int* __restrict__ child,
+                             const int* __restrict__ parent, const int* __restrict__ pull_idx,
+                             const int* __restrict__ push_idx, int* ref_cnt, int* pull_cnt,
+                             int* nchild, int* flags) {
+  int v = blockIdx.x * blockDim.x + threadIdx.x;
+  int links = 0, withp = 0, lab = 0, leafnoin = 0, innerin = 0, npull = 0, bad = 0;
+  if (v < V) {
+    int nc = 0;
+    for (int k = 0; k < N; ++k) {
+      int c = child[(size_t)v * N + k];
+      if (c < -1 || c >= V) {
+        bad = 1;
+      } else if (c >= 0) {
+        atomicAdd(&ref_cnt[c], 1);
+        ++nc;
+      }
+    }
+    int p = parent[v];
+    if (p < -1 || p >= V) bad = 1;
+    else if (p >= 0) withp = 1;
+    int r = pull_idx ? pull_idx[v] : -1;
+    if (r < -1 || r >= n_x) {
+      bad = 1;
+      r = -1;
+    } else if (r >= 0) {
+      atomicAdd(&pull_cnt[r], 1);
+      npull = 1;
+    }
+    int q = push_idx ? push_idx[v] : -1;
+    if (q < -1 || q >= n_push) bad = 1;
+    else if (q >= 0) lab = 1;
+    nchild[v] = nc;
+    links = nc;
+    leafnoin = (nc == 0 && r < 0);
+    innerin = (nc > 0 && r >= 0);
+  }
+  links = wave_sum_int(links);
+  withp = wave_sum_int(withp);
+  lab = wave_sum_int(lab);
+  leafnoin = wave_sum_int(leafnoin);
+  innerin = wave_sum_int(innerin);
+  npull = wave_sum_int(npull);
+  bad = wave_sum_int(bad);
+  if (lane_id() == 0) {
+    if (links) atomicAdd(&flags[F_LINKS], links);
+    if (withp) atomicAdd(&flags[F_WITHPARENT], withp);
+    if (lab) atomicAdd(&flags[F_LABELLED], lab);
+    if (leafnoin) atomicAdd(&flags[F_LEAF_NOIN], leafnoin);
+    if (innerin) atomicAdd(&flags[F_INNER_IN], innerin);
+    if (npull) atomicAdd(&flags[F_NPULL], npull);
+    if (bad) atomicOr(&flags[F_RANGE], 1);
+  }
+}
+
+__global__ void k_check_links(int V, int N, int n_x, const int* __restrict__ child,
+                              const int* __restrict__ parent, const int* __restrict__ ref_cnt,
+                              const int* __restrict__ pull_cnt, int* flags) {
+  int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < V) {
+    if (ref_cnt[v] > 1) atomicOr(&flags[F_MULTI], 1);
+    for (int k = 0; k < N; ++k) {
+      int c = child[(size_t)v * N + k];
+      if (c >= 0 && c < V && parent[c] != v) atomicOr(&flags[F_MISMATCH], 1);
+    }
+  }
+  if (v < n_x && pull_cnt[v] > 1) atomicOr(&flags[F_DUP], 1);
+}
+
+// -------------------------------------------------------------------------
+// 2. levels: leaf-to-root walks with arrival counters
+// -------------------------------------------------------------------------
+__global__ void k_levels(int V, int N, const int* __restrict__ child,
+                         const int* __restrict__ parent, const int* __restrict__ nchild,
+                         int* arrive, int* level) {
+  int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V || nchild[v] != 0) return;
+  st_relaxed_int(&level[v], 0);
+  int cur = v;
+  // Each vertex is passed by at most one walker (only the arrival that makes
+  // the counter equal its child count continues), so V steps bound any walk.
+  for (int step = 0; step < V; ++step) {
+    int p = parent[cur];
+    if (p < 0 || p >= V) break;
+    __threadfence();
+    int old = atomicAdd(&arrive[p], 1);
+    if (old + 1 != nchild[p]) break;
+    __threadfence();
+    int m = -1;
+    for (int k = 0; k < N; ++k) {
+      int c = child[(size_t)p * N + k];
+      if (c >= 0 && c < V) m = max(m, ld_acquire_int(&level[c]));
+    }
+    st_relaxed_int(&level[p], m + 1);
+    cur = p;
+  }
+}
+
+// -------------------------------------------------------------------------
+// 3. per-level histogram, T, cycle detection, and the offsets scan
+// -------------------------------------------------------------------------
+__global__ void k_level_hist(int V, const int* __restrict__ level, int* hist, int* flags) {
+  int v = blockIdx.x * blockDim.x + threadIdx.x;
+  int tmax = 0, cyc = 0;
+  if (v < V) {
+    int l = level[v];
+    if (l < 0 || l >= V) {
+      cyc = 1;
+    } else {
+      atomicAdd(&hist[l], 1);
+      tmax = l + 1;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) tmax = max(tmax, __shfl_xor(tmax, o, kWave));
+  cyc = wave_sum_int(cyc);
+  if (lane_id() == 0) {
+    if (tmax) atomicMax(&flags[F_T], tmax);
+    if (cyc) atomicOr(&flags[F_CYCLE], 1);
+  }
+}
+
+// Single-block exclusive scan of n ints (src may equal dst).  If n_dev is
+// non-null the element count is *n_dev + 1 (scan of hist[0..T]).
+__global__ void __launch_bounds__(1024) k_scan_excl(const int* src, int* dst, int n,
+                                                    const int* n_dev) {
+  __shared__ int wsum[16];
+  __shared__ int carry_s;
+  if (n_dev) n = *n_dev + 1;
+  int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (tid == 0) carry_s = 0;
+  __syncthreads();
+  for (int base = 0; base < n; base += 1024) {
+    int i = base + tid;
+    int x = i < n ? src[i] : 0;
+    int incl = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    if (w == 0) {
+      int s = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        int t = __shfl_up(s, o, kWave);
+        if (lane >= o) s += t;
+      }
+      if (lane < 16) wsum[lane] = s;  // inclusive over waves
+    }
+    __syncthreads();
+    int carry = carry_s;
+    int wave_off = w > 0 ? wsum[w - 1] : 0;
+    if (i < n) dst[i] = carry + wave_off + incl - x;
+    __syncthreads();
+    if (tid == 0) carry_s = carry + wsum[15];
+    __syncthreads();
+  }
+}
+
+// -------------------------------------------------------------------------
+// 4. stable LSD radix sort, 8-bit digits
+// -------------------------------------------------------------------------
+__device__ __forceinline__ unsigned digit_of(int key, int shift) {
+  return ((unsigned)key >> shift) & 255u;
+}
+
+// tile_hist is digit-major: entry [d * ntiles + tile]
+__global__ void __launch_bounds__(256) k_radix_hist(const int* __restrict__ keys, int n, int shift,
+                                                    int ntiles, int* tile_hist) {
+  __shared__ int h[256];
+  int tid = threadIdx.x;
+  h[tid] = 0;
+  __syncthreads();
+  int base = blockIdx.x * kTile;
+#pragma unroll
+  for (int r = 0; r < kTile / 256; ++r) {
+    int e = base + r * 256 + tid;
+    if (e < n) atomicAdd(&h[digit_of(keys[e], shift)], 1);
+  }
+  __syncthreads();
+  tile_hist[tid * ntiles + blockIdx.x] = h[tid];
+}
+
+// vals_in == nullptr means the identity (value = element index).
+__global__ void __launch_bounds__(256) k_radix_scatter(const int* __restrict__ keys_in,
+                                                       const int* __restrict__ vals_in, int n,
+                                                       int shift, int ntiles,
+                                                       const int* __restrict__ offs,
+                                                       int* __restrict__ keys_out,
+                                                       int* __restrict__ vals_out) {
+  __shared__ int base_cnt[256];
+  __shared__ int wcnt[4][256];
+  int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  base_cnt[tid] = 0;
+  const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int tile = blockIdx.x;
+  for (int r = 0; r < kTile / 256; ++r) {
+    int e = tile * kTile + r * 256 + tid;
+    bool valid = e < n;
+    int key = valid ? keys_in[e] : 0;
+    int val = valid ? (vals_in ? vals_in[e] : e) : 0;
+    unsigned d = digit_of(key, shift);
+    unsigned long long peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      bool bit = (d >> b) & 1u;
+      unsigned long long bb = __ballot(valid && bit);
+      peers &= bit ? bb : ~bb;
+    }
+    int rank_in_wave = __popcll(peers & lt_mask);
+    int wave_cnt = __popcll(peers);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wcnt[q][tid] = 0;
+    __syncthreads();
+    if (valid && rank_in_wave == 0) wcnt[w][d] = wave_cnt;
+    __syncthreads();
+    if (valid) {
+      int rank = base_cnt[d] + rank_in_wave;
+      for (int q = 0; q < w; ++q) rank += wcnt[q][d];
+      int dst = offs[d * ntiles + tile] + rank;
+      keys_out[dst] = key;
+      vals_out[dst] = val;
+    }
+    __syncthreads();
+    base_cnt[tid] += wcnt[0][tid] + wcnt[1][tid] + wcnt[2][tid] + wcnt[3][tid];
+    __syncthreads();
+  }
+}
+
+// -------------------------------------------------------------------------
+// 5. remap to positions
+// -------------------------------------------------------------------------
+__global__ void k_pos(int V, const int* __restrict__ order, int* pos) {
+  int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < V) {
+    int v = order[p];
+    if (v >= 0 && v < V) pos[v] = p;
+  }
+}
+
+__global__ void k_remap(int V, int N, const int* __restrict__ order, const int* __restrict__ pos,
+                        const int* __restrict__ child, const int* __restrict__ parent,
+                        const int* __restrict__ pull_idx, const int* __restrict__ push_idx,
+                        int* child_pos, int* parent_pos, int* pull_pos, int* push_pos,
+                        int* pull_key) {
+  int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= V) return;
+  int v = order[p];
+  if (v < 0 || v >= V) v = 0;
+  for (int k = 0; k < N; ++k) {
+    int c = child[(size_t)v * N + k];
+    child_pos[(size_t)p * N + k] = (c >= 0 && c < V) ? pos[c] : -1;
+  }
+  int q = parent[v];
+  parent_pos[p] = (q >= 0 && q < V) ? pos[q] : -1;
+  int r = pull_idx ? pull_idx[v] : -1;
+  pull_pos[p] = r;
+  push_pos[p] = push_idx ? push_idx[v] : -1;
+  pull_key[p] = r >= 0 ? 0 : 1;
+}
+
+// -------------------------------------------------------------------------
+// 6. staging for the single device->host copy
+// -------------------------------------------------------------------------
+__global__ void k_stage(const int* __restrict__ flags, const int* __restrict__ level_offsets,
+                        int cap, int* stage) {
+  int T = flags[F_T];
+  int n = min(T + 1, cap);
+  for (int i = threadIdx.x; i < kStageHead; i += blockDim.x) stage[i] = flags[i];
+  for (int i = threadIdx.x; i < n; i += blockDim.x) stage[kStageHead + i] = level_offsets[i];
+}
+
+struct Layout {
+  size_t flags, ref_cnt, arrive, pull_cnt, hist, zero_end;
+  size_t nchild, keysA, valsA, keysB, valsB, tile_hist, stage, total;
+  int ntiles;
+};
+
+Layout layout(int32_t V, int32_t N, int32_t n_x) {
+  (void)N;
+  Layout L;
+  size_t o = 0;
+  auto take = [&](size_t ints) {
+    size_t r = o;
+    o = align_up(o + ints * sizeof(int), 256);
+    return r;
+  };
+  L.ntiles = cdiv(V > 0 ? V : 1, kTile);
+  L.flags = take(F_COUNT);
+  L.ref_cnt = take((size_t)V + 1);
+  L.arrive = take((size_t)V + 1);
+  L.pull_cnt = take((size_t)n_x + 1);
+  L.hist = take((size_t)V + 2);
+  L.zero_end = o;
+  L.nchild = take((size_t)V + 1);
+  L.keysA = take((size_t)V + 1);
+  L.valsA = take((size_t)V + 1);
+  L.keysB = take((size_t)V + 1);
+  L.valsB = take((size_t)V + 1);
+  L.tile_hist = take((size_t)256 * L.ntiles);
+  L.stage = take(kHostStageInts);
+  L.total = o;
+  return L;
+}
+
+// Sorts (keys_in, vals_in) by key.  Pass p writes keys to bufK[p % 2] and
+// values to bufV[p % 2], except that the last pass writes its values to
+// vals_final.  keys_in must not alias bufK[0].
+cavs_status radix_sort(cavs_ctx* ctx, const int* keys_in, const int* vals_in, int n, int passes,
+                       int* const bufK[2], int* const bufV[2], int* vals_final, int* tile_hist,
+                       int ntiles) {
+  const int* ki = keys_in;
+  const int* vi = vals_in;
+  for (int pass = 0; pass < passes; ++pass) {
+    int* ko = bufK[pass % 2];
+    int* vo = pass == passes - 1 ? vals_final : bufV[pass % 2];
+    int shift = 8 * pass;
+    CAVS_LAUNCH("k_radix_hist", k_radix_hist, dim3(ntiles), dim3(256), 0, ctx->stream, ki, n, shift,
+                       ntiles, tile_hist);
+    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, ctx->stream, tile_hist, tile_hist,
+                       256 * ntiles, (const int*)nullptr);
+    CAVS_LAUNCH("k_radix_scatter", k_radix_scatter, dim3(ntiles), dim3(256), 0, ctx->stream, ki, vi, n,
+                       shift, ntiles, tile_hist, ko, vo);
+    CAVS_LAUNCH_CHECK(ctx);
+    ki = ko;
+    vi = vo;
+  }
+  return CAVS_OK;
+}
+
+}  // namespace
+
+size_t schedule_ws_bytes(int32_t V, int32_t N, int32_t n_x) {
+  if (V < 0 || N < 1 || n_x < 0) return 0;
+  return layout(V, N, n_x).total;
+}
+
+cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
+                         size_t ws_bytes) {
+  const int V = g->V, N = g->N, n_x = g->n_x;
+  Layout L = layout(V, N, n_x);
+  if (ws_bytes < L.total)
+    return fail(ctx, CAVS_ERR_WORKSPACE, "schedule workspace too small: %zu < %zu", ws_bytes,
+                L.total);
+  char* base = (char*)ws;
+  int* flags = (int*)(base + L.flags);
+  int* ref_cnt = (int*)(base + L.ref_cnt);
+  int* arrive = (int*)(base + L.arrive);
+  int* pull_cnt = (int*)(base + L.pull_cnt);
+  int* hist = (int*)(base + L.hist);
+  int* nchild = (int*)(base + L.nchild);
+  int* kA = (int*)(base + L.keysA);
+  int* vA = (int*)(base + L.valsA);
+  int* kB = (int*)(base + L.keysB);
+  int* vB = (int*)(base + L.valsB);
+  int* tile_hist = (int*)(base + L.tile_hist);
+  int* stage = (int*)(base + L.stage);
+  hipStream_t st = ctx->stream;
+  s->V = V;
+  s->N = N;
+  s->n_x = n_x;
+  s->n_push = g->n_push;
+  if (V == 0) {  // nothing to schedule: no launches, no device access
+    s->T = 0;
+    s->n_pull = s->n_labelled = s->n_leaf_noinput = s->n_inner_input = 0;
+    s->level_offsets_host[0] = 0;
+    return CAVS_OK;
+  }
+
+  CAVS_HIP_CHECK(ctx, hipMemsetAsync(base, 0, L.zero_end, st));
+  CAVS_HIP_CHECK(ctx, hipMemsetAsync(s->level, 0xFF, sizeof(int) * (size_t)V, st));
+  const int nb = cdiv(V, 256);
+  if (V > 0) {
+    CAVS_LAUNCH("k_scan_edges", k_scan_edges, dim3(nb), dim3(256), 0, st, V, N, n_x, g->n_push, g->child,
+                       g->parent, g->pull_idx, g->push_idx, ref_cnt, pull_cnt, nchild, flags);
+    CAVS_LAUNCH("k_check_links", k_check_links, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256), 0, st, V, N,
+                       n_x, g->child, g->parent, ref_cnt, pull_cnt, flags);
+    CAVS_LAUNCH("k_levels", k_levels, dim3(nb), dim3(256), 0, st, V, N, g->child, g->parent, nchild,
+                       arrive, s->level);
+    CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
+    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
+                       (const int*)(flags + F_T));
+    CAVS_LAUNCH_CHECK(ctx);
+    // passes: enough 8-bit digits for any level in [0, V)
+    int passes = 1;
+    while (passes < 4 && ((long)(V - 1) >> (8 * passes)) > 0) ++passes;
+    int* const lvK[2] = {kA, kB};
+    int* const lvV[2] = {vA, vB};
+    cavs_status r = radix_sort(ctx, s->level, nullptr, V, passes, lvK, lvV, s->order, tile_hist,
+                               L.ntiles);
+    if (r != CAVS_OK) return r;
+    CAVS_LAUNCH("k_pos", k_pos, dim3(nb), dim3(256), 0, st, V, s->order, s->pos);
+    CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, s->order, s->pos, g->child,
+                       g->parent, g->pull_idx, g->push_idx, s->child_pos, s->parent_pos,
+                       s->pull_pos, s->push_pos, kA);
+    CAVS_LAUNCH_CHECK(ctx);
+    int* const plK[2] = {kB, kB};
+    int* const plV[2] = {vA, vA};
+    r = radix_sort(ctx, kA, nullptr, V, 1, plK, plV, s->pull_list, tile_hist, L.ntiles);
+    if (r != CAVS_OK) return r;
+  }
+  const int cap = kHostStageInts - kStageHead;
+  CAVS_LAUNCH("k_stage", k_stage, dim3(1), dim3(256), 0, st, flags, s->level_offsets, cap, stage);
+  CAVS_LAUNCH_CHECK(ctx);
+  CAVS_HIP_CHECK(ctx, hipMemcpyAsync(ctx->host_stage, stage, sizeof(int) * kHostStageInts,
+                                     hipMemcpyDeviceToHost, st));
+  CAVS_HIP_CHECK(ctx, hipStreamSynchronize(st));
+  const int* h = ctx->host_stage;
+  if (h[F_RANGE]) return fail(ctx, CAVS_ERR_RANGE, "an index array holds an out-of-range value");
+  if (h[F_MULTI]) return fail(ctx, CAVS_ERR_MULTIPARENT, "a vertex is a child more than once");
+  if (h[F_DUP]) return fail(ctx, CAVS_ERR_DUP_PULL, "two vertices pull the same input row");
+  if (h[F_MISMATCH] || h[F_LINKS] != h[F_WITHPARENT])
+    return fail(ctx, CAVS_ERR_MISMATCH, "child[] and parent[] disagree");
+  if (h[F_CYCLE]) return fail(ctx, CAVS_ERR_CYCLE, "the child links contain a cycle");
+  const int T = h[F_T];
+  s->T = T;
+  s->n_pull = h[F_NPULL];
+  s->n_labelled = h[F_LABELLED];
+  s->n_leaf_noinput = h[F_LEAF_NOIN];
+  s->n_inner_input = h[F_INNER_IN];
+  int n = T + 1 < cap ? T + 1 : cap;
+  for (int i = 0; i < n; ++i) s->level_offsets_host[i] = h[kStageHead + i];
+  if (T + 1 > cap) {
+    CAVS_HIP_CHECK(ctx, hipMemcpyAsync(s->level_offsets_host + cap, s->level_offsets + cap,
+                                       sizeof(int) * (size_t)(T + 1 - cap),
+                                       hipMemcpyDeviceToHost, st));
+    CAVS_HIP_CHECK(ctx, hipStreamSynchronize(st));
+  }
+  return CAVS_OK;
+}
+
+}  // namespace cavs

@@ -1,0 +1,89 @@
+"""The C ABI library loads and exports every function include/cavs.h declares,
+and the Python binding's struct layouts match the header (CPU only)."""
+import ctypes as ct
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+from paper_1712_04048_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cavs.h")
+
+
+def _ensure_built():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_1712_04048_amd import build
+        build.build()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cavs_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert _declared_functions() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    _ensure_built()
+    lib = ct.CDLL(B.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (cavs_\w+)", out))
+    assert set(_declared_functions()) <= exported
+
+
+PROBE = r"""
+#include <stddef.h>
+#include <stdio.h>
+#include "cavs.h"
+#define F(S, m) printf(#S "." #m " %zu\n", offsetof(S, m));
+int main(void) {
+  printf("cavs_graphs %zu\ncavs_sched %zu\ncavs_params %zu\ncavs_inputs %zu\ncavs_grads %zu\n",
+         sizeof(cavs_graphs), sizeof(cavs_sched), sizeof(cavs_params), sizeof(cavs_inputs),
+         sizeof(cavs_grads));
+  F(cavs_graphs, child) F(cavs_graphs, push_idx)
+  F(cavs_sched, n_inner_input) F(cavs_sched, level) F(cavs_sched, level_offsets_host)
+  F(cavs_params, C) F(cavs_params, Wx) F(cavs_params, bs)
+  F(cavs_inputs, n_y) F(cavs_grads, dX)
+  return 0;
+}
+"""
+
+
+def test_struct_layouts_match_header():
+    with tempfile.TemporaryDirectory() as d:
+        src = os.path.join(d, "probe.c")
+        exe = os.path.join(d, "probe")
+        open(src, "w").write(PROBE)
+        subprocess.check_call(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), src, "-o", exe])
+        out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout
+    vals = dict(line.split() for line in out.strip().splitlines())
+    for cname, cls in [("cavs_graphs", B.cavs_graphs), ("cavs_sched", B.cavs_sched),
+                       ("cavs_params", B.cavs_params), ("cavs_inputs", B.cavs_inputs),
+                       ("cavs_grads", B.cavs_grads)]:
+        assert int(vals[cname]) == ct.sizeof(cls), cname
+    for key, v in vals.items():
+        if "." in key:
+            s, m = key.split(".")
+            cls = getattr(B, s)
+            assert getattr(cls, m).offset == int(v), key
+
+
+def test_workspace_query_needs_no_gpu():
+    _ensure_built()
+    lib = B.lib()
+    assert lib.cavs_schedule_workspace_bytes(1000, 2, 500) > 0
+    assert lib.cavs_schedule_workspace_bytes(-1, 2, 0) == 0
+    p = B.cavs_params(B.TREE_LSTM, B.FP32, B.LOSS_CE, 300, 512, 2, 5)
+    s = B.cavs_sched()
+    s.V, s.N = 1000, 2
+    assert lib.cavs_workspace_bytes(ct.byref(p), ct.byref(s)) > 1000 * 512 * 4

@@ -1,0 +1,250 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Schedules must match bit for bit; fp32 states, loss and gradients must match
+the fp64 oracle to 1e-4 under the floored relative error of parity.rel_err.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from parity import check, subset
+from paper_1712_04048_amd import binding as B
+from paper_1712_04048_amd import workloads as W
+from paper_1712_04048_amd.runner import Batch
+
+pytestmark = pytest.mark.gpu
+
+TOL_FP32 = 1e-4
+ALL_KEYS = ["h", "c", "loss", "dWx", "dU", "db", "dWs", "dbs", "dX"]
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    c = B.Context(0)
+    yield c
+    c.close()
+
+
+def _forest(seed, N=2, shuffle=False, max_trees=40, max_leaves=40):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    trees = []
+    for _ in range(int(rng.integers(1, max_trees))):
+        L = int(rng.integers(1, max_leaves))
+        kind = int(rng.integers(0, 4))
+        if N == 1:
+            trees.append(W.chain(L))
+        elif kind == 0:
+            trees.append(W.random_split_tree(L, rng))
+        elif kind == 1:
+            trees.append(W.left_branching_tree(L))
+        elif kind == 2:
+            trees.append(W.right_branching_tree(L))
+        else:
+            trees.append(W.complete_tree(1 << int(rng.integers(0, 6))))
+    return W.make_workload("forest", trees, N=N, D=4, H=64, C=5, rng=rng,
+                           inputs="leaves" if seed % 3 else "all",
+                           labels="all" if seed % 2 else "root", shuffle_ids=shuffle)
+
+
+def _gpu_schedule(ctx, wl):
+    b = Batch(wl, ctx)
+    s = b.schedule()
+    return s.host()
+
+
+def _compare_schedule(got, want):
+    assert got["T"] == want["T"]
+    for k in ("level", "order", "pos", "child_pos", "parent_pos", "pull_pos", "push_pos",
+              "level_offsets", "pull_list"):
+        assert np.array_equal(got[k], want[k]), k
+    assert got["n_pull"] == want["n_pull"]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_schedule_bit_exact(ctx, seed):
+    N = 1 if seed % 4 == 0 else 2
+    wl = _forest(seed, N=N, shuffle=seed % 2 == 1)
+    print("schedule case seed=%d V=%d N=%d" % (seed, wl.V, N), flush=True)
+    got = _gpu_schedule(ctx, wl)
+    want = oracle.schedule(wl.child, wl.parent, wl.pull_idx, wl.push_idx)
+    _compare_schedule(got, want)
+    assert got["n_labelled"] == int((wl.push_idx >= 0).sum())
+
+
+@pytest.mark.parametrize("maker", ["sst", "varlstm", "treefc", "deep_bf16", "big"])
+def test_schedule_bit_exact_benchmark_shapes(ctx, maker):
+    if maker == "big":   # > 65536 vertices: three radix passes
+        rng = np.random.Generator(np.random.PCG64(5))
+        trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 300, size=500)]
+        wl = W.make_workload("big", trees, N=2, D=4, H=64, C=5, rng=rng, shuffle_ids=True)
+        assert wl.V > 65536
+    else:
+        wl = W.CONFIGS[maker](0)
+    print("schedule shape %s V=%d" % (maker, wl.V), flush=True)
+    got = _gpu_schedule(ctx, wl)
+    want = oracle.schedule(wl.child, wl.parent, wl.pull_idx, wl.push_idx)
+    _compare_schedule(got, want)
+
+
+def _raw_schedule_status(ctx, child, parent, pull=None, push=None, n_x=0, n_push=0):
+    dev = ctx.torch_device
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+    try:
+        B.schedule(ctx, t(child), t(parent), None if pull is None else t(pull),
+                   None if push is None else t(push), n_x=n_x, n_push=n_push)
+        return B.OK
+    except B.CavsError as e:
+        return e.status
+
+
+def test_schedule_rejects_invalid_graphs(ctx):
+    child = np.array([[-1, -1], [-1, -1], [0, 1]])
+    parent = np.array([2, 2, -1])
+    cases = []
+    c = child.copy(); c[2, 1] = 3; cases.append((c, parent, None, None, 0, 0))
+    p = parent.copy(); p[0] = -2; cases.append((child, p, None, None, 0, 0))
+    c = child.copy(); c[2, 1] = 0; cases.append((c, parent, None, None, 0, 0))
+    cases.append((np.array([[-1, -1], [0, -1], [0, 1]]), np.array([1, 2, -1]), None, None, 0, 0))
+    p = parent.copy(); p[1] = -1; cases.append((child, p, None, None, 0, 0))
+    p = parent.copy(); p[2] = 0; cases.append((child, p, None, None, 0, 0))
+    cases.append((np.array([[-1, -1], [-1, -1], [0, 1], [4, -1], [3, -1]]),
+                  np.array([2, 2, -1, 4, 3]), None, None, 0, 0))
+    cases.append((np.array([[0, -1]]), np.array([0]), None, None, 0, 0))
+    cases.append((child, parent, np.array([0, 0, -1]), None, 2, 0))
+    cases.append((child, parent, np.array([0, 2, -1]), None, 2, 0))
+    cases.append((child, parent, None, np.array([0, 5, -1]), 0, 5))
+    cases.append((np.array([[-1, -1], [0, 7], [0, 1]]), parent, None, None, 0, 0))
+    for i, (c, p, pl, ps, nx, npush) in enumerate(cases):
+        want = oracle.validate(c, p, pl, nx, ps, npush)
+        got = _raw_schedule_status(ctx, c, p, pl, ps, nx, npush)
+        assert want != oracle.OK
+        assert got == want, (i, got, want)
+    # a valid graph still schedules after the failures
+    assert _raw_schedule_status(ctx, child, parent) == B.OK
+
+
+def _parity(ctx, wl, tol=TOL_FP32, keys=ALL_KEYS, label=""):
+    print("parity %s V=%d H=%d" % (label or wl.name, wl.V, wl.H), flush=True)
+    got = Batch(wl, ctx).run()
+    want = oracle.run(wl)
+    return check(got, want, keys, tol, label or wl.name)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_tiny_treelstm(ctx, seed):
+    _parity(ctx, W.config_tiny_treelstm(seed))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_tiny_treelstm_shuffled_ids(ctx, seed):
+    _parity(ctx, W.config_tiny_treelstm(seed, shuffle_ids=True))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_sst_shaped_reduced(ctx, seed):
+    _parity(ctx, W.config_treelstm_sst(seed, K=12))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_varlstm_reduced(ctx, seed):
+    _parity(ctx, W.config_varlstm(seed, K=6))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_treefc_reduced(ctx, seed):
+    _parity(ctx, W.config_treefc(seed, K=2, leaves=64))
+
+
+def test_parity_treefc_cross_entropy(ctx):
+    rng = np.random.Generator(np.random.PCG64(3))
+    trees = [W.random_split_tree(int(L), rng) for L in rng.integers(1, 30, size=7)]
+    wl = W.make_workload("fc_ce", trees, cell=W.CELL_TREE_FC, loss=W.LOSS_CE, N=2, H=64, C=5,
+                         sigma=0.2, rng=rng, labels="all")
+    _parity(ctx, wl)
+
+
+EDGE = {
+    "single_vertex_trees": lambda rng: ([[[-1, -1]]] * 37, dict()),
+    "chain_len1_and_mixed": lambda rng: ([W.chain(1), W.chain(3), W.chain(1), W.chain(70)],
+                                         dict(N=1, inputs="all", labels="all")),
+    "left_branching": lambda rng: ([W.left_branching_tree(L) for L in (2, 9, 33)],
+                                   dict(labels="all")),
+    "right_branching": lambda rng: ([W.right_branching_tree(L) for L in (2, 9, 33)],
+                                    dict(labels="all")),
+    "unary_vertices": lambda rng: ([[[-1, -1], [0, -1], [-1, -1], [1, 2], [-1, 3]]] * 5,
+                                   dict(labels="all")),
+    "inputs_everywhere": lambda rng: ([W.random_split_tree(int(L), rng) for L in (5, 17, 3, 40)],
+                                      dict(inputs="all", labels="all")),
+    "leaves_without_input": lambda rng: ([W.random_split_tree(int(L), rng) for L in (5, 17, 3)],
+                                         dict(inputs="none", labels="all")),
+    "no_labels": lambda rng: ([W.random_split_tree(int(L), rng) for L in (5, 6)],
+                              dict(labels="none")),
+    "wide_ragged_level": lambda rng: ([W.random_split_tree(int(L), rng)
+                                       for L in rng.integers(1, 9, size=150)],
+                                      dict(labels="all")),
+}
+
+
+@pytest.mark.parametrize("case", sorted(EDGE))
+def test_parity_edge_cases(ctx, case):
+    rng = np.random.Generator(np.random.PCG64(11))
+    trees, kw = EDGE[case](rng)
+    args = dict(N=2, D=12, H=64, C=5, sigma=0.3, rng=rng)
+    args.update(kw)
+    wl = W.make_workload(case, trees, **args)
+    wl.b[:] = (0.1 * rng.standard_normal(wl.b.shape)).astype(np.float32)
+    _parity(ctx, wl, label=case)
+
+
+@pytest.mark.parametrize("maker", ["sst", "varlstm", "treefc"])
+def test_full_size_states_on_sampled_graphs(ctx, maker):
+    """Full benchmark-size batch on the GPU (the launch configuration the
+    benchmark times); states of sampled graphs against the oracle run on
+    those graphs alone (a graph's states depend only on itself)."""
+    wl = W.CONFIGS[maker](0)
+    print("full-size %s V=%d" % (maker, wl.V), flush=True)
+    b = Batch(wl, ctx)
+    got = b.run()
+    rng = np.random.Generator(np.random.PCG64(1))
+    trees = sorted(rng.choice(wl.K, size=3, replace=False).tolist())
+    sub = subset(wl, trees)
+    want = oracle.run(sub, backward=False)
+    ids = np.concatenate([np.arange(wl.tree_offsets[k], wl.tree_offsets[k + 1]) for k in trees])
+    errs = check({k: got[k][ids] for k in ("h", "c") if k in got},
+                 {k: want[k] for k in ("h", "c") if k in want}, ["h", "c"], TOL_FP32, maker)
+    # properties at full size
+    assert np.isfinite(got["loss"])
+    if wl.loss == W.LOSS_CE:
+        assert abs(got["dbs"].sum()) < 1e-5 * max(1.0, np.abs(got["dbs"]).max() * wl.C)
+    if wl.cell == W.CELL_TREE_LSTM and wl.N == 2:
+        assert np.all(got["dWx"][:, wl.H:2 * wl.H] == 0.0)   # leaf-only inputs
+    print(errs)
+
+
+def test_determinism_bitwise(ctx):
+    wl = W.config_treelstm_sst(0, K=24)
+    b = Batch(wl, ctx)
+    r1 = b.run()
+    r2 = b.run()
+    for k in r1:
+        assert np.array_equal(np.asarray(r1[k]), np.asarray(r2[k])), k
+
+
+def test_forward_rejects_bad_arguments(ctx):
+    wl = W.config_tiny_treelstm(0)
+    b = Batch(wl, ctx)
+    b.schedule()
+    b.alloc()
+    small = torch.empty(16, dtype=torch.uint8, device=ctx.torch_device)
+    with pytest.raises(B.CavsError) as e:
+        B.forward(ctx, b.params, b.sched, b.X, b.Y, small, b.h, b.c, b.loss)
+    assert e.value.status == B.ERR_WORKSPACE
+    p = B.Params(**{**b.params.__dict__, "H": 48})
+    with pytest.raises(B.CavsError) as e:
+        B.forward(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
+    assert e.value.status in (B.ERR_UNSUPPORTED, B.ERR_WORKSPACE)
+    p = B.Params(**{**b.params.__dict__, "N": 1})
+    with pytest.raises(B.CavsError) as e:
+        B.forward(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
+    assert e.value.status == B.ERR_ARG
