@@ -85,7 +85,8 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
   if (p->N != s->N) return fail(ctx, CAVS_ERR_ARG, "params N=%d != schedule N=%d", p->N, s->N);
   if (p->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots (max 2)", p->N);
   if (p->H % 64 != 0) return fail(ctx, CAVS_ERR_UNSUPPORTED, "H=%d not a multiple of 64", p->H);
-  if (p->prec == CAVS_BF16) return fail(ctx, CAVS_ERR_UNSUPPORTED, "bf16 products not built");
+  if (p->prec == CAVS_BF16 && p->cell != CAVS_TREE_LSTM)
+    return fail(ctx, CAVS_ERR_UNSUPPORTED, "bf16 products are built for the Tree-LSTM only");
   if (s->V < 0 || s->T < 0 || (s->V > 0 && s->T <= 0))
     return fail(ctx, CAVS_ERR_ARG, "schedule not built");
   if (s->V > 0 && (!s->child_pos || !s->parent_pos || !s->pull_pos || !s->push_pos ||
@@ -122,6 +123,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.H = p->H;
   n.C = p->C;
   n.loss = p->loss;
+  n.bf = p->prec == CAVS_BF16;
   n.GW = p->cell == CAVS_TREE_LSTM ? (3 + p->N) * p->H : p->H;
   n.inv_denom = 1.f / (float)(s->n_labelled > 0 ? s->n_labelled : 1);
   n.child_pos = s->child_pos;

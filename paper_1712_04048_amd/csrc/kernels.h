@@ -10,6 +10,7 @@ namespace cavs {
 // layout produced by the scheduler: task V_t = positions [off_t, off_{t+1}).
 struct Net {
   int V, N, D, H, C, loss;
+  int bf;                       // 1: matrix-product operands rounded to bf16
   int GW;                       // saved-gate / dA row width: (3+N)H (LSTM) or H (FC)
   float inv_denom;              // 1 / |Lambda|
   // schedule
@@ -142,6 +143,64 @@ __device__ __forceinline__ void st4_scalar(float* p, float4 v) {
 }
 __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA engine (v_mfma_f32_16x16x32_bf16): lane l = 16*g + r supplies
+// A[row r][k = 8g .. 8g+7] and B[k = 8g .. 8g+7][col r] as 8 bf16 values and
+// receives C[row 4g+i][col r].  Tiles live in LDS as rows of kBK bf16 values
+// (k contiguous), padded to kLDH, so each operand fragment is one 16-byte
+// read.  Operands are rounded to bf16 (nearest-even) when staged into LDS;
+// accumulation is fp32.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16;
+constexpr int kLDH = kBK + 8;   // 40 bf16 = 80 bytes per row (16-byte aligned)
+
+__device__ __forceinline__ u16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);   // round to nearest, ties to even (finite inputs)
+  return (u16)(u >> 16);
+}
+
+// 4 consecutive k of one row (8-byte store)
+__device__ __forceinline__ void st_bf4(u16* dst, float4 v) {
+  uint2 w;
+  w.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  w.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *reinterpret_cast<uint2*>(dst) = w;
+}
+
+// the same 4 values into 4 consecutive rows at column k (transposed store)
+__device__ __forceinline__ void st_bf4_t(u16* dst, int ld, float4 v) {
+  dst[0] = f2bf(v.x);
+  dst[ld] = f2bf(v.y);
+  dst[2 * ld] = f2bf(v.z);
+  dst[3 * ld] = f2bf(v.w);
+}
+
+__device__ __forceinline__ bf16x8 frag_bf(const u16* S, int row, int gq) {
+  return *reinterpret_cast<const bf16x8*>(&S[row * kLDH + 8 * gq]);
+}
+
+__device__ __forceinline__ v4f mfma_bf16_16x16x32(bf16x8 a, bf16x8 b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void mfma_chunk_bf(const u16* __restrict__ As,
+                                              const u16* __restrict__ Bs, int wrow, int wcol,
+                                              v4f (&acc)[TM][TN]) {
+  const int lane = threadIdx.x & 63, gq = lane >> 4, r = lane & 15;
+  bf16x8 a[TM], b[TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) a[tm] = frag_bf(As, wrow + 16 * tm + r, gq);
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) b[tn] = frag_bf(Bs, wcol + 16 * tn + r, gq);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma_bf16_16x16x32(a[tm], b[tn], acc[tm][tn]);
 }
 
 }  // namespace cavs

@@ -169,7 +169,8 @@ __global__ void __launch_bounds__(256) k_dx_gemm(Net n, int n_pull, int with_f, 
 // out[s][m][n] = sum_{q in split s} A(q, m) B(q, n).  The loader supplies
 // 4 consecutive m (or n) of row q; rows outside [0, Q) are never requested.
 struct LdDUiou {
-  static constexpr const char* kName = "k_tn_gemm<LdDUiou>";  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
+  static constexpr const char* kName = "k_tn_gemm<LdDUiou>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
   Net n;
   int off1;
   __device__ float4 a4(int q, int m) const {
@@ -189,7 +190,8 @@ struct LdDUiou {
 };
 
 struct LdDUf {
-  static constexpr const char* kName = "k_tn_gemm<LdDUf>";  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
+  static constexpr const char* kName = "k_tn_gemm<LdDUf>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
   Net n;
   int off1, MI;
   __device__ float4 a4(int q, int m) const {
@@ -204,7 +206,8 @@ struct LdDUf {
 };
 
 struct LdDWx {
-  static constexpr const char* kName = "k_tn_gemm<LdDWx>";  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
+  static constexpr const char* kName = "k_tn_gemm<LdDWx>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
   Net n;
   int with_f;
   __device__ float4 a4(int q, int m) const {
@@ -223,7 +226,8 @@ struct LdDWx {
 };
 
 struct LdFCdW {
-  static constexpr const char* kName = "k_tn_gemm<LdFCdW>";  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
+  static constexpr const char* kName = "k_tn_gemm<LdFCdW>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   Net n;
   int off1, slot;
   __device__ float4 a4(int q, int m) const {
@@ -286,6 +290,203 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
     }
 }
 
+
+// ------------------------------------------------------------ bf16 variants
+// Same tiles as the fp32 kernels above; operands are rounded to bf16 while
+// they are staged into LDS (k-contiguous rows), accumulation is fp32.
+__global__ void __launch_bounds__(256) k_pull_gemm_bf(Net n, int n_pull, int with_f) {
+  constexpr int BM = 64, BN = 64;
+  __shared__ __attribute__((aligned(16))) u16 As[BM * kLDH];
+  __shared__ __attribute__((aligned(16))) u16 Bs[BN * kLDH];
+  const int H = n.H, H4 = 4 * H, D = n.D;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int m0 = blockIdx.x * BM;
+  const int tpg = H / BN, gsel = blockIdx.y / tpg;
+  const int gate = with_f ? gsel : (gsel == 0 ? G_I : gsel + 1);
+  const int n0 = gate * H + (blockIdx.y % tpg) * BN;
+  const float* asrc[2];
+  int arow[2], aq[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int idx = tid + 256 * a;
+    arow[a] = idx / 8;
+    aq[a] = idx % 8;
+    asrc[a] = nullptr;
+    if (m0 + arow[a] < n_pull) asrc[a] = n.X + (size_t)n.pull_pos[n.pull_list[m0 + arow[a]]] * D;
+  }
+  float4 ra[2], rb[2];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int k = k0 + 4 * aq[a];
+      ra[a] = (asrc[a] && k < D) ? ldg4(asrc[a] + k) : f4zero();
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
+      rb[b] = k0 + kk < D ? ldg4(n.Wx + (size_t)(k0 + kk) * H4 + n0 + 4 * q) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) st_bf4(&As[arow[a] * kLDH + 4 * aq[a]], ra[a]);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
+      st_bf4_t(&Bs[(4 * q) * kLDH + kk], kLDH, rb[b]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  const int nk = (D + kBK - 1) / kBK;
+  gload(0);
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (kc + 1 < nk) gload((kc + 1) * kBK);
+    mfma_chunk_bf<2, 2>(As, Bs, wrow, wcol, acc);
+  }
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= n_pull) continue;
+      const int p = n.pull_list[m];
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn)
+        n.P[(size_t)p * H4 + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+    }
+}
+
+__global__ void __launch_bounds__(256) k_dx_gemm_bf(Net n, int n_pull, int with_f, float* dX) {
+  constexpr int BM = 64, BN = 64;
+  __shared__ __attribute__((aligned(16))) u16 As[BM * kLDH];
+  __shared__ __attribute__((aligned(16))) u16 Bs[BN * kLDH];
+  const int H = n.H, H4 = 4 * H, D = n.D, GW = n.GW, N = n.N;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int m0 = blockIdx.x * BM, d0 = blockIdx.y * BN;
+  const float* asrc[2];
+  int arow[2], aq[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int idx = tid + 256 * a;
+    arow[a] = idx / 8;
+    aq[a] = idx % 8;
+    asrc[a] = m0 + arow[a] < n_pull ? n.dA + (size_t)n.pull_list[m0 + arow[a]] * GW : nullptr;
+  }
+  float4 ra[2], rb[2];
+  auto col_of = [&](int kc) {
+    const int c = kc * kBK;
+    if (with_f) return c;
+    return c < H ? c : c + H;
+  };
+  auto gload = [&](int kc) {
+    const int c0 = col_of(kc);
+    const bool fblock = c0 >= H && c0 < 2 * H;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      float4 v = f4zero();
+      if (asrc[a]) {
+        v = ldg4(asrc[a] + c0 + 4 * aq[a]);
+        if (fblock && N == 2) v = add4(v, ldg4(asrc[a] + 3 * H + c0 + 4 * aq[a]));
+      }
+      ra[a] = v;
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b, dr = idx / 8, q = idx % 8;
+      rb[b] = d0 + dr < D ? ldg4(n.Wx + (size_t)(d0 + dr) * H4 + c0 + 4 * q) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) st_bf4(&As[arow[a] * kLDH + 4 * aq[a]], ra[a]);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int idx = tid + 256 * b;
+      st_bf4(&Bs[(idx / 8) * kLDH + 4 * (idx % 8)], rb[b]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  const int nk = (with_f ? H4 : 3 * H) / kBK;
+  gload(0);
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (kc + 1 < nk) gload(kc + 1);
+    mfma_chunk_bf<2, 2>(As, Bs, wrow, wcol, acc);
+  }
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= n_pull) continue;
+      const int row = n.pull_pos[n.pull_list[m]];
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) {
+        const int d = d0 + wcol + tn * 16 + r;
+        if (d < D) dX[(size_t)row * D + d] = acc[tm][tn][i];
+      }
+    }
+}
+
+template <class L>
+__global__ void __launch_bounds__(256) k_tn_gemm_bf(L ld, int Q, int qchunk, int Mo, int No,
+                                                    float* out) {
+  constexpr int BM = 64, BN = 64;
+  __shared__ __attribute__((aligned(16))) u16 As[BM * kLDH];
+  __shared__ __attribute__((aligned(16))) u16 Bs[BN * kLDH];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
+  float4 ra[2], rb[2];
+  auto gload = [&](int q0) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+      const int q = q0 + qq;
+      ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(q, m0 + 4 * c4) : f4zero();
+      rb[a] = (q < q_hi) ? ld.b4(q, n0 + 4 * c4) : f4zero();
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+      st_bf4_t(&As[(4 * c4) * kLDH + qq], kLDH, ra[a]);
+      st_bf4_t(&Bs[(4 * c4) * kLDH + qq], kLDH, rb[a]);
+    }
+  };
+  v4f acc[2][2];
+  zero_acc(acc);
+  gload(q_lo);
+  for (int q0 = q_lo; q0 < q_hi; q0 += kBK) {
+    __syncthreads();
+    sstore();
+    __syncthreads();
+    if (q0 + kBK < q_hi) gload(q0 + kBK);
+    mfma_chunk_bf<2, 2>(As, Bs, wrow, wcol, acc);
+  }
+  float* o = out + (size_t)s * Mo * No;
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
+      if (m >= Mo) continue;
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+    }
+}
+
 // dst[m, col(n)] = sum_s part[s][m][n] in split order; col(n) = col_off + n
 // (+ gap for n >= gap_start).
 __global__ void k_reduce_splits(const float* __restrict__ part, int S, int Mo, int No,
@@ -317,6 +518,10 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
   while (S > 1 && (size_t)S * Mo * No > part_floats) --S;
   int qchunk = cdiv(cdiv(Q, S), kBK) * kBK;
   S = cdiv(Q, qchunk);
+  if (ld.n.bf)
+    CAVS_LAUNCH(L::kNameBf, k_tn_gemm_bf<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld,
+                Q, qchunk, Mo, No, part);
+  else
   CAVS_LAUNCH(L::kName, k_tn_gemm<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld, Q,
                      qchunk, Mo, No, part);
   CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
@@ -465,13 +670,19 @@ size_t lazy_part_floats(int V, int D, int H, int N, int C) {
 void pull_gemm(const Net& n, int n_pull, bool with_f, hipStream_t s) {
   if (n_pull <= 0) return;
   dim3 grid(cdiv(n_pull, 64), (with_f ? 4 : 3) * (n.H / 64));
-  CAVS_LAUNCH("k_pull_gemm", k_pull_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
+  if (n.bf)
+    CAVS_LAUNCH("k_pull_gemm_bf", k_pull_gemm_bf, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
+  else
+    CAVS_LAUNCH("k_pull_gemm", k_pull_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
 }
 
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
   if (n_pull <= 0) return;
   dim3 grid(cdiv(n_pull, 64), cdiv(n.D, 64));
-  CAVS_LAUNCH("k_dx_gemm", k_dx_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
+  if (n.bf)
+    CAVS_LAUNCH("k_dx_gemm_bf", k_dx_gemm_bf, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
+  else
+    CAVS_LAUNCH("k_dx_gemm", k_dx_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
 }
 
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {

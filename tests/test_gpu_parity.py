@@ -248,3 +248,60 @@ def test_forward_rejects_bad_arguments(ctx):
     with pytest.raises(B.CavsError) as e:
         B.forward(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
     assert e.value.status == B.ERR_ARG
+
+
+# ---------------------------------------------------------------------------
+# bf16 matrix products (fp32 accumulation) against the oracle that rounds the
+# same operands to bf16; the error against the plain fp64 oracle is reported.
+# ---------------------------------------------------------------------------
+TOL_BF16 = 2e-2
+
+
+def _parity_bf16(ctx, wl, label):
+    print("bf16 parity %s V=%d H=%d" % (label, wl.V, wl.H), flush=True)
+    got = Batch(wl, ctx).run()
+    want = oracle.run(wl, bf16=True)
+    errs = check(got, want, ALL_KEYS, TOL_BF16, label)
+    plain = oracle.run(wl, bf16=False)
+    from parity import rel_err
+    vs64 = {k: rel_err(got[k], plain[k]) for k in ALL_KEYS if k in plain and k != "loss"}
+    print("  vs bf16-emulating oracle:", errs)
+    print("  vs fp64 oracle:", vs64)
+    return errs
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_bf16_deep_reduced(ctx, seed):
+    wl = W.config_treelstm_deep_bf16(seed, K=4, D=300, H=1024, lo=8, hi=40)
+    _parity_bf16(ctx, wl, "deep_bf16_reduced_%d" % seed)
+
+
+def test_parity_bf16_small_shapes(ctx):
+    rng = np.random.Generator(np.random.PCG64(21))
+    trees = [W.random_split_tree(int(L), rng) for L in (1, 3, 9, 20)] + [W.left_branching_tree(12)]
+    wl = W.make_workload("bf16_inputs_everywhere", trees, prec=W.PREC_BF16, N=2, D=36, H=64,
+                         C=5, sigma=0.2, rng=rng, inputs="all", labels="all")
+    _parity_bf16(ctx, wl, "bf16_inputs_everywhere")
+    wl = W.make_workload("bf16_chains", [W.chain(n) for n in (1, 7, 40)], prec=W.PREC_BF16, N=1,
+                         D=64, H=128, C=5, sigma=0.1, rng=rng, inputs="all", labels="all")
+    _parity_bf16(ctx, wl, "bf16_chains")
+
+
+def test_full_size_bf16_states_on_sampled_graphs(ctx):
+    """Config of 256 trees, H=1024, half left-branching (T=128), bf16 products:
+    full batch on the GPU, states of two sampled graphs against the oracle."""
+    wl = W.config_treelstm_deep_bf16(0)
+    print("full-size deep_bf16 V=%d" % wl.V, flush=True)
+    got = Batch(wl, ctx).run()
+    sizes = np.diff(wl.tree_offsets)
+    left = int(np.argmin(np.where(np.arange(wl.K) < wl.K // 2, sizes, 10 ** 9)))
+    rand = int(wl.K // 2 + np.argmin(sizes[wl.K // 2:]))
+    trees = sorted([left, rand])
+    sub = subset(wl, trees)
+    want = oracle.run(sub, backward=False, bf16=True)
+    ids = np.concatenate([np.arange(wl.tree_offsets[k], wl.tree_offsets[k + 1]) for k in trees])
+    check({k: got[k][ids] for k in ("h", "c")}, want, ["h", "c"], TOL_BF16, "deep_bf16_full")
+    assert np.isfinite(got["loss"])
+    assert np.all(got["dWx"][:, wl.H:2 * wl.H] == 0.0)
+    for k in ("dWx", "dU", "db", "dWs", "dbs", "dX"):
+        assert np.all(np.isfinite(got[k])), k
