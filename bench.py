@@ -16,6 +16,7 @@ on a bounded sample of the same workload.
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -24,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Tree-LSTM fwd+bwd vertices/sec (h=512, batch 256); % MFMA / HBM roofline"
 PEAK_FP32_TFLOPS = 157.3     # MI355X dense fp32 matrix
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 
 
@@ -38,56 +40,35 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_costs(wl, sh, n_pull, with_f):
-    """Algorithmic FLOPs (and bytes for elementwise kernels) per kernel name
-    for one step, from the schedule.  Only work the method must do counts:
-    absent children and unused gate blocks contribute nothing."""
+def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
+    """Algorithmic (FLOPs, bytes) of one launch.  Level kernels are costed
+    over the rows [row0, row0 + rows) they covered; only work the method must
+    do counts (absent children and unused gate blocks contribute nothing).
+    The lazy and pull products run once per step over all vertices."""
     import numpy as np
     H, D, N = wl.H, wl.D, wl.N
-    lo = sh["level_offsets"]
-    cp = sh["child_pos"].reshape(-1, N)
-    nc = (cp >= 0).sum(axis=1)
-    costs = {}
-
-    def add(name, flops=0.0, nbytes=0.0):
-        f, b = costs.get(name, (0.0, 0.0))
-        costs[name] = (f + flops, b + nbytes)
-
-    T = sh["T"]
-    for t in range(T):
-        a, b = int(lo[t]), int(lo[t + 1])
-        M = b - a
-        if wl.cell == 0:
-            if t == 0:
-                add("k_lstm_leaf", 0.0, M * H * 4.0 * 12)
-                add("k_lstm_bwd_gates", 0.0, M * H * 4.0 * 12)
-                continue
-            fl = float(np.sum(2.0 * H * (3 * H + nc[a:b] * H)))
-            v = 16 if M <= 32 else 64
-            add("k_lstm_fwd_level<%d, %d>" % (N, v), fl)
-            add("k_lstm_bwd_level<%d, %d>" % (N, v), fl)
-            add("k_lstm_bwd_gates", 0.0, M * H * 4.0 * (10 + 3 * N))
-        else:
-            if t == 0:
-                continue
-            fl = float(np.sum(2.0 * nc[a:b] * H * H))
-            v = 16 if M <= 32 else 64
-            add("k_fc_fwd_level<%d>" % v, fl)
-            add("k_fc_bwd_level<%d>" % v, fl)
+    c = nc[row0:row0 + rows]
+    gates_x = 4 if with_f else 3
+    if name.startswith(("k_lstm_fwd_level", "k_lstm_bwd_level", "k_lstm_fwd_persist",
+                        "k_lstm_bwd_persist")):
+        return float(np.sum(2.0 * H * (3 * H + c * H))), 0.0
+    if name.startswith(("k_fc_fwd_level", "k_fc_bwd_level")):
+        return float(np.sum(2.0 * c * H * H)), 0.0
+    if name == "k_lstm_leaf":          # reads 3 columns of P, writes h, c, 5 gates, h_out, c_out
+        return 0.0, rows * H * 4.0 * 12
+    if name == "k_lstm_bwd_gates":     # reads dh, dc, 3 gates, c (+ f_k, c_k per child),
+        return 0.0, float(np.sum(H * 4.0 * (6 + (3 + N) + 3 * c)))  # writes dA (+ dc_k)
     inner = nc > 0
-    if wl.cell == 0:
-        gates_x = 4 if with_f else 3
-        add("k_pull_gemm", 2.0 * n_pull * D * gates_x * H)
-        add("k_dx_gemm", 2.0 * n_pull * D * gates_x * H)
-        add("k_tn_gemm<LdDWx>", 2.0 * n_pull * D * gates_x * H)
-        if N == 2:
-            add("k_tn_gemm<LdDUiou>", 2.0 * H * 3 * H * int(inner.sum()))
-            add("k_tn_gemm<LdDUf>", 2.0 * H * H * float(nc.sum()))
-        else:
-            add("k_tn_gemm<LdDUiou>", 2.0 * H * 4 * H * int(inner.sum()))
-    else:
-        add("k_tn_gemm<LdFCdW>", 2.0 * H * H * float(nc.sum()))
-    return costs
+    lazy = {
+        "k_pull_gemm": 2.0 * n_pull * D * gates_x * H,
+        "k_dx_gemm": 2.0 * n_pull * D * gates_x * H,
+        "k_tn_gemm<LdDWx>": 2.0 * n_pull * D * gates_x * H,
+        "k_tn_gemm<LdDUiou>": 2.0 * H * (3 if N == 2 else 4) * H * int(inner.sum()),
+        "k_tn_gemm<LdDUf>": 2.0 * H * H * float(nc.sum()),
+        "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()),
+    }
+    base = re.sub(r", (64|128)>", ">", name.replace("_bf", ""))
+    return lazy.get(base, 0.0), 0.0
 
 
 def cpu_baseline(wl, n_trees):
@@ -168,42 +149,63 @@ def main():
     ctx.timing(True)
     for _ in range(args.steps):
         batch.step()
-    times = ctx.timing_read()
+    recs = ctx.timing_read()
     ctx.timing(False)
 
     sh = batch.sched.host()
-    costs = algorithmic_costs(wl, sh, sh["n_pull"], sh["n_inner_input"] > 0)
+    nc = (sh["child_pos"] >= 0).sum(axis=1)
+    with_f = sh["n_inner_input"] > 0
+    agg = {}
+    for name, row0, rows, ms in recs:
+        fl, nb = launch_cost(wl, nc, name, row0, rows, sh["n_pull"], with_f)
+        a = agg.setdefault(name, [0, 0.0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += ms
+        a[2] += fl
+        a[3] += nb
+    # per-level breakdown (microseconds per step) of the level kernels
+    per_level = {}
+    for name, row0, rows, ms in recs:
+        if rows <= 0:
+            continue
+        kind = ("fwd" if ("fwd" in name or "leaf" in name) else
+                "bwd_gemm" if "bwd_level" in name else "bwd_gates")
+        e = per_level.setdefault(row0, {"rows": rows, "fwd": 0.0, "bwd_gates": 0.0,
+                                        "bwd_gemm": 0.0})
+        e[kind] += ms * 1e3 / args.steps
+    level_table = [[v["rows"], round(v["fwd"], 1), round(v["bwd_gates"], 1),
+                    round(v["bwd_gemm"], 1)] for _, v in sorted(per_level.items())]
     kernels = []
-    for name, (launches, ms) in times.items():
-        fl, nb = costs.get(name, (0.0, 0.0))
-        per_step_ms = ms / args.steps
+    for name, (launches, ms, fl, nb) in agg.items():
         k = {"name": name, "launches_per_step": launches / args.steps,
-             "ms_per_step": round(per_step_ms, 4)}
+             "ms_per_step": round(ms / args.steps, 4)}
         if fl > 0:
-            k["tflops"] = round(fl / (per_step_ms * 1e-3) / 1e12, 2)
+            k["tflops"] = round(fl / (ms * 1e-3) / 1e12, 2)
         if nb > 0:
-            k["gbs"] = round(nb / (per_step_ms * 1e-3) / 1e9, 1)
+            k["gbs"] = round(nb / (ms * 1e-3) / 1e9, 1)
         kernels.append(k)
     kernels.sort(key=lambda k: -k["ms_per_step"])
-    dom = next(k for k in kernels if costs.get(k["name"], (0, 0)) != (0, 0))
-    fl, nb = costs[dom["name"]]
-    launches, ms = times[dom["name"]]
+    dom = next(k for k in kernels if agg[k["name"]][2] > 0 or agg[k["name"]][3] > 0)
+    launches, ms, fl, nb = agg[dom["name"]]
     avg_ms = ms / launches
-    per_launch = fl / (launches / args.steps) if fl > 0 else nb / (launches / args.steps)
     if fl > 0:
+        per_launch = fl / launches
         achieved = per_launch / (avg_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_FP32_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
-                "traffic": None}
+        bf = "_bf" in dom["name"] or ", true>" in dom["name"]
+        peak = PEAK_BF16_TFLOPS if bf else PEAK_FP32_TFLOPS
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None}
     else:
+        per_launch = nb / launches
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
     roof["kernel"] = dom["name"]
+    roof["launches_per_step"] = launches / args.steps
     roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
     roof["algorithmic_per_launch"] = per_launch
 
-    total_flops = sum(f for f, _ in costs.values())
+    total_flops = sum(a[2] for a in agg.values()) / args.steps
     out = {
         "metric": METRIC,
         "value": wl.V / (wall_ms * 1e-3),
@@ -228,6 +230,7 @@ def main():
         "whole_step_tflops": round(total_flops / (wall_ms * 1e-3) / 1e12, 2),
         "algorithmic_gflop_per_step": round(total_flops / 1e9, 3),
         "kernels": kernels[:10],
+        "levels_us": {"columns": ["rows", "fwd", "bwd_gates", "bwd_gemm"], "rows": level_table},
     }
     if args.cpu_trees > 0:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_trees)

@@ -211,18 +211,19 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* params, const cavs_s
  * ------------------------------------------------------------------------- */
 typedef struct {
   char name[96];            /* kernel name, e.g. "k_lstm_fwd_level<2, 64>" */
-  int32_t launches;         /* launches since the last read */
-  double total_ms;          /* summed GPU duration of those launches */
-} cavs_kernel_time;
+  int32_t row0;             /* first level-major position the launch covers (0 if n/a) */
+  int32_t rows;             /* positions covered (a level's size; 0 if n/a) */
+  double ms;                /* GPU duration of the launch */
+} cavs_launch_time;
 
 /* Turns per-launch timing on (1) or off (0); either way discards pending
    records.  CAVS_ERR_ARG on a null context. */
 cavs_status cavs_timing_enable(cavs_ctx* ctx, int32_t on);
-/* Synchronises the context's stream, aggregates the pending records by
-   kernel name into out[0..max) (host array, caller-owned), clears them, and
-   returns the number of distinct kernels (which may exceed max; only max are
+/* Synchronises the context's stream, writes the pending launch records, in
+   launch order, to out[0..max) (host array, caller-owned), clears them, and
+   returns the number of records (which may exceed max; only max are
    written), or a negative status. */
-int32_t cavs_timing_read(cavs_ctx* ctx, cavs_kernel_time* out, int32_t max);
+int32_t cavs_timing_read(cavs_ctx* ctx, cavs_launch_time* out, int32_t max);
 
 #ifdef __cplusplus
 }

@@ -68,8 +68,8 @@ class cavs_grads(ct.Structure):
     _fields_ = [("dWx", _vp), ("dU", _vp), ("db", _vp), ("dWs", _vp), ("dbs", _vp), ("dX", _vp)]
 
 
-class cavs_kernel_time(ct.Structure):
-    _fields_ = [("name", ct.c_char * 96), ("launches", _i32), ("total_ms", ct.c_double)]
+class cavs_launch_time(ct.Structure):
+    _fields_ = [("name", ct.c_char * 96), ("row0", _i32), ("rows", _i32), ("ms", ct.c_double)]
 
 
 EXPORTS = ["cavs_create", "cavs_set_stream", "cavs_destroy", "cavs_last_error",
@@ -111,7 +111,7 @@ def lib():
         L.cavs_timing_enable.restype = _i32
         L.cavs_timing_enable.argtypes = [_vp, _i32]
         L.cavs_timing_read.restype = _i32
-        L.cavs_timing_read.argtypes = [_vp, ct.POINTER(cavs_kernel_time), _i32]
+        L.cavs_timing_read.argtypes = [_vp, ct.POINTER(cavs_launch_time), _i32]
         _lib = L
     return _lib
 
@@ -163,15 +163,15 @@ class Context:
         """Per-launch HIP-event timing of every library kernel (instrumentation)."""
         self.check(lib().cavs_timing_enable(self._h, int(bool(on))))
 
-    def timing_read(self) -> dict:
-        """{kernel name: (launches, total ms)} since the last read; synchronises."""
-        cap = 256
-        buf = (cavs_kernel_time * cap)()
+    def timing_read(self) -> list:
+        """[(kernel name, row0, rows, ms)] per launch since the last read; synchronises."""
+        cap = 1 << 16
+        buf = (cavs_launch_time * cap)()
         n = lib().cavs_timing_read(self._h, buf, cap)
         if n < 0:
             self.check(n)
-        return {buf[i].name.decode(): (int(buf[i].launches), float(buf[i].total_ms))
-                for i in range(min(n, cap))}
+        return [(buf[i].name.decode(), int(buf[i].row0), int(buf[i].rows), float(buf[i].ms))
+                for i in range(min(n, cap))]
 
 
 @dataclass

@@ -6,7 +6,6 @@
 
 #include "kernels.h"
 
-#include <map>
 #include <string.h>
 
 namespace cavs {
@@ -40,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, total;
+  size_t P, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
   size_t part_floats;
 };
 
@@ -67,6 +66,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   L.dA = take(V * GW);
   L.part_floats = lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
   L.part = take(L.part_floats);
+  L.bar = take(256);
   L.total = o;
   return L;
 }
@@ -205,37 +205,26 @@ cavs_status cavs_timing_enable(cavs_ctx* ctx, int32_t on) {
   return CAVS_OK;
 }
 
-int32_t cavs_timing_read(cavs_ctx* ctx, cavs_kernel_time* out, int32_t max) {
+int32_t cavs_timing_read(cavs_ctx* ctx, cavs_launch_time* out, int32_t max) {
   if (!ctx || (max > 0 && !out)) return CAVS_ERR_ARG;
   if (hipStreamSynchronize(ctx->stream) != hipSuccess)
     return fail(ctx, CAVS_ERR_HIP, "hipStreamSynchronize failed");
-  std::map<std::string, std::pair<int, double>> agg;
-  std::vector<std::string> first_seen;
+  int32_t n = 0;
   for (auto& r : ctx->timed) {
     float ms = 0.f;
     (void)hipEventElapsedTime(&ms, r.start, r.stop);
-    auto it = agg.find(r.name);
-    if (it == agg.end()) {
-      first_seen.push_back(r.name);
-      agg[r.name] = {1, (double)ms};
-    } else {
-      it->second.first += 1;
-      it->second.second += ms;
+    if (n < max) {
+      memset(out[n].name, 0, sizeof out[n].name);
+      strncpy(out[n].name, r.name, sizeof out[n].name - 1);
+      out[n].row0 = r.row0;
+      out[n].rows = r.rows;
+      out[n].ms = ms;
     }
+    ++n;
     ctx->event_pool.push_back(r.start);
     ctx->event_pool.push_back(r.stop);
   }
   ctx->timed.clear();
-  int32_t n = 0;
-  for (auto& name : first_seen) {
-    if (n < max) {
-      memset(out[n].name, 0, sizeof out[n].name);
-      strncpy(out[n].name, name.c_str(), sizeof out[n].name - 1);
-      out[n].launches = agg[name].first;
-      out[n].total_ms = agg[name].second;
-    }
-    ++n;
-  }
   return n;
 }
 
@@ -297,7 +286,11 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
   if (p->cell == CAVS_TREE_LSTM) {
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, str);
     lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
-    for (int t = 1; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+    const int ts = persist_first_level(n, lo, s->T);
+    for (int t = 1; t < ts; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+    int* bar = (int*)((char*)ws + L.bar);
+    if (!lstm_fwd_persist(n, s->level_offsets, lo, ts, s->T, bar, str))
+      for (int t = ts; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
   } else {
     fc_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
     for (int t = 1; t < s->T; ++t) fc_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
@@ -350,7 +343,10 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   if (s->n_x > 0 && s->n_pull < s->n_x)
     CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
   if (lstm) {
-    for (int t = T - 1; t >= 0; --t) {
+    int ts = persist_first_level(n, lo, T);
+    int* bar = (int*)((char*)ws + L.bar);
+    if (!lstm_bwd_persist(n, s->level_offsets, lo, ts, T, bar, str)) ts = T;
+    for (int t = ts - 1; t >= 0; --t) {
       const int M = lo[t + 1] - lo[t];
       lstm_bwd_gates(n, lo[t], M, str);
       if (t >= 1) lstm_bwd_level(n, lo[t], M, str);

@@ -12,6 +12,7 @@
 // One timed launch: events recorded on the context stream around it.
 struct cavs_timed_launch {
   const char* name;
+  int row0, rows;
   hipEvent_t start, stop;
 };
 
@@ -94,12 +95,14 @@ hipEvent_t timing_event(cavs_ctx* c);
 struct TimedScope {
   cavs_ctx* c;
   cavs_timed_launch rec;
-  TimedScope(const char* name, hipStream_t s) : c(t_active_ctx) {
+  TimedScope(const char* name, hipStream_t s, int row0 = 0, int rows = 0) : c(t_active_ctx) {
     if (!c || !c->timing) {
       c = nullptr;
       return;
     }
     rec.name = name;
+    rec.row0 = row0;
+    rec.rows = rows;
     rec.start = timing_event(c);
     rec.stop = timing_event(c);
     (void)hipEventRecord(rec.start, s);
@@ -120,6 +123,13 @@ struct TimedScope {
   do {                                                                      \
     ::cavs::TimedScope ts_(name, stream);                                   \
     hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);    \
+  } while (0)
+
+// Same, recording the level-major rows [row0, row0 + rows) the launch covers.
+#define CAVS_LAUNCH_ROWS(name, row0, rows, kernel, grid, block, shmem, stream, ...) \
+  do {                                                                            \
+    ::cavs::TimedScope ts_(name, stream, row0, rows);                             \
+    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);          \
   } while (0)
 
 // ---------------------------------------------------------------------------

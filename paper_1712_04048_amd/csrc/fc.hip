@@ -43,16 +43,25 @@ __global__ void __launch_bounds__(256) k_fc_fwd_level(Net n, int off, int M) {
     aq[a] = idx % 8;
     aval[a] = idx < A_N && row0 + arow[a] < rowend;
   }
+  // child rows of this thread's A row, looked up once (slots 0 and 1)
+  const float* crow[A_PER][2];
+#pragma unroll
+  for (int a = 0; a < A_PER; ++a)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      crow[a][k] = nullptr;
+      if (aval[a] && k < N) {
+        const int cp = n.child_pos[(size_t)(row0 + arow[a]) * N + k];
+        if (cp >= 0) crow[a][k] = n.Hs + (size_t)cp * H + 4 * aq[a];
+      }
+    }
   float4 ra[A_PER], rb[B_PER];
   auto gload = [&](int kc) {
     const int k0 = kc * kBK, slot = k0 / H, r0 = k0 % H;
 #pragma unroll
     for (int a = 0; a < A_PER; ++a) {
-      ra[a] = f4zero();
-      if (aval[a]) {
-        const int cp = n.child_pos[(size_t)(row0 + arow[a]) * N + slot];
-        if (cp >= 0) ra[a] = ldg4(n.Hs + (size_t)cp * H + r0 + 4 * aq[a]);
-      }
+      const float* src = slot == 0 ? crow[a][0] : crow[a][1];
+      ra[a] = src ? ldg4(src + r0) : f4zero();
     }
 #pragma unroll
     for (int b = 0; b < B_PER; ++b) {
@@ -208,32 +217,32 @@ __global__ void __launch_bounds__(256) k_fc_bwd_level(Net n, int off, int M) {
 
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH("k_fc_leaf", k_fc_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
+  CAVS_LAUNCH_ROWS("k_fc_leaf", off, M, k_fc_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
 }
 
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
   if (M <= 32)
-    CAVS_LAUNCH("k_fc_fwd_level<16>", (k_fc_fwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
+    CAVS_LAUNCH_ROWS("k_fc_fwd_level<16>", off, M, (k_fc_fwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
                        M);
   else
-    CAVS_LAUNCH("k_fc_fwd_level<64>", (k_fc_fwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
+    CAVS_LAUNCH_ROWS("k_fc_fwd_level<64>", off, M, (k_fc_fwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
                        M);
 }
 
 void fc_bwd_gates(const Net& n, int off, int M, int leaf, float* dX, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH("k_fc_bwd_gates", k_fc_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M,
+  CAVS_LAUNCH_ROWS("k_fc_bwd_gates", off, M, k_fc_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M,
                      leaf, dX);
 }
 
 void fc_bwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
   if (M <= 32)
-    CAVS_LAUNCH("k_fc_bwd_level<16>", (k_fc_bwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
+    CAVS_LAUNCH_ROWS("k_fc_bwd_level<16>", off, M, (k_fc_bwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
                        M);
   else
-    CAVS_LAUNCH("k_fc_bwd_level<64>", (k_fc_bwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
+    CAVS_LAUNCH_ROWS("k_fc_bwd_level<64>", off, M, (k_fc_bwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
                        M);
 }
 

@@ -54,6 +54,18 @@ void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s);
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s);
 void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s);
+// Persistent loop over levels [t0, t1) (forward) or t1-1 .. t0 (backward:
+// gates and products) in one cooperative launch.  `lo` is the device copy of
+// the level offsets, `lo_host` the host copy, `bar` 256 zeroed ints of
+// barrier state.  Returns false (nothing launched) when the path does not
+// apply or the cooperative launch is refused; the caller then falls back to
+// per-level launches.
+bool lstm_fwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,
+                      hipStream_t s);
+bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,
+                      hipStream_t s);
+// First level >= 1 small enough for the persistent loop (T if none).
+int persist_first_level(const Net& n, const int* lo_host, int T);
 // fc.hip
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);
@@ -132,6 +144,7 @@ __device__ __forceinline__ void zero_acc(v4f (&acc)[TM][TN]) {
     for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = v4f{0.f, 0.f, 0.f, 0.f};
 }
 
+__device__ __forceinline__ int cdiv_dev(int a, int b) { return (a + b - 1) / b; }
 __device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 __device__ __forceinline__ float4 ldg4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }

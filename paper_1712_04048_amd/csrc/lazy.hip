@@ -11,7 +11,7 @@ namespace cavs {
 namespace {
 
 constexpr int kLossMaxC = 16;
-constexpr int kMaxSplits = 8;
+constexpr int kMaxSplits = 16;
 
 // ------------------------------------------------------------- pull GEMM
 // P[p, n] = X[pull_pos[p], :] W_x[:, n] for p = pull_list[m]; tile 64 x 64.
@@ -168,129 +168,169 @@ __global__ void __launch_bounds__(256) k_dx_gemm(Net n, int n_pull, int with_f, 
 // ------------------------------------------------ long-K "A^T B" products
 // out[s][m][n] = sum_{q in split s} A(q, m) B(q, n).  The loader supplies
 // 4 consecutive m (or n) of row q; rows outside [0, Q) are never requested.
-struct LdDUiou {
-  static constexpr const char* kName = "k_tn_gemm<LdDUiou>";
-  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
+struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
+  static constexpr const char* kName = "k_tn_gemm<LdDUiou, 64>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDUiou, 128>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";
+  struct Idx {
+    int c0, c1;
+  };
   Net n;
   int off1;
-  __device__ float4 a4(int q, int m) const {
+  __device__ Idx idx(int q) const {
     const int p = off1 + q;
-    float4 s = f4zero();
-    for (int k = 0; k < n.N; ++k) {
-      const int cp = n.child_pos[(size_t)p * n.N + k];
-      if (cp >= 0) s = add4(s, ldg4(n.Hs + (size_t)cp * n.H + m));
-    }
+    return {n.child_pos[(size_t)p * n.N], n.N == 2 ? n.child_pos[(size_t)p * n.N + 1] : -1};
+  }
+  __device__ float4 a4(const Idx& x, int q, int m) const {
+    float4 s = x.c0 >= 0 ? ldg4(n.Hs + (size_t)x.c0 * n.H + m) : f4zero();
+    if (x.c1 >= 0) s = add4(s, ldg4(n.Hs + (size_t)x.c1 * n.H + m));
     return s;
   }
-  __device__ float4 b4(int q, int c) const {
+  __device__ float4 b4(const Idx&, int q, int c) const {
     const int p = off1 + q;
     const int col = (n.N == 2 && c >= n.H) ? c + n.H : c;
     return ldg4(n.dA + (size_t)p * n.GW + col);
   }
 };
 
-struct LdDUf {
-  static constexpr const char* kName = "k_tn_gemm<LdDUf>";
-  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
+struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
+  static constexpr const char* kName = "k_tn_gemm<LdDUf, 64>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDUf, 128>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";
+  struct Idx {
+    int cp;
+  };
   Net n;
   int off1, MI;
-  __device__ float4 a4(int q, int m) const {
+  __device__ Idx idx(int q) const {
     const int k = q >= MI, p = off1 + q - k * MI;
-    const int cp = n.child_pos[(size_t)p * 2 + k];
-    return cp >= 0 ? ldg4(n.Hs + (size_t)cp * n.H + m) : f4zero();
+    return {n.child_pos[(size_t)p * 2 + k]};
   }
-  __device__ float4 b4(int q, int c) const {
+  __device__ float4 a4(const Idx& x, int q, int m) const {
+    return x.cp >= 0 ? ldg4(n.Hs + (size_t)x.cp * n.H + m) : f4zero();
+  }
+  __device__ float4 b4(const Idx&, int q, int c) const {
     const int k = q >= MI, p = off1 + q - k * MI;
     return ldg4(n.dA + (size_t)p * n.GW + (k ? 4 * n.H : n.H) + c);
   }
 };
 
-struct LdDWx {
-  static constexpr const char* kName = "k_tn_gemm<LdDWx>";
-  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
+struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
+  static constexpr const char* kName = "k_tn_gemm<LdDWx, 64>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDWx, 128>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";
+  struct Idx {
+    int p, row;
+  };
   Net n;
   int with_f;
-  __device__ float4 a4(int q, int m) const {
+  __device__ Idx idx(int q) const {
     const int p = n.pull_list[q];
-    return m < n.D ? ldg4(n.X + (size_t)n.pull_pos[p] * n.D + m) : f4zero();
+    return {p, n.pull_pos[p]};
   }
-  __device__ float4 b4(int q, int c) const {
-    const int p = n.pull_list[q];
+  __device__ float4 a4(const Idx& x, int q, int m) const {
+    return m < n.D ? ldg4(n.X + (size_t)x.row * n.D + m) : f4zero();
+  }
+  __device__ float4 b4(const Idx& x, int q, int c) const {
     const int H = n.H;
     const int col = (with_f || c < H) ? c : c + H;
-    const float* row = n.dA + (size_t)p * n.GW;
+    const float* row = n.dA + (size_t)x.p * n.GW;
     float4 v = ldg4(row + col);
     if (n.N == 2 && col >= H && col < 2 * H) v = add4(v, ldg4(row + 3 * H + col));
     return v;
   }
 };
 
-struct LdFCdW {
-  static constexpr const char* kName = "k_tn_gemm<LdFCdW>";
-  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
+struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
+  static constexpr const char* kName = "k_tn_gemm<LdFCdW, 64>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdFCdW, 128>";
+  static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";
+  struct Idx {
+    int cp;
+  };
   Net n;
   int off1, slot;
-  __device__ float4 a4(int q, int m) const {
-    const int p = off1 + q;
-    const int cp = n.child_pos[(size_t)p * n.N + slot];
-    return cp >= 0 ? ldg4(n.Hs + (size_t)cp * n.H + m) : f4zero();
+  __device__ Idx idx(int q) const {
+    return {n.child_pos[(size_t)(off1 + q) * n.N + slot]};
   }
-  __device__ float4 b4(int q, int c) const {
+  __device__ float4 a4(const Idx& x, int q, int m) const {
+    return x.cp >= 0 ? ldg4(n.Hs + (size_t)x.cp * n.H + m) : f4zero();
+  }
+  __device__ float4 b4(const Idx&, int q, int c) const {
     return ldg4(n.dA + (size_t)(off1 + q) * n.H + c);
   }
 };
 
-template <class L>
+template <class L, int BT>
 __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo, int No,
                                                  float* out) {
-  constexpr int BM = 64, BN = 64, LD = 64 + 2;
+  // BT x BT output tile; 2 x 2 wavefronts of (BT/2) x (BT/2); K (= q) chunks
+  // of 32.  The per-row indices (gathers) of chunk c+2 are loaded while the
+  // data of chunk c+1 is loaded and chunk c is multiplied, so no data load
+  // waits on an index load.
+  constexpr int LD = BT + 2, TT = BT / 32, C4 = BT / 4, PER = kBK * C4 / 256;
+  using Idx = typename L::Idx;
   __shared__ float As[kBK * LD];
   __shared__ float Bs[kBK * LD];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int wrow = (w >> 1) * (BT / 2), wcol = (w & 1) * (BT / 2);
+  const int n0 = blockIdx.x * BT, m0 = blockIdx.y * BT, s = blockIdx.z;
   const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
-  float4 ra[2], rb[2];
-  auto gload = [&](int q0) {
+  float4 ra[PER], rb[PER];
+  Idx ix_next[PER];
+  auto load_idx = [&](int q0, Idx (&ix)[PER]) {
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+    for (int a = 0; a < PER; ++a) {
+      const int q = q0 + (tid + 256 * a) / C4;
+      if (q < q_hi) ix[a] = ld.idx(q);
+    }
+  };
+  auto gload = [&](int q0, const Idx (&ix)[PER]) {
+#pragma unroll
+    for (int a = 0; a < PER; ++a) {
+      const int idx = tid + 256 * a, qq = idx / C4, c4 = idx % C4;
       const int q = q0 + qq;
-      ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(q, m0 + 4 * c4) : f4zero();
-      rb[a] = (q < q_hi) ? ld.b4(q, n0 + 4 * c4) : f4zero();
+      ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(ix[a], q, m0 + 4 * c4) : f4zero();
+      rb[a] = (q < q_hi) ? ld.b4(ix[a], q, n0 + 4 * c4) : f4zero();
     }
   };
   auto sstore = [&]() {
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
+    for (int a = 0; a < PER; ++a) {
+      const int idx = tid + 256 * a, qq = idx / C4, c4 = idx % C4;
       st4_scalar(&As[qq * LD + 4 * c4], ra[a]);
       st4_scalar(&Bs[qq * LD + 4 * c4], rb[a]);
     }
   };
-  v4f acc[2][2];
+  v4f acc[TT][TT];
   zero_acc(acc);
-  gload(q_lo);
+  {
+    Idx ix0[PER];
+    load_idx(q_lo, ix0);
+    load_idx(q_lo + kBK, ix_next);
+    gload(q_lo, ix0);
+  }
   for (int q0 = q_lo; q0 < q_hi; q0 += kBK) {
     __syncthreads();
     sstore();
     __syncthreads();
-    if (q0 + kBK < q_hi) gload(q0 + kBK);
-    mfma_chunk<2, 2, false, false, LD, LD>(As, Bs, wrow, wcol, acc);
+    if (q0 + kBK < q_hi) {
+      gload(q0 + kBK, ix_next);
+      load_idx(q0 + 2 * kBK, ix_next);
+    }
+    mfma_chunk<TT, TT, false, false, LD, LD>(As, Bs, wrow, wcol, acc);
   }
   float* o = out + (size_t)s * Mo * No;
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int tm = 0; tm < TT; ++tm)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m0 + wrow + tm * 16 + 4 * gq + i;
       if (m >= Mo) continue;
 #pragma unroll
-      for (int tn = 0; tn < 2; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+      for (int tn = 0; tn < TT; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
     }
 }
-
-
 // ------------------------------------------------------------ bf16 variants
 // Same tiles as the fp32 kernels above; operands are rounded to bf16 while
 // they are staged into LDS (k-contiguous rows), accumulation is fp32.
@@ -453,8 +493,14 @@ __global__ void __launch_bounds__(256) k_tn_gemm_bf(L ld, int Q, int qchunk, int
     for (int a = 0; a < 2; ++a) {
       const int idx = tid + 256 * a, qq = idx / 16, c4 = idx % 16;
       const int q = q0 + qq;
-      ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(q, m0 + 4 * c4) : f4zero();
-      rb[a] = (q < q_hi) ? ld.b4(q, n0 + 4 * c4) : f4zero();
+      if (q < q_hi) {
+        const typename L::Idx ix = ld.idx(q);
+        ra[a] = m0 + 4 * c4 < Mo ? ld.a4(ix, q, m0 + 4 * c4) : f4zero();
+        rb[a] = ld.b4(ix, q, n0 + 4 * c4);
+      } else {
+        ra[a] = f4zero();
+        rb[a] = f4zero();
+      }
     }
   };
   auto sstore = [&]() {
@@ -509,8 +555,9 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
                        (const float*)part, 0, Mo, No, dst, ldd, col_off, gap_start, gap);
     return;
   }
-  const int tiles = (No / 64) * cdiv(Mo, 64);
-  int S = cdiv(1024, tiles);
+  const int BT = (!ld.n.bf && No % 128 == 0) ? 128 : 64;
+  const int tiles = (No / BT) * cdiv(Mo, BT);
+  int S = cdiv(512, tiles);
   S = S < 1 ? 1 : S;
   S = S > kMaxSplits ? kMaxSplits : S;
   int maxS = cdiv(Q, 256);
@@ -521,9 +568,12 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
   if (ld.n.bf)
     CAVS_LAUNCH(L::kNameBf, k_tn_gemm_bf<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld,
                 Q, qchunk, Mo, No, part);
+  else if (BT == 128)
+    CAVS_LAUNCH(L::kName128, (k_tn_gemm<L, 128>), dim3(No / 128, cdiv(Mo, 128), S), dim3(256), 0,
+                st, ld, Q, qchunk, Mo, No, part);
   else
-  CAVS_LAUNCH(L::kName, k_tn_gemm<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld, Q,
-                     qchunk, Mo, No, part);
+    CAVS_LAUNCH(L::kName, (k_tn_gemm<L, 64>), dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st,
+                ld, Q, qchunk, Mo, No, part);
   CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
                      (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
 }

@@ -17,6 +17,10 @@
 // GEMM kernel computes dL/dh_k = dA_iou U_iou^T + dA_fk U_f^T and scatters it
 // to child k.  Every vertex has one parent, so each child row is written by
 // exactly one thread: plain stores, no atomics.
+#include <stdlib.h>
+
+#include <map>
+
 #include "kernels.h"
 
 namespace cavs {
@@ -214,11 +218,9 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
 }
 
 // ----------------------------------------------------------------- backward
-__global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
+// dA and the dc scatter for position p, unit j.
+__device__ __forceinline__ void lstm_bwd_gates_elem(const Net& n, int p, int j) {
   const int H = n.H;
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)M * H) return;
-  const int p = off + (int)(idx / H), j = (int)(idx % H);
   const int par = n.parent_pos[p];
   float gh = par >= 0 ? n.dHp[(size_t)p * H + j] : 0.f;
   float gcin = par >= 0 ? n.dCp[(size_t)p * H + j] : 0.f;
@@ -257,6 +259,12 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
   da[j] = d_i;
   da[2 * H + j] = d_o;
   da[3 * H + j] = d_u;
+}
+
+__global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)M * n.H) return;
+  lstm_bwd_gates_elem(n, off + (int)(idx / n.H), (int)(idx % n.H));
 }
 
 // dL/dh_k for every vertex of the level: tile BM positions x 64 hidden units.
@@ -589,22 +597,402 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_level_bf(Net n, int off, int M
                               acc_f1[tm][tn][i]);
     }
 }
+
+// --------------------------------------------------- split-K level kernels
+// For levels too small to fill the chip with the tiles above: a workgroup
+// owns 16 positions x 16 units (forward) or 16 positions x 16 columns
+// (backward); wavefront w accumulates the w-th quarter of the contraction.
+// MFMA fragments are loaded straight from global memory into registers: in
+// the permuted-K order lane group g needs k = 8g .. 8g+7 of its A row (two
+// float4) and of its B column.  The four partial sums are reduced in LDS in
+// a fixed order (deterministic) and the epilogue is shared with the tiled
+// kernels.  BF selects bf16 operands (one 16x16x32 MFMA per 32-deep chunk)
+// instead of fp32 (eight 16x16x4 steps).
+template <bool BF>
+__device__ __forceinline__ v4f mfma_chunk8(const float (&a)[8], const float (&b)[8], v4f acc) {
+  if constexpr (BF) {
+    bf16x8 av, bv;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const u16 ua = f2bf(a[s]), ub = f2bf(b[s]);
+      av[s] = __builtin_bit_cast(__bf16, ua);
+      bv[s] = __builtin_bit_cast(__bf16, ub);
+    }
+    return mfma_bf16_16x16x32(av, bv, acc);
+  } else {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) acc = mfma_f32_16x16x4(a[s], b[s], acc);
+    return acc;
+  }
+}
+
+__device__ __forceinline__ void ld8(const float* p, float (&v)[8]) {
+  const float4 x = ldg4(p), y = ldg4(p + 4);
+  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+}
+
+// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch), and each
+// XCD has its own L2.  Tiles are mapped so that XCD x only touches unit tiles
+// x, x+8, ...: each L2 then holds 1/8 of the weight columns instead of all.
+__device__ __forceinline__ void xcd_tile(int n_unit_tiles, int& row_tile, int& unit_tile) {
+  const int bid = blockIdx.x, xcd = bid & 7, local = bid >> 3, per = n_unit_tiles >> 3;
+  unit_tile = xcd + 8 * (local % per);
+  row_tile = local / per;
+}
+
+template <int NCH, int TR>
+struct FwdRed {
+  float v[4][TR][3 + NCH][4][64];
+};
+
+// One 16*TR-position x 16-unit forward tile (row tile rt, unit tile ut).
+template <int NCH, bool BF, int TR>
+__device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
+                                                 FwdRed<NCH, TR>& R) {
+  constexpr int NACC = 3 + NCH;
+  auto& red = R.v;
+  const int H = n.H, H4 = 4 * H;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int row0 = off + rt * 16 * TR, rowend = off + M;
+  const int u0 = ut * 16;
+  const float* ap[TR][NCH];               // A rows of this lane: row0 + 16 tr + r
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr) {
+    const int pa = row0 + 16 * tr + r;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      ap[tr][c] = nullptr;
+      if (pa < rowend) {
+        const int cp = n.child_pos[(size_t)pa * NCH + c];
+        if (cp >= 0) ap[tr][c] = n.Hs + (size_t)cp * H;
+      }
+    }
+  }
+  const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
+  const int kq = H / 4, kbeg = w * kq, kend = kbeg + kq;
+  v4f acc[TR][NACC];
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  struct Frag {
+    float a[TR][NCH][8];
+    float b[4][8];
+  };
+  auto load = [&](int k0, Frag& f) {
+    const int kk = k0 + 8 * gq;
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        if (ap[tr][c]) ld8(ap[tr][c] + kk, f.a[tr][c]);
+        else {
+#pragma unroll
+          for (int s = 0; s < 8; ++s) f.a[tr][c][s] = 0.f;
+        }
+      }
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
+  };
+  auto compute = [&](const Frag& f) {
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr) {
+      float ah[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        ah[s] = NCH == 2 ? f.a[tr][0][s] + f.a[tr][NCH - 1][s] : f.a[tr][0][s];
+      acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
+      acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
+      acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
+      acc[tr][3] = mfma_chunk8<BF>(f.a[tr][0], f.b[G_F], acc[tr][3]);
+      if constexpr (NCH == 2) acc[tr][4] = mfma_chunk8<BF>(f.a[tr][NCH - 1], f.b[G_F], acc[tr][4]);
+    }
+  };
+  // two register buffers: loads of the next chunk overlap the current MFMAs
+  Frag fa, fb;
+  load(kbeg, fa);
+  for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
+    load(k0 + kBK, fb);
+    compute(fa);
+    if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
+    compute(fb);
+  }
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int g = 0; g < NACC; ++g)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
+  __syncthreads();
+  // wave w finishes element i = w of every lane: rows 16 tr + 4 gq + w, unit u0 + r
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr) {
+    float z[NACC];
+#pragma unroll
+    for (int g = 0; g < NACC; ++g)
+      z[g] = ((red[0][tr][g][w][lane] + red[1][tr][g][w][lane]) + red[2][tr][g][w][lane]) +
+             red[3][tr][g][w][lane];
+    const int p = row0 + 16 * tr + 4 * gq + w;
+    if (p < rowend)
+      lstm_fwd_epilogue<NCH>(n, p, u0 + r, z[0], z[1], z[2], z[3], NCH == 2 ? z[NACC - 1] : 0.f);
+  }
+}
+
+template <int NCH, bool BF, int TR>
+__global__ void __launch_bounds__(256) k_lstm_fwd_level_sk(Net n, int off, int M) {
+  __shared__ FwdRed<NCH, TR> red;
+  int rt, ut;
+  xcd_tile(n.H / 16, rt, ut);
+  lstm_fwd_sk_tile<NCH, BF, TR>(n, off, M, rt, ut, red);
+}
+
+template <int NCH, int TR>
+struct BwdRed {
+  float v[4][TR][NCH == 2 ? 3 : 1][4][64];
+};
+
+// One 16*TR-position x 16-column backward tile (row tile rt, column tile ut).
+template <int NCH, bool BF, int TR>
+__device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
+                                                 BwdRed<NCH, TR>& R) {
+  constexpr int NACC = 1 + (NCH == 2 ? 2 : 0);
+  auto& red = R.v;
+  const int H = n.H, H4 = 4 * H, GW = n.GW;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int row0 = off + rt * 16 * TR, rowend = off + M;
+  const int n0 = ut * 16;
+  const float* da[TR];
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr) {
+    const int pa = row0 + 16 * tr + r;
+    da[tr] = pa < rowend ? n.dA + (size_t)pa * GW : nullptr;
+  }
+  const float* ub = n.U + (size_t)(n0 + r) * H4;   // row n0 + r of U: B^T[n][k]
+  v4f acc[TR][NACC];
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
+  auto zero8 = [](float (&v)[8]) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) v[s] = 0.f;
+  };
+  // phase 1: i|o|u columns (all four blocks with one child slot)
+  struct F1 {
+    float a[TR][8], b[8];
+  };
+  const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / 4;
+  auto load1 = [&](int c0, F1& f) {
+    const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr) {
+      if (da[tr]) ld8(da[tr] + col, f.a[tr]);
+      else zero8(f.a[tr]);
+    }
+    ld8(ub + col, f.b);
+  };
+  auto comp1 = [&](const F1& f) {
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
+  };
+  F1 x, y;
+  load1(w * q1, x);
+  for (int c0 = w * q1; c0 < (w + 1) * q1; c0 += 2 * kBK) {
+    load1(c0 + kBK, y);
+    comp1(x);
+    if (c0 + 2 * kBK < (w + 1) * q1) load1(c0 + 2 * kBK, x);
+    comp1(y);
+  }
+  if constexpr (NCH == 2) {
+    struct F2 {
+      float a0[TR][8], a1[TR][8], b[8];
+    };
+    const int q2 = H / 4;
+    auto load2 = [&](int c0, F2& f) {
+      const int col = c0 + 8 * gq;
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) {
+        if (da[tr]) {
+          ld8(da[tr] + H + col, f.a0[tr]);
+          ld8(da[tr] + 4 * H + col, f.a1[tr]);
+        } else {
+          zero8(f.a0[tr]);
+          zero8(f.a1[tr]);
+        }
+      }
+      ld8(ub + H + col, f.b);
+    };
+    auto comp2 = [&](const F2& f) {
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) {
+        acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
+        acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
+      }
+    };
+    F2 u, v;
+    load2(w * q2, u);
+    for (int c0 = w * q2; c0 < (w + 1) * q2; c0 += 2 * kBK) {
+      load2(c0 + kBK, v);
+      comp2(u);
+      if (c0 + 2 * kBK < (w + 1) * q2) load2(c0 + 2 * kBK, u);
+      comp2(v);
+    }
+  }
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int g = 0; g < NACC; ++g)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
+  __syncthreads();
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr) {
+    float z[NACC];
+#pragma unroll
+    for (int g = 0; g < NACC; ++g)
+      z[g] = ((red[0][tr][g][w][lane] + red[1][tr][g][w][lane]) + red[2][tr][g][w][lane]) +
+             red[3][tr][g][w][lane];
+    const int p = row0 + 16 * tr + 4 * gq + w;
+    if (p < rowend)
+      lstm_bwd_scatter<NCH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f, NCH == 2 ? z[NACC - 1] : 0.f);
+  }
+}
+
+template <int NCH, bool BF, int TR>
+__global__ void __launch_bounds__(256) k_lstm_bwd_level_sk(Net n, int off, int M) {
+  __shared__ BwdRed<NCH, TR> red;
+  int rt, ut;
+  xcd_tile(n.H / 16, rt, ut);
+  lstm_bwd_sk_tile<NCH, BF, TR>(n, off, M, rt, ut, red);
+}
+
+// ----------------------------------------------- persistent small-level loop
+// Levels shrink towards the roots (each vertex of level t+1 has its own child
+// on level t), so the small levels form a suffix of the schedule.  One
+// cooperative launch runs that whole suffix: tiles of a level are spread over
+// the grid, and a grid barrier separates dependent levels, instead of one or
+// two kernel launches per level.  Level offsets are read on the device.
+//
+// Grid barrier: counters only grow (zeroed before the launch).  Barrier e
+// completes when the root counter reaches (e+1) * groups; the last arrival
+// publishes gen = e+1.  Waiting is bounded: after kBarrierSpin polls the
+// barrier records an error flag and returns rather than hang.
+constexpr int kBarrierSpin = 1 << 24;
+
+struct GridBar {
+  int* cnt;   // [1 + groups]: root, then one counter per group of 16 workgroups
+  int* gen;
+  int* err;
+};
+
+__device__ __forceinline__ void grid_sync(const GridBar& b, int& epoch) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int G = gridDim.x, grp = blockIdx.x >> 4;
+    const int gsize = min(16, G - (grp << 4)), ngroups = (G + 15) >> 4;
+    __threadfence();   // release this workgroup's writes
+    const int old = atomicAdd(&b.cnt[1 + grp], 1);
+    bool release = false;
+    if (old == epoch * gsize + gsize - 1) {
+      const int o2 = atomicAdd(&b.cnt[0], 1);
+      release = o2 == epoch * ngroups + ngroups - 1;
+    }
+    if (release) {
+      __threadfence();
+      atomicAdd(b.gen, 1);
+    } else {
+      int it = 0;
+      while (__hip_atomic_load(b.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= epoch) {
+        if (++it > kBarrierSpin) {
+          atomicOr(b.err, 1);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    __threadfence();   // acquire
+  }
+  ++epoch;
+  __syncthreads();
+}
+
+template <int NCH, bool BF>
+__global__ void __launch_bounds__(256) k_lstm_fwd_persist(Net n, const int* lo, int t0, int t1,
+                                                          GridBar bar) {
+  __shared__ FwdRed<NCH, 1> red;
+  const int ut = n.H / 16;
+  int epoch = 0;
+  for (int t = t0; t < t1; ++t) {
+    const int off = lo[t], M = lo[t + 1] - off;
+    const int tiles = cdiv_dev(M, 16) * ut;
+    for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+      lstm_fwd_sk_tile<NCH, BF, 1>(n, off, M, tile / ut, tile % ut, red);
+      __syncthreads();
+    }
+    if (t + 1 < t1) grid_sync(bar, epoch);
+  }
+}
+
+// Levels t1-1 down to t0 (all with children): dA + dc scatter, barrier, the
+// dh_k products, barrier.
+template <int NCH, bool BF>
+__global__ void __launch_bounds__(256) k_lstm_bwd_persist(Net n, const int* lo, int t0, int t1,
+                                                          GridBar bar) {
+  __shared__ BwdRed<NCH, 1> red;
+  const int ut = n.H / 16, H = n.H;
+  int epoch = 0;
+  for (int t = t1 - 1; t >= t0; --t) {
+    const int off = lo[t], M = lo[t + 1] - off;
+    const long elems = (long)M * H;
+    for (long idx = (long)blockIdx.x * 256 + threadIdx.x; idx < elems; idx += (long)gridDim.x * 256)
+      lstm_bwd_gates_elem(n, off + (int)(idx / H), (int)(idx % H));
+    grid_sync(bar, epoch);
+    const int tiles = cdiv_dev(M, 16) * ut;
+    for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+      lstm_bwd_sk_tile<NCH, BF, 1>(n, off, M, tile / ut, tile % ut, red);
+      __syncthreads();
+    }
+    if (t > t0) grid_sync(bar, epoch);
+  }
+}
 }  // namespace
 
 void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH("k_lstm_leaf", k_lstm_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
+  CAVS_LAUNCH_ROWS("k_lstm_leaf", off, M, k_lstm_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
 }
 
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
+  if (n.H % 256 == 0 && M < 1024) {
+    // two 16-row tiles per wave once that still gives >= 2 workgroups per CU
+    const int ut = n.H / 16;
+    const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
+    dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
+#define CAVS_FWD_SK(NCH, BF, TR)                                                               \
+  CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ">", off, M,                   \
+                   (k_lstm_fwd_level_sk<NCH, BF, TR>), g, dim3(256), 0, s, n, off, M)
+    if (n.N == 2) {
+      if (n.bf) { if (tr2) CAVS_FWD_SK(2, true, 2); else CAVS_FWD_SK(2, true, 1); }
+      else { if (tr2) CAVS_FWD_SK(2, false, 2); else CAVS_FWD_SK(2, false, 1); }
+    } else {
+      if (n.bf) { if (tr2) CAVS_FWD_SK(1, true, 2); else CAVS_FWD_SK(1, true, 1); }
+      else { if (tr2) CAVS_FWD_SK(1, false, 2); else CAVS_FWD_SK(1, false, 1); }
+    }
+#undef CAVS_FWD_SK
+    return;
+  }
   const bool small = M <= 32;
   dim3 grid = small ? dim3(cdiv(M, 16), n.H / 64) : dim3(cdiv(M, 64), n.H / 16);
 #define CAVS_FWD(NCH, BM)                                                                      \
   do {                                                                                         \
-    if (n.bf) CAVS_LAUNCH("k_lstm_fwd_level_bf<" #NCH ", " #BM ">", (k_lstm_fwd_level_bf<NCH, BM>), \
+    if (n.bf) CAVS_LAUNCH_ROWS("k_lstm_fwd_level_bf<" #NCH ", " #BM ">", off, M, (k_lstm_fwd_level_bf<NCH, BM>), \
                           grid, dim3(256), 0, s, n, off, M);                                   \
-    else CAVS_LAUNCH("k_lstm_fwd_level<" #NCH ", " #BM ">", (k_lstm_fwd_level<NCH, BM>), grid,    \
+    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level<" #NCH ", " #BM ">", off, M, (k_lstm_fwd_level<NCH, BM>), grid,    \
                      dim3(256), 0, s, n, off, M);                                              \
   } while (0)
   if (small) {
@@ -619,19 +1007,36 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH("k_lstm_bwd_gates", k_lstm_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off,
+  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates", off, M, k_lstm_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off,
                      M);
 }
 
 void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
+  if (n.H % 256 == 0) {
+    const int ut = n.H / 16;
+    const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
+    dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
+#define CAVS_BWD_SK(NCH, BF, TR)                                                               \
+  CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ">", off, M,                   \
+                   (k_lstm_bwd_level_sk<NCH, BF, TR>), g, dim3(256), 0, s, n, off, M)
+    if (n.N == 2) {
+      if (n.bf) { if (tr2) CAVS_BWD_SK(2, true, 2); else CAVS_BWD_SK(2, true, 1); }
+      else { if (tr2) CAVS_BWD_SK(2, false, 2); else CAVS_BWD_SK(2, false, 1); }
+    } else {
+      if (n.bf) { if (tr2) CAVS_BWD_SK(1, true, 2); else CAVS_BWD_SK(1, true, 1); }
+      else { if (tr2) CAVS_BWD_SK(1, false, 2); else CAVS_BWD_SK(1, false, 1); }
+    }
+#undef CAVS_BWD_SK
+    return;
+  }
   const bool small = M <= 32;
   dim3 grid(cdiv(M, small ? 16 : 64), n.H / 64);
 #define CAVS_BWD(NCH, BM)                                                                      \
   do {                                                                                         \
-    if (n.bf) CAVS_LAUNCH("k_lstm_bwd_level_bf<" #NCH ", " #BM ">", (k_lstm_bwd_level_bf<NCH, BM>), \
+    if (n.bf) CAVS_LAUNCH_ROWS("k_lstm_bwd_level_bf<" #NCH ", " #BM ">", off, M, (k_lstm_bwd_level_bf<NCH, BM>), \
                           grid, dim3(256), 0, s, n, off, M);                                   \
-    else CAVS_LAUNCH("k_lstm_bwd_level<" #NCH ", " #BM ">", (k_lstm_bwd_level<NCH, BM>), grid,    \
+    else CAVS_LAUNCH_ROWS("k_lstm_bwd_level<" #NCH ", " #BM ">", off, M, (k_lstm_bwd_level<NCH, BM>), grid,    \
                      dim3(256), 0, s, n, off, M);                                              \
   } while (0)
   if (small) {
@@ -642,6 +1047,84 @@ void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
     else CAVS_BWD(1, 64);
   }
 #undef CAVS_BWD
+}
+
+namespace {
+
+// Levels of at most this many positions run in the persistent loop.
+constexpr int kPersistRows = 256;
+
+// The persistent loop is an opt-in ablation (CAVS_PERSIST=1): measured on
+// MI355X, one grid barrier with the agent-scope fences it needs costs
+// 2.7-17 us (32-512 workgroups) against 2.4 us for a back-to-back kernel
+// launch, so per-level launches are the default.
+bool persist_enabled() {
+  const char* e = getenv("CAVS_PERSIST");
+  return e && e[0] && e[0] != '0';
+}
+
+int coresident_blocks(const void* fn) {
+  static std::map<const void*, int> cache;
+  auto it = cache.find(fn);
+  if (it != cache.end()) return it->second;
+  int dev = 0, ncu = 0, per = 0, coop = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, 256, 0) != hipSuccess || !coop)
+    per = 0;
+  const int v = per * ncu;
+  cache[fn] = v;
+  return v;
+}
+
+bool launch_persist(const char* name, const void* fn, const Net& n, const int* lo,
+                    const int* lo_host, int t0, int t1, int* bar, int max_rows, hipStream_t s) {
+  const int tiles = cdiv(max_rows, 16) * (n.H / 16);
+  int G = coresident_blocks(fn);
+  if (G > 512) G = 512;
+  if (G > tiles) G = tiles;
+  if (G <= 0) return false;
+  GridBar gb{bar, bar + 64, bar + 65};
+  void* args[] = {(void*)&n, (void*)&lo, (void*)&t0, (void*)&t1, (void*)&gb};
+  if (hipMemsetAsync(bar, 0, 256 * sizeof(int), s) != hipSuccess) return false;
+  TimedScope ts(name, s, lo_host[t0], lo_host[t1] - lo_host[t0]);
+  return hipLaunchCooperativeKernel(fn, dim3(G), dim3(256), args, 0, s) == hipSuccess;
+}
+
+}  // namespace
+
+int persist_first_level(const Net& n, const int* lo_host, int T) {
+  if (!persist_enabled() || n.H % 256 != 0) return T;
+  for (int t = 1; t < T; ++t)
+    if (lo_host[t + 1] - lo_host[t] <= kPersistRows) return t;
+  return T;
+}
+
+bool lstm_fwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,
+                      hipStream_t s) {
+  if (t0 >= t1) return true;
+  const int maxM = lo_host[t0 + 1] - lo_host[t0];
+#define CAVS_FP(NCH, BF)                                                                   \
+  launch_persist("k_lstm_fwd_persist<" #NCH ", " #BF ">",                                  \
+                 reinterpret_cast<const void*>(&k_lstm_fwd_persist<NCH, BF>), n, lo, lo_host, \
+                 t0, t1, bar, maxM, s)
+  if (n.N == 2) return n.bf ? CAVS_FP(2, true) : CAVS_FP(2, false);
+  return n.bf ? CAVS_FP(1, true) : CAVS_FP(1, false);
+#undef CAVS_FP
+}
+
+bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,
+                      hipStream_t s) {
+  if (t0 >= t1) return true;
+  const int maxM = lo_host[t0 + 1] - lo_host[t0];
+#define CAVS_BP(NCH, BF)                                                                   \
+  launch_persist("k_lstm_bwd_persist<" #NCH ", " #BF ">",                                  \
+                 reinterpret_cast<const void*>(&k_lstm_bwd_persist<NCH, BF>), n, lo, lo_host, \
+                 t0, t1, bar, maxM, s)
+  if (n.N == 2) return n.bf ? CAVS_BP(2, true) : CAVS_BP(2, false);
+  return n.bf ? CAVS_BP(1, true) : CAVS_BP(1, false);
+#undef CAVS_BP
 }
 
 }  // namespace cavs

@@ -124,28 +124,28 @@ __global__ void k_check_links(int V, int N, int n_x, const int* __restrict__ chi
 // -------------------------------------------------------------------------
 // 2. levels: leaf-to-root walks with arrival counters
 // -------------------------------------------------------------------------
-__global__ void k_levels(int V, int N, const int* __restrict__ child,
-                         const int* __restrict__ parent, const int* __restrict__ nchild,
-                         int* arrive, int* level) {
+// arrive[p] packs the number of children that have arrived at p (low 32
+// bits) with the sum of their levels (high 32 bits).  With at most two child
+// slots, the child that arrives second reads the first one's level from the
+// value its own atomic returns, so the walk needs no other communication
+// (and no memory fences).  The count never wraps, so only the arrival that
+// completes p continues: each vertex is passed by at most one walker.
+__global__ void k_levels(int V, int N, const int* __restrict__ parent,
+                         const int* __restrict__ nchild, unsigned long long* arrive, int* level) {
   int v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v >= V || nchild[v] != 0) return;
-  st_relaxed_int(&level[v], 0);
-  int cur = v;
-  // Each vertex is passed by at most one walker (only the arrival that makes
-  // the counter equal its child count continues), so V steps bound any walk.
+  level[v] = 0;
+  int cur = v, lev = 0;
   for (int step = 0; step < V; ++step) {
-    int p = parent[cur];
+    const int p = parent[cur];
     if (p < 0 || p >= V) break;
-    __threadfence();
-    int old = atomicAdd(&arrive[p], 1);
-    if (old + 1 != nchild[p]) break;
-    __threadfence();
-    int m = -1;
-    for (int k = 0; k < N; ++k) {
-      int c = child[(size_t)p * N + k];
-      if (c >= 0 && c < V) m = max(m, ld_acquire_int(&level[c]));
-    }
-    st_relaxed_int(&level[p], m + 1);
+    const unsigned long long old =
+        atomicAdd(&arrive[p], 1ull | ((unsigned long long)(unsigned)lev << 32));
+    const unsigned cnt = (unsigned)(old & 0xFFFFFFFFull);
+    if ((int)cnt + 1 != nchild[p]) break;
+    if (cnt == 1) lev = max(lev, (int)(old >> 32));   // the other child's level
+    lev += 1;
+    level[p] = lev;
     cur = p;
   }
 }
@@ -153,7 +153,13 @@ __global__ void k_levels(int V, int N, const int* __restrict__ child,
 // -------------------------------------------------------------------------
 // 3. per-level histogram, T, cycle detection, and the offsets scan
 // -------------------------------------------------------------------------
-__global__ void k_level_hist(int V, const int* __restrict__ level, int* hist, int* flags) {
+constexpr int kHistLds = 256;   // levels below this are counted in LDS first
+
+__global__ void __launch_bounds__(256) k_level_hist(int V, const int* __restrict__ level,
+                                                    int* hist, int* flags) {
+  __shared__ int h[kHistLds];
+  h[threadIdx.x] = 0;
+  __syncthreads();
   int v = blockIdx.x * blockDim.x + threadIdx.x;
   int tmax = 0, cyc = 0;
   if (v < V) {
@@ -161,7 +167,8 @@ __global__ void k_level_hist(int V, const int* __restrict__ level, int* hist, in
     if (l < 0 || l >= V) {
       cyc = 1;
     } else {
-      atomicAdd(&hist[l], 1);
+      if (l < kHistLds) atomicAdd(&h[l], 1);
+      else atomicAdd(&hist[l], 1);
       tmax = l + 1;
     }
   }
@@ -172,6 +179,8 @@ __global__ void k_level_hist(int V, const int* __restrict__ level, int* hist, in
     if (tmax) atomicMax(&flags[F_T], tmax);
     if (cyc) atomicOr(&flags[F_CYCLE], 1);
   }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
 }
 
 // Single-block exclusive scan of n ints (src may equal dst).  If n_dev is
@@ -345,9 +354,9 @@ Layout layout(int32_t V, int32_t N, int32_t n_x) {
   L.ntiles = cdiv(V > 0 ? V : 1, kTile);
   L.flags = take(F_COUNT);
   L.ref_cnt = take((size_t)V + 1);
-  L.arrive = take((size_t)V + 1);
+  L.arrive = take(2 * ((size_t)V + 1));   // 64-bit words
   L.pull_cnt = take((size_t)n_x + 1);
-  L.hist = take((size_t)V + 2);
+  L.hist = take((size_t)(V + 2 > 256 ? V + 2 : 256));
   L.zero_end = o;
   L.nchild = take((size_t)V + 1);
   L.keysA = take((size_t)V + 1);
@@ -402,7 +411,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   char* base = (char*)ws;
   int* flags = (int*)(base + L.flags);
   int* ref_cnt = (int*)(base + L.ref_cnt);
-  int* arrive = (int*)(base + L.arrive);
+  unsigned long long* arrive = (unsigned long long*)(base + L.arrive);
   int* pull_cnt = (int*)(base + L.pull_cnt);
   int* hist = (int*)(base + L.hist);
   int* nchild = (int*)(base + L.nchild);
@@ -432,7 +441,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
                        g->parent, g->pull_idx, g->push_idx, ref_cnt, pull_cnt, nchild, flags);
     CAVS_LAUNCH("k_check_links", k_check_links, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256), 0, st, V, N,
                        n_x, g->child, g->parent, ref_cnt, pull_cnt, flags);
-    CAVS_LAUNCH("k_levels", k_levels, dim3(nb), dim3(256), 0, st, V, N, g->child, g->parent, nchild,
+    CAVS_LAUNCH("k_levels", k_levels, dim3(nb), dim3(256), 0, st, V, N, g->parent, nchild,
                        arrive, s->level);
     CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
     CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,

@@ -47,13 +47,13 @@ PROBE = r"""
 #include "cavs.h"
 #define F(S, m) printf(#S "." #m " %zu\n", offsetof(S, m));
 int main(void) {
-  printf("cavs_graphs %zu\ncavs_sched %zu\ncavs_params %zu\ncavs_inputs %zu\ncavs_grads %zu\n",
+  printf("cavs_graphs %zu\ncavs_sched %zu\ncavs_params %zu\ncavs_inputs %zu\ncavs_grads %zu\ncavs_launch_time %zu\n",
          sizeof(cavs_graphs), sizeof(cavs_sched), sizeof(cavs_params), sizeof(cavs_inputs),
-         sizeof(cavs_grads));
+         sizeof(cavs_grads), sizeof(cavs_launch_time));
   F(cavs_graphs, child) F(cavs_graphs, push_idx)
   F(cavs_sched, n_inner_input) F(cavs_sched, level) F(cavs_sched, level_offsets_host)
   F(cavs_params, C) F(cavs_params, Wx) F(cavs_params, bs)
-  F(cavs_inputs, n_y) F(cavs_grads, dX)
+  F(cavs_inputs, n_y) F(cavs_grads, dX) F(cavs_launch_time, rows) F(cavs_launch_time, ms)
   return 0;
 }
 """
@@ -69,7 +69,7 @@ def test_struct_layouts_match_header():
     vals = dict(line.split() for line in out.strip().splitlines())
     for cname, cls in [("cavs_graphs", B.cavs_graphs), ("cavs_sched", B.cavs_sched),
                        ("cavs_params", B.cavs_params), ("cavs_inputs", B.cavs_inputs),
-                       ("cavs_grads", B.cavs_grads)]:
+                       ("cavs_grads", B.cavs_grads), ("cavs_launch_time", B.cavs_launch_time)]:
         assert int(vals[cname]) == ct.sizeof(cls), cname
     for key, v in vals.items():
         if "." in key:

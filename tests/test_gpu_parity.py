@@ -305,3 +305,13 @@ def test_full_size_bf16_states_on_sampled_graphs(ctx):
     assert np.all(got["dWx"][:, wl.H:2 * wl.H] == 0.0)
     for k in ("dWx", "dU", "db", "dWs", "dbs", "dX"):
         assert np.all(np.isfinite(got[k])), k
+
+
+def test_persistent_level_loop_opt_in(ctx, monkeypatch):
+    """The opt-in persistent small-level loop (one cooperative launch with
+    grid barriers) gives the same results as per-level launches."""
+    monkeypatch.setenv("CAVS_PERSIST", "1")
+    _parity(ctx, W.config_treelstm_sst(1, K=16), label="persistent_fp32")
+    wl = W.config_treelstm_deep_bf16(1, K=4, D=300, H=1024, lo=8, hi=40)
+    _parity_bf16(ctx, wl, "persistent_bf16")
+    monkeypatch.delenv("CAVS_PERSIST")
