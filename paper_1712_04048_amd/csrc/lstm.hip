@@ -113,10 +113,13 @@ __device__ __forceinline__ void lstm_bwd_scatter(const Net& n, int p, int col, f
 }
 
 // Tile: BM positions x BHU hidden units; 4 wavefronts arranged WR x WU, each
-// owning 16 positions x 16 units and all (3 + NCH) gate accumulators for them.
-template <int NCH, int BM>
+// owning TR = BM / (16 WR) row tiles of 16 positions x 16 units and all
+// (3 + NCH) gate accumulators for them (B fragments are reused across the
+// TR row tiles).  With XCD set, the 1D grid is mapped so that each XCD
+// touches 1/8 of the unit tiles (see xcd_tile).
+template <int NCH, int BM, int WR, bool XCD>
 __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
-  constexpr int WR = BM / 16, WU = 4 / WR, BHU = 16 * WU;
+  constexpr int WU = 4 / WR, BHU = 16 * WU, TR = BM / (16 * WR);
   constexpr int LDA = kBK + 4;
   constexpr int LDB = BHU + 2;
   constexpr int A_N = BM * NCH * (kBK / 4);          // float4 per chunk
@@ -124,6 +127,7 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
   constexpr int B_ROW4 = BHU / 4;                    // float4 per (gate, k) row
   constexpr int B_N = 4 * kBK * B_ROW4;
   constexpr int B_PER = B_N / 256;
+  constexpr int NACC = 3 + NCH;
   static_assert(B_N % 256 == 0, "B tile must split evenly");
   __shared__ __attribute__((aligned(16))) float As[NCH][BM * LDA];
   __shared__ float Bs[4][kBK * LDB];
@@ -131,9 +135,18 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
   const int H = n.H, H4 = 4 * H;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int wr = w % WR, wu = w / WR;
-  const int row0 = off + blockIdx.x * BM;
+  int rt, utile;
+  if constexpr (XCD) {
+    const int nut = H / BHU, bid = blockIdx.x, xcd = bid & 7, local = bid >> 3, per = nut >> 3;
+    utile = xcd + 8 * (local % per);
+    rt = local / per;
+  } else {
+    rt = blockIdx.x;
+    utile = blockIdx.y;
+  }
+  const int row0 = off + rt * BM;
   const int rowend = off + M;
-  const int u0 = blockIdx.y * BHU;
+  const int u0 = utile * BHU;
 
   const float* asrc[A_PER];
   int adst[A_PER];
@@ -179,7 +192,11 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
     for (int bq = 0; bq < B_PER; ++bq) st4_scalar(Bs_flat + bdst[bq], rb[bq]);
   };
 
-  v4f acc_i = {0.f, 0.f, 0.f, 0.f}, acc_o = acc_i, acc_u = acc_i, acc_f0 = acc_i, acc_f1 = acc_i;
+  v4f acc[TR][NACC];
+#pragma unroll
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
   gload(0);
   for (int k0 = 0; k0 < H; k0 += kBK) {
     __syncthreads();
@@ -188,22 +205,27 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
     if (k0 + kBK < H) gload(k0 + kBK);
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      float a0[4], a1[4], bi[4], bf[4], bo[4], bu[4];
-      load_frag4<true, LDA>(As[0], wr * 16 + r, gq, half, a0);
-      if constexpr (NCH == 2) load_frag4<true, LDA>(As[NCH - 1], wr * 16 + r, gq, half, a1);
+      float bi[4], bf[4], bo[4], bu[4];
       load_frag4<false, LDB>(Bs[G_I], wu * 16 + r, gq, half, bi);
       load_frag4<false, LDB>(Bs[G_F], wu * 16 + r, gq, half, bf);
       load_frag4<false, LDB>(Bs[G_O], wu * 16 + r, gq, half, bo);
       load_frag4<false, LDB>(Bs[G_U], wu * 16 + r, gq, half, bu);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        float ah = a0[s];
-        if constexpr (NCH == 2) ah = a0[s] + a1[s];
-        acc_i = mfma_f32_16x16x4(ah, bi[s], acc_i);
-        acc_o = mfma_f32_16x16x4(ah, bo[s], acc_o);
-        acc_u = mfma_f32_16x16x4(ah, bu[s], acc_u);
-        acc_f0 = mfma_f32_16x16x4(a0[s], bf[s], acc_f0);
-        if constexpr (NCH == 2) acc_f1 = mfma_f32_16x16x4(a1[s], bf[s], acc_f1);
+      for (int tr = 0; tr < TR; ++tr) {
+        const int row = (wr * TR + tr) * 16 + r;
+        float a0[4], a1[4];
+        load_frag4<true, LDA>(As[0], row, gq, half, a0);
+        if constexpr (NCH == 2) load_frag4<true, LDA>(As[NCH - 1], row, gq, half, a1);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          float ah = a0[s];
+          if constexpr (NCH == 2) ah = a0[s] + a1[s];
+          acc[tr][0] = mfma_f32_16x16x4(ah, bi[s], acc[tr][0]);
+          acc[tr][1] = mfma_f32_16x16x4(ah, bo[s], acc[tr][1]);
+          acc[tr][2] = mfma_f32_16x16x4(ah, bu[s], acc[tr][2]);
+          acc[tr][3] = mfma_f32_16x16x4(a0[s], bf[s], acc[tr][3]);
+          if constexpr (NCH == 2) acc[tr][4] = mfma_f32_16x16x4(a1[s], bf[s], acc[tr][4]);
+        }
       }
     }
   }
@@ -211,10 +233,14 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
   // epilogue: gates, cell update, scatter of (c, h)
   const int j = u0 + wu * 16 + r;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int p = row0 + wr * 16 + 4 * gq + i;
-    if (p < rowend) lstm_fwd_epilogue<NCH>(n, p, j, acc_i[i], acc_o[i], acc_u[i], acc_f0[i], acc_f1[i]);
-  }
+  for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = row0 + (wr * TR + tr) * 16 + 4 * gq + i;
+      if (p < rowend)
+        lstm_fwd_epilogue<NCH>(n, p, j, acc[tr][0][i], acc[tr][1][i], acc[tr][2][i],
+                               acc[tr][3][i], NCH == 2 ? acc[tr][NACC - 1][i] : 0.f);
+    }
 }
 
 // ----------------------------------------------------------------- backward
@@ -641,15 +667,15 @@ __device__ __forceinline__ void xcd_tile(int n_unit_tiles, int& row_tile, int& u
   row_tile = local / per;
 }
 
-template <int NCH, int TR>
+template <int NCH, int TR, int KW = 4>
 struct FwdRed {
-  float v[4][TR][3 + NCH][4][64];
+  float v[KW][TR][3 + NCH][4][64];
 };
 
 // One 16*TR-position x 16-unit forward tile (row tile rt, unit tile ut).
-template <int NCH, bool BF, int TR>
+template <int NCH, bool BF, int TR, int KW = 4>
 __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
-                                                 FwdRed<NCH, TR>& R) {
+                                                 FwdRed<NCH, TR, KW>& R) {
   constexpr int NACC = 3 + NCH;
   auto& red = R.v;
   const int H = n.H, H4 = 4 * H;
@@ -670,7 +696,7 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
     }
   }
   const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
-  const int kq = H / 4, kbeg = w * kq, kend = kbeg + kq;
+  const int kq = H / KW, kbeg = w * kq, kend = kbeg + kq;
   v4f acc[TR][NACC];
 #pragma unroll
   for (int tr = 0; tr < TR; ++tr)
@@ -728,37 +754,42 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
   __syncthreads();
-  // wave w finishes element i = w of every lane: rows 16 tr + 4 gq + w, unit u0 + r
+  // wave w finishes element i = w % 4 of row tiles tr = w / 4, w / 4 + KW / 4, ...:
+  // rows 16 tr + 4 gq + i, unit u0 + r; partial sums added in wave order
+  const int i = w & 3;
 #pragma unroll
-  for (int tr = 0; tr < TR; ++tr) {
+  for (int tr = w >> 2; tr < TR; tr += KW / 4) {
     float z[NACC];
 #pragma unroll
-    for (int g = 0; g < NACC; ++g)
-      z[g] = ((red[0][tr][g][w][lane] + red[1][tr][g][w][lane]) + red[2][tr][g][w][lane]) +
-             red[3][tr][g][w][lane];
-    const int p = row0 + 16 * tr + 4 * gq + w;
+    for (int g = 0; g < NACC; ++g) {
+      float t = red[0][tr][g][i][lane];
+#pragma unroll
+      for (int q = 1; q < KW; ++q) t += red[q][tr][g][i][lane];
+      z[g] = t;
+    }
+    const int p = row0 + 16 * tr + 4 * gq + i;
     if (p < rowend)
       lstm_fwd_epilogue<NCH>(n, p, u0 + r, z[0], z[1], z[2], z[3], NCH == 2 ? z[NACC - 1] : 0.f);
   }
 }
 
-template <int NCH, bool BF, int TR>
-__global__ void __launch_bounds__(256) k_lstm_fwd_level_sk(Net n, int off, int M) {
-  __shared__ FwdRed<NCH, TR> red;
+template <int NCH, bool BF, int TR, int KW>
+__global__ void __launch_bounds__(64 * KW) k_lstm_fwd_level_sk(Net n, int off, int M) {
+  __shared__ FwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_fwd_sk_tile<NCH, BF, TR>(n, off, M, rt, ut, red);
+  lstm_fwd_sk_tile<NCH, BF, TR, KW>(n, off, M, rt, ut, red);
 }
 
-template <int NCH, int TR>
+template <int NCH, int TR, int KW = 4>
 struct BwdRed {
-  float v[4][TR][NCH == 2 ? 3 : 1][4][64];
+  float v[KW][TR][NCH == 2 ? 3 : 1][4][64];
 };
 
 // One 16*TR-position x 16-column backward tile (row tile rt, column tile ut).
-template <int NCH, bool BF, int TR>
+template <int NCH, bool BF, int TR, int KW = 4>
 __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
-                                                 BwdRed<NCH, TR>& R) {
+                                                 BwdRed<NCH, TR, KW>& R) {
   constexpr int NACC = 1 + (NCH == 2 ? 2 : 0);
   auto& red = R.v;
   const int H = n.H, H4 = 4 * H, GW = n.GW;
@@ -785,7 +816,7 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
   struct F1 {
     float a[TR][8], b[8];
   };
-  const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / 4;
+  const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / KW;
   auto load1 = [&](int c0, F1& f) {
     const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
@@ -811,7 +842,7 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     struct F2 {
       float a0[TR][8], a1[TR][8], b[8];
     };
-    const int q2 = H / 4;
+    const int q2 = H / KW;
     auto load2 = [&](int c0, F2& f) {
       const int col = c0 + 8 * gq;
 #pragma unroll
@@ -849,25 +880,29 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
   __syncthreads();
+  const int i = w & 3;
 #pragma unroll
-  for (int tr = 0; tr < TR; ++tr) {
+  for (int tr = w >> 2; tr < TR; tr += KW / 4) {
     float z[NACC];
 #pragma unroll
-    for (int g = 0; g < NACC; ++g)
-      z[g] = ((red[0][tr][g][w][lane] + red[1][tr][g][w][lane]) + red[2][tr][g][w][lane]) +
-             red[3][tr][g][w][lane];
-    const int p = row0 + 16 * tr + 4 * gq + w;
+    for (int g = 0; g < NACC; ++g) {
+      float t = red[0][tr][g][i][lane];
+#pragma unroll
+      for (int q = 1; q < KW; ++q) t += red[q][tr][g][i][lane];
+      z[g] = t;
+    }
+    const int p = row0 + 16 * tr + 4 * gq + i;
     if (p < rowend)
       lstm_bwd_scatter<NCH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f, NCH == 2 ? z[NACC - 1] : 0.f);
   }
 }
 
-template <int NCH, bool BF, int TR>
-__global__ void __launch_bounds__(256) k_lstm_bwd_level_sk(Net n, int off, int M) {
-  __shared__ BwdRed<NCH, TR> red;
+template <int NCH, bool BF, int TR, int KW>
+__global__ void __launch_bounds__(64 * KW) k_lstm_bwd_level_sk(Net n, int off, int M) {
+  __shared__ BwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_bwd_sk_tile<NCH, BF, TR>(n, off, M, rt, ut, red);
+  lstm_bwd_sk_tile<NCH, BF, TR, KW>(n, off, M, rt, ut, red);
 }
 
 // ----------------------------------------------- persistent small-level loop
@@ -972,10 +1007,15 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
     // two 16-row tiles per wave once that still gives >= 2 workgroups per CU
     const int ut = n.H / 16;
     const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
+    const bool kw8 = (n.H / 8) % 64 == 0;
     dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
 #define CAVS_FWD_SK(NCH, BF, TR)                                                               \
-  CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ">", off, M,                   \
-                   (k_lstm_fwd_level_sk<NCH, BF, TR>), g, dim3(256), 0, s, n, off, M)
+  do {                                                                                         \
+    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ", 8>", off, M,       \
+                              (k_lstm_fwd_level_sk<NCH, BF, TR, 8>), g, dim3(512), 0, s, n, off, M); \
+    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ", 4>", off, M,           \
+                          (k_lstm_fwd_level_sk<NCH, BF, TR, 4>), g, dim3(256), 0, s, n, off, M);  \
+  } while (0)
     if (n.N == 2) {
       if (n.bf) { if (tr2) CAVS_FWD_SK(2, true, 2); else CAVS_FWD_SK(2, true, 1); }
       else { if (tr2) CAVS_FWD_SK(2, false, 2); else CAVS_FWD_SK(2, false, 1); }
@@ -992,9 +1032,14 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
   do {                                                                                         \
     if (n.bf) CAVS_LAUNCH_ROWS("k_lstm_fwd_level_bf<" #NCH ", " #BM ">", off, M, (k_lstm_fwd_level_bf<NCH, BM>), \
                           grid, dim3(256), 0, s, n, off, M);                                   \
-    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level<" #NCH ", " #BM ">", off, M, (k_lstm_fwd_level<NCH, BM>), grid,    \
+    else if (BM == 64 && xcd)                                                                  \
+      CAVS_LAUNCH_ROWS("k_lstm_fwd_level<" #NCH ", 64, 2, xcd>", off, M,                        \
+                       (k_lstm_fwd_level<NCH, 64, 2, true>), dim3(cdiv(M, 64) * (n.H / 32)),     \
+                       dim3(256), 0, s, n, off, M);                                            \
+    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level<" #NCH ", " #BM ">", off, M, (k_lstm_fwd_level<NCH, BM, BM / 16, false>), grid,    \
                      dim3(256), 0, s, n, off, M);                                              \
   } while (0)
+  const bool xcd = (n.H / 32) % 8 == 0;
   if (small) {
     if (n.N == 2) CAVS_FWD(2, 16);
     else CAVS_FWD(1, 16);
@@ -1016,10 +1061,15 @@ void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (n.H % 256 == 0) {
     const int ut = n.H / 16;
     const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
+    const bool kw8 = (n.H / 8) % 64 == 0 && (3 * n.H / 8) % 64 == 0;
     dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
 #define CAVS_BWD_SK(NCH, BF, TR)                                                               \
-  CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ">", off, M,                   \
-                   (k_lstm_bwd_level_sk<NCH, BF, TR>), g, dim3(256), 0, s, n, off, M)
+  do {                                                                                         \
+    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ", 8>", off, M,       \
+                              (k_lstm_bwd_level_sk<NCH, BF, TR, 8>), g, dim3(512), 0, s, n, off, M); \
+    else CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ", 4>", off, M,           \
+                          (k_lstm_bwd_level_sk<NCH, BF, TR, 4>), g, dim3(256), 0, s, n, off, M);  \
+  } while (0)
     if (n.N == 2) {
       if (n.bf) { if (tr2) CAVS_BWD_SK(2, true, 2); else CAVS_BWD_SK(2, true, 1); }
       else { if (tr2) CAVS_BWD_SK(2, false, 2); else CAVS_BWD_SK(2, false, 1); }

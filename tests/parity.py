@@ -39,7 +39,9 @@ def normwise_err(got, ref):
     return float(np.abs(got - ref).max() / scale)
 
 
-def check(gpu: dict, ref: dict, keys, tol, label=""):
+def check(gpu: dict, ref: dict, keys, tol, label="", floor=FLOOR):
+    """Fails if any tensor's rel_err (with the given floor) exceeds tol.
+    floor=1.0 makes the test normwise: max |g - o| / max |o|."""
     errs = {}
     for k in keys:
         if k not in ref:
@@ -47,7 +49,7 @@ def check(gpu: dict, ref: dict, keys, tol, label=""):
         if k == "loss":
             errs[k] = abs(gpu[k] - ref[k]) / max(abs(ref[k]), 1e-30)
         else:
-            errs[k] = rel_err(gpu[k], ref[k])
+            errs[k] = rel_err(gpu[k], ref[k], floor)
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, "%s: errors above %g: %s (all: %s)" % (label, tol, bad, errs)
     return errs
