@@ -50,7 +50,7 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
     c = nc[row0:row0 + rows]
     gates_x = 4 if with_f else 3
     if name.startswith(("k_lstm_fwd_level", "k_lstm_bwd_level", "k_lstm_fwd_persist",
-                        "k_lstm_bwd_persist")):
+                        "k_lstm_bwd_persist", "k_lstm_fwd_tile", "k_lstm_bwd_tile")):
         return float(np.sum(2.0 * H * (3 * H + c * H))), 0.0
     if name.startswith(("k_fc_fwd_level", "k_fc_bwd_level")):
         return float(np.sum(2.0 * c * H * H)), 0.0
@@ -169,7 +169,7 @@ def main():
         if rows <= 0:
             continue
         kind = ("fwd" if ("fwd" in name or "leaf" in name) else
-                "bwd_gemm" if "bwd_level" in name else "bwd_gates")
+                "bwd_gates" if "bwd_gates" in name else "bwd_gemm")
         e = per_level.setdefault(row0, {"rows": rows, "fwd": 0.0, "bwd_gates": 0.0,
                                         "bwd_gemm": 0.0})
         e[kind] += ms * 1e3 / args.steps

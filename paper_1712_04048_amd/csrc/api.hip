@@ -39,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
+  size_t P, UT, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
   size_t part_floats;
 };
 
@@ -56,6 +56,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
     return r;
   };
   L.P = take(lstm ? V * 4 * H : 0);
+  L.UT = take(lstm ? 4 * H * H : 0);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
   L.Gs = take(lstm ? V * GW : 0);
@@ -140,6 +141,8 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.X = in->X;
   n.Y = in->Y;
   n.P = (float*)(base + L.P);
+  n.UT = (float*)(base + L.UT);
+  n.fuse_from = s->V;
   n.Hs = (float*)(base + L.Hs);
   n.Cs = (float*)(base + L.Cs);
   n.Gs = (float*)(base + L.Gs);
@@ -285,6 +288,7 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
   const int* lo = s->level_offsets_host;
   if (p->cell == CAVS_TREE_LSTM) {
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, str);
+    if (s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) lstm_transpose_u(n, str);
     lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
     const int ts = persist_first_level(n, lo, s->T);
     for (int t = 1; t < ts; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
@@ -343,19 +347,26 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   if (s->n_x > 0 && s->n_pull < s->n_x)
     CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
   if (lstm) {
+    // Levels tf.. get dA in their parent's level epilogue (roots: one
+    // kernel); levels below tf by an elementwise kernel just before their
+    // own product, once every parent has stored dL/dh and dL/dc.
+    const int tf = lstm_fuse_level(lo, T);
+    n.fuse_from = lo[tf];
+    lstm_bwd_roots(n, str);
     int ts = persist_first_level(n, lo, T);
+    if (ts < tf) ts = tf;
     int* bar = (int*)((char*)ws + L.bar);
     if (!lstm_bwd_persist(n, s->level_offsets, lo, ts, T, bar, str)) ts = T;
     for (int t = ts - 1; t >= 0; --t) {
       const int M = lo[t + 1] - lo[t];
-      lstm_bwd_gates(n, lo[t], M, str);
+      if (t < tf) lstm_bwd_gates(n, lo[t], M, str);
       if (t >= 1) lstm_bwd_level(n, lo[t], M, str);
     }
     const bool with_f = s->n_inner_input > 0;
     lstm_dU(n, off1, g->dU, part, L.part_floats, str);
     if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part, L.part_floats, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
-    bias_grad(n, 0, s->V, g->db, part, L.part_floats, str);
+    bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);
   } else {
     for (int t = T - 1; t >= 0; --t) {
       const int M = lo[t + 1] - lo[t];
@@ -363,9 +374,8 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       if (t >= 1) fc_bwd_level(n, lo[t], M, str);
     }
     fc_dW(n, off1, g->dU, part, L.part_floats, str);
-    bias_grad(n, off1, s->V, g->db, part, L.part_floats, str);
+    bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);
   }
-  if (p->loss == CAVS_LOSS_CE) head_grad(n, g->dWs, g->dbs, part, L.part_floats, str);
   CAVS_LAUNCH_CHECK(ctx);
   return CAVS_OK;
 }

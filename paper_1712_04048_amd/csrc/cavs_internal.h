@@ -1,6 +1,7 @@
 // Internal declarations shared by the HIP sources of libcavs.so (gfx950).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -92,10 +93,16 @@ struct ActiveCtx {
 
 hipEvent_t timing_event(cavs_ctx* c);
 
+// A timed launch hands its two events to the dispatch itself
+// (hipExtLaunchKernelGGL), so they carry the kernel's own start and end and
+// leave out the queue gap before it.  Cooperative launches have no such form:
+// those record the events on the stream around the launch (bracket = true).
 struct TimedScope {
   cavs_ctx* c;
   cavs_timed_launch rec;
-  TimedScope(const char* name, hipStream_t s, int row0 = 0, int rows = 0) : c(t_active_ctx) {
+  bool bracket;
+  TimedScope(const char* name, hipStream_t s, int row0 = 0, int rows = 0, bool bracket_ = false)
+      : c(t_active_ctx), bracket(bracket_) {
     if (!c || !c->timing) {
       c = nullptr;
       return;
@@ -105,12 +112,14 @@ struct TimedScope {
     rec.rows = rows;
     rec.start = timing_event(c);
     rec.stop = timing_event(c);
-    (void)hipEventRecord(rec.start, s);
     stream = s;
+    if (bracket) (void)hipEventRecord(rec.start, s);
   }
+  hipEvent_t start_ev() const { return c && !bracket ? rec.start : nullptr; }
+  hipEvent_t stop_ev() const { return c && !bracket ? rec.stop : nullptr; }
   ~TimedScope() {
     if (!c) return;
-    (void)hipEventRecord(rec.stop, stream);
+    if (bracket) (void)hipEventRecord(rec.stop, stream);
     c->timed.push_back(rec);
   }
   hipStream_t stream = nullptr;
@@ -118,18 +127,21 @@ struct TimedScope {
 
 }  // namespace cavs
 
-// Launch on `stream`, bracketed by timing events when timing is enabled.
+// Launch on `stream`; with timing enabled the dispatch records its own
+// start and end events.
 #define CAVS_LAUNCH(name, kernel, grid, block, shmem, stream, ...)            \
   do {                                                                      \
     ::cavs::TimedScope ts_(name, stream);                                   \
-    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);    \
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ts_.start_ev(), \
+                          ts_.stop_ev(), 0, __VA_ARGS__);                   \
   } while (0)
 
 // Same, recording the level-major rows [row0, row0 + rows) the launch covers.
 #define CAVS_LAUNCH_ROWS(name, row0, rows, kernel, grid, block, shmem, stream, ...) \
   do {                                                                            \
     ::cavs::TimedScope ts_(name, stream, row0, rows);                             \
-    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);          \
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ts_.start_ev(),     \
+                          ts_.stop_ev(), 0, __VA_ARGS__);                         \
   } while (0)
 
 // ---------------------------------------------------------------------------

@@ -13,6 +13,7 @@ struct Net {
   int bf;                       // 1: matrix-product operands rounded to bf16
   int GW;                       // saved-gate / dA row width: (3+N)H (LSTM) or H (FC)
   float inv_denom;              // 1 / |Lambda|
+  int fuse_from;                // LSTM backward: positions >= this get dA in the parent's epilogue
   // schedule
   const int* child_pos;         // [V*N]
   const int* parent_pos;        // [V]
@@ -23,6 +24,7 @@ struct Net {
   // parameters and inputs
   const float* Wx;              // [D, 4H]
   const float* U;               // LSTM [H, 4H]; FC [N*H, H]
+  float* UT;                    // LSTM: U transposed, [4H, H] (workspace)
   const float* b;
   const float* Ws;              // [H, C]
   const float* bs;              // [C]
@@ -52,8 +54,22 @@ enum { G_I = 0, G_F = 1, G_O = 2, G_U = 3 };
 // lstm.hip
 void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s);
+// Backward dA of the levels below n.fuse_from: elementwise over level rows
+// (dL/dh and dL/dc as stored by the parents); roots at or above it.
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s);
+void lstm_bwd_roots(const Net& n, hipStream_t s);
 void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s);
+// First level whose rows (and those of every level above) get their dA in
+// the parent's epilogue: levels of at most kFuseRows positions.
+constexpr int kFuseRows = 256;
+int lstm_fuse_level(const int* lo_host, int T);
+// lstm_tile.hip: LDS-tiled level products for levels of >= kTileMinRows
+// positions (needs n.UT, written by lstm_transpose_u in the same pass).
+constexpr int kTileMinRows = 300;
+bool lstm_tile_applies(const Net& n, int M);
+void lstm_transpose_u(const Net& n, hipStream_t s);
+void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s);
+void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s);
 // Persistent loop over levels [t0, t1) (forward) or t1-1 .. t0 (backward:
 // gates and products) in one cooperative launch.  `lo` is the device copy of
 // the level offsets, `lo_host` the host copy, `bar` 256 zeroed ints of
@@ -81,10 +97,10 @@ void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
               size_t part_floats, hipStream_t s);
 void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);
 // column sums over positions [row0, row1) of the gate gradients -> db
-void bias_grad(const Net& n, int row0, int row1, float* db, float* part, size_t part_floats,
-               hipStream_t s);
-void head_grad(const Net& n, float* dWs, float* dbs, float* part, size_t part_floats,
-               hipStream_t s);
+// db over rows [row0, row1) and, for the CE head, dW_s and db_s over all rows;
+// rows below lo1 are level 0 (no children).
+void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float* dWs, float* dbs,
+                     float* part, size_t part_floats, hipStream_t s);
 size_t lazy_part_floats(int V, int D, int H, int N, int C);
 
 // ---------------------------------------------------------------------------

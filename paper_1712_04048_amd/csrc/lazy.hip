@@ -579,58 +579,105 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
 }
 
 // -------------------------------------------------------------- col sums
-// mode 0: LSTM db (4H columns, f = f_0 + f_1); mode 1: FC db (H columns);
-// mode 2: db_s (C columns of dZ); mode 3: dW_s (H*C columns: h_j dZ_c).
-template <int MODE>
-__global__ void k_colsum_part(Net n, int row0, int row1, int width, int rows_per,
-                              float* part) {
-  const int col = blockIdx.x * 256 + threadIdx.x;
-  if (col >= width) return;
-  const int lo = row0 + blockIdx.y * rows_per, hi = min(row1, lo + rows_per);
+// The bias and head gradients are column sums over the level-major rows
+// (lazy batching, Section 3.4): db sums dA (LSTM: 4H columns with
+// f = f_0 + f_1; FC: H columns) over rows [row0, row1); dW_s[j][c] sums
+// h_j dZ_c and db_s[c] sums dZ_c over all rows.  One launch writes per-chunk
+// partials (each thread: 4 adjacent columns, its chunk's rows in order), a
+// second adds the chunks in order, so the result is deterministic.
+constexpr int kBiasChunks = 256;
+
+__global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, int lo1,
+                                                   int rows_per, int bxA, int wA, int W,
+                                                   float* __restrict__ part) {
   const int H = n.H;
-  float s = 0.f;
-  for (int p = lo; p < hi; ++p) {
-    if constexpr (MODE == 0) {
-      const float* row = n.dA + (size_t)p * n.GW;
-      float v = row[col];
-      if (n.N == 2 && col >= H && col < 2 * H) v += row[3 * H + col];
-      s += v;
-    } else if constexpr (MODE == 1) {
-      s += n.dA[(size_t)p * H + col];
-    } else if constexpr (MODE == 2) {
-      s += n.dZ[(size_t)p * n.C + col];
+  const int lo = blockIdx.y * rows_per, hi = min(n.V, lo + rows_per);
+  float* out = part + (size_t)blockIdx.y * W;
+  if ((int)blockIdx.x < bxA) {
+    const int c = 4 * (blockIdx.x * 256 + threadIdx.x);
+    if (c >= wA) return;
+    int r0 = max(lo, row0);
+    const int r1 = min(hi, row1);
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (n.GW == H) {  // Tree-FC
+      for (int p = r0; p < r1; ++p) {
+        const float4 v = *reinterpret_cast<const float4*>(n.dA + (size_t)p * H + c);
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+      }
     } else {
-      const int j = col / n.C, c = col % n.C;
-      s += n.Hs[(size_t)p * H + j] * n.dZ[(size_t)p * n.C + c];
+      const bool fcol = c >= G_F * H && c < (G_F + 1) * H;
+      if (fcol) r0 = max(r0, lo1);  // level-0 rows have no children: f is zero
+      const bool two = fcol && n.N == 2;
+      for (int p = r0; p < r1; ++p) {
+        const float* row = n.dA + (size_t)p * n.GW;
+        float4 v = *reinterpret_cast<const float4*>(row + c);
+        if (two) {
+          const float4 u = *reinterpret_cast<const float4*>(row + 3 * H + c);
+          v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+        }
+        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+      }
     }
+    *reinterpret_cast<float4*>(out + c) = s;
+    return;
   }
-  part[(size_t)blockIdx.y * width + col] = s;
+  // head: columns wA + j*C + c (dW_s row-major), then wA + H*C + c (db_s)
+  const int j = 4 * ((blockIdx.x - bxA) * 256 + threadIdx.x);
+  if (j >= H) return;
+  const int C = n.C;
+  float acc[4][kLossMaxC], zs[kLossMaxC];
+#pragma unroll
+  for (int c = 0; c < kLossMaxC; ++c) {
+    zs[c] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e][c] = 0.f;
+  }
+  for (int p = lo; p < hi; ++p) {
+    const float4 h = *reinterpret_cast<const float4*>(n.Hs + (size_t)p * H + j);
+    const float* dz = n.dZ + (size_t)p * C;
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C) {
+        const float z = dz[c];
+        acc[0][c] += h.x * z;
+        acc[1][c] += h.y * z;
+        acc[2][c] += h.z * z;
+        acc[3][c] += h.w * z;
+        zs[c] += z;
+      }
+  }
+  float* o = out + wA + (size_t)j * C;
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C) o[e * C + c] = acc[e][c];
+  if (j == 0)
+#pragma unroll
+    for (int c = 0; c < kLossMaxC; ++c)
+      if (c < C) out[wA + H * C + c] = zs[c];
 }
 
-__global__ void k_colsum_reduce(const float* __restrict__ part, int nblk, int width,
-                                float* __restrict__ dst) {
-  const int col = blockIdx.x * 256 + threadIdx.x;
-  if (col >= width) return;
+// 16 wavefronts per block: wavefront y adds chunks y, y + 16, ... of 64
+// columns; the 16 sums are then added in order.
+__global__ void __launch_bounds__(1024) k_bias_reduce(const float* __restrict__ part, int nchunk,
+                                                      int W, int wA, int HC, float* db,
+                                                      float* dWs, float* dbs) {
+  __shared__ float red[16][64];
+  const int x = threadIdx.x & 63, y = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + x;
   float s = 0.f;
-  for (int b = 0; b < nblk; ++b) s += part[(size_t)b * width + col];
-  dst[col] = s;
-}
-
-constexpr const char* kColsumName[4] = {"k_colsum_part<0>", "k_colsum_part<1>",
-                                        "k_colsum_part<2>", "k_colsum_part<3>"};
-
-template <int MODE>
-void colsum(const Net& n, int row0, int row1, int width, float* dst, float* part,
-            size_t part_floats, hipStream_t st) {
-  const int rows = row1 - row0;
-  int nblk = rows > 0 ? cdiv(rows, 128) : 1;
-  if (nblk > 256) nblk = 256;
-  while (nblk > 1 && (size_t)nblk * width > part_floats) --nblk;
-  const int rows_per = rows > 0 ? cdiv(rows, nblk) : 0;
-  CAVS_LAUNCH(kColsumName[MODE], k_colsum_part<MODE>, dim3(cdiv(width, 256), nblk), dim3(256), 0, st, n,
-                     row0, row1, width, rows_per, part);
-  CAVS_LAUNCH("k_colsum_reduce", k_colsum_reduce, dim3(cdiv(width, 256)), dim3(256), 0, st,
-                     (const float*)part, nblk, width, dst);
+  if (col < W)
+    for (int b = y; b < nchunk; b += 16) s += part[(size_t)b * W + col];
+  red[y][x] = s;
+  __syncthreads();
+  if (y != 0 || col >= W) return;
+  float t = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) t += red[k][x];
+  if (col < wA) db[col] = t;
+  else if (col < wA + HC) dWs[col - wA] = t;
+  else dbs[col - wA - HC] = t;
 }
 
 // ---------------------------------------------------------------- loss
@@ -711,7 +758,7 @@ size_t lazy_part_floats(int V, int D, int H, int N, int C) {
   (void)V;
   size_t a = (size_t)kMaxSplits * 4 * H * (size_t)H;        // dU / FC dW
   size_t b = (size_t)kMaxSplits * 4 * H * (size_t)(D + 64);  // dW_x (m tail padding)
-  size_t c = (size_t)256 * (4 * H + (size_t)H * (C > 0 ? C : 1));
+  size_t c = (size_t)kBiasChunks * (4 * H + (size_t)(H + 1) * (C > 0 ? C : 0));
   (void)N;
   size_t m = a > b ? a : b;
   return m > c ? m : c;
@@ -776,16 +823,23 @@ void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, h
   }
 }
 
-void bias_grad(const Net& n, int row0, int row1, float* db, float* part, size_t part_floats,
-               hipStream_t s) {
-  if (n.GW == n.H) colsum<1>(n, row0, row1, n.H, db, part, part_floats, s);
-  else colsum<0>(n, row0, row1, 4 * n.H, db, part, part_floats, s);
-}
-
-void head_grad(const Net& n, float* dWs, float* dbs, float* part, size_t part_floats,
-               hipStream_t s) {
-  colsum<2>(n, 0, n.V, n.C, dbs, part, part_floats, s);
-  colsum<3>(n, 0, n.V, n.H * n.C, dWs, part, part_floats, s);
+void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float* dWs, float* dbs,
+                     float* part, size_t part_floats, hipStream_t s) {
+  const int wA = n.GW == n.H ? n.H : 4 * n.H;
+  const bool head = n.loss == CAVS_LOSS_CE;
+  const int HC = head ? n.H * n.C : 0;
+  const int W = wA + HC + (head ? n.C : 0);
+  int nchunk = cdiv(n.V, 16);
+  if (nchunk > kBiasChunks) nchunk = kBiasChunks;
+  if (nchunk < 1) nchunk = 1;
+  while (nchunk > 1 && (size_t)nchunk * W > part_floats) --nchunk;
+  const int rows_per = cdiv(n.V > 0 ? n.V : 1, nchunk);
+  nchunk = cdiv(n.V > 0 ? n.V : 1, rows_per);
+  const int bxA = cdiv(wA / 4, 256), bxB = head ? cdiv(n.H / 4, 256) : 0;
+  CAVS_LAUNCH("k_bias_part", k_bias_part, dim3(bxA + bxB, nchunk), dim3(256), 0, s, n, row0, row1,
+              lo1, rows_per, bxA, wA, W, part);
+  CAVS_LAUNCH("k_bias_reduce", k_bias_reduce, dim3(cdiv(W, 64)), dim3(1024), 0, s,
+              (const float*)part, nchunk, W, wA, HC, db, dWs, dbs);
 }
 
 }  // namespace cavs

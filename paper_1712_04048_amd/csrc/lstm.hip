@@ -11,17 +11,19 @@
 // pulled-input term x W_x was produced beforehand by one GEMM over all
 // vertices (pull is eager).  Level 0 (leaves) is elementwise.
 //
-// Backward, reverse level order: an elementwise kernel turns dL/dh, dL/dc of
-// the level into the pre-activation gradients dA (kept level-major for the
-// lazy weight gradients) and scatters dL/dc_k = g_c * f_k to the children; a
-// GEMM kernel computes dL/dh_k = dA_iou U_iou^T + dA_fk U_f^T and scatters it
-// to child k.  Every vertex has one parent, so each child row is written by
-// exactly one thread: plain stores, no atomics.
+// Backward, reverse level order: one GEMM kernel per level computes
+// dL/dh_k = dA_iou U_iou^T + dA_fk U_f^T for every child k.  A vertex has one
+// parent, so that product is the child's whole dL/dh: the epilogue turns it
+// (with the dL/dc scattered earlier and the child's own loss term) into the
+// child's pre-activation gradients dA, kept level-major for the lazy weight
+// gradients, and scatters dL/dc_k' = g_c * f_k' to the grandchildren.  Roots
+// are handled by one kernel before the level loop.  Every child row is
+// written by exactly one thread: plain stores, no atomics.
 #include <stdlib.h>
 
 #include <map>
 
-#include "kernels.h"
+#include "lstm_dev.h"
 
 namespace cavs {
 namespace {
@@ -55,61 +57,24 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M) {
   if (n.c_out) n.c_out[(size_t)v * H + j] = c;
 }
 
-// Gates, cell update and the scatter of (c, h) for position p, unit j, from
-// the matrix-product parts of the pre-activations (shared by both precisions).
-template <int NCH>
-__device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, float zi, float zo,
-                                                  float zu, float zf0, float zf1) {
-  const int H = n.H, H4 = 4 * H;
-  const int pr = n.pull_pos[p];
-  float ai = zi + n.b[G_I * H + j], ao = zo + n.b[G_O * H + j], au = zu + n.b[G_U * H + j];
-  float fb = n.b[G_F * H + j];
-  if (pr >= 0) {
-    const float* Pp = n.P + (size_t)p * H4;
-    ai += Pp[G_I * H + j];
-    ao += Pp[G_O * H + j];
-    au += Pp[G_U * H + j];
-    fb += Pp[G_F * H + j];
-  }
-  const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanhf(au);
-  float c = ig * ug;
-  float f0 = 0.f, f1 = 0.f;
-  const int cp0 = n.child_pos[(size_t)p * NCH];
-  if (cp0 >= 0) {
-    f0 = sigmoidf_(zf0 + fb);
-    c += f0 * n.Cs[(size_t)cp0 * H + j];
-  }
-  if constexpr (NCH == 2) {
-    const int cp1 = n.child_pos[(size_t)p * NCH + 1];
-    if (cp1 >= 0) {
-      f1 = sigmoidf_(zf1 + fb);
-      c += f1 * n.Cs[(size_t)cp1 * H + j];
-    }
-  }
-  const float h = og * tanhf(c);
-  n.Hs[(size_t)p * H + j] = h;
-  n.Cs[(size_t)p * H + j] = c;
-  float* g = n.Gs + (size_t)p * n.GW;
-  g[j] = ig;
-  g[H + j] = f0;
-  g[2 * H + j] = og;
-  g[3 * H + j] = ug;
-  if constexpr (NCH == 2) g[4 * H + j] = f1;
-  const int v = n.order[p];
-  n.h_out[(size_t)v * H + j] = h;
-  if (n.c_out) n.c_out[(size_t)v * H + j] = c;
+// dA of every position of a level below n.fuse_from (dL/dh, dL/dc stored by
+// the parent; zero at a root).
+__global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)M * n.H) return;
+  const int p = off + (int)(idx / n.H), j = (int)(idx % n.H);
+  const bool root = n.parent_pos[p] < 0;
+  lstm_bwd_gates_elem(n, p, j, root ? 0.f : n.dHp[(size_t)p * n.H + j],
+                      root ? 0.f : n.dCp[(size_t)p * n.H + j]);
 }
 
-// Child scatter of the backward level product for position p, column col.
-template <int NCH>
-__device__ __forceinline__ void lstm_bwd_scatter(const Net& n, int p, int col, float zh, float zf0,
-                                                 float zf1) {
-  const int cp0 = n.child_pos[(size_t)p * NCH];
-  if (cp0 >= 0) n.dHp[(size_t)cp0 * n.H + col] = zh + zf0;
-  if constexpr (NCH == 2) {
-    const int cp1 = n.child_pos[(size_t)p * NCH + 1];
-    if (cp1 >= 0) n.dHp[(size_t)cp1 * n.H + col] = zh + zf1;
-  }
+// Roots at positions >= n.fuse_from: one workgroup per position (the others
+// exit at once); every other position there gets its dA in the epilogue of
+// its parent's level product.
+__global__ void __launch_bounds__(256) k_lstm_bwd_roots(Net n) {
+  const int p = n.fuse_from + blockIdx.x;
+  if (n.parent_pos[p] >= 0) return;
+  for (int j = threadIdx.x; j < n.H; j += 256) lstm_bwd_gates_elem(n, p, j, 0.f, 0.f);
 }
 
 // Tile: BM positions x BHU hidden units; 4 wavefronts arranged WR x WU, each
@@ -241,56 +206,6 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_level(Net n, int off, int M) {
         lstm_fwd_epilogue<NCH>(n, p, j, acc[tr][0][i], acc[tr][1][i], acc[tr][2][i],
                                acc[tr][3][i], NCH == 2 ? acc[tr][NACC - 1][i] : 0.f);
     }
-}
-
-// ----------------------------------------------------------------- backward
-// dA and the dc scatter for position p, unit j.
-__device__ __forceinline__ void lstm_bwd_gates_elem(const Net& n, int p, int j) {
-  const int H = n.H;
-  const int par = n.parent_pos[p];
-  float gh = par >= 0 ? n.dHp[(size_t)p * H + j] : 0.f;
-  float gcin = par >= 0 ? n.dCp[(size_t)p * H + j] : 0.f;
-  const int q = n.push_pos[p];
-  if (q >= 0) {
-    if (n.loss == CAVS_LOSS_CE) {
-      const float* dz = n.dZ + (size_t)p * n.C;
-      const float* ws = n.Ws + (size_t)j * n.C;
-      float s = 0.f;
-      for (int c = 0; c < n.C; ++c) s += dz[c] * ws[c];
-      gh += s;
-    } else {
-      gh += (n.Hs[(size_t)p * H + j] - n.Y[(size_t)q * H + j]) * n.inv_denom;
-    }
-  }
-  const float* g = n.Gs + (size_t)p * n.GW;
-  const float ig = g[j], og = g[2 * H + j], ug = g[3 * H + j];
-  const float c = n.Cs[(size_t)p * H + j];
-  const float tau = tanhf(c);
-  const float d_o = gh * tau * og * (1.f - og);
-  const float gc = gcin + gh * og * (1.f - tau * tau);
-  const float d_i = gc * ug * ig * (1.f - ig);
-  const float d_u = gc * ig * (1.f - ug * ug);
-  float* da = n.dA + (size_t)p * n.GW;
-  for (int k = 0; k < n.N; ++k) {
-    const int cp = n.child_pos[(size_t)p * n.N + k];
-    const int col = k == 0 ? H : 4 * H;
-    float d_f = 0.f;
-    if (cp >= 0) {
-      const float fk = g[col + j];
-      d_f = gc * n.Cs[(size_t)cp * H + j] * fk * (1.f - fk);
-      n.dCp[(size_t)cp * H + j] = gc * fk;
-    }
-    da[col + j] = d_f;
-  }
-  da[j] = d_i;
-  da[2 * H + j] = d_o;
-  da[3 * H + j] = d_u;
-}
-
-__global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)M * n.H) return;
-  lstm_bwd_gates_elem(n, off + (int)(idx / n.H), (int)(idx % n.H));
 }
 
 // dL/dh_k for every vertex of the level: tile BM positions x 64 hidden units.
@@ -634,39 +549,6 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_level_bf(Net n, int off, int M
 // a fixed order (deterministic) and the epilogue is shared with the tiled
 // kernels.  BF selects bf16 operands (one 16x16x32 MFMA per 32-deep chunk)
 // instead of fp32 (eight 16x16x4 steps).
-template <bool BF>
-__device__ __forceinline__ v4f mfma_chunk8(const float (&a)[8], const float (&b)[8], v4f acc) {
-  if constexpr (BF) {
-    bf16x8 av, bv;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const u16 ua = f2bf(a[s]), ub = f2bf(b[s]);
-      av[s] = __builtin_bit_cast(__bf16, ua);
-      bv[s] = __builtin_bit_cast(__bf16, ub);
-    }
-    return mfma_bf16_16x16x32(av, bv, acc);
-  } else {
-#pragma unroll
-    for (int s = 0; s < 8; ++s) acc = mfma_f32_16x16x4(a[s], b[s], acc);
-    return acc;
-  }
-}
-
-__device__ __forceinline__ void ld8(const float* p, float (&v)[8]) {
-  const float4 x = ldg4(p), y = ldg4(p + 4);
-  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-  v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
-}
-
-// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch), and each
-// XCD has its own L2.  Tiles are mapped so that XCD x only touches unit tiles
-// x, x+8, ...: each L2 then holds 1/8 of the weight columns instead of all.
-__device__ __forceinline__ void xcd_tile(int n_unit_tiles, int& row_tile, int& unit_tile) {
-  const int bid = blockIdx.x, xcd = bid & 7, local = bid >> 3, per = n_unit_tiles >> 3;
-  unit_tile = xcd + 8 * (local % per);
-  row_tile = local / per;
-}
-
 template <int NCH, int TR, int KW = 4>
 struct FwdRed {
   float v[KW][TR][3 + NCH][4][64];
@@ -972,20 +854,16 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_persist(Net n, const int* lo, 
   }
 }
 
-// Levels t1-1 down to t0 (all with children): dA + dc scatter, barrier, the
-// dh_k products, barrier.
+// Levels t1-1 down to t0 (all with children): the dh_k products, whose
+// epilogue forms the children's dA, then a barrier.
 template <int NCH, bool BF>
 __global__ void __launch_bounds__(256) k_lstm_bwd_persist(Net n, const int* lo, int t0, int t1,
                                                           GridBar bar) {
   __shared__ BwdRed<NCH, 1> red;
-  const int ut = n.H / 16, H = n.H;
+  const int ut = n.H / 16;
   int epoch = 0;
   for (int t = t1 - 1; t >= t0; --t) {
     const int off = lo[t], M = lo[t + 1] - off;
-    const long elems = (long)M * H;
-    for (long idx = (long)blockIdx.x * 256 + threadIdx.x; idx < elems; idx += (long)gridDim.x * 256)
-      lstm_bwd_gates_elem(n, off + (int)(idx / H), (int)(idx % H));
-    grid_sync(bar, epoch);
     const int tiles = cdiv_dev(M, 16) * ut;
     for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
       lstm_bwd_sk_tile<NCH, BF, 1>(n, off, M, tile / ut, tile % ut, red);
@@ -1003,6 +881,10 @@ void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
+  if (lstm_tile_applies(n, M)) {
+    lstm_fwd_tile(n, off, M, s);
+    return;
+  }
   if (n.H % 256 == 0 && M < 1024) {
     // two 16-row tiles per wave once that still gives >= 2 workgroups per CU
     const int ut = n.H / 16;
@@ -1052,12 +934,27 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates", off, M, k_lstm_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off,
-                     M);
+  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates", off, M, k_lstm_bwd_gates, dim3(cdiv((long)M * n.H, 256)),
+                   dim3(256), 0, s, n, off, M);
+}
+
+void lstm_bwd_roots(const Net& n, hipStream_t s) {
+  if (n.fuse_from >= n.V) return;
+  CAVS_LAUNCH("k_lstm_bwd_roots", k_lstm_bwd_roots, dim3(n.V - n.fuse_from), dim3(256), 0, s, n);
+}
+
+int lstm_fuse_level(const int* lo_host, int T) {
+  for (int t = 0; t < T; ++t)
+    if (lo_host[t + 1] - lo_host[t] <= kFuseRows) return t;
+  return T;
 }
 
 void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
+  if (lstm_tile_applies(n, M)) {
+    lstm_bwd_tile(n, off, M, s);
+    return;
+  }
   if (n.H % 256 == 0) {
     const int ut = n.H / 16;
     const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
@@ -1138,7 +1035,7 @@ bool launch_persist(const char* name, const void* fn, const Net& n, const int* l
   GridBar gb{bar, bar + 64, bar + 65};
   void* args[] = {(void*)&n, (void*)&lo, (void*)&t0, (void*)&t1, (void*)&gb};
   if (hipMemsetAsync(bar, 0, 256 * sizeof(int), s) != hipSuccess) return false;
-  TimedScope ts(name, s, lo_host[t0], lo_host[t1] - lo_host[t0]);
+  TimedScope ts(name, s, lo_host[t0], lo_host[t1] - lo_host[t0], /*bracket=*/true);
   return hipLaunchCooperativeKernel(fn, dim3(G), dim3(256), args, 0, s) == hipSuccess;
 }
 
