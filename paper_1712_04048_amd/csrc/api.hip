@@ -39,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, UT, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
+  size_t P, UT, zrow, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
   size_t part_floats;
 };
 
@@ -57,6 +57,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   };
   L.P = take(lstm ? V * 4 * H : 0);
   L.UT = take(lstm ? 4 * H * H : 0);
+  L.zrow = take(lstm ? H : 0);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
   L.Gs = take(lstm ? V * GW : 0);
@@ -142,6 +143,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.Y = in->Y;
   n.P = (float*)(base + L.P);
   n.UT = (float*)(base + L.UT);
+  n.zrow = (float*)(base + L.zrow);
   n.fuse_from = s->V;
   n.Hs = (float*)(base + L.Hs);
   n.Cs = (float*)(base + L.Cs);

@@ -64,8 +64,10 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
   if (idx >= (long)M * n.H) return;
   const int p = off + (int)(idx / n.H), j = (int)(idx % n.H);
   const bool root = n.parent_pos[p] < 0;
-  lstm_bwd_gates_elem(n, p, j, root ? 0.f : n.dHp[(size_t)p * n.H + j],
-                      root ? 0.f : n.dCp[(size_t)p * n.H + j]);
+  const float gh = root ? 0.f : n.dHp[(size_t)p * n.H + j];
+  const float gc = root ? 0.f : n.dCp[(size_t)p * n.H + j];
+  if (n.N == 2) lstm_gates_elem<2>(n, p, j, gh, gc);
+  else lstm_gates_elem<1>(n, p, j, gh, gc);
 }
 
 // Roots at positions >= n.fuse_from: one workgroup per position (the others
@@ -74,7 +76,10 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
 __global__ void __launch_bounds__(256) k_lstm_bwd_roots(Net n) {
   const int p = n.fuse_from + blockIdx.x;
   if (n.parent_pos[p] >= 0) return;
-  for (int j = threadIdx.x; j < n.H; j += 256) lstm_bwd_gates_elem(n, p, j, 0.f, 0.f);
+  for (int j = threadIdx.x; j < n.H; j += 256) {
+    if (n.N == 2) lstm_gates_elem<2>(n, p, j, 0.f, 0.f);
+    else lstm_gates_elem<1>(n, p, j, 0.f, 0.f);
+  }
 }
 
 // Tile: BM positions x BHU hidden units; 4 wavefronts arranged WR x WU, each
@@ -555,7 +560,12 @@ struct FwdRed {
 };
 
 // One 16*TR-position x 16-unit forward tile (row tile rt, unit tile ut).
-template <int NCH, bool BF, int TR, int KW = 4>
+// Wavefronts 0 .. KW-1 split the contraction.  With EPI, four more
+// wavefronts (KW .. KW+3) own the epilogue: they read everything it needs
+// besides the product (bias, pulled term, children's c) while the others
+// multiply, then finish element i = w - KW of every row tile.  Without EPI
+// (persistent loop, 64*KW threads) the contraction wavefronts finish it.
+template <int NCH, bool BF, int TR, int KW, bool EPI>
 __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
                                                  FwdRed<NCH, TR, KW>& R) {
   constexpr int NACC = 3 + NCH;
@@ -564,84 +574,81 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int u0 = ut * 16;
-  const float* ap[TR][NCH];               // A rows of this lane: row0 + 16 tr + r
+  if (w < KW) {
+    const float* ap[TR][NCH];               // A rows of this lane: row0 + 16 tr + r
 #pragma unroll
-  for (int tr = 0; tr < TR; ++tr) {
-    const int pa = row0 + 16 * tr + r;
+    for (int tr = 0; tr < TR; ++tr) {
+      const int pa = row0 + 16 * tr + r;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      ap[tr][c] = nullptr;
-      if (pa < rowend) {
-        const int cp = n.child_pos[(size_t)pa * NCH + c];
-        if (cp >= 0) ap[tr][c] = n.Hs + (size_t)cp * H;
+      for (int c = 0; c < NCH; ++c) {
+        ap[tr][c] = nullptr;
+        if (pa < rowend) {
+          const int cp = n.child_pos[(size_t)pa * NCH + c];
+          if (cp >= 0) ap[tr][c] = n.Hs + (size_t)cp * H;
+        }
       }
     }
-  }
-  const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
-  const int kq = H / KW, kbeg = w * kq, kend = kbeg + kq;
-  v4f acc[TR][NACC];
-#pragma unroll
-  for (int tr = 0; tr < TR; ++tr)
-#pragma unroll
-    for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  struct Frag {
-    float a[TR][NCH][8];
-    float b[4][8];
-  };
-  auto load = [&](int k0, Frag& f) {
-    const int kk = k0 + 8 * gq;
+    const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
+    const int kq = H / KW, kbeg = w * kq, kend = kbeg + kq;
+    v4f acc[TR][NACC];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        if (ap[tr][c]) ld8(ap[tr][c] + kk, f.a[tr][c]);
-        else {
+      for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    struct Frag {
+      float a[TR][NCH][8];
+      float b[4][8];
+    };
+    auto load = [&](int k0, Frag& f) {
+      const int kk = k0 + 8 * gq;
 #pragma unroll
-          for (int s = 0; s < 8; ++s) f.a[tr][c][s] = 0.f;
+      for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          if (ap[tr][c]) ld8(ap[tr][c] + kk, f.a[tr][c]);
+          else {
+#pragma unroll
+            for (int s = 0; s < 8; ++s) f.a[tr][c][s] = 0.f;
+          }
         }
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
+    };
+    auto compute = [&](const Frag& f) {
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) {
+        float ah[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          ah[s] = NCH == 2 ? f.a[tr][0][s] + f.a[tr][NCH - 1][s] : f.a[tr][0][s];
+        acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
+        acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
+        acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
+        acc[tr][3] = mfma_chunk8<BF>(f.a[tr][0], f.b[G_F], acc[tr][3]);
+        if constexpr (NCH == 2)
+          acc[tr][4] = mfma_chunk8<BF>(f.a[tr][NCH - 1], f.b[G_F], acc[tr][4]);
       }
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
-  };
-  auto compute = [&](const Frag& f) {
-#pragma unroll
-    for (int tr = 0; tr < TR; ++tr) {
-      float ah[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        ah[s] = NCH == 2 ? f.a[tr][0][s] + f.a[tr][NCH - 1][s] : f.a[tr][0][s];
-      acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
-      acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
-      acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
-      acc[tr][3] = mfma_chunk8<BF>(f.a[tr][0], f.b[G_F], acc[tr][3]);
-      if constexpr (NCH == 2) acc[tr][4] = mfma_chunk8<BF>(f.a[tr][NCH - 1], f.b[G_F], acc[tr][4]);
+    };
+    // two register buffers: loads of the next chunk overlap the current MFMAs
+    Frag fa, fb;
+    load(kbeg, fa);
+    for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
+      load(k0 + kBK, fb);
+      compute(fa);
+      if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
+      compute(fb);
     }
-  };
-  // two register buffers: loads of the next chunk overlap the current MFMAs
-  Frag fa, fb;
-  load(kbeg, fa);
-  for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
-    load(k0 + kBK, fb);
-    compute(fa);
-    if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
-    compute(fb);
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+      for (int g = 0; g < NACC; ++g)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
   }
-#pragma unroll
-  for (int tr = 0; tr < TR; ++tr)
-#pragma unroll
-    for (int g = 0; g < NACC; ++g)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
-  __syncthreads();
-  // wave w finishes element i = w % 4 of row tiles tr = w / 4, w / 4 + KW / 4, ...:
-  // rows 16 tr + 4 gq + i, unit u0 + r; partial sums added in wave order
-  const int i = w & 3;
-#pragma unroll
-  for (int tr = w >> 2; tr < TR; tr += KW / 4) {
-    float z[NACC];
+  auto zsum = [&](int tr, int i, float (&z)[NACC]) {
 #pragma unroll
     for (int g = 0; g < NACC; ++g) {
       float t = red[0][tr][g][i][lane];
@@ -649,18 +656,49 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
       for (int q = 1; q < KW; ++q) t += red[q][tr][g][i][lane];
       z[g] = t;
     }
-    const int p = row0 + 16 * tr + 4 * gq + i;
-    if (p < rowend)
+  };
+  if constexpr (EPI) {
+    const int i = w - KW;
+    FwdPre<NCH> pre[TR];
+    if (w >= KW) {
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) {
+        const int p = row0 + 16 * tr + 4 * gq + i;
+        if (p < rowend) lstm_fwd_pre<NCH>(n, p, u0 + r, pre[tr]);
+      }
+    }
+    __syncthreads();
+    if (w < KW) return;
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr) {
+      const int p = row0 + 16 * tr + 4 * gq + i;
+      if (p >= rowend) continue;
+      float z[NACC];
+      zsum(tr, i, z);
+      lstm_fwd_fin<NCH>(n, p, u0 + r, pre[tr], z[0], z[1], z[2], z[3],
+                        NCH == 2 ? z[NACC - 1] : 0.f);
+    }
+  } else {
+    __syncthreads();
+    // wave w finishes element i = w % 4 of row tiles tr = w / 4, w / 4 + KW / 4, ...
+    const int i = w & 3;
+#pragma unroll
+    for (int tr = w >> 2; tr < TR; tr += KW / 4) {
+      const int p = row0 + 16 * tr + 4 * gq + i;
+      if (p >= rowend) continue;
+      float z[NACC];
+      zsum(tr, i, z);
       lstm_fwd_epilogue<NCH>(n, p, u0 + r, z[0], z[1], z[2], z[3], NCH == 2 ? z[NACC - 1] : 0.f);
+    }
   }
 }
 
 template <int NCH, bool BF, int TR, int KW>
-__global__ void __launch_bounds__(64 * KW) k_lstm_fwd_level_sk(Net n, int off, int M) {
+__global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_fwd_level_sk(Net n, int off, int M) {
   __shared__ FwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_fwd_sk_tile<NCH, BF, TR, KW>(n, off, M, rt, ut, red);
+  lstm_fwd_sk_tile<NCH, BF, TR, KW, true>(n, off, M, rt, ut, red);
 }
 
 template <int NCH, int TR, int KW = 4>
@@ -668,8 +706,10 @@ struct BwdRed {
   float v[KW][TR][NCH == 2 ? 3 : 1][4][64];
 };
 
-// One 16*TR-position x 16-column backward tile (row tile rt, column tile ut).
-template <int NCH, bool BF, int TR, int KW = 4>
+// One 16*TR-position x 16-column backward tile (row tile rt, column tile ut);
+// wavefront roles as in the forward tile (EPI: four epilogue wavefronts
+// that prefetch the children's saved state while the others multiply).
+template <int NCH, bool BF, int TR, int KW, bool EPI>
 __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
                                                  BwdRed<NCH, TR, KW>& R) {
   constexpr int NACC = 1 + (NCH == 2 ? 2 : 0);
@@ -678,94 +718,92 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int n0 = ut * 16;
-  const float* da[TR];
-#pragma unroll
-  for (int tr = 0; tr < TR; ++tr) {
-    const int pa = row0 + 16 * tr + r;
-    da[tr] = pa < rowend ? n.dA + (size_t)pa * GW : nullptr;
-  }
-  const float* ub = n.U + (size_t)(n0 + r) * H4;   // row n0 + r of U: B^T[n][k]
-  v4f acc[TR][NACC];
-#pragma unroll
-  for (int tr = 0; tr < TR; ++tr)
-#pragma unroll
-    for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
-  auto zero8 = [](float (&v)[8]) {
-#pragma unroll
-    for (int s = 0; s < 8; ++s) v[s] = 0.f;
-  };
-  // phase 1: i|o|u columns (all four blocks with one child slot)
-  struct F1 {
-    float a[TR][8], b[8];
-  };
-  const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / KW;
-  auto load1 = [&](int c0, F1& f) {
-    const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
+  if (w < KW) {
+    const float* da[TR];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
-      if (da[tr]) ld8(da[tr] + col, f.a[tr]);
-      else zero8(f.a[tr]);
+      const int pa = row0 + 16 * tr + r;
+      da[tr] = pa < rowend ? n.dA + (size_t)pa * GW : nullptr;
     }
-    ld8(ub + col, f.b);
-  };
-  auto comp1 = [&](const F1& f) {
+    const float* ub = n.U + (size_t)(n0 + r) * H4;   // row n0 + r of U: B^T[n][k]
+    v4f acc[TR][NACC];
 #pragma unroll
-    for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
-  };
-  F1 x, y;
-  load1(w * q1, x);
-  for (int c0 = w * q1; c0 < (w + 1) * q1; c0 += 2 * kBK) {
-    load1(c0 + kBK, y);
-    comp1(x);
-    if (c0 + 2 * kBK < (w + 1) * q1) load1(c0 + 2 * kBK, x);
-    comp1(y);
-  }
-  if constexpr (NCH == 2) {
-    struct F2 {
-      float a0[TR][8], a1[TR][8], b[8];
+    for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+      for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
+    auto zero8 = [](float (&v)[8]) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) v[s] = 0.f;
     };
-    const int q2 = H / KW;
-    auto load2 = [&](int c0, F2& f) {
-      const int col = c0 + 8 * gq;
+    // phase 1: i|o|u columns (all four blocks with one child slot)
+    struct F1 {
+      float a[TR][8], b[8];
+    };
+    const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / KW;
+    auto load1 = [&](int c0, F1& f) {
+      const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) {
-        if (da[tr]) {
-          ld8(da[tr] + H + col, f.a0[tr]);
-          ld8(da[tr] + 4 * H + col, f.a1[tr]);
-        } else {
-          zero8(f.a0[tr]);
-          zero8(f.a1[tr]);
+        if (da[tr]) ld8(da[tr] + col, f.a[tr]);
+        else zero8(f.a[tr]);
+      }
+      ld8(ub + col, f.b);
+    };
+    auto comp1 = [&](const F1& f) {
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
+    };
+    F1 x, y;
+    load1(w * q1, x);
+    for (int c0 = w * q1; c0 < (w + 1) * q1; c0 += 2 * kBK) {
+      load1(c0 + kBK, y);
+      comp1(x);
+      if (c0 + 2 * kBK < (w + 1) * q1) load1(c0 + 2 * kBK, x);
+      comp1(y);
+    }
+    if constexpr (NCH == 2) {
+      struct F2 {
+        float a0[TR][8], a1[TR][8], b[8];
+      };
+      const int q2 = H / KW;
+      auto load2 = [&](int c0, F2& f) {
+        const int col = c0 + 8 * gq;
+#pragma unroll
+        for (int tr = 0; tr < TR; ++tr) {
+          if (da[tr]) {
+            ld8(da[tr] + H + col, f.a0[tr]);
+            ld8(da[tr] + 4 * H + col, f.a1[tr]);
+          } else {
+            zero8(f.a0[tr]);
+            zero8(f.a1[tr]);
+          }
         }
-      }
-      ld8(ub + H + col, f.b);
-    };
-    auto comp2 = [&](const F2& f) {
+        ld8(ub + H + col, f.b);
+      };
+      auto comp2 = [&](const F2& f) {
 #pragma unroll
-      for (int tr = 0; tr < TR; ++tr) {
-        acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
-        acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
+        for (int tr = 0; tr < TR; ++tr) {
+          acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
+          acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
+        }
+      };
+      F2 u, v;
+      load2(w * q2, u);
+      for (int c0 = w * q2; c0 < (w + 1) * q2; c0 += 2 * kBK) {
+        load2(c0 + kBK, v);
+        comp2(u);
+        if (c0 + 2 * kBK < (w + 1) * q2) load2(c0 + 2 * kBK, u);
+        comp2(v);
       }
-    };
-    F2 u, v;
-    load2(w * q2, u);
-    for (int c0 = w * q2; c0 < (w + 1) * q2; c0 += 2 * kBK) {
-      load2(c0 + kBK, v);
-      comp2(u);
-      if (c0 + 2 * kBK < (w + 1) * q2) load2(c0 + 2 * kBK, u);
-      comp2(v);
     }
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+      for (int g = 0; g < NACC; ++g)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
   }
-#pragma unroll
-  for (int tr = 0; tr < TR; ++tr)
-#pragma unroll
-    for (int g = 0; g < NACC; ++g)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
-  __syncthreads();
-  const int i = w & 3;
-#pragma unroll
-  for (int tr = w >> 2; tr < TR; tr += KW / 4) {
-    float z[NACC];
+  auto zsum = [&](int tr, int i, float (&z)[NACC]) {
 #pragma unroll
     for (int g = 0; g < NACC; ++g) {
       float t = red[0][tr][g][i][lane];
@@ -773,18 +811,49 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
       for (int q = 1; q < KW; ++q) t += red[q][tr][g][i][lane];
       z[g] = t;
     }
-    const int p = row0 + 16 * tr + 4 * gq + i;
-    if (p < rowend)
-      lstm_bwd_scatter<NCH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f, NCH == 2 ? z[NACC - 1] : 0.f);
+  };
+  if constexpr (EPI) {
+    const int i = w - KW;
+    BwdPre<NCH> pre[TR];
+    if (w >= KW) {
+#pragma unroll
+      for (int tr = 0; tr < TR; ++tr) {
+        const int p = row0 + 16 * tr + 4 * gq + i;
+        if (p < rowend) lstm_bwd_pre<NCH>(n, p, n0 + r, pre[tr]);
+      }
+    }
+    __syncthreads();
+    if (w < KW) return;
+#pragma unroll
+    for (int tr = 0; tr < TR; ++tr) {
+      const int p = row0 + 16 * tr + 4 * gq + i;
+      if (p >= rowend) continue;
+      float z[NACC];
+      zsum(tr, i, z);
+      lstm_bwd_fin<NCH>(n, n0 + r, pre[tr], z[0], NCH == 2 ? z[1] : 0.f,
+                        NCH == 2 ? z[NACC - 1] : 0.f);
+    }
+  } else {
+    __syncthreads();
+    const int i = w & 3;
+#pragma unroll
+    for (int tr = w >> 2; tr < TR; tr += KW / 4) {
+      const int p = row0 + 16 * tr + 4 * gq + i;
+      if (p >= rowend) continue;
+      float z[NACC];
+      zsum(tr, i, z);
+      lstm_bwd_scatter<NCH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f,
+                            NCH == 2 ? z[NACC - 1] : 0.f);
+    }
   }
 }
 
 template <int NCH, bool BF, int TR, int KW>
-__global__ void __launch_bounds__(64 * KW) k_lstm_bwd_level_sk(Net n, int off, int M) {
+__global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_bwd_level_sk(Net n, int off, int M) {
   __shared__ BwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_bwd_sk_tile<NCH, BF, TR, KW>(n, off, M, rt, ut, red);
+  lstm_bwd_sk_tile<NCH, BF, TR, KW, true>(n, off, M, rt, ut, red);
 }
 
 // ----------------------------------------------- persistent small-level loop
@@ -847,7 +916,7 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_persist(Net n, const int* lo, 
     const int off = lo[t], M = lo[t + 1] - off;
     const int tiles = cdiv_dev(M, 16) * ut;
     for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-      lstm_fwd_sk_tile<NCH, BF, 1>(n, off, M, tile / ut, tile % ut, red);
+      lstm_fwd_sk_tile<NCH, BF, 1, 4, false>(n, off, M, tile / ut, tile % ut, red);
       __syncthreads();
     }
     if (t + 1 < t1) grid_sync(bar, epoch);
@@ -866,7 +935,7 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_persist(Net n, const int* lo, 
     const int off = lo[t], M = lo[t + 1] - off;
     const int tiles = cdiv_dev(M, 16) * ut;
     for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-      lstm_bwd_sk_tile<NCH, BF, 1>(n, off, M, tile / ut, tile % ut, red);
+      lstm_bwd_sk_tile<NCH, BF, 1, 4, false>(n, off, M, tile / ut, tile % ut, red);
       __syncthreads();
     }
     if (t > t0) grid_sync(bar, epoch);
@@ -885,25 +954,22 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
     lstm_fwd_tile(n, off, M, s);
     return;
   }
-  if (n.H % 256 == 0 && M < 1024) {
-    // two 16-row tiles per wave once that still gives >= 2 workgroups per CU
-    const int ut = n.H / 16;
-    const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
+  if (n.H % 256 == 0) {
     const bool kw8 = (n.H / 8) % 64 == 0;
-    dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
-#define CAVS_FWD_SK(NCH, BF, TR)                                                               \
+    dim3 g(cdiv(M, 16) * (n.H / 16));
+#define CAVS_FWD_SK(NCH, BF)                                                                   \
   do {                                                                                         \
-    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ", 8>", off, M,       \
-                              (k_lstm_fwd_level_sk<NCH, BF, TR, 8>), g, dim3(512), 0, s, n, off, M); \
-    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", " #TR ", 4>", off, M,           \
-                          (k_lstm_fwd_level_sk<NCH, BF, TR, 4>), g, dim3(256), 0, s, n, off, M);  \
+    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", 1, 8>", off, M,            \
+                              (k_lstm_fwd_level_sk<NCH, BF, 1, 8>), g, dim3(768), 0, s, n, off, M); \
+    else CAVS_LAUNCH_ROWS("k_lstm_fwd_level_sk<" #NCH ", " #BF ", 1, 4>", off, M,                \
+                          (k_lstm_fwd_level_sk<NCH, BF, 1, 4>), g, dim3(512), 0, s, n, off, M);  \
   } while (0)
     if (n.N == 2) {
-      if (n.bf) { if (tr2) CAVS_FWD_SK(2, true, 2); else CAVS_FWD_SK(2, true, 1); }
-      else { if (tr2) CAVS_FWD_SK(2, false, 2); else CAVS_FWD_SK(2, false, 1); }
+      if (n.bf) CAVS_FWD_SK(2, true);
+      else CAVS_FWD_SK(2, false);
     } else {
-      if (n.bf) { if (tr2) CAVS_FWD_SK(1, true, 2); else CAVS_FWD_SK(1, true, 1); }
-      else { if (tr2) CAVS_FWD_SK(1, false, 2); else CAVS_FWD_SK(1, false, 1); }
+      if (n.bf) CAVS_FWD_SK(1, true);
+      else CAVS_FWD_SK(1, false);
     }
 #undef CAVS_FWD_SK
     return;
@@ -956,23 +1022,21 @@ void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
     return;
   }
   if (n.H % 256 == 0) {
-    const int ut = n.H / 16;
-    const bool tr2 = (long)cdiv(M, 32) * ut >= 512;
     const bool kw8 = (n.H / 8) % 64 == 0 && (3 * n.H / 8) % 64 == 0;
-    dim3 g(cdiv(M, tr2 ? 32 : 16) * ut);
-#define CAVS_BWD_SK(NCH, BF, TR)                                                               \
+    dim3 g(cdiv(M, 16) * (n.H / 16));
+#define CAVS_BWD_SK(NCH, BF)                                                                   \
   do {                                                                                         \
-    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ", 8>", off, M,       \
-                              (k_lstm_bwd_level_sk<NCH, BF, TR, 8>), g, dim3(512), 0, s, n, off, M); \
-    else CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", " #TR ", 4>", off, M,           \
-                          (k_lstm_bwd_level_sk<NCH, BF, TR, 4>), g, dim3(256), 0, s, n, off, M);  \
+    if (kw8) CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", 1, 8>", off, M,            \
+                              (k_lstm_bwd_level_sk<NCH, BF, 1, 8>), g, dim3(768), 0, s, n, off, M); \
+    else CAVS_LAUNCH_ROWS("k_lstm_bwd_level_sk<" #NCH ", " #BF ", 1, 4>", off, M,                \
+                          (k_lstm_bwd_level_sk<NCH, BF, 1, 4>), g, dim3(512), 0, s, n, off, M);  \
   } while (0)
     if (n.N == 2) {
-      if (n.bf) { if (tr2) CAVS_BWD_SK(2, true, 2); else CAVS_BWD_SK(2, true, 1); }
-      else { if (tr2) CAVS_BWD_SK(2, false, 2); else CAVS_BWD_SK(2, false, 1); }
+      if (n.bf) CAVS_BWD_SK(2, true);
+      else CAVS_BWD_SK(2, false);
     } else {
-      if (n.bf) { if (tr2) CAVS_BWD_SK(1, true, 2); else CAVS_BWD_SK(1, true, 1); }
-      else { if (tr2) CAVS_BWD_SK(1, false, 2); else CAVS_BWD_SK(1, false, 1); }
+      if (n.bf) CAVS_BWD_SK(1, true);
+      else CAVS_BWD_SK(1, false);
     }
 #undef CAVS_BWD_SK
     return;

@@ -6,35 +6,68 @@
 
 namespace cavs {
 
+// The epilogues are split into a part that needs only saved state (issued
+// early, e.g. by wavefronts that wait for the matrix product) and a part
+// that consumes the product.
+
+// ------------------------------------------------------------------ forward
+// Everything the forward epilogue of position p, unit j reads besides the
+// matrix-product terms: bias (+ pulled input term) and the children's c.
+template <int NCH>
+struct FwdPre {
+  float bi, bo, bu, pi, po, pu, fb;
+  float cc[NCH];
+  int cp[NCH], v, pulled;
+};
+
+template <int NCH>
+__device__ __forceinline__ void lstm_fwd_pre(const Net& n, int p, int j, FwdPre<NCH>& q) {
+  const int H = n.H;
+  const int pr = n.pull_pos[p];
+  q.pulled = pr >= 0;
+  q.bi = n.b[G_I * H + j];
+  q.bo = n.b[G_O * H + j];
+  q.bu = n.b[G_U * H + j];
+  q.fb = n.b[G_F * H + j];
+  q.pi = q.po = q.pu = 0.f;
+  if (pr >= 0) {
+    const float* Pp = n.P + (size_t)p * 4 * H;
+    q.pi = Pp[G_I * H + j];
+    q.po = Pp[G_O * H + j];
+    q.pu = Pp[G_U * H + j];
+    q.fb += Pp[G_F * H + j];
+  }
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    q.cp[k] = n.child_pos[(size_t)p * NCH + k];
+    q.cc[k] = q.cp[k] >= 0 ? n.Cs[(size_t)q.cp[k] * H + j] : 0.f;
+  }
+  q.v = n.order[p];
+}
+
 // Gates, cell update and the scatter of (c, h) for position p, unit j, from
 // the matrix-product parts of the pre-activations (shared by both precisions).
 template <int NCH>
-__device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, float zi, float zo,
-                                                  float zu, float zf0, float zf1) {
-  const int H = n.H, H4 = 4 * H;
-  const int pr = n.pull_pos[p];
-  float ai = zi + n.b[G_I * H + j], ao = zo + n.b[G_O * H + j], au = zu + n.b[G_U * H + j];
-  float fb = n.b[G_F * H + j];
-  if (pr >= 0) {
-    const float* Pp = n.P + (size_t)p * H4;
-    ai += Pp[G_I * H + j];
-    ao += Pp[G_O * H + j];
-    au += Pp[G_U * H + j];
-    fb += Pp[G_F * H + j];
+__device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const FwdPre<NCH>& q,
+                                             float zi, float zo, float zu, float zf0, float zf1) {
+  const int H = n.H;
+  float ai = zi + q.bi, ao = zo + q.bo, au = zu + q.bu;
+  if (q.pulled) {
+    ai += q.pi;
+    ao += q.po;
+    au += q.pu;
   }
   const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanhf(au);
   float c = ig * ug;
   float f0 = 0.f, f1 = 0.f;
-  const int cp0 = n.child_pos[(size_t)p * NCH];
-  if (cp0 >= 0) {
-    f0 = sigmoidf_(zf0 + fb);
-    c += f0 * n.Cs[(size_t)cp0 * H + j];
+  if (q.cp[0] >= 0) {
+    f0 = sigmoidf_(zf0 + q.fb);
+    c += f0 * q.cc[0];
   }
   if constexpr (NCH == 2) {
-    const int cp1 = n.child_pos[(size_t)p * NCH + 1];
-    if (cp1 >= 0) {
-      f1 = sigmoidf_(zf1 + fb);
-      c += f1 * n.Cs[(size_t)cp1 * H + j];
+    if (q.cp[NCH - 1] >= 0) {
+      f1 = sigmoidf_(zf1 + q.fb);
+      c += f1 * q.cc[NCH - 1];
     }
   }
   const float h = og * tanhf(c);
@@ -46,77 +79,137 @@ __device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, fl
   g[2 * H + j] = og;
   g[3 * H + j] = ug;
   if constexpr (NCH == 2) g[4 * H + j] = f1;
-  const int v = n.order[p];
-  n.h_out[(size_t)v * H + j] = h;
-  if (n.c_out) n.c_out[(size_t)v * H + j] = c;
+  n.h_out[(size_t)q.v * H + j] = h;
+  if (n.c_out) n.c_out[(size_t)q.v * H + j] = c;
+}
+
+template <int NCH>
+__device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, float zi, float zo,
+                                                  float zu, float zf0, float zf1) {
+  FwdPre<NCH> q;
+  lstm_fwd_pre<NCH>(n, p, j, q);
+  lstm_fwd_fin<NCH>(n, p, j, q, zi, zo, zu, zf0, zf1);
 }
 
 // ----------------------------------------------------------------- backward
-// dA of position p, unit j, and the dc scatter to its children, given the
-// parent's contributions gh = dL/dh and gcin = dL/dc (zero at a root); the
-// vertex's own loss term is added here.
-__device__ __forceinline__ void lstm_bwd_gates_elem(const Net& n, int p, int j, float gh,
-                                                    float gcin) {
+// Everything dA of position p, unit j reads besides the parent's dL/dh: the
+// vertex's own loss term of dL/dh, dL/dc from the parent, the saved gates and
+// c, and the children's f_k and c_k.
+template <int NCH>
+struct GatePre {
+  float lg, gcin, ig, og, ug, c;
+  float fk[NCH], ck[NCH];
+  int cp[NCH];
+};
+
+template <int NCH>
+__device__ __forceinline__ void lstm_gates_pre(const Net& n, int p, int j, float gcin,
+                                               GatePre<NCH>& q) {
   const int H = n.H;
-  const int q = n.push_pos[p];
-  if (q >= 0) {
+  const int push = n.push_pos[p];
+  float s = 0.f;
+  if (push >= 0) {
     if (n.loss == CAVS_LOSS_CE) {
       const float* dz = n.dZ + (size_t)p * n.C;
       const float* ws = n.Ws + (size_t)j * n.C;
-      float s = 0.f;
       for (int c = 0; c < n.C; ++c) s += dz[c] * ws[c];
-      gh += s;
     } else {
-      gh += (n.Hs[(size_t)p * H + j] - n.Y[(size_t)q * H + j]) * n.inv_denom;
+      s = (n.Hs[(size_t)p * H + j] - n.Y[(size_t)push * H + j]) * n.inv_denom;
     }
   }
+  q.lg = s;
+  q.gcin = gcin;
   const float* g = n.Gs + (size_t)p * n.GW;
-  const float ig = g[j], og = g[2 * H + j], ug = g[3 * H + j];
-  const float c = n.Cs[(size_t)p * H + j];
-  const float tau = tanhf(c);
-  const float d_o = gh * tau * og * (1.f - og);
-  const float gc = gcin + gh * og * (1.f - tau * tau);
-  const float d_i = gc * ug * ig * (1.f - ig);
-  const float d_u = gc * ig * (1.f - ug * ug);
+  q.ig = g[j];
+  q.og = g[2 * H + j];
+  q.ug = g[3 * H + j];
+  q.c = n.Cs[(size_t)p * H + j];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int cp = n.child_pos[(size_t)p * NCH + k];
+    q.cp[k] = cp;
+    q.fk[k] = cp >= 0 ? g[(k == 0 ? H : 4 * H) + j] : 0.f;
+    q.ck[k] = cp >= 0 ? n.Cs[(size_t)cp * H + j] : 0.f;
+  }
+}
+
+// dA of position p, unit j, and the dc scatter to its children, from the
+// parent's dL/dh (gh_parent; zero at a root) and the prefetched state.
+template <int NCH>
+__device__ __forceinline__ void lstm_gates_fin(const Net& n, int p, int j, float gh_parent,
+                                               const GatePre<NCH>& q) {
+  const int H = n.H;
+  const float gh = gh_parent + q.lg;
+  const float tau = tanhf(q.c);
+  const float d_o = gh * tau * q.og * (1.f - q.og);
+  const float gc = q.gcin + gh * q.og * (1.f - tau * tau);
+  const float d_i = gc * q.ug * q.ig * (1.f - q.ig);
+  const float d_u = gc * q.ig * (1.f - q.ug * q.ug);
   float* da = n.dA + (size_t)p * n.GW;
-  for (int k = 0; k < n.N; ++k) {
-    const int cp = n.child_pos[(size_t)p * n.N + k];
-    const int col = k == 0 ? H : 4 * H;
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
     float d_f = 0.f;
-    if (cp >= 0) {
-      const float fk = g[col + j];
-      d_f = gc * n.Cs[(size_t)cp * H + j] * fk * (1.f - fk);
-      n.dCp[(size_t)cp * H + j] = gc * fk;
+    if (q.cp[k] >= 0) {
+      d_f = gc * q.ck[k] * q.fk[k] * (1.f - q.fk[k]);
+      n.dCp[(size_t)q.cp[k] * H + j] = gc * q.fk[k];
     }
-    da[col + j] = d_f;
+    da[(k == 0 ? H : 4 * H) + j] = d_f;
   }
   da[j] = d_i;
   da[2 * H + j] = d_o;
   da[3 * H + j] = d_u;
 }
 
-// Epilogue of the backward level product for position p, unit col: child k
-// receives dL/dh_k = zh + zf_k.  p is the child's only parent, so that is the
-// child's whole dL/dh: a child at a position >= n.fuse_from (the small top
-// levels) gets its dA and dc scatter here at once (its dL/dc was scattered
-// when p's dA was formed); a child below that stores dL/dh for the
-// elementwise gates kernel of its level.
+// dA of position p, unit j given the parent's contributions gh = dL/dh and
+// gcin = dL/dc (zero at a root).
+template <int NCH>
+__device__ __forceinline__ void lstm_gates_elem(const Net& n, int p, int j, float gh, float gcin) {
+  GatePre<NCH> q;
+  lstm_gates_pre<NCH>(n, p, j, gcin, q);
+  lstm_gates_fin<NCH>(n, p, j, gh, q);
+}
+
+// Backward level epilogue for position p, unit col: child k receives
+// dL/dh_k = zh + zf_k.  p is the child's only parent, so that is the child's
+// whole dL/dh: a child at a position >= n.fuse_from (the small top levels)
+// gets its dA and dc scatter here at once (its dL/dc was scattered when p's
+// dA was formed); a child below that stores dL/dh for the elementwise gates
+// kernel of its level.  BwdPre holds what can be read before the product.
+template <int NCH>
+struct BwdPre {
+  GatePre<NCH> q[NCH];
+  int cp[NCH];
+};
+
+template <int NCH>
+__device__ __forceinline__ void lstm_bwd_pre(const Net& n, int p, int col, BwdPre<NCH>& e) {
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int cp = n.child_pos[(size_t)p * NCH + k];
+    e.cp[k] = cp;
+    if (cp >= n.fuse_from) lstm_gates_pre<NCH>(n, cp, col, n.dCp[(size_t)cp * n.H + col], e.q[k]);
+  }
+}
+
+template <int NCH>
+__device__ __forceinline__ void lstm_bwd_fin(const Net& n, int col, const BwdPre<NCH>& e, float zh,
+                                             float zf0, float zf1) {
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int cp = e.cp[k];
+    if (cp < 0) continue;
+    const float gh = zh + (k == 0 ? zf0 : zf1);
+    if (cp >= n.fuse_from) lstm_gates_fin<NCH>(n, cp, col, gh, e.q[k]);
+    else n.dHp[(size_t)cp * n.H + col] = gh;
+  }
+}
+
 template <int NCH>
 __device__ __forceinline__ void lstm_bwd_scatter(const Net& n, int p, int col, float zh, float zf0,
                                                  float zf1) {
-  const int H = n.H;
-  const int cp0 = n.child_pos[(size_t)p * NCH];
-  if (cp0 >= 0) {
-    if (cp0 >= n.fuse_from) lstm_bwd_gates_elem(n, cp0, col, zh + zf0, n.dCp[(size_t)cp0 * H + col]);
-    else n.dHp[(size_t)cp0 * H + col] = zh + zf0;
-  }
-  if constexpr (NCH == 2) {
-    const int cp1 = n.child_pos[(size_t)p * NCH + 1];
-    if (cp1 >= 0) {
-      if (cp1 >= n.fuse_from) lstm_bwd_gates_elem(n, cp1, col, zh + zf1, n.dCp[(size_t)cp1 * H + col]);
-      else n.dHp[(size_t)cp1 * H + col] = zh + zf1;
-    }
-  }
+  BwdPre<NCH> e;
+  lstm_bwd_pre<NCH>(n, p, col, e);
+  lstm_bwd_fin<NCH>(n, col, e, zh, zf0, zf1);
 }
 
 // Register-direct MFMA chunk: a[s], b[s] hold k = 8g + s of a 32-deep chunk

@@ -4,54 +4,141 @@
 // element fetched from L2 feeds many MFMAs.
 //
 // A workgroup (4 wavefronts, 2 x 2) owns BM positions x BU hidden units.
-// Each 32-deep chunk of both operands is copied global -> registers -> LDS
-// with two LDS stages: the loads of chunk c+1 are in flight while chunk c is
-// multiplied, and one barrier per chunk separates the stages.  Rows are
-// stored k-contiguous (padded to kLDK floats), so every MFMA fragment is two
-// 16-byte LDS reads in the permuted-K order of mfma_chunk8.
+// Operands move in 32-deep chunks straight from global memory into LDS
+// (global_load_lds_dwordx4: lane i of a wavefront writes 16 bytes at
+// m0 + 16 i, so one copy fills eight 128-byte LDS rows).  S stages form a
+// ring: the copies of chunk c+S-1 are in flight while chunk c is multiplied.
+// Each LDS row holds the 32 k of one operand row with its eight 16-byte
+// quads XOR-swizzled by (row & 7), and each MFMA fragment is two 16-byte
+// reads in the permuted-K order of mfma_chunk8.
+//
+// The copies are issued by inline asm, so the compiler neither counts them
+// as LDS writes (it would otherwise wait for every copy in flight before
+// each LDS read) nor orders them: the kernel waits for its own copies with
+// s_waitcnt vmcnt(n) and separates the stages with a bare s_barrier (the
+// workgroup fence of __syncthreads would also wait for every copy).  No
+// other vector memory operation is issued inside the chunk loop, so vmcnt
+// counts exactly these copies; the stages are distinct LDS variables.
 //
 // Forward: A = the gathered child rows h_0, h_1 (h~ = h_0 + h_1 is formed in
-// registers), B = U^T (U transposed once per forward pass so that B rows are
-// k-contiguous too); five accumulators per 16 x 16 block (i, o, u from h~,
-// f_0 from h_0, f_1 from h_1).
+// registers; an absent child reads a zero row), B = U^T (U transposed once
+// per forward pass so that B rows are k-contiguous too); five accumulators
+// per 16 x 16 block (i, o, u from h~, f_0 from h_0, f_1 from h_1).
 // Backward: A = dA rows of the level, B = U (row n of U is column n of U^T);
 // phase 1 contracts the i|o|u columns, phase 2 the f_0 and f_1 columns with
 // the shared U_f block.
+#include <type_traits>
+
 #include "lstm_dev.h"
 
 namespace cavs {
 namespace {
 
-constexpr int kLDK = kBK + 4;
-
-// UT[c][k] = U[k][c] for the [H, 4H] recurrent weight.
+// UT[c][k] = U[k][c] for the [H, 4H] recurrent weight; block (0, 0) also
+// clears the zero row read for absent children.
 __global__ void __launch_bounds__(256) k_transpose_u(const float* __restrict__ U,
-                                                     float* __restrict__ UT, int H) {
+                                                     float* __restrict__ UT,
+                                                     float* __restrict__ zrow, int H) {
   __shared__ float t[32][33];
   const int H4 = 4 * H;
   const int c0 = blockIdx.x * 32, k0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int j = threadIdx.x; j < H; j += 256) zrow[j] = 0.f;
   for (int y = ty; y < 32; y += 8) t[y][tx] = U[(size_t)(k0 + y) * H4 + c0 + tx];
   __syncthreads();
   for (int y = ty; y < 32; y += 8) UT[(size_t)(c0 + y) * H + k0 + tx] = t[tx][y];
 }
 
-__device__ __forceinline__ void lds8(const float* p, float (&v)[8]) {
-  const float4 x = *reinterpret_cast<const float4*>(p);
-  const float4 y = *reinterpret_cast<const float4*>(p + 4);
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt at max
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16 bytes per lane from g into LDS at lds_addr + 16 * lane.
+__device__ __forceinline__ void copy16_to_lds(const float* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds_addr) : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr_of(const float* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
+}
+
+// k = 8 gq .. 8 gq + 7 of LDS row `row` (quads swizzled by row & 7)
+__device__ __forceinline__ void frag_sw(const float* L, int row, int gq, float (&v)[8]) {
+  const float* rp = L + row * 32;
+  const int sw = row & 7;
+  const float4 x = *reinterpret_cast<const float4*>(rp + 4 * ((2 * gq) ^ sw));
+  const float4 y = *reinterpret_cast<const float4*>(rp + 4 * ((2 * gq + 1) ^ sw));
   v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
 }
 
-template <int NCH, bool BF, int BM, int BU>
+template <int K>
+using IC = std::integral_constant<int, K>;
+
+// Stage ring: S distinct LDS arrays of ROWS x 32 floats, selected at compile
+// time (the chunk loop is unrolled by S).
+template <int ROWS, int S>
+struct Ring {
+  float* s0;
+  float* s1;
+  float* s2;
+  float* s3;
+  template <int K>
+  __device__ __forceinline__ float* at(IC<K>) const {
+    if constexpr (K == 0) return s0;
+    else if constexpr (K == 1) return s1;
+    else if constexpr (K == 2) return s2;
+    else return s3;
+  }
+};
+
+// Runs chunks 0 .. nch-1 through an S-stage ring: issue(stage, c) starts the
+// IPW copies of chunk c, compute(stage ptr, c) consumes it.
+template <int S, int IPW, class Issue, class Compute, class RingT>
+__device__ __forceinline__ void ring_loop(int nch, const RingT& ring, Issue&& issue,
+                                          Compute&& compute) {
+  issue(IC<0>{}, 0);
+  if constexpr (S > 2) if (1 < nch) issue(IC<1>{}, 1);
+  if constexpr (S > 3) if (2 < nch) issue(IC<2>{}, 2);
+  auto step = [&](auto sc, int c) {
+    constexpr int k = decltype(sc)::value;
+    if (c + S - 2 < nch) wait_vmcnt<(S - 2) * IPW>();
+    else wait_vmcnt<0>();
+    barrier_nofence();
+    if (c + S - 1 < nch) issue(IC<(k + S - 1) % S>{}, c + S - 1);
+    compute(ring.at(sc), c);
+  };
+  for (int c = 0; c < nch; c += S) {
+    step(IC<0>{}, c);
+    if (c + 1 < nch) step(IC<1>{}, c + 1);
+    if constexpr (S > 2) if (c + 2 < nch) step(IC<2>{}, c + 2);
+    if constexpr (S > 3) if (c + 3 < nch) step(IC<3>{}, c + 3);
+  }
+}
+
+template <int NCH, bool BF, int BM, int BU, int S>
 __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TU = BU / 32;   // 16 x 16 blocks per wavefront
   constexpr int NACC = 3 + NCH;
-  constexpr int A_PER = BM * NCH * 8 / 256;   // float4 per thread per chunk
-  constexpr int B_PER = 4 * BU * 8 / 256;
-  static_assert(A_PER * 256 == BM * NCH * 8 && B_PER * 256 == 4 * BU * 8, "tile split");
-  __shared__ __attribute__((aligned(16))) float As[2][NCH][BM][kLDK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][4][BU][kLDK];
+  constexpr int AROWS = NCH * BM, ROWS = AROWS + 4 * BU;
+  constexpr int IPW = ROWS / 32;               // copies per wavefront per chunk
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
 
   const int H = n.H;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
@@ -60,42 +147,26 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   xcd_tile(H / BU, rt, ut);
   const int row0 = off + rt * BM, rowend = off + M, u0 = ut * BU;
 
-  const float* asrc[A_PER];
-  int adst[A_PER];
+  // source of each of this lane's copies: LDS rows [0, AROWS) are child
+  // rows (child slot ch of position row0 + rr), the rest rows of U^T
+  const float* src[IPW];
 #pragma unroll
-  for (int a = 0; a < A_PER; ++a) {
-    const int idx = tid + 256 * a, row = idx / (NCH * 8), ch = (idx / 8) % NCH, q = idx & 7;
-    adst[a] = (ch * BM + row) * kLDK + 4 * q;
-    asrc[a] = nullptr;
-    const int p = row0 + row;
-    if (p < rowend) {
-      const int cp = n.child_pos[(size_t)p * NCH + ch];
-      if (cp >= 0) asrc[a] = n.Hs + (size_t)cp * H + 4 * q;
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    if (row < AROWS) {
+      const int ch = row / BM, p = row0 + row % BM;
+      const float* ptr = n.zrow;
+      if (p < rowend) {
+        const int cp = n.child_pos[(size_t)p * NCH + ch];
+        if (cp >= 0) ptr = n.Hs + (size_t)cp * H;
+      }
+      src[t] = ptr + 4 * qg;
+    } else {
+      const int b = row - AROWS, g = b / BU, u = b % BU;
+      src[t] = n.UT + (size_t)(g * H + u0 + u) * H + 4 * qg;
     }
   }
-  const float* bsrc[B_PER];
-  int bdst[B_PER];
-#pragma unroll
-  for (int b = 0; b < B_PER; ++b) {
-    const int idx = tid + 256 * b, g = idx / (BU * 8), u = (idx / 8) % BU, q = idx & 7;
-    bsrc[b] = n.UT + (size_t)(g * H + u0 + u) * H + 4 * q;
-    bdst[b] = (g * BU + u) * kLDK + 4 * q;
-  }
-  float4 ra[A_PER], rb[B_PER];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a) ra[a] = asrc[a] ? ldg4(asrc[a] + k0) : f4zero();
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) rb[b] = ldg4(bsrc[b] + k0);
-  };
-  auto sstore = [&](int st) {
-    float* A = &As[st][0][0][0];
-    float* B = &Bs[st][0][0][0];
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a) st4(A + adst[a], ra[a]);
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) st4(B + bdst[b], rb[b]);
-  };
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
 
   v4f acc[TM][TU][NACC];
 #pragma unroll
@@ -105,26 +176,25 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tm][tu][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  const int nch = H / kBK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const int st = c & 1;
-    if (c + 1 < nch) gload((c + 1) * kBK);
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+  };
+  auto compute = [&](const float* Ls, int) {
     float bfr[4][TU][8];
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
       for (int tu = 0; tu < TU; ++tu)
-        lds8(&Bs[st][g][wu * (BU / 2) + tu * 16 + r][8 * gq], bfr[g][tu]);
+        frag_sw(Ls, AROWS + g * BU + wu * (BU / 2) + tu * 16 + r, gq, bfr[g][tu]);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
-      const int row = wr * (BM / 2) + tm * 16 + r;
+      const int ra = wr * (BM / 2) + tm * 16 + r;
       float a0[8], a1[8], ah[8];
-      lds8(&As[st][0][row][8 * gq], a0);
+      frag_sw(Ls, ra, gq, a0);
       if constexpr (NCH == 2) {
-        lds8(&As[st][NCH - 1][row][8 * gq], a1);
+        frag_sw(Ls, BM + ra, gq, a1);
 #pragma unroll
         for (int s = 0; s < 8; ++s) ah[s] = a0[s] + a1[s];
       } else {
@@ -140,9 +210,8 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
         if constexpr (NCH == 2) acc[tm][tu][4] = mfma_chunk8<BF>(a1, bfr[G_F][tu], acc[tm][tu][4]);
       }
     }
-    if (c + 1 < nch) sstore(st ^ 1);
-    __syncthreads();
-  }
+  };
+  ring_loop<S, IPW>(H / kBK, ring, issue, compute);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -158,16 +227,20 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
       }
 }
 
-template <int NCH, bool BF, int BM, int BN>
+template <int NCH, bool BF, int BM, int BN, int S>
 __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TN = BN / 32;
-  constexpr int NA = NCH == 2 ? 2 : 1;        // A operands of phase 2
+  constexpr int NA = NCH == 2 ? 2 : 1;         // A operands of phase 2
   constexpr int NACC = NCH == 2 ? 3 : 1;
-  constexpr int A_PER = BM * 8 / 256;         // float4 per thread per operand per chunk
-  constexpr int B_PER = BN * 8 / 256;
-  static_assert(A_PER * 256 == BM * 8 && B_PER * 256 == BN * 8, "tile split");
-  __shared__ __attribute__((aligned(16))) float As[2][NA][BM][kLDK];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN][kLDK];
+  // stage rows: [0, BM) A0, [BM, BM + BN) B, [BM + BN, ROWS) A1 (phase 2)
+  constexpr int ROWS = NA * BM + BN;
+  constexpr int IPW1 = (BM + BN) / 32, IPW = ROWS / 32;
+  static_assert(IPW1 * 32 == BM + BN && IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
 
   const int H = n.H, H4 = 4 * H, GW = n.GW;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
@@ -176,56 +249,31 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   xcd_tile(H / BN, rt, ut);
   const int row0 = off + rt * BM, rowend = off + M, n0 = ut * BN;
 
-  const float* asrc[A_PER];
-  int adst[A_PER];
+  // Phase-1 chunks fill rows [0, BM + BN) with IPW1 copies per wavefront,
+  // phase-2 chunks all ROWS with IPW; a phase-1 chunk repeats its first
+  // copies so that every chunk issues IPW (same data to the same place),
+  // which keeps the vmcnt bookkeeping of the ring uniform.  Rows past the
+  // level read its last row (their products are never stored).
+  const float* src1[IPW1];
+  const float* src2[IPW];
 #pragma unroll
-  for (int a = 0; a < A_PER; ++a) {
-    const int idx = tid + 256 * a, row = idx / 8, q = idx & 7;
-    const int p = row0 + row;
-    asrc[a] = p < rowend ? n.dA + (size_t)p * GW + 4 * q : nullptr;
-    adst[a] = row * kLDK + 4 * q;
+  for (int t = 0; t < IPW1; ++t) {
+    const int row = (w * IPW1 + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const float* ptr;
+    if (row < BM) ptr = n.dA + (size_t)min(row0 + row, rowend - 1) * GW;
+    else ptr = n.U + (size_t)(n0 + row - BM) * H4;
+    src1[t] = ptr + 4 * qg;
   }
-  const float* bsrc[B_PER];
-  int bdst[B_PER];
 #pragma unroll
-  for (int b = 0; b < B_PER; ++b) {
-    const int idx = tid + 256 * b, nn = idx / 8, q = idx & 7;
-    bsrc[b] = n.U + (size_t)(n0 + nn) * H4 + 4 * q;
-    bdst[b] = nn * kLDK + 4 * q;
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const float* ptr;
+    if (row < BM) ptr = n.dA + (size_t)min(row0 + row, rowend - 1) * GW;             // f_0 at +H
+    else if (row < BM + BN) ptr = n.U + (size_t)(n0 + row - BM) * H4;               // U_f at +H
+    else ptr = n.dA + (size_t)min(row0 + row - BM - BN, rowend - 1) * GW + 3 * H;   // f_1 at +4H
+    src2[t] = ptr + 4 * qg;
   }
-  // phase 1: NCH == 2 contracts i|o|u (dA / U columns [0,H) and [2H,4H));
-  // NCH == 1 all 4H columns.  Phase 2 (NCH == 2): f_0 at H, f_1 at 4H of dA,
-  // both against U columns [H, 2H).
   const int nc1 = (NCH == 2 ? 3 * H : H4) / kBK, nc2 = NCH == 2 ? H / kBK : 0;
-  const int nch = nc1 + nc2;
-  float4 ra[NA][A_PER], rb[B_PER];
-  auto gload = [&](int c) {
-    if (c < nc1) {
-      const int k0 = c * kBK, col = (NCH == 2 && k0 >= H) ? k0 + H : k0;
-#pragma unroll
-      for (int a = 0; a < A_PER; ++a) ra[0][a] = asrc[a] ? ldg4(asrc[a] + col) : f4zero();
-#pragma unroll
-      for (int b = 0; b < B_PER; ++b) rb[b] = ldg4(bsrc[b] + col);
-    } else {
-      const int k0 = (c - nc1) * kBK;
-#pragma unroll
-      for (int a = 0; a < A_PER; ++a) {
-        ra[0][a] = asrc[a] ? ldg4(asrc[a] + H + k0) : f4zero();
-        ra[NA - 1][a] = asrc[a] ? ldg4(asrc[a] + 4 * H + k0) : f4zero();
-      }
-#pragma unroll
-      for (int b = 0; b < B_PER; ++b) rb[b] = ldg4(bsrc[b] + H + k0);
-    }
-  };
-  auto sstore = [&](int st, int c) {
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a) st4(&As[st][0][0][0] + adst[a], ra[0][a]);
-    if (NCH == 2 && c >= nc1)
-#pragma unroll
-      for (int a = 0; a < A_PER; ++a) st4(&As[st][NA - 1][0][0] + adst[a], ra[NA - 1][a]);
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) st4(&Bs[st][0][0] + bdst[b], rb[b]);
-  };
 
   v4f acc[TM][TN][NACC];
 #pragma unroll
@@ -235,29 +283,39 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tm][tn][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  gload(0);
-  sstore(0, 0);
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    const int st = c & 1;
-    if (c + 1 < nch) gload(c + 1);
+  auto issue = [&](auto sc, int c) {
+    const uint32_t stage = lds_addr_of(ring.at(sc));
+    if (c < nc1) {
+      const uint32_t base = __builtin_amdgcn_readfirstlane(stage + 4u * (w * IPW1 * 256));
+      const int k0 = c * kBK, col = (NCH == 2 && k0 >= H) ? k0 + H : k0;
+#pragma unroll
+      for (int t = 0; t < IPW; ++t) copy16_to_lds(src1[t % IPW1] + col, base + 1024u * (t % IPW1));
+    } else {
+      const uint32_t base = __builtin_amdgcn_readfirstlane(stage + 4u * (w * IPW * 256));
+      const int k0 = H + (c - nc1) * kBK;
+#pragma unroll
+      for (int t = 0; t < IPW; ++t) copy16_to_lds(src2[t] + k0, base + 1024u * t);
+    }
+  };
+  auto compute = [&](const float* Ls, int c) {
     float bfr[TN][8];
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) lds8(&Bs[st][wn * (BN / 2) + tn * 16 + r][8 * gq], bfr[tn]);
+    for (int tn = 0; tn < TN; ++tn) frag_sw(Ls, BM + wn * (BN / 2) + tn * 16 + r, gq, bfr[tn]);
     if (c < nc1) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         float a[8];
-        lds8(&As[st][0][wr * (BM / 2) + tm * 16 + r][8 * gq], a);
+        frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, a);
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) acc[tm][tn][0] = mfma_chunk8<BF>(a, bfr[tn], acc[tm][tn][0]);
       }
     } else if constexpr (NCH == 2) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
+        const int ra = wr * (BM / 2) + tm * 16 + r;
         float a0[8], a1[8];
-        lds8(&As[st][0][wr * (BM / 2) + tm * 16 + r][8 * gq], a0);
-        lds8(&As[st][NA - 1][wr * (BM / 2) + tm * 16 + r][8 * gq], a1);
+        frag_sw(Ls, ra, gq, a0);
+        frag_sw(Ls, BM + BN + ra, gq, a1);
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
           acc[tm][tn][1] = mfma_chunk8<BF>(a0, bfr[tn], acc[tm][tn][1]);
@@ -265,9 +323,8 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
         }
       }
     }
-    if (c + 1 < nch) sstore(st ^ 1, c + 1);
-    __syncthreads();
-  }
+  };
+  ring_loop<S, IPW>(nc1 + nc2, ring, issue, compute);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -287,22 +344,22 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
 
 void lstm_transpose_u(const Net& n, hipStream_t s) {
   CAVS_LAUNCH("k_transpose_u", k_transpose_u, dim3(4 * n.H / 32, n.H / 32), dim3(256), 0, s, n.U,
-              n.UT, n.H);
+              n.UT, n.zrow, n.H);
 }
 
-#define CAVS_TILE_LAUNCH(KIND, NCH, BF, BM, BU)                                                \
-  CAVS_LAUNCH_ROWS("k_lstm_" #KIND "_tile<" #NCH ", " #BF ", " #BM ", " #BU ">", off, M,        \
-                   (k_lstm_##KIND##_tile<NCH, BF, BM, BU>),                                     \
+#define CAVS_TILE_LAUNCH(KIND, NCH, BF, BM, BU, S)                                             \
+  CAVS_LAUNCH_ROWS("k_lstm_" #KIND "_tile<" #NCH ", " #BF ", " #BM ", " #BU ", " #S ">", off, M, \
+                   (k_lstm_##KIND##_tile<NCH, BF, BM, BU, S>),                                  \
                    dim3(cdiv(M, BM) * (n.H / BU)), dim3(256), 0, s, n, off, M)
 
-#define CAVS_TILE_DISPATCH(KIND, BM, BU)                                                       \
+#define CAVS_TILE_DISPATCH(KIND, BM, BU, S)                                                    \
   do {                                                                                         \
     if (n.N == 2) {                                                                            \
-      if (n.bf) CAVS_TILE_LAUNCH(KIND, 2, true, BM, BU);                                       \
-      else CAVS_TILE_LAUNCH(KIND, 2, false, BM, BU);                                           \
+      if (n.bf) CAVS_TILE_LAUNCH(KIND, 2, true, BM, BU, S);                                    \
+      else CAVS_TILE_LAUNCH(KIND, 2, false, BM, BU, S);                                        \
     } else {                                                                                   \
-      if (n.bf) CAVS_TILE_LAUNCH(KIND, 1, true, BM, BU);                                       \
-      else CAVS_TILE_LAUNCH(KIND, 1, false, BM, BU);                                           \
+      if (n.bf) CAVS_TILE_LAUNCH(KIND, 1, true, BM, BU, S);                                    \
+      else CAVS_TILE_LAUNCH(KIND, 1, false, BM, BU, S);                                        \
     }                                                                                          \
   } while (0)
 
@@ -310,14 +367,16 @@ bool lstm_tile_applies(const Net& n, int M) {
   return n.H % 256 == 0 && M >= kTileMinRows;
 }
 
+// Tile shapes and ring depths measured on MI355X (H = 512): 64-position
+// tiles once a level fills the chip twice over, 32 below.
 void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s) {
-  if (M >= 1024) CAVS_TILE_DISPATCH(fwd, 64, 32);
-  else CAVS_TILE_DISPATCH(fwd, 32, 32);
+  if (M >= 1024) CAVS_TILE_DISPATCH(fwd, 64, 32, 2);
+  else CAVS_TILE_DISPATCH(fwd, 32, 32, 3);
 }
 
 void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s) {
-  if (M >= 1024) CAVS_TILE_DISPATCH(bwd, 64, 32);
-  else CAVS_TILE_DISPATCH(bwd, 32, 32);
+  if (M >= 1024) CAVS_TILE_DISPATCH(bwd, 64, 32, 3);
+  else CAVS_TILE_DISPATCH(bwd, 32, 32, 4);
 }
 
 }  // namespace cavs
