@@ -229,7 +229,7 @@ def main():
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
         "whole_step_tflops": round(total_flops / (wall_ms * 1e-3) / 1e12, 2),
         "algorithmic_gflop_per_step": round(total_flops / 1e9, 3),
-        "kernels": kernels[:10],
+        "kernels": kernels,
         "levels_us": {"columns": ["rows", "fwd", "bwd_gates", "bwd_gemm"], "rows": level_table},
     }
     if args.cpu_trees > 0:

@@ -11,7 +11,8 @@ namespace cavs {
 namespace {
 
 constexpr int kLossMaxC = 16;
-constexpr int kMaxSplits = 16;
+constexpr int kMaxSplits = 16;   // sizes the split-K scratch: 16 x (4H x H) floats
+constexpr int kSplitCap = 32;    // more splits only where the scratch holds them
 
 // ------------------------------------------------------------- pull GEMM
 // P[p, n] = X[pull_pos[p], :] W_x[:, n] for p = pull_list[m]; tile 64 x 64.
@@ -265,13 +266,16 @@ template <class L, int BT>
 __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo, int No,
                                                  float* out) {
   // BT x BT output tile; 2 x 2 wavefronts of (BT/2) x (BT/2); K (= q) chunks
-  // of 32.  The per-row indices (gathers) of chunk c+2 are loaded while the
-  // data of chunk c+1 is loaded and chunk c is multiplied, so no data load
-  // waits on an index load.
+  // of 32 in two LDS stages.  While chunk c is multiplied, the data of chunk
+  // c+1 and the per-row indices (gathers) of chunk c+2 are loaded, so no
+  // data load waits on an index load; chunk c+1 is then stored to the other
+  // stage and one barrier per chunk separates the stages.  The barrier is a
+  // bare s_barrier after the LDS writes have completed: the workgroup fence
+  // of __syncthreads would also wait for the loads in flight.
   constexpr int LD = BT + 2, TT = BT / 32, C4 = BT / 4, PER = kBK * C4 / 256;
   using Idx = typename L::Idx;
-  __shared__ float As[kBK * LD];
-  __shared__ float Bs[kBK * LD];
+  __shared__ float As[2][kBK * LD];
+  __shared__ float Bs[2][kBK * LD];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int wrow = (w >> 1) * (BT / 2), wcol = (w & 1) * (BT / 2);
   const int n0 = blockIdx.x * BT, m0 = blockIdx.y * BT, s = blockIdx.z;
@@ -294,13 +298,19 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
       rb[a] = (q < q_hi) ? ld.b4(ix[a], q, n0 + 4 * c4) : f4zero();
     }
   };
-  auto sstore = [&]() {
+  auto sstore = [&](int st) {
 #pragma unroll
     for (int a = 0; a < PER; ++a) {
       const int idx = tid + 256 * a, qq = idx / C4, c4 = idx % C4;
-      st4_scalar(&As[qq * LD + 4 * c4], ra[a]);
-      st4_scalar(&Bs[qq * LD + 4 * c4], rb[a]);
+      st4_scalar(&As[st][qq * LD + 4 * c4], ra[a]);
+      st4_scalar(&Bs[st][qq * LD + 4 * c4], rb[a]);
     }
+  };
+  auto barrier = []() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes done
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
   v4f acc[TT][TT];
   zero_acc(acc);
@@ -310,15 +320,19 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
     load_idx(q_lo + kBK, ix_next);
     gload(q_lo, ix0);
   }
+  sstore(0);
+  barrier();
+  int st = 0;
   for (int q0 = q_lo; q0 < q_hi; q0 += kBK) {
-    __syncthreads();
-    sstore();
-    __syncthreads();
-    if (q0 + kBK < q_hi) {
+    const bool more = q0 + kBK < q_hi;
+    if (more) {
       gload(q0 + kBK, ix_next);
       load_idx(q0 + 2 * kBK, ix_next);
     }
-    mfma_chunk<TT, TT, false, false, LD, LD>(As, Bs, wrow, wcol, acc);
+    mfma_chunk<TT, TT, false, false, LD, LD>(As[st], Bs[st], wrow, wcol, acc);
+    if (more) sstore(st ^ 1);
+    barrier();
+    st ^= 1;
   }
   float* o = out + (size_t)s * Mo * No;
 #pragma unroll
@@ -557,9 +571,12 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
   }
   const int BT = (!ld.n.bf && No % 128 == 0) ? 128 : 64;
   const int tiles = (No / BT) * cdiv(Mo, BT);
-  int S = cdiv(512, tiles);
+  // about two workgroups per CU (256 CUs), never three on some: a CU's
+  // co-resident workgroups share its matrix cores, so the busiest CU sets
+  // the time
+  int S = 512 / tiles;
   S = S < 1 ? 1 : S;
-  S = S > kMaxSplits ? kMaxSplits : S;
+  S = S > kSplitCap ? kSplitCap : S;
   int maxS = cdiv(Q, 256);
   if (S > maxS) S = maxS;
   while (S > 1 && (size_t)S * Mo * No > part_floats) --S;

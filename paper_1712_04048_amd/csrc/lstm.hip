@@ -46,12 +46,11 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M) {
   const float c = i * u, h = o * tanhf(c);
   n.Hs[(size_t)p * H + j] = h;
   n.Cs[(size_t)p * H + j] = c;
+  // a leaf has no forget gates: their saved columns are never read
   float* g = n.Gs + (size_t)p * n.GW;
   g[j] = i;
-  g[H + j] = 0.f;
   g[2 * H + j] = o;
   g[3 * H + j] = u;
-  if (n.N == 2) g[4 * H + j] = 0.f;
   const int v = n.order[p];
   n.h_out[(size_t)v * H + j] = h;
   if (n.c_out) n.c_out[(size_t)v * H + j] = c;
