@@ -617,6 +617,7 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
     const int r1 = min(hi, row1);
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (n.GW == H) {  // Tree-FC
+#pragma unroll 4
       for (int p = r0; p < r1; ++p) {
         const float4 v = *reinterpret_cast<const float4*>(n.dA + (size_t)p * H + c);
         s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
@@ -625,6 +626,7 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
       const bool fcol = c >= G_F * H && c < (G_F + 1) * H;
       if (fcol) r0 = max(r0, lo1);  // level-0 rows have no children: f is zero
       const bool two = fcol && n.N == 2;
+#pragma unroll 4
       for (int p = r0; p < r1; ++p) {
         const float* row = n.dA + (size_t)p * n.GW;
         float4 v = *reinterpret_cast<const float4*>(row + c);
@@ -649,6 +651,7 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[e][c] = 0.f;
   }
+#pragma unroll 4
   for (int p = lo; p < hi; ++p) {
     const float4 h = *reinterpret_cast<const float4*>(n.Hs + (size_t)p * H + j);
     const float* dz = n.dZ + (size_t)p * C;
@@ -715,6 +718,7 @@ __global__ void __launch_bounds__(256) k_loss(Net n) {
     float z[kLossMaxC];
 #pragma unroll
     for (int c = 0; c < kLossMaxC; ++c) z[c] = 0.f;
+#pragma unroll 8
     for (int j = lane; j < H; j += 64) {
       const float hj = h[j];
       const float* ws = n.Ws + (size_t)j * C;

@@ -752,13 +752,18 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
     };
-    F1 x, y;
-    load1(w * q1, x);
-    for (int c0 = w * q1; c0 < (w + 1) * q1; c0 += 2 * kBK) {
-      load1(c0 + kBK, y);
-      comp1(x);
-      if (c0 + 2 * kBK < (w + 1) * q1) load1(c0 + 2 * kBK, x);
-      comp1(y);
+    // groups of G chunks: all loads of a group are in flight together, so a
+    // small level pays about one memory latency per group, not per chunk
+    constexpr int G1 = 6;
+    const int end1 = (w + 1) * q1;
+    for (int c0 = w * q1; c0 < end1; c0 += G1 * kBK) {
+      F1 f[G1];
+#pragma unroll
+      for (int g = 0; g < G1; ++g)
+        if (c0 + g * kBK < end1) load1(c0 + g * kBK, f[g]);
+#pragma unroll
+      for (int g = 0; g < G1; ++g)
+        if (c0 + g * kBK < end1) comp1(f[g]);
     }
     if constexpr (NCH == 2) {
       struct F2 {
@@ -786,13 +791,16 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
           acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
         }
       };
-      F2 u, v;
-      load2(w * q2, u);
-      for (int c0 = w * q2; c0 < (w + 1) * q2; c0 += 2 * kBK) {
-        load2(c0 + kBK, v);
-        comp2(u);
-        if (c0 + 2 * kBK < (w + 1) * q2) load2(c0 + 2 * kBK, u);
-        comp2(v);
+      constexpr int G2 = 4;
+      const int end2 = (w + 1) * q2;
+      for (int c0 = w * q2; c0 < end2; c0 += G2 * kBK) {
+        F2 f[G2];
+#pragma unroll
+        for (int g = 0; g < G2; ++g)
+          if (c0 + g * kBK < end2) load2(c0 + g * kBK, f[g]);
+#pragma unroll
+        for (int g = 0; g < G2; ++g)
+          if (c0 + g * kBK < end2) comp2(f[g]);
       }
     }
 #pragma unroll
