@@ -71,6 +71,38 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
     return lazy.get(base, 0.0), 0.0
 
 
+def source_sha256():
+    """Hash of the HIP sources and headers, in the order the traffic record
+    was hashed: a record taken on other kernels is not used."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_1712_04048_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(ROOT, "paper_1712_04048_amd", "csrc", "*.h")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in sorted(files, key=lambda f: os.path.relpath(f, ROOT)):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    record (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by what the
+    counter reads for a plain copy of known size), or None when there is no
+    record for this kernel or the sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    k = rec.get("kernels", {}).get(kernel)
+    if k is None or rec.get("source_sha256") != source_sha256():
+        return None
+    return (k["fetch_kib"] * rec["copy_bytes"] / rec["copy_fetch_kib"] +
+            k["write_kib"] * rec["copy_bytes"] / rec["copy_write_kib"])
+
+
 def cpu_baseline(wl, n_trees):
     """The oracle as it stands (fp64, recursive, one thread) on the first
     n_trees graphs of the batch."""
@@ -200,6 +232,10 @@ def main():
         achieved = per_launch / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(wl.name, dom["name"])
+    if roof["traffic"] is not None:
+        roof["traffic"] = round(roof["traffic"])
+        roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = dom["name"]
     roof["launches_per_step"] = launches / args.steps
     roof["avg_launch_us"] = round(avg_ms * 1e3, 2)
