@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-trees", type=int, default=48,
+    ap.add_argument("--cpu-trees", type=int, default=256,
                     help="graphs in the CPU-oracle sample (0 skips the CPU baseline)")
     return ap.parse_args()
 

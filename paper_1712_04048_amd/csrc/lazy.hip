@@ -262,22 +262,27 @@ struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   }
 };
 
-template <class L, int BT>
-__global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo, int No,
-                                                 float* out) {
-  // BT x BT output tile; 2 x 2 wavefronts of (BT/2) x (BT/2); K (= q) chunks
-  // of 32 in two LDS stages.  While chunk c is multiplied, the data of chunk
-  // c+1 and the per-row indices (gathers) of chunk c+2 are loaded, so no
-  // data load waits on an index load; chunk c+1 is then stored to the other
-  // stage and one barrier per chunk separates the stages.  The barrier is a
-  // bare s_barrier after the LDS writes have completed: the workgroup fence
-  // of __syncthreads would also wait for the loads in flight.
-  constexpr int LD = BT + 2, TT = BT / 32, C4 = BT / 4, PER = kBK * C4 / 256;
+template <class L, int BT, int NW>
+__global__ void __launch_bounds__(64 * NW) k_tn_gemm(L ld, int Q, int qchunk, int Mo, int No,
+                                                     float* out) {
+  // BT x BT output tile; NW wavefronts as 2 x NW/2 of (BT/2) x (2BT/NW); K
+  // (= q) chunks of 32 in two LDS stages.  While chunk c is multiplied, the
+  // data of chunk c+1 and the per-row indices (gathers) of chunk c+2 are
+  // loaded, so no data load waits on an index load; chunk c+1 is then stored
+  // to the other stage and one barrier per chunk separates the stages.  The
+  // barrier is a bare s_barrier after the LDS writes have completed: the
+  // workgroup fence of __syncthreads would also wait for the loads in flight.
+  // LDS rows hold 32 q x BT columns; float4 c4 of row q sits at quad
+  // c4 ^ 4((q >> 3) & 3), so the fragment reads of the four lane groups
+  // (rows 8g + ...) fall in four different bank ranges.
+  constexpr int NT = 64 * NW, TM = BT / 32, TN = BT / (8 * NW), C4 = BT / 4;
+  constexpr int PER = kBK * C4 / NT;
+  static_assert(PER * NT == kBK * C4 && TN >= 1, "tile split");
   using Idx = typename L::Idx;
-  __shared__ float As[2][kBK * LD];
-  __shared__ float Bs[2][kBK * LD];
+  __shared__ __attribute__((aligned(16))) float As[2][kBK * BT];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kBK * BT];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int wrow = (w >> 1) * (BT / 2), wcol = (w & 1) * (BT / 2);
+  const int wrow = (w / (NW / 2)) * (BT / 2), wcol = (w % (NW / 2)) * (16 * TN);
   const int n0 = blockIdx.x * BT, m0 = blockIdx.y * BT, s = blockIdx.z;
   const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
   float4 ra[PER], rb[PER];
@@ -285,14 +290,14 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
   auto load_idx = [&](int q0, Idx (&ix)[PER]) {
 #pragma unroll
     for (int a = 0; a < PER; ++a) {
-      const int q = q0 + (tid + 256 * a) / C4;
+      const int q = q0 + (tid + NT * a) / C4;
       if (q < q_hi) ix[a] = ld.idx(q);
     }
   };
   auto gload = [&](int q0, const Idx (&ix)[PER]) {
 #pragma unroll
     for (int a = 0; a < PER; ++a) {
-      const int idx = tid + 256 * a, qq = idx / C4, c4 = idx % C4;
+      const int idx = tid + NT * a, qq = idx / C4, c4 = idx % C4;
       const int q = q0 + qq;
       ra[a] = (q < q_hi && m0 + 4 * c4 < Mo) ? ld.a4(ix[a], q, m0 + 4 * c4) : f4zero();
       rb[a] = (q < q_hi) ? ld.b4(ix[a], q, n0 + 4 * c4) : f4zero();
@@ -301,10 +306,16 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
   auto sstore = [&](int st) {
 #pragma unroll
     for (int a = 0; a < PER; ++a) {
-      const int idx = tid + 256 * a, qq = idx / C4, c4 = idx % C4;
-      st4_scalar(&As[st][qq * LD + 4 * c4], ra[a]);
-      st4_scalar(&Bs[st][qq * LD + 4 * c4], rb[a]);
+      const int idx = tid + NT * a, qq = idx / C4, c4 = idx % C4;
+      const int col = 4 * (c4 ^ (4 * ((qq >> 3) & 3)));
+      st4(&As[st][qq * BT + col], ra[a]);
+      st4(&Bs[st][qq * BT + col], rb[a]);
     }
+  };
+  // k = 8 gq + 4 h + e of column x (lane group gq reads rows 8 gq ..)
+  auto frag = [&](const float* S, int x, int h, float (&f)[4]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = S[(8 * gq + 4 * h + e) * BT + (x ^ (16 * gq))];
   };
   auto barrier = []() {
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes done
@@ -312,7 +323,7 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-  v4f acc[TT][TT];
+  v4f acc[TM][TN];
   zero_acc(acc);
   {
     Idx ix0[PER];
@@ -329,20 +340,34 @@ __global__ void __launch_bounds__(256) k_tn_gemm(L ld, int Q, int qchunk, int Mo
       gload(q0 + kBK, ix_next);
       load_idx(q0 + 2 * kBK, ix_next);
     }
-    mfma_chunk<TT, TT, false, false, LD, LD>(As[st], Bs[st], wrow, wcol, acc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float af[TM][4], bf[TN][4];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) frag(As[st], wrow + 16 * tm + r, h, af[tm]);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) frag(Bs[st], wcol + 16 * tn + r, h, bf[tn]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = mfma_f32_16x16x4(af[tm][e], bf[tn][e], acc[tm][tn]);
+    }
     if (more) sstore(st ^ 1);
     barrier();
     st ^= 1;
   }
   float* o = out + (size_t)s * Mo * No;
 #pragma unroll
-  for (int tm = 0; tm < TT; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m0 + wrow + tm * 16 + 4 * gq + i;
       if (m >= Mo) continue;
 #pragma unroll
-      for (int tn = 0; tn < TT; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+      for (int tn = 0; tn < TN; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
     }
 }
 // ------------------------------------------------------------ bf16 variants
@@ -586,10 +611,10 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
     CAVS_LAUNCH(L::kNameBf, k_tn_gemm_bf<L>, dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st, ld,
                 Q, qchunk, Mo, No, part);
   else if (BT == 128)
-    CAVS_LAUNCH(L::kName128, (k_tn_gemm<L, 128>), dim3(No / 128, cdiv(Mo, 128), S), dim3(256), 0,
-                st, ld, Q, qchunk, Mo, No, part);
+    CAVS_LAUNCH(L::kName128, (k_tn_gemm<L, 128, 8>), dim3(No / 128, cdiv(Mo, 128), S), dim3(512),
+                0, st, ld, Q, qchunk, Mo, No, part);
   else
-    CAVS_LAUNCH(L::kName, (k_tn_gemm<L, 64>), dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st,
+    CAVS_LAUNCH(L::kName, (k_tn_gemm<L, 64, 4>), dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st,
                 ld, Q, qchunk, Mo, No, part);
   CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
                      (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
