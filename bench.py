@@ -61,7 +61,10 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
     inner = nc > 0
     lazy = {
         "k_pull_gemm": 2.0 * n_pull * D * gates_x * H,
+        "k_pull_leaf<3>": 2.0 * n_pull * D * gates_x * H,
+        "k_pull_leaf<4>": 2.0 * n_pull * D * gates_x * H,
         "k_dx_gemm": 2.0 * n_pull * D * gates_x * H,
+        "k_dx_tile<64, 64, 3>": 2.0 * n_pull * D * gates_x * H,
         "k_tn_gemm<LdDWx>": 2.0 * n_pull * D * gates_x * H,
         "k_tn_gemm<LdDUiou>": 2.0 * H * (3 if N == 2 else 4) * H * int(inner.sum()),
         "k_tn_gemm<LdDUf>": 2.0 * H * H * float(nc.sum()),

@@ -289,9 +289,10 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
   if (p->cell == CAVS_TREE_LSTM) {
-    pull_gemm(n, s->n_pull, s->n_inner_input > 0, str);
+    pull_gemm(n, s->n_pull, s->n_inner_input > 0, lo[1], str);
     if (s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) lstm_transpose_u(n, str);
-    lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
+    // fp32: pulled leaves were finished by the pull product
+    if (n.bf || s->n_leaf_noinput > 0) lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], !n.bf, str);
     const int ts = persist_first_level(n, lo, s->T);
     for (int t = 1; t < ts; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
     int* bar = (int*)((char*)ws + L.bar);

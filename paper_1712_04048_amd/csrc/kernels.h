@@ -53,7 +53,7 @@ enum { G_I = 0, G_F = 1, G_O = 2, G_U = 3 };
 // launchers
 // ---------------------------------------------------------------------------
 // lstm.hip
-void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
+void lstm_fwd_leaf(const Net& n, int off, int M, bool skip_pulled, hipStream_t s);
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s);
 // Backward dA of the levels below n.fuse_from: elementwise over level rows
 // (dL/dh and dL/dc as stored by the parents); roots at or above it.
@@ -89,7 +89,10 @@ void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);
 void fc_bwd_gates(const Net& n, int off, int M, int leaf, float* dX, hipStream_t s);
 void fc_bwd_level(const Net& n, int off, int M, hipStream_t s);
 // lazy.hip
-void pull_gemm(const Net& n, int n_pull, bool with_f, hipStream_t s);
+// Pull projection; in fp32 the cell of every pulled leaf (position < lo1) is
+// finished in the same kernel, so lstm_fwd_leaf only handles leaves without
+// input (skip_pulled); in bf16 it writes P for all pulled rows.
+void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s);
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s);
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s);
 // Lazy weight-gradient products; `part` is split-K scratch of part_floats floats.

@@ -5,7 +5,8 @@
 //   - push:   the loss head over every labelled vertex (z = h W_s + b_s);
 //   - dF:     dW_x, dU, db, dX, dW_s, db_s as long-K products over all
 //             vertices, with deterministic split-K (fixed-order reduction).
-#include "kernels.h"
+#include "lds_ring.h"
+#include "lstm_dev.h"
 
 namespace cavs {
 namespace {
@@ -17,31 +18,35 @@ constexpr int kSplitCap = 32;    // more splits only where the scratch holds the
 // ------------------------------------------------------------- pull GEMM
 // P[p, n] = X[pull_pos[p], :] W_x[:, n] for p = pull_list[m]; tile 64 x 64.
 // Column tiles cover the gate blocks i,f,o,u (with_f) or i,o,u.
-__global__ void __launch_bounds__(256) k_pull_gemm(Net n, int n_pull, int with_f) {
-  constexpr int BM = 64, BN = 64, LDA = kBK + 4, LDB = BN + 2;
-  __shared__ __attribute__((aligned(16))) float As[BM * LDA];
-  __shared__ float Bs[kBK * LDB];
+// Pull projection P = x W_x fused with the cell of the pulled leaves: a
+// workgroup owns 64 pulled rows x 32 hidden units for all NG gate blocks
+// (i|o|u when no vertex with children pulls, else i|f|o|u); wavefront w owns
+// rows 16w.. of the tile and every gate block of its units, so each lane
+// holds all gates of its (row, unit).  A leaf row (position below lo1)
+// finishes its cell here (h, c, saved gates, outputs); any other pulled row
+// stores its P row for the level epilogue.  K = D runs in 32-deep chunks
+// through two LDS stages (the last chunk zero-filled past D).
+template <int NG>
+__global__ void __launch_bounds__(256) k_pull_leaf(Net n, int n_pull, int lo1) {
+  constexpr int BM = 64, BU = 32, NB = NG * BU / 16;
+  constexpr int LDA = kBK + 4, LDB = NG * BU + 2;
+  constexpr int B4 = NG * BU / 4;                     // float4 per B k-row
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LDA];
+  __shared__ float Bs[2][kBK * LDB];
   const int H = n.H, H4 = 4 * H, D = n.D;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int wrow = (w >> 1) * 32, wcol = (w & 1) * 32;
-  const int m0 = blockIdx.x * BM;
-  const int tpg = H / BN, gsel = blockIdx.y / tpg;
-  const int gate = with_f ? gsel : (gsel == 0 ? G_I : gsel + 1);
-  const int n0 = gate * H + (blockIdx.y % tpg) * BN;
+  const int m0 = blockIdx.x * BM, u0 = blockIdx.y * BU;
+  auto gcol = [&](int g) { return NG == 4 ? g : (g == 0 ? G_I : g + 1); };
   const float* asrc[2];
-  int arow[2], aq[2];
+  int adst[2], aq[2];
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
-    const int idx = tid + 256 * a;
-    arow[a] = idx / 8;
+    const int idx = tid + 256 * a, row = idx / 8;
     aq[a] = idx % 8;
-    asrc[a] = nullptr;
-    if (m0 + arow[a] < n_pull) {
-      const int p = n.pull_list[m0 + arow[a]];
-      asrc[a] = n.X + (size_t)n.pull_pos[p] * D;
-    }
+    adst[a] = row * LDA + 4 * aq[a];
+    asrc[a] = m0 + row < n_pull ? n.X + (size_t)n.pull_pos[n.pull_list[m0 + row]] * D : nullptr;
   }
-  float4 ra[2], rb[2];
+  float4 ra[2], rb[NG];
   auto gload = [&](int k0) {
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
@@ -49,42 +54,74 @@ __global__ void __launch_bounds__(256) k_pull_gemm(Net n, int n_pull, int with_f
       ra[a] = (asrc[a] && k < D) ? ldg4(asrc[a] + k) : f4zero();
     }
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
-      rb[b] = k0 + kk < D ? ldg4(n.Wx + (size_t)(k0 + kk) * H4 + n0 + 4 * q) : f4zero();
+    for (int b = 0; b < NG; ++b) {
+      const int idx = tid + 256 * b, kk = idx / B4, c = 4 * (idx % B4);
+      rb[b] = k0 + kk < D ? ldg4(n.Wx + (size_t)(k0 + kk) * H4 + gcol(c / BU) * H + u0 + c % BU)
+                          : f4zero();
     }
   };
-  auto sstore = [&]() {
+  auto sstore = [&](int st) {
 #pragma unroll
-    for (int a = 0; a < 2; ++a) st4(&As[arow[a] * LDA + 4 * aq[a]], ra[a]);
+    for (int a = 0; a < 2; ++a) st4(&As[st][adst[a]], ra[a]);
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int idx = tid + 256 * b, kk = idx / 16, q = idx % 16;
-      st4_scalar(&Bs[kk * LDB + 4 * q], rb[b]);
+    for (int b = 0; b < NG; ++b) {
+      const int idx = tid + 256 * b, kk = idx / B4, c = 4 * (idx % B4);
+      st4_scalar(&Bs[st][kk * LDB + c], rb[b]);
     }
   };
-  v4f acc[2][2];
+  auto barrier = []() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes done
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  v4f acc[1][NB];
   zero_acc(acc);
   const int nk = (D + kBK - 1) / kBK;
   gload(0);
+  sstore(0);
+  barrier();
   for (int kc = 0; kc < nk; ++kc) {
-    __syncthreads();
-    sstore();
-    __syncthreads();
+    const int st = kc & 1;
     if (kc + 1 < nk) gload((kc + 1) * kBK);
-    mfma_chunk<2, 2, true, false, LDA, LDB>(As, Bs, wrow, wcol, acc);
+    mfma_chunk<1, NB, true, false, LDA, LDB>(As[st], Bs[st], 16 * w, 0, acc);
+    if (kc + 1 < nk) sstore(st ^ 1);
+    barrier();
   }
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + 16 * w + 4 * gq + i;
+    if (m >= n_pull) continue;
+    const int p = n.pull_list[m];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + wrow + tm * 16 + 4 * gq + i;
-      if (m >= n_pull) continue;
-      const int p = n.pull_list[m];
+    for (int ub = 0; ub < 2; ++ub) {
+      const int j = u0 + 16 * ub + r;
+      // block of gate g, unit block ub: columns [32 g + 16 ub, +16)
+      if (p < lo1) {
+        const float zi = acc[0][0 * 2 + ub][i];
+        const float zo = acc[0][(NG == 4 ? 2 : 1) * 2 + ub][i];
+        const float zu = acc[0][(NG == 4 ? 3 : 2) * 2 + ub][i];
+        float ai = n.b[G_I * H + j], ao = n.b[G_O * H + j], au = n.b[G_U * H + j];
+        ai += zi;
+        ao += zo;
+        au += zu;
+        const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanhf(au);
+        const float c = ig * ug, h = og * tanhf(c);
+        n.Hs[(size_t)p * H + j] = h;
+        n.Cs[(size_t)p * H + j] = c;
+        float* g = n.Gs + (size_t)p * n.GW;   // a leaf's forget gates are never read
+        g[j] = ig;
+        g[2 * H + j] = og;
+        g[3 * H + j] = ug;
+        const int v = n.order[p];
+        n.h_out[(size_t)v * H + j] = h;
+        if (n.c_out) n.c_out[(size_t)v * H + j] = c;
+      } else {
 #pragma unroll
-      for (int tn = 0; tn < 2; ++tn)
-        n.P[(size_t)p * H4 + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
+        for (int g = 0; g < NG; ++g) n.P[(size_t)p * H4 + gcol(g) * H + j] = acc[0][g * 2 + ub][i];
+      }
     }
+  }
 }
 
 // --------------------------------------------------------------- dX GEMM
@@ -370,6 +407,70 @@ __global__ void __launch_bounds__(64 * NW) k_tn_gemm(L ld, int Q, int qchunk, in
       for (int tn = 0; tn < TN; ++tn) o[(size_t)m * No + n0 + wcol + tn * 16 + r] = acc[tm][tn][i];
     }
 }
+// dX through the LDS ring (lds_ring.h), for gate columns that need no
+// f_0 + f_1 sum (i|o|u, or all four blocks with one child slot): a
+// workgroup owns BM pulled rows x BN input columns; stage rows [0, BM) are
+// dA rows (gathered through pull_list), [BM, BM + BN) rows of W_x.  Rows
+// past n_pull or D read the last valid row; their products are not stored.
+template <int BM, int BN, int S>
+__global__ void __launch_bounds__(256) k_dx_tile(Net n, int n_pull, int four, float* dX) {
+  constexpr int TM = BM / 32, TN = BN / 32, ROWS = BM + BN, IPW = ROWS / 32;
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+  const int H = n.H, H4 = 4 * H, D = n.D, GW = n.GW;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wr = w & 1, wn = w >> 1;
+  const int m0 = blockIdx.x * BM, d0 = blockIdx.y * BN;
+  const float* src[IPW];
+#pragma unroll
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const float* ptr;
+    if (row < BM) ptr = n.dA + (size_t)n.pull_list[min(m0 + row, n_pull - 1)] * GW;
+    else ptr = n.Wx + (size_t)min(d0 + row - BM, D - 1) * H4;
+    src[t] = ptr + 4 * qg;
+  }
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
+  v4f acc[TM][TN];
+  zero_acc(acc);
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
+    const int k0 = c * kBK, col = (four || k0 < H) ? k0 : k0 + H;
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + col, base + 1024u * t);
+  };
+  auto compute = [&](const float* Ls, int) {
+    float b[TN][8];
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) frag_sw(Ls, BM + wn * (BN / 2) + tn * 16 + r, gq, b[tn]);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      float a[8];
+      frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, a);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma_chunk8<false>(a, b[tn], acc[tm][tn]);
+    }
+  };
+  ring_loop<S, IPW>((four ? H4 : 3 * H) / kBK, ring, issue, compute);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + wr * (BM / 2) + tm * 16 + 4 * gq + i;
+      if (m >= n_pull) continue;
+      const int row = n.pull_pos[n.pull_list[m]];
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int d = d0 + wn * (BN / 2) + tn * 16 + r;
+        if (d < D) dX[(size_t)row * D + d] = acc[tm][tn][i];
+      }
+    }
+}
+
 // ------------------------------------------------------------ bf16 variants
 // Same tiles as the fp32 kernels above; operands are rounded to bf16 while
 // they are staged into LDS (k-contiguous rows), accumulation is fp32.
@@ -810,18 +911,28 @@ size_t lazy_part_floats(int V, int D, int H, int N, int C) {
   return m > c ? m : c;
 }
 
-void pull_gemm(const Net& n, int n_pull, bool with_f, hipStream_t s) {
+void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s) {
   if (n_pull <= 0) return;
-  dim3 grid(cdiv(n_pull, 64), (with_f ? 4 : 3) * (n.H / 64));
-  if (n.bf)
+  if (n.bf) {
+    dim3 grid(cdiv(n_pull, 64), (with_f ? 4 : 3) * (n.H / 64));
     CAVS_LAUNCH("k_pull_gemm_bf", k_pull_gemm_bf, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
+    return;
+  }
+  dim3 grid(cdiv(n_pull, 64), n.H / 32);
+  if (with_f)
+    CAVS_LAUNCH("k_pull_leaf<4>", k_pull_leaf<4>, grid, dim3(256), 0, s, n, n_pull, lo1);
   else
-    CAVS_LAUNCH("k_pull_gemm", k_pull_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
+    CAVS_LAUNCH("k_pull_leaf<3>", k_pull_leaf<3>, grid, dim3(256), 0, s, n, n_pull, lo1);
 }
 
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
   if (n_pull <= 0) return;
   dim3 grid(cdiv(n_pull, 64), cdiv(n.D, 64));
+  if (!n.bf && (!with_f || n.N == 1)) {
+    CAVS_LAUNCH("k_dx_tile<64, 64, 3>", (k_dx_tile<64, 64, 3>), grid, dim3(256), 0, s, n, n_pull,
+                (int)with_f, dX);
+    return;
+  }
   if (n.bf)
     CAVS_LAUNCH("k_dx_gemm_bf", k_dx_gemm_bf, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
   else

@@ -29,12 +29,13 @@ namespace cavs {
 namespace {
 
 // ------------------------------------------------------------------ forward
-__global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M) {
+__global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int skip_pulled) {
   const int H = n.H;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long)M * H) return;
   const int p = off + (int)(idx / H), j = (int)(idx % H);
   const int pr = n.pull_pos[p];
+  if (skip_pulled && pr >= 0) return;   // finished by the pull product
   float ai = n.b[G_I * H + j], ao = n.b[G_O * H + j], au = n.b[G_U * H + j];
   if (pr >= 0) {
     const float* Pp = n.P + (size_t)p * 4 * H;
@@ -950,9 +951,10 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_persist(Net n, const int* lo, 
 }
 }  // namespace
 
-void lstm_fwd_leaf(const Net& n, int off, int M, hipStream_t s) {
+void lstm_fwd_leaf(const Net& n, int off, int M, bool skip_pulled, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH_ROWS("k_lstm_leaf", off, M, k_lstm_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
+  CAVS_LAUNCH_ROWS("k_lstm_leaf", off, M, k_lstm_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0,
+                   s, n, off, M, (int)skip_pulled);
 }
 
 void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {

@@ -27,8 +27,7 @@
 // Backward: A = dA rows of the level, B = U (row n of U is column n of U^T);
 // phase 1 contracts the i|o|u columns, phase 2 the f_0 and f_1 columns with
 // the shared U_f block.
-#include <type_traits>
-
+#include "lds_ring.h"
 #include "lstm_dev.h"
 
 namespace cavs {
@@ -48,83 +47,6 @@ __global__ void __launch_bounds__(256) k_transpose_u(const float* __restrict__ U
   for (int y = ty; y < 32; y += 8) t[y][tx] = U[(size_t)(k0 + y) * H4 + c0 + tx];
   __syncthreads();
   for (int y = ty; y < 32; y += 8) UT[(size_t)(c0 + y) * H + k0 + tx] = t[tx][y];
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // gfx9 s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt at max
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-__device__ __forceinline__ void barrier_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// 16 bytes per lane from g into LDS at lds_addr + 16 * lane.
-__device__ __forceinline__ void copy16_to_lds(const float* g, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(g), "s"(lds_addr) : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_addr_of(const float* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
-}
-
-// k = 8 gq .. 8 gq + 7 of LDS row `row` (quads swizzled by row & 7)
-__device__ __forceinline__ void frag_sw(const float* L, int row, int gq, float (&v)[8]) {
-  const float* rp = L + row * 32;
-  const int sw = row & 7;
-  const float4 x = *reinterpret_cast<const float4*>(rp + 4 * ((2 * gq) ^ sw));
-  const float4 y = *reinterpret_cast<const float4*>(rp + 4 * ((2 * gq + 1) ^ sw));
-  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-  v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
-}
-
-template <int K>
-using IC = std::integral_constant<int, K>;
-
-// Stage ring: S distinct LDS arrays of ROWS x 32 floats, selected at compile
-// time (the chunk loop is unrolled by S).
-template <int ROWS, int S>
-struct Ring {
-  float* s0;
-  float* s1;
-  float* s2;
-  float* s3;
-  template <int K>
-  __device__ __forceinline__ float* at(IC<K>) const {
-    if constexpr (K == 0) return s0;
-    else if constexpr (K == 1) return s1;
-    else if constexpr (K == 2) return s2;
-    else return s3;
-  }
-};
-
-// Runs chunks 0 .. nch-1 through an S-stage ring: issue(stage, c) starts the
-// IPW copies of chunk c, compute(stage ptr, c) consumes it.
-template <int S, int IPW, class Issue, class Compute, class RingT>
-__device__ __forceinline__ void ring_loop(int nch, const RingT& ring, Issue&& issue,
-                                          Compute&& compute) {
-  issue(IC<0>{}, 0);
-  if constexpr (S > 2) if (1 < nch) issue(IC<1>{}, 1);
-  if constexpr (S > 3) if (2 < nch) issue(IC<2>{}, 2);
-  auto step = [&](auto sc, int c) {
-    constexpr int k = decltype(sc)::value;
-    if (c + S - 2 < nch) wait_vmcnt<(S - 2) * IPW>();
-    else wait_vmcnt<0>();
-    barrier_nofence();
-    if (c + S - 1 < nch) issue(IC<(k + S - 1) % S>{}, c + S - 1);
-    compute(ring.at(sc), c);
-  };
-  for (int c = 0; c < nch; c += S) {
-    step(IC<0>{}, c);
-    if (c + 1 < nch) step(IC<1>{}, c + 1);
-    if constexpr (S > 2) if (c + 2 < nch) step(IC<2>{}, c + 2);
-    if constexpr (S > 3) if (c + 3 < nch) step(IC<3>{}, c + 3);
-  }
 }
 
 template <int NCH, bool BF, int BM, int BU, int S>
