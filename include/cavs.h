@@ -133,7 +133,9 @@ size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x);
 
 /* Validates the graphs and builds the schedule on the GPU.  Synchronises the
    context's stream once, to return T, the counts, level_offsets_host and the
-   validation result.  Graph errors, by priority: CAVS_ERR_RANGE,
+   validation result; the device arrays (order, pos, the remapped indices,
+   pull_list) are written by work enqueued after that point, so they are
+   complete for later work on the same stream (or after a synchronisation).  Graph errors, by priority: CAVS_ERR_RANGE,
    CAVS_ERR_MULTIPARENT, CAVS_ERR_DUP_PULL, CAVS_ERR_MISMATCH, CAVS_ERR_CYCLE;
    on such an error the device outputs are unspecified.  N outside {1, 2}
    gives CAVS_ERR_UNSUPPORTED; a null required pointer, CAVS_ERR_ARG; a short

@@ -3,18 +3,21 @@
 //
 // A vertex is activated once all of its children are evaluated, so the task
 // that evaluates v is its level: 0 for a leaf, else 1 + the largest level of
-// its children.  The schedule is built without host round trips:
+// its children.  The schedule is built on the GPU:
 //   1. validation counters (range, references per vertex, pull rows, links);
 //   2. level assignment: one thread per leaf walks towards the root; at each
 //      parent it bumps an arrival counter and only the last child to arrive
 //      continues, so every vertex is assigned exactly once, in O(V) total;
 //   3. per-level histogram and exclusive scan -> level_offsets;
-//   4. stable LSD radix sort of vertex ids by level (8-bit digits, ranks from
-//      wavefront ballots), giving ascending ids inside each task;
-//   5. index remap to positions, and a stable compaction of the positions
-//      that pull an input;
-//   6. one device->host copy of T, the counts, the error flags and the
-//      offsets, and the only stream synchronisation.
+//   4. one device->host copy of T, the counts, the error flags and the
+//      offsets, and the only stream synchronisation: everything the host
+//      needs is known at this point, and T fixes the number of sort passes;
+//   5. stable LSD radix sort of vertex ids by level (8-bit digits, ranks from
+//      wavefront ballots), giving ascending ids inside each task; its last
+//      pass also writes pos and the list of positions that pull an input
+//      (their ranks counted the same way over the pulling subset);
+//   6. index remap to positions.
+// Steps 5 and 6 are only enqueued: later calls on the stream see them done.
 #include <stdarg.h>
 #include <stdio.h>
 
@@ -107,10 +110,11 @@ __global__ void k_scan_edges(int V, int N, int n_x, int n_push, const int* __res
   }
 }
 
-__global__ void k_check_links(int V, int N, int n_x, const int* __restrict__ child,
-                              const int* __restrict__ parent, const int* __restrict__ ref_cnt,
-                              const int* __restrict__ pull_cnt, int* flags) {
-  int v = blockIdx.x * blockDim.x + threadIdx.x;
+__device__ __forceinline__ void check_links_of(int v, int V, int N, int n_x,
+                                               const int* __restrict__ child,
+                                               const int* __restrict__ parent,
+                                               const int* __restrict__ ref_cnt,
+                                               const int* __restrict__ pull_cnt, int* flags) {
   if (v < V) {
     if (ref_cnt[v] > 1) atomicOr(&flags[F_MULTI], 1);
     for (int k = 0; k < N; ++k) {
@@ -130,9 +134,14 @@ __global__ void k_check_links(int V, int N, int n_x, const int* __restrict__ chi
 // value its own atomic returns, so the walk needs no other communication
 // (and no memory fences).  The count never wraps, so only the arrival that
 // completes p continues: each vertex is passed by at most one walker.
-__global__ void k_levels(int V, int N, const int* __restrict__ parent,
-                         const int* __restrict__ nchild, unsigned long long* arrive, int* level) {
-  int v = blockIdx.x * blockDim.x + threadIdx.x;
+// The same launch runs the link checks of step 1 (like the walk, they only
+// read the counters of k_scan_edges).
+__global__ void k_links_levels(int V, int N, int n_x, const int* __restrict__ child,
+                               const int* __restrict__ parent, const int* __restrict__ ref_cnt,
+                               const int* __restrict__ pull_cnt, const int* __restrict__ nchild,
+                               unsigned long long* arrive, int* level, int* flags) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  check_links_of(v, V, N, n_x, child, parent, ref_cnt, pull_cnt, flags);
   if (v >= V || nchild[v] != 0) return;
   level[v] = 0;
   int cur = v, lev = 0;
@@ -148,6 +157,14 @@ __global__ void k_levels(int V, int N, const int* __restrict__ parent,
     level[p] = lev;
     cur = p;
   }
+}
+
+// Clears the counters of steps 1-3 and marks every level unassigned (-1),
+// in one launch.
+__global__ void k_sched_init(int* zero_base, long zero_ints, int* level, int V) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < zero_ints) zero_base[i] = 0;
+  if (i < V) level[i] = -1;
 }
 
 // -------------------------------------------------------------------------
@@ -224,40 +241,64 @@ __global__ void __launch_bounds__(1024) k_scan_excl(const int* src, int* dst, in
 }
 
 // -------------------------------------------------------------------------
-// 4. stable LSD radix sort, 8-bit digits
+// 5. stable LSD radix sort, 8-bit digits
 // -------------------------------------------------------------------------
 __device__ __forceinline__ unsigned digit_of(int key, int shift) {
   return ((unsigned)key >> shift) & 255u;
 }
 
-// tile_hist is digit-major: entry [d * ntiles + tile]
-__global__ void __launch_bounds__(256) k_radix_hist(const int* __restrict__ keys, int n, int shift,
-                                                    int ntiles, int* tile_hist) {
-  __shared__ int h[256];
+// tile_hist is digit-major: entry [d * ntiles + tile].  With pull_idx set
+// (last pass) the counts of elements whose vertex pulls an input follow at
+// [(256 + d) * ntiles + tile]; vals_in == nullptr means value = index.
+__global__ void __launch_bounds__(256) k_radix_hist(const int* __restrict__ keys,
+                                                    const int* __restrict__ vals_in, int n,
+                                                    int shift, int ntiles,
+                                                    const int* __restrict__ pull_idx,
+                                                    int* tile_hist) {
+  __shared__ int h[2][256];
   int tid = threadIdx.x;
-  h[tid] = 0;
+  h[0][tid] = 0;
+  h[1][tid] = 0;
   __syncthreads();
   int base = blockIdx.x * kTile;
 #pragma unroll
   for (int r = 0; r < kTile / 256; ++r) {
     int e = base + r * 256 + tid;
-    if (e < n) atomicAdd(&h[digit_of(keys[e], shift)], 1);
+    if (e < n) {
+      const unsigned d = digit_of(keys[e], shift);
+      atomicAdd(&h[0][d], 1);
+      if (pull_idx) {
+        const int v = vals_in ? vals_in[e] : e;
+        if (pull_idx[v] >= 0) atomicAdd(&h[1][d], 1);
+      }
+    }
   }
   __syncthreads();
-  tile_hist[tid * ntiles + blockIdx.x] = h[tid];
+  tile_hist[tid * ntiles + blockIdx.x] = h[0][tid];
+  if (pull_idx) tile_hist[(256 + tid) * ntiles + blockIdx.x] = h[1][tid];
 }
 
-// vals_in == nullptr means the identity (value = element index).
+// vals_in == nullptr means the identity (value = element index).  In the
+// last pass (pos_out set) every value v also gets pos_out[v] = dst, and with
+// pull_idx set the values that pull an input are listed in order: their
+// rank among the pulling elements of the same digit comes from the same
+// ballots restricted to the pulling lanes, and offs[(256 + d) * ntiles +
+// tile] - n counts the pulling elements before them (the scan ran over both
+// tables, and the first one sums to n).
 __global__ void __launch_bounds__(256) k_radix_scatter(const int* __restrict__ keys_in,
                                                        const int* __restrict__ vals_in, int n,
                                                        int shift, int ntiles,
                                                        const int* __restrict__ offs,
                                                        int* __restrict__ keys_out,
-                                                       int* __restrict__ vals_out) {
-  __shared__ int base_cnt[256];
-  __shared__ int wcnt[4][256];
+                                                       int* __restrict__ vals_out,
+                                                       int* __restrict__ pos_out,
+                                                       const int* __restrict__ pull_idx,
+                                                       int* __restrict__ pull_list) {
+  __shared__ int base_cnt[2][256];
+  __shared__ int wcnt[2][4][256];
   int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  base_cnt[tid] = 0;
+  base_cnt[0][tid] = 0;
+  base_cnt[1][tid] = 0;
   const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int tile = blockIdx.x;
   for (int r = 0; r < kTile / 256; ++r) {
@@ -265,6 +306,7 @@ __global__ void __launch_bounds__(256) k_radix_scatter(const int* __restrict__ k
     bool valid = e < n;
     int key = valid ? keys_in[e] : 0;
     int val = valid ? (vals_in ? vals_in[e] : e) : 0;
+    const bool pulls = valid && pull_idx && pull_idx[val] >= 0;
     unsigned d = digit_of(key, shift);
     unsigned long long peers = __ballot(valid);
 #pragma unroll
@@ -273,42 +315,49 @@ __global__ void __launch_bounds__(256) k_radix_scatter(const int* __restrict__ k
       unsigned long long bb = __ballot(valid && bit);
       peers &= bit ? bb : ~bb;
     }
-    int rank_in_wave = __popcll(peers & lt_mask);
-    int wave_cnt = __popcll(peers);
+    const unsigned long long ppeers = peers & __ballot(pulls);
+    const int rank_in_wave = __popcll(peers & lt_mask);
+    const int wave_cnt = __popcll(peers);
+    const int prank_in_wave = __popcll(ppeers & lt_mask);
+    const int pwave_cnt = __popcll(ppeers);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wcnt[q][tid] = 0;
-    __syncthreads();
-    if (valid && rank_in_wave == 0) wcnt[w][d] = wave_cnt;
-    __syncthreads();
-    if (valid) {
-      int rank = base_cnt[d] + rank_in_wave;
-      for (int q = 0; q < w; ++q) rank += wcnt[q][d];
-      int dst = offs[d * ntiles + tile] + rank;
-      keys_out[dst] = key;
-      vals_out[dst] = val;
+    for (int q = 0; q < 4; ++q) {
+      wcnt[0][q][tid] = 0;
+      wcnt[1][q][tid] = 0;
     }
     __syncthreads();
-    base_cnt[tid] += wcnt[0][tid] + wcnt[1][tid] + wcnt[2][tid] + wcnt[3][tid];
+    if (valid && rank_in_wave == 0) {
+      wcnt[0][w][d] = wave_cnt;
+      wcnt[1][w][d] = pwave_cnt;
+    }
+    __syncthreads();
+    if (valid) {
+      int rank = base_cnt[0][d] + rank_in_wave;
+      for (int q = 0; q < w; ++q) rank += wcnt[0][q][d];
+      const int dst = offs[d * ntiles + tile] + rank;
+      keys_out[dst] = key;
+      vals_out[dst] = val;
+      if (pos_out) pos_out[val] = dst;
+      if (pulls) {
+        int prank = base_cnt[1][d] + prank_in_wave;
+        for (int q = 0; q < w; ++q) prank += wcnt[1][q][d];
+        pull_list[offs[(256 + d) * ntiles + tile] - n + prank] = dst;
+      }
+    }
+    __syncthreads();
+    base_cnt[0][tid] += wcnt[0][0][tid] + wcnt[0][1][tid] + wcnt[0][2][tid] + wcnt[0][3][tid];
+    base_cnt[1][tid] += wcnt[1][0][tid] + wcnt[1][1][tid] + wcnt[1][2][tid] + wcnt[1][3][tid];
     __syncthreads();
   }
 }
 
 // -------------------------------------------------------------------------
-// 5. remap to positions
+// 6. remap to positions
 // -------------------------------------------------------------------------
-__global__ void k_pos(int V, const int* __restrict__ order, int* pos) {
-  int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p < V) {
-    int v = order[p];
-    if (v >= 0 && v < V) pos[v] = p;
-  }
-}
-
 __global__ void k_remap(int V, int N, const int* __restrict__ order, const int* __restrict__ pos,
                         const int* __restrict__ child, const int* __restrict__ parent,
                         const int* __restrict__ pull_idx, const int* __restrict__ push_idx,
-                        int* child_pos, int* parent_pos, int* pull_pos, int* push_pos,
-                        int* pull_key) {
+                        int* child_pos, int* parent_pos, int* pull_pos, int* push_pos) {
   int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= V) return;
   int v = order[p];
@@ -322,11 +371,10 @@ __global__ void k_remap(int V, int N, const int* __restrict__ order, const int* 
   int r = pull_idx ? pull_idx[v] : -1;
   pull_pos[p] = r;
   push_pos[p] = push_idx ? push_idx[v] : -1;
-  pull_key[p] = r >= 0 ? 0 : 1;
 }
 
 // -------------------------------------------------------------------------
-// 6. staging for the single device->host copy
+// 4. staging for the single device->host copy
 // -------------------------------------------------------------------------
 __global__ void k_stage(const int* __restrict__ flags, const int* __restrict__ level_offsets,
                         int cap, int* stage) {
@@ -363,7 +411,7 @@ Layout layout(int32_t V, int32_t N, int32_t n_x) {
   L.valsA = take((size_t)V + 1);
   L.keysB = take((size_t)V + 1);
   L.valsB = take((size_t)V + 1);
-  L.tile_hist = take((size_t)256 * L.ntiles);
+  L.tile_hist = take((size_t)512 * L.ntiles);   // digit counts, then pulling counts
   L.stage = take(kHostStageInts);
   L.total = o;
   return L;
@@ -371,22 +419,27 @@ Layout layout(int32_t V, int32_t N, int32_t n_x) {
 
 // Sorts (keys_in, vals_in) by key.  Pass p writes keys to bufK[p % 2] and
 // values to bufV[p % 2], except that the last pass writes its values to
-// vals_final.  keys_in must not alias bufK[0].
+// vals_final, pos_final[value] = its position and, for the values whose
+// vertex pulls an input, their positions to pull_list in order.  keys_in
+// must not alias bufK[0].
 cavs_status radix_sort(cavs_ctx* ctx, const int* keys_in, const int* vals_in, int n, int passes,
-                       int* const bufK[2], int* const bufV[2], int* vals_final, int* tile_hist,
-                       int ntiles) {
+                       int* const bufK[2], int* const bufV[2], int* vals_final, int* pos_final,
+                       const int* pull_idx, int* pull_list, int* tile_hist, int ntiles) {
   const int* ki = keys_in;
   const int* vi = vals_in;
   for (int pass = 0; pass < passes; ++pass) {
+    const bool last = pass == passes - 1;
     int* ko = bufK[pass % 2];
-    int* vo = pass == passes - 1 ? vals_final : bufV[pass % 2];
-    int shift = 8 * pass;
-    CAVS_LAUNCH("k_radix_hist", k_radix_hist, dim3(ntiles), dim3(256), 0, ctx->stream, ki, n, shift,
-                       ntiles, tile_hist);
-    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, ctx->stream, tile_hist, tile_hist,
-                       256 * ntiles, (const int*)nullptr);
-    CAVS_LAUNCH("k_radix_scatter", k_radix_scatter, dim3(ntiles), dim3(256), 0, ctx->stream, ki, vi, n,
-                       shift, ntiles, tile_hist, ko, vo);
+    int* vo = last ? vals_final : bufV[pass % 2];
+    const int* pl = last ? pull_idx : nullptr;
+    const int shift = 8 * pass;
+    CAVS_LAUNCH("k_radix_hist", k_radix_hist, dim3(ntiles), dim3(256), 0, ctx->stream, ki, vi, n,
+                shift, ntiles, pl, tile_hist);
+    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, ctx->stream, tile_hist,
+                tile_hist, (pl ? 512 : 256) * ntiles, (const int*)nullptr);
+    CAVS_LAUNCH("k_radix_scatter", k_radix_scatter, dim3(ntiles), dim3(256), 0, ctx->stream, ki,
+                vi, n, shift, ntiles, (const int*)tile_hist, ko, vo, last ? pos_final : nullptr, pl,
+                last ? pull_list : nullptr);
     CAVS_LAUNCH_CHECK(ctx);
     ki = ko;
     vi = vo;
@@ -433,38 +486,18 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
     return CAVS_OK;
   }
 
-  CAVS_HIP_CHECK(ctx, hipMemsetAsync(base, 0, L.zero_end, st));
-  CAVS_HIP_CHECK(ctx, hipMemsetAsync(s->level, 0xFF, sizeof(int) * (size_t)V, st));
   const int nb = cdiv(V, 256);
-  if (V > 0) {
-    CAVS_LAUNCH("k_scan_edges", k_scan_edges, dim3(nb), dim3(256), 0, st, V, N, n_x, g->n_push, g->child,
-                       g->parent, g->pull_idx, g->push_idx, ref_cnt, pull_cnt, nchild, flags);
-    CAVS_LAUNCH("k_check_links", k_check_links, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256), 0, st, V, N,
-                       n_x, g->child, g->parent, ref_cnt, pull_cnt, flags);
-    CAVS_LAUNCH("k_levels", k_levels, dim3(nb), dim3(256), 0, st, V, N, g->parent, nchild,
-                       arrive, s->level);
-    CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
-    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
-                       (const int*)(flags + F_T));
-    CAVS_LAUNCH_CHECK(ctx);
-    // passes: enough 8-bit digits for any level in [0, V)
-    int passes = 1;
-    while (passes < 4 && ((long)(V - 1) >> (8 * passes)) > 0) ++passes;
-    int* const lvK[2] = {kA, kB};
-    int* const lvV[2] = {vA, vB};
-    cavs_status r = radix_sort(ctx, s->level, nullptr, V, passes, lvK, lvV, s->order, tile_hist,
-                               L.ntiles);
-    if (r != CAVS_OK) return r;
-    CAVS_LAUNCH("k_pos", k_pos, dim3(nb), dim3(256), 0, st, V, s->order, s->pos);
-    CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, s->order, s->pos, g->child,
-                       g->parent, g->pull_idx, g->push_idx, s->child_pos, s->parent_pos,
-                       s->pull_pos, s->push_pos, kA);
-    CAVS_LAUNCH_CHECK(ctx);
-    int* const plK[2] = {kB, kB};
-    int* const plV[2] = {vA, vA};
-    r = radix_sort(ctx, kA, nullptr, V, 1, plK, plV, s->pull_list, tile_hist, L.ntiles);
-    if (r != CAVS_OK) return r;
-  }
+  const long zero_ints = (long)(L.zero_end / sizeof(int));
+  CAVS_LAUNCH("k_sched_init", k_sched_init, dim3(cdiv(zero_ints > V ? zero_ints : V, 256)),
+              dim3(256), 0, st, (int*)base, zero_ints, s->level, V);
+  CAVS_LAUNCH("k_scan_edges", k_scan_edges, dim3(nb), dim3(256), 0, st, V, N, n_x, g->n_push,
+              g->child, g->parent, g->pull_idx, g->push_idx, ref_cnt, pull_cnt, nchild, flags);
+  CAVS_LAUNCH("k_links_levels", k_links_levels, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256), 0,
+              st, V, N, n_x, g->child, g->parent, (const int*)ref_cnt, (const int*)pull_cnt,
+              (const int*)nchild, arrive, s->level, flags);
+  CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
+  CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
+              (const int*)(flags + F_T));
   const int cap = kHostStageInts - kStageHead;
   CAVS_LAUNCH("k_stage", k_stage, dim3(1), dim3(256), 0, st, flags, s->level_offsets, cap, stage);
   CAVS_LAUNCH_CHECK(ctx);
@@ -492,6 +525,18 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
                                        hipMemcpyDeviceToHost, st));
     CAVS_HIP_CHECK(ctx, hipStreamSynchronize(st));
   }
+  // levels lie in [0, T): enough 8-bit digits for T - 1
+  int passes = 1;
+  while (passes < 4 && ((long)(T > 0 ? T - 1 : 0) >> (8 * passes)) > 0) ++passes;
+  int* const lvK[2] = {kA, kB};
+  int* const lvV[2] = {vA, vB};
+  cavs_status r = radix_sort(ctx, s->level, nullptr, V, passes, lvK, lvV, s->order, s->pos,
+                             g->pull_idx, s->pull_list, tile_hist, L.ntiles);
+  if (r != CAVS_OK) return r;
+  CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, (const int*)s->order,
+              (const int*)s->pos, g->child, g->parent, g->pull_idx, g->push_idx, s->child_pos,
+              s->parent_pos, s->pull_pos, s->push_pos);
+  CAVS_LAUNCH_CHECK(ctx);
   return CAVS_OK;
 }
 

@@ -72,13 +72,23 @@ def test_schedule_bit_exact(ctx, seed):
     assert got["n_labelled"] == int((wl.push_idx >= 0).sum())
 
 
-@pytest.mark.parametrize("maker", ["sst", "varlstm", "treefc", "deep_bf16", "big"])
+@pytest.mark.parametrize("maker", ["sst", "varlstm", "treefc", "deep_bf16", "big",
+                                   "deep_chains_leaf_inputs", "deep_chains_all_inputs"])
 def test_schedule_bit_exact_benchmark_shapes(ctx, maker):
-    if maker == "big":   # > 65536 vertices: three radix passes
+    if maker == "big":   # > 65536 vertices, more than 64 radix tiles
         rng = np.random.Generator(np.random.PCG64(5))
         trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 300, size=500)]
         wl = W.make_workload("big", trees, N=2, D=4, H=64, C=5, rng=rng, shuffle_ids=True)
         assert wl.V > 65536
+    elif maker.startswith("deep_chains"):
+        # T > 256: the level sort takes two 8-bit passes, and its last pass
+        # also lists the pulling positions
+        rng = np.random.Generator(np.random.PCG64(6))
+        trees = [W.chain(600), W.chain(257), W.chain(1)]
+        trees += [W.random_split_tree(int(L), rng) for L in rng.integers(2, 60, size=80)]
+        inputs = "all" if maker.endswith("all_inputs") else "leaves"
+        wl = W.make_workload(maker, trees, N=2, D=4, H=64, C=5, rng=rng, inputs=inputs,
+                             shuffle_ids=True)
     else:
         wl = W.CONFIGS[maker](0)
     print("schedule shape %s V=%d" % (maker, wl.V), flush=True)
