@@ -145,6 +145,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.UT = (float*)(base + L.UT);
   n.zrow = (float*)(base + L.zrow);
   n.fuse_from = s->V;
+  n.f_unread_below = 0;
   n.Hs = (float*)(base + L.Hs);
   n.Cs = (float*)(base + L.Cs);
   n.Gs = (float*)(base + L.Gs);
@@ -355,6 +356,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     // own product, once every parent has stored dL/dh and dL/dc.
     const int tf = lstm_fuse_level(lo, T);
     n.fuse_from = lo[tf];
+    n.f_unread_below = s->n_inner_input > 0 ? 0 : lo[1];
     lstm_bwd_roots(n, str);
     int ts = persist_first_level(n, lo, T);
     if (ts < tf) ts = tf;

@@ -14,6 +14,8 @@ struct Net {
   int GW;                       // saved-gate / dA row width: (3+N)H (LSTM) or H (FC)
   float inv_denom;              // 1 / |Lambda|
   int fuse_from;                // LSTM backward: positions >= this get dA in the parent's epilogue
+  int f_unread_below;           // LSTM backward: rows below this (leaves, when no vertex with
+                                // children pulls) skip their dA forget columns: nothing reads them
   // schedule
   const int* child_pos;         // [V*N]
   const int* parent_pos;        // [V]

@@ -153,7 +153,7 @@ __device__ __forceinline__ void lstm_gates_fin(const Net& n, int p, int j, float
       d_f = gc * q.ck[k] * q.fk[k] * (1.f - q.fk[k]);
       n.dCp[(size_t)q.cp[k] * H + j] = gc * q.fk[k];
     }
-    da[(k == 0 ? H : 4 * H) + j] = d_f;
+    if (q.cp[k] >= 0 || p >= n.f_unread_below) da[(k == 0 ? H : 4 * H) + j] = d_f;
   }
   da[j] = d_i;
   da[2 * H + j] = d_o;

@@ -92,21 +92,26 @@ __global__ void k_scan_edges(int V, int N, int n_x, int n_push, const int* __res
     leafnoin = (nc == 0 && r < 0);
     innerin = (nc > 0 && r >= 0);
   }
-  links = wave_sum_int(links);
-  withp = wave_sum_int(withp);
-  lab = wave_sum_int(lab);
-  leafnoin = wave_sum_int(leafnoin);
-  innerin = wave_sum_int(innerin);
-  npull = wave_sum_int(npull);
-  bad = wave_sum_int(bad);
-  if (lane_id() == 0) {
-    if (links) atomicAdd(&flags[F_LINKS], links);
-    if (withp) atomicAdd(&flags[F_WITHPARENT], withp);
-    if (lab) atomicAdd(&flags[F_LABELLED], lab);
-    if (leafnoin) atomicAdd(&flags[F_LEAF_NOIN], leafnoin);
-    if (innerin) atomicAdd(&flags[F_INNER_IN], innerin);
-    if (npull) atomicAdd(&flags[F_NPULL], npull);
-    if (bad) atomicOr(&flags[F_RANGE], 1);
+  // counts summed per wavefront, then per workgroup in LDS: one atomic per
+  // workgroup and counter (the counters are few, contended addresses)
+  __shared__ int part[7][4];
+  int cnt[7] = {links, withp, lab, leafnoin, innerin, npull, bad};
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 7; ++i) {
+    cnt[i] = wave_sum_int(cnt[i]);
+    if (lane_id() == 0) part[i][w] = cnt[i];
+  }
+  __syncthreads();
+  if (threadIdx.x < 7) {
+    const int i = threadIdx.x;
+    const int t = part[i][0] + part[i][1] + part[i][2] + part[i][3];
+    constexpr int dst[7] = {F_LINKS, F_WITHPARENT, F_LABELLED, F_LEAF_NOIN, F_INNER_IN, F_NPULL,
+                            F_RANGE};
+    if (t) {
+      if (i == 6) atomicOr(&flags[F_RANGE], 1);
+      else atomicAdd(&flags[dst[i]], t);
+    }
   }
 }
 
@@ -201,9 +206,12 @@ __global__ void __launch_bounds__(256) k_level_hist(int V, const int* __restrict
 }
 
 // Single-block exclusive scan of n ints (src may equal dst).  If n_dev is
-// non-null the element count is *n_dev + 1 (scan of hist[0..T]).
+// non-null the element count is *n_dev + 1 (scan of hist[0..T]).  With
+// stage set, the block then fills the host staging area: the flags and
+// the first cap scanned values (the level offsets).
 __global__ void __launch_bounds__(1024) k_scan_excl(const int* src, int* dst, int n,
-                                                    const int* n_dev) {
+                                                    const int* n_dev, const int* flags, int cap,
+                                                    int* stage) {
   __shared__ int wsum[16];
   __shared__ int carry_s;
   if (n_dev) n = *n_dev + 1;
@@ -237,6 +245,11 @@ __global__ void __launch_bounds__(1024) k_scan_excl(const int* src, int* dst, in
     __syncthreads();
     if (tid == 0) carry_s = carry + wsum[15];
     __syncthreads();
+  }
+  if (stage) {
+    const int m = min(n, cap);
+    for (int i = tid; i < kStageHead; i += 1024) stage[i] = flags[i];
+    for (int i = tid; i < m; i += 1024) stage[kStageHead + i] = dst[i];
   }
 }
 
@@ -374,15 +387,8 @@ __global__ void k_remap(int V, int N, const int* __restrict__ order, const int* 
 }
 
 // -------------------------------------------------------------------------
-// 4. staging for the single device->host copy
+// 4. staging for the single device->host copy: done by the offsets scan
 // -------------------------------------------------------------------------
-__global__ void k_stage(const int* __restrict__ flags, const int* __restrict__ level_offsets,
-                        int cap, int* stage) {
-  int T = flags[F_T];
-  int n = min(T + 1, cap);
-  for (int i = threadIdx.x; i < kStageHead; i += blockDim.x) stage[i] = flags[i];
-  for (int i = threadIdx.x; i < n; i += blockDim.x) stage[kStageHead + i] = level_offsets[i];
-}
 
 struct Layout {
   size_t flags, ref_cnt, arrive, pull_cnt, hist, zero_end;
@@ -436,7 +442,8 @@ cavs_status radix_sort(cavs_ctx* ctx, const int* keys_in, const int* vals_in, in
     CAVS_LAUNCH("k_radix_hist", k_radix_hist, dim3(ntiles), dim3(256), 0, ctx->stream, ki, vi, n,
                 shift, ntiles, pl, tile_hist);
     CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, ctx->stream, tile_hist,
-                tile_hist, (pl ? 512 : 256) * ntiles, (const int*)nullptr);
+                tile_hist, (pl ? 512 : 256) * ntiles, (const int*)nullptr, (const int*)nullptr, 0,
+                (int*)nullptr);
     CAVS_LAUNCH("k_radix_scatter", k_radix_scatter, dim3(ntiles), dim3(256), 0, ctx->stream, ki,
                 vi, n, shift, ntiles, (const int*)tile_hist, ko, vo, last ? pos_final : nullptr, pl,
                 last ? pull_list : nullptr);
@@ -496,10 +503,9 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
               st, V, N, n_x, g->child, g->parent, (const int*)ref_cnt, (const int*)pull_cnt,
               (const int*)nchild, arrive, s->level, flags);
   CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
-  CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
-              (const int*)(flags + F_T));
   const int cap = kHostStageInts - kStageHead;
-  CAVS_LAUNCH("k_stage", k_stage, dim3(1), dim3(256), 0, st, flags, s->level_offsets, cap, stage);
+  CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
+              (const int*)(flags + F_T), (const int*)flags, cap, stage);
   CAVS_LAUNCH_CHECK(ctx);
   CAVS_HIP_CHECK(ctx, hipMemcpyAsync(ctx->host_stage, stage, sizeof(int) * kHostStageInts,
                                      hipMemcpyDeviceToHost, st));
