@@ -207,8 +207,8 @@ __global__ void __launch_bounds__(256) k_dx_gemm(Net n, int n_pull, int with_f, 
 // out[s][m][n] = sum_{q in split s} A(q, m) B(q, n).  The loader supplies
 // 4 consecutive m (or n) of row q; rows outside [0, Q) are never requested.
 struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = dA
-  static constexpr const char* kName = "k_tn_gemm<LdDUiou, 64>";
-  static constexpr const char* kName128 = "k_tn_gemm<LdDUiou, 128>";
+  static constexpr const char* kName = "k_tn_gemm<LdDUiou, 64, 4>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDUiou, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";
   struct Idx {
     int c0, c1;
@@ -232,8 +232,8 @@ struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = 
 };
 
 struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
-  static constexpr const char* kName = "k_tn_gemm<LdDUf, 64>";
-  static constexpr const char* kName128 = "k_tn_gemm<LdDUf, 128>";
+  static constexpr const char* kName = "k_tn_gemm<LdDUf, 64, 4>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDUf, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";
   struct Idx {
     int cp;
@@ -254,8 +254,8 @@ struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_f
 };
 
 struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
-  static constexpr const char* kName = "k_tn_gemm<LdDWx, 64>";
-  static constexpr const char* kName128 = "k_tn_gemm<LdDWx, 128>";
+  static constexpr const char* kName = "k_tn_gemm<LdDWx, 64, 4>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdDWx, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";
   struct Idx {
     int p, row;
@@ -280,8 +280,8 @@ struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1
 };
 
 struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
-  static constexpr const char* kName = "k_tn_gemm<LdFCdW, 64>";
-  static constexpr const char* kName128 = "k_tn_gemm<LdFCdW, 128>";
+  static constexpr const char* kName = "k_tn_gemm<LdFCdW, 64, 4>";
+  static constexpr const char* kName128 = "k_tn_gemm<LdFCdW, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";
   struct Idx {
     int cp;
