@@ -39,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, UT, zrow, Hs, Cs, Gs, dZ, lossv, dHp, dCp, dA, part, bar, total;
+  size_t P, UT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bar, total;
   size_t part_floats;
 };
 
@@ -48,7 +48,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   const size_t V = (size_t)(s->V > 0 ? s->V : 1), H = (size_t)p->H;
   const bool lstm = p->cell == CAVS_TREE_LSTM;
   const size_t GW = lstm ? (size_t)(3 + p->N) * H : H;
-  const size_t C = p->loss == CAVS_LOSS_CE ? (size_t)p->C : 0;
+  const size_t C = p->loss == CAVS_LOSS_CE ? (size_t)(p->C + 3) / 4 * 4 : 0;
   size_t o = 0;
   auto take = [&](size_t floats) {
     size_t r = o;
@@ -63,6 +63,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   L.Gs = take(lstm ? V * GW : 0);
   L.dZ = take(V * (C > 0 ? C : 1));
   L.lossv = take(V);
+  L.dHL = take(V * H);
   L.dHp = take(V * H);
   L.dCp = take(lstm ? V * H : 0);
   L.dA = take(V * GW);
@@ -124,6 +125,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.D = p->D;
   n.H = p->H;
   n.C = p->C;
+  n.CP = p->loss == CAVS_LOSS_CE ? (p->C + 3) / 4 * 4 : 0;
   n.loss = p->loss;
   n.bf = p->prec == CAVS_BF16;
   n.GW = p->cell == CAVS_TREE_LSTM ? (3 + p->N) * p->H : p->H;
@@ -151,6 +153,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.Gs = (float*)(base + L.Gs);
   n.dZ = (float*)(base + L.dZ);
   n.lossv = (float*)(base + L.lossv);
+  n.dHL = (float*)(base + L.dHL);
   n.dHp = (float*)(base + L.dHp);
   n.dCp = (float*)(base + L.dCp);
   n.dA = (float*)(base + L.dA);

@@ -118,18 +118,7 @@ __global__ void __launch_bounds__(256) k_fc_bwd_gates(Net n, int off, int M, int
   const int par = n.parent_pos[p];
   float gh = par >= 0 ? n.dHp[(size_t)p * H + j] : 0.f;
   const float h = n.Hs[(size_t)p * H + j];
-  const int q = n.push_pos[p];
-  if (q >= 0) {
-    if (n.loss == CAVS_LOSS_CE) {
-      const float* dz = n.dZ + (size_t)p * n.C;
-      const float* ws = n.Ws + (size_t)j * n.C;
-      float s = 0.f;
-      for (int c = 0; c < n.C; ++c) s += dz[c] * ws[c];
-      gh += s;
-    } else {
-      gh += (h - n.Y[(size_t)q * H + j]) * n.inv_denom;
-    }
-  }
+  gh += n.dHL[(size_t)p * H + j];
   if (leaf) dX[(size_t)n.pull_pos[p] * H + j] = gh;
   else n.dA[(size_t)p * H + j] = gh * (1.f - h * h);
 }

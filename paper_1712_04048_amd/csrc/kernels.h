@@ -10,6 +10,7 @@ namespace cavs {
 // layout produced by the scheduler: task V_t = positions [off_t, off_{t+1}).
 struct Net {
   int V, N, D, H, C, loss;
+  int CP;                       // row stride of dZ: C rounded up to a multiple of 4
   int bf;                       // 1: matrix-product operands rounded to bf16
   int GW;                       // saved-gate / dA row width: (3+N)H (LSTM) or H (FC)
   float inv_denom;              // 1 / |Lambda|
@@ -38,7 +39,8 @@ struct Net {
   float* Hs;                    // [V, H]
   float* Cs;                    // [V, H]
   float* Gs;                    // [V, GW] saved gates  i | f_0 | o | u | f_1
-  float* dZ;                    // [V, C]  d loss / d logits
+  float* dZ;                    // [V, CP] d loss / d logits (columns >= C are zero)
+  float* dHL;                   // [V, H]  the loss head's share of dL/dh (zero if unlabelled)
   float* lossv;                 // [V]     per-vertex loss terms
   float* dHp;                   // [V, H]  dL/dh contributed by the parent
   float* dCp;                   // [V, H]  dL/dc contributed by the parent

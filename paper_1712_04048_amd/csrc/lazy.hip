@@ -11,7 +11,6 @@
 namespace cavs {
 namespace {
 
-constexpr int kLossMaxC = 16;
 constexpr int kMaxSplits = 16;   // sizes the split-K scratch: 16 x (4H x H) floats
 constexpr int kSplitCap = 32;    // more splits only where the scratch holds them
 
@@ -730,6 +729,7 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
 // second adds the chunks in order, so the result is deterministic.
 constexpr int kBiasChunks = 256;
 
+template <int CP4>
 __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, int lo1,
                                                    int rows_per, int bxA, int wA, int W,
                                                    float* __restrict__ part) {
@@ -766,13 +766,15 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
     *reinterpret_cast<float4*>(out + c) = s;
     return;
   }
-  // head: columns wA + j*C + c (dW_s row-major), then wA + H*C + c (db_s)
+  // head: columns wA + j*C + c (dW_s row-major), then wA + H*C + c (db_s);
+  // dZ rows hold CP = 4 CP4 columns, zero past C
   const int j = 4 * ((blockIdx.x - bxA) * 256 + threadIdx.x);
   if (j >= H) return;
   const int C = n.C;
-  float acc[4][kLossMaxC], zs[kLossMaxC];
+  constexpr int CP = 4 * CP4;
+  float acc[4][CP], zs[CP];
 #pragma unroll
-  for (int c = 0; c < kLossMaxC; ++c) {
+  for (int c = 0; c < CP; ++c) {
     zs[c] = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[e][c] = 0.f;
@@ -780,27 +782,31 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
 #pragma unroll 4
   for (int p = lo; p < hi; ++p) {
     const float4 h = *reinterpret_cast<const float4*>(n.Hs + (size_t)p * H + j);
-    const float* dz = n.dZ + (size_t)p * C;
+    const float4* dz = reinterpret_cast<const float4*>(n.dZ + (size_t)p * CP);
 #pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
-      if (c < C) {
-        const float z = dz[c];
-        acc[0][c] += h.x * z;
-        acc[1][c] += h.y * z;
-        acc[2][c] += h.z * z;
-        acc[3][c] += h.w * z;
-        zs[c] += z;
+    for (int c4 = 0; c4 < CP4; ++c4) {
+      const float4 z4 = dz[c4];
+      const float z[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int c = 4 * c4 + e;
+        acc[0][c] += h.x * z[e];
+        acc[1][c] += h.y * z[e];
+        acc[2][c] += h.z * z[e];
+        acc[3][c] += h.w * z[e];
+        zs[c] += z[e];
       }
+    }
   }
   float* o = out + wA + (size_t)j * C;
 #pragma unroll
   for (int e = 0; e < 4; ++e)
 #pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
+    for (int c = 0; c < CP; ++c)
       if (c < C) o[e * C + c] = acc[e][c];
   if (j == 0)
 #pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
+    for (int c = 0; c < CP; ++c)
       if (c < C) out[wA + H * C + c] = zs[c];
 }
 
@@ -827,62 +833,137 @@ __global__ void __launch_bounds__(1024) k_bias_reduce(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------- loss
-// One wavefront per position: logits (or the L2 residual), the loss term and
-// d loss / d logits = (softmax - onehot) / |Lambda|.
-__global__ void __launch_bounds__(256) k_loss(Net n) {
+// Cross-entropy head over every position (the push of Section 3.4, batched
+// lazily).  A workgroup owns 16 positions; its eight wavefronts split both
+// products:
+//   z = h W_s + b_s       16 positions x 16 class columns on MFMA, wavefront
+//                         w taking the K chunks w, w+8, ... (MC at a time,
+//                         loads first); the eight partial blocks are added in
+//                         order in LDS (columns >= C repeat class C-1 and are
+//                         masked);
+//   log-sum-exp and softmax across the 16 lanes that hold a row's classes;
+//   dZ = (softmax - onehot(label)) / |Lambda| for labelled positions, zero
+//   rows otherwise (row stride CP, pad columns zero);
+//   dHL = dZ W_s^T, the head's share of dL/dh, on MFMA (K = CP), wavefront w
+//   taking the 16-unit blocks w, w+8, ...
+constexpr int kLossWaves = 8;
+
+template <int MC>
+__global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
+  constexpr int NW = kLossWaves;
+  __shared__ float zp[NW][16][17];
+  __shared__ float dzl[NW][16][17];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+  const int p0 = blockIdx.x * 16;
+  const int H = n.H, C = n.C, CP = n.CP, V = n.V;
+  const int cm = min(r, C - 1);
+  const bool cval = r < C;
+  int q[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = p0 + 4 * g + i < V ? n.push_pos[p0 + 4 * g + i] : -1;
+  const float bsc = n.bs[cm];
+
+  const float* hrow = n.Hs + (size_t)min(p0 + r, V - 1) * H + 8 * g;
+  const float* wcol = n.Ws + cm;
+  const int nch = H / kBK;
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+  for (int c0 = w; c0 < nch; c0 += NW * MC) {
+    float a[MC][8], b[MC][8];
+#pragma unroll
+    for (int t = 0; t < MC; ++t) {
+      const int k0 = min(c0 + NW * t, nch - 1) * kBK;
+      ld8(hrow + k0, a[t]);
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) b[t][s2] = wcol[(size_t)(k0 + 8 * g + s2) * C];
+    }
+#pragma unroll
+    for (int t = 0; t < MC; ++t)
+      if (c0 + NW * t < nch) acc = mfma_chunk8<false>(a[t], b[t], acc);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) zp[w][4 * g + i][r] = acc[i];
+  __syncthreads();
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int p = p0 + 4 * g + i;
+    float z = zp[0][4 * g + i][r];
+#pragma unroll
+    for (int v = 1; v < NW; ++v) z += zp[v][4 * g + i][r];
+    z += bsc;
+    float m = cval ? z : -INFINITY;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+    float se = cval ? expf(z - m) : 0.f;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) se += __shfl_xor(se, o, kWave);
+    const float lse = m + logf(se);
+    float d = 0.f;
+    if (q[i] >= 0 && cval) d = (expf(z - lse) - (r == q[i] ? 1.f : 0.f)) * n.inv_denom;
+    dzl[w][4 * g + i][r] = d;
+    if (w == 0 && p < V) {
+      if (r < CP) n.dZ[(size_t)p * CP + r] = d;
+      if (q[i] < 0 && r == 0) n.lossv[p] = 0.f;
+      if (q[i] >= 0 && r == q[i]) n.lossv[p] = lse - z;
+    }
+  }
+  // each wavefront re-reads only its own copy of dZ: its LDS operations
+  // complete in order
+  __builtin_amdgcn_wave_barrier();
+  float a[4];
+  const int KT = CP / 4;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) a[t] = t < KT ? dzl[w][r][4 * t + g] : 0.f;
+  const int nb = H / 16;
+  constexpr int MB = 4;
+  for (int b0 = w; b0 < nb; b0 += NW * MB) {
+    float wb[MB][4];
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      const float* wrow = n.Ws + (size_t)(min(b0 + NW * u, nb - 1) * 16 + r) * C;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) wb[u][t] = t < KT ? wrow[min(4 * t + g, C - 1)] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      const int jb = b0 + NW * u;
+      if (jb >= nb) break;
+      v4f o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (t < KT) o = mfma_f32_16x16x4(a[t], wb[u][t], o);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int p = p0 + 4 * g + i;
+        if (p < V) n.dHL[(size_t)p * H + jb * 16 + r] = o[i];
+      }
+    }
+  }
+}
+
+// Squared-error head: one wavefront per position; loss 0.5 |h - y|^2 and
+// dHL = (h - y) / |Lambda| (zero rows for unlabelled positions).
+__global__ void __launch_bounds__(256) k_loss_l2(Net n) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + w;
   if (p >= n.V) return;
-  const int q = n.push_pos[p], H = n.H, C = n.C;
+  const int q = n.push_pos[p], H = n.H;
   const float* h = n.Hs + (size_t)p * H;
+  float* dh = n.dHL + (size_t)p * H;
   if (q < 0) {
     if (lane == 0) n.lossv[p] = 0.f;
-    if (n.loss == CAVS_LOSS_CE && lane < C) n.dZ[(size_t)p * C + lane] = 0.f;
+    for (int j = lane; j < H; j += 64) dh[j] = 0.f;
     return;
   }
-  if (n.loss == CAVS_LOSS_CE) {
-    float z[kLossMaxC];
-#pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c) z[c] = 0.f;
-#pragma unroll 8
-    for (int j = lane; j < H; j += 64) {
-      const float hj = h[j];
-      const float* ws = n.Ws + (size_t)j * C;
-#pragma unroll
-      for (int c = 0; c < kLossMaxC; ++c)
-        if (c < C) z[c] += hj * ws[c];
-    }
-    float zmax = -INFINITY;
-#pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
-      if (c < C) {
-        z[c] = wave_sum(z[c]) + n.bs[c];
-        zmax = fmaxf(zmax, z[c]);
-      }
-    float se = 0.f;
-#pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
-      if (c < C) se += expf(z[c] - zmax);
-    const float lse = zmax + logf(se);
-    float zq = 0.f;
-#pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
-      if (c == q) zq = z[c];
-#pragma unroll
-    for (int c = 0; c < kLossMaxC; ++c)
-      if (c < C && lane == c)
-        n.dZ[(size_t)p * C + c] = (expf(z[c] - lse) - (c == q ? 1.f : 0.f)) * n.inv_denom;
-    if (lane == 0) n.lossv[p] = lse - zq;
-  } else {
-    const float* y = n.Y + (size_t)q * H;
-    float s = 0.f;
-    for (int j = lane; j < H; j += 64) {
-      const float d = h[j] - y[j];
-      s += d * d;
-    }
-    s = wave_sum(s);
-    if (lane == 0) n.lossv[p] = 0.5f * s;
+  const float* y = n.Y + (size_t)q * H;
+  float s = 0.f;
+  for (int j = lane; j < H; j += 64) {
+    const float d = h[j] - y[j];
+    s += d * d;
+    dh[j] = d * n.inv_denom;
   }
+  s = wave_sum(s);
+  if (lane == 0) n.lossv[p] = 0.5f * s;
 }
 
 __global__ void __launch_bounds__(1024) k_loss_sum(const float* __restrict__ lossv, int V,
@@ -940,7 +1021,15 @@ void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
 }
 
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
-  CAVS_LAUNCH("k_loss", k_loss, dim3(cdiv(n.V, 4)), dim3(256), 0, s, n);
+  if (n.loss == CAVS_LOSS_CE) {
+    const int per = cdiv(n.H / kBK, kLossWaves);  // K chunks per wavefront
+    const dim3 grid(cdiv(n.V, 16)), block(64 * kLossWaves);
+    if (per <= 1) CAVS_LAUNCH("k_loss_ce<1>", k_loss_ce<1>, grid, block, 0, s, n);
+    else if (per <= 2) CAVS_LAUNCH("k_loss_ce<2>", k_loss_ce<2>, grid, block, 0, s, n);
+    else CAVS_LAUNCH("k_loss_ce<4>", k_loss_ce<4>, grid, block, 0, s, n);
+  } else {
+    CAVS_LAUNCH("k_loss_l2", k_loss_l2, dim3(cdiv(n.V, 4)), dim3(256), 0, s, n);
+  }
   CAVS_LAUNCH("k_loss_sum", k_loss_sum, dim3(1), dim3(1024), 0, s, (const float*)n.lossv, n.V,
                      n.inv_denom, loss_out);
 }
@@ -993,8 +1082,16 @@ void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float
   const int rows_per = cdiv(n.V > 0 ? n.V : 1, nchunk);
   nchunk = cdiv(n.V > 0 ? n.V : 1, rows_per);
   const int bxA = cdiv(wA / 4, 256), bxB = head ? cdiv(n.H / 4, 256) : 0;
-  CAVS_LAUNCH("k_bias_part", k_bias_part, dim3(bxA + bxB, nchunk), dim3(256), 0, s, n, row0, row1,
-              lo1, rows_per, bxA, wA, W, part);
+  const dim3 grid(bxA + bxB, nchunk);
+  auto part_launch = [&](auto kern, const char* name) {
+    CAVS_LAUNCH(name, kern, grid, dim3(256), 0, s, n, row0, row1, lo1, rows_per, bxA, wA, W, part);
+  };
+  switch (head ? n.CP / 4 : 1) {
+    case 1: part_launch(k_bias_part<1>, "k_bias_part<1>"); break;
+    case 2: part_launch(k_bias_part<2>, "k_bias_part<2>"); break;
+    case 3: part_launch(k_bias_part<3>, "k_bias_part<3>"); break;
+    default: part_launch(k_bias_part<4>, "k_bias_part<4>"); break;
+  }
   CAVS_LAUNCH("k_bias_reduce", k_bias_reduce, dim3(cdiv(W, 64)), dim3(1024), 0, s,
               (const float*)part, nchunk, W, wA, HC, db, dWs, dbs);
 }

@@ -93,8 +93,8 @@ __device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, fl
 
 // ----------------------------------------------------------------- backward
 // Everything dA of position p, unit j reads besides the parent's dL/dh: the
-// vertex's own loss term of dL/dh, dL/dc from the parent, the saved gates and
-// c, and the children's f_k and c_k.
+// loss head's term of dL/dh (written by the loss kernel), dL/dc from the
+// parent, the saved gates and c, and the children's f_k and c_k.
 template <int NCH>
 struct GatePre {
   float lg, gcin, ig, og, ug, c;
@@ -106,18 +106,7 @@ template <int NCH>
 __device__ __forceinline__ void lstm_gates_pre(const Net& n, int p, int j, float gcin,
                                                GatePre<NCH>& q) {
   const int H = n.H;
-  const int push = n.push_pos[p];
-  float s = 0.f;
-  if (push >= 0) {
-    if (n.loss == CAVS_LOSS_CE) {
-      const float* dz = n.dZ + (size_t)p * n.C;
-      const float* ws = n.Ws + (size_t)j * n.C;
-      for (int c = 0; c < n.C; ++c) s += dz[c] * ws[c];
-    } else {
-      s = (n.Hs[(size_t)p * H + j] - n.Y[(size_t)push * H + j]) * n.inv_denom;
-    }
-  }
-  q.lg = s;
+  q.lg = n.dHL[(size_t)p * H + j];
   q.gcin = gcin;
   const float* g = n.Gs + (size_t)p * n.GW;
   q.ig = g[j];
