@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(256) k_fc_fwd_level(Net n, int off, int M) {
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int col = n0 + wcol + tn * 16 + r;
-        const float h = tanhf(acc[tm][tn][i] + n.b[col]);
+        const float h = tanh_(acc[tm][tn][i] + n.b[col]);
         n.Hs[(size_t)p * H + col] = h;
         n.h_out[(size_t)v * H + col] = h;
       }

@@ -104,8 +104,8 @@ __global__ void __launch_bounds__(256) k_pull_leaf(Net n, int n_pull, int lo1) {
         ai += zi;
         ao += zo;
         au += zu;
-        const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanhf(au);
-        const float c = ig * ug, h = og * tanhf(c);
+        const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanh_(au);
+        const float c = ig * ug, h = og * tanh_(c);
         n.Hs[(size_t)p * H + j] = h;
         n.Cs[(size_t)p * H + j] = c;
         float* g = n.Gs + (size_t)p * n.GW;   // a leaf's forget gates are never read

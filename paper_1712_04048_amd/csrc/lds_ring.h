@@ -26,6 +26,14 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// s_waitcnt vmcnt(N) lgkmcnt(0): this wavefront's older copies beyond the
+// newest N have landed and its LDS reads have returned.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+}
+
 __device__ __forceinline__ void barrier_nofence() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -93,6 +101,54 @@ __device__ __forceinline__ void ring_loop(int nch, const RingT& ring, Issue&& is
     if (c + 1 < nch) step(IC<1>{}, c + 1);
     if constexpr (S > 2) if (c + 2 < nch) step(IC<2>{}, c + 2);
     if constexpr (S > 3) if (c + 3 < nch) step(IC<3>{}, c + 3);
+  }
+}
+
+// The same ring with the MFMA fragments double-buffered in registers: while
+// chunk c is multiplied from one register set, the LDS reads of chunk c+1
+// fill the other, and sched() interleaves those reads with the MFMAs so that
+// they issue while the matrix core is busy.  One barrier per chunk covers
+// both hazards: after it every wavefront holds chunk c's fragments (so the
+// copies of chunk c+S may overwrite its stage) and chunk c+1 has landed.
+//   issue(stage, c): the IPW copies of chunk c;
+//   read(stage ptr, F&): the LDS reads of one chunk's fragments;
+//   mma(const F&): its MFMAs;  sched(): the interleaving directives.
+template <int S, int IPW, class F, class Issue, class Read, class Mma, class Sched, class RingT>
+__device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&& issue,
+                                             Read&& read, Mma&& mma, Sched&& sched) {
+  issue(IC<0>{}, 0);
+  if (1 < nch) issue(IC<1>{}, 1);
+  if constexpr (S > 2) if (2 < nch) issue(IC<2>{}, 2);
+  if constexpr (S > 3) if (3 < nch) issue(IC<3>{}, 3);
+  if (S - 1 < nch) wait_vmcnt<(S - 1) * IPW>();
+  else wait_vmcnt<0>();
+  barrier_nofence();
+  F f0, f1;
+  read(ring.at(IC<0>{}), f0);
+  auto step = [&](auto sc, F& cur, F& nxt, int c) {
+    constexpr int k = decltype(sc)::value;
+    if (c + S - 1 < nch) wait_vmcnt_lgkm0<(S - 2) * IPW>();
+    else wait_vmcnt_lgkm0<0>();
+    barrier_nofence();
+    if (c + S < nch) issue(IC<k>{}, c + S);
+    // past the last chunk this reads a stale stage: in bounds, never used
+    read(ring.at(IC<(k + 1) % S>{}), nxt);
+    mma(cur);
+    sched();
+  };
+  for (int c = 0; c < nch; c += 2 * S) {
+    step(IC<0>{}, f0, f1, c);
+    if (c + 1 < nch) step(IC<1 % S>{}, f1, f0, c + 1);
+    if (c + 2 < nch) step(IC<2 % S>{}, f0, f1, c + 2);
+    if (c + 3 < nch) step(IC<3 % S>{}, f1, f0, c + 3);
+    if constexpr (S > 2) {
+      if (c + 4 < nch) step(IC<4 % S>{}, f0, f1, c + 4);
+      if (c + 5 < nch) step(IC<5 % S>{}, f1, f0, c + 5);
+    }
+    if constexpr (S > 3) {
+      if (c + 6 < nch) step(IC<6 % S>{}, f0, f1, c + 6);
+      if (c + 7 < nch) step(IC<7 % S>{}, f1, f0, c + 7);
+    }
   }
 }
 

@@ -43,8 +43,8 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int sk
     ao += Pp[G_O * H + j];
     au += Pp[G_U * H + j];
   }
-  const float i = sigmoidf_(ai), o = sigmoidf_(ao), u = tanhf(au);
-  const float c = i * u, h = o * tanhf(c);
+  const float i = sigmoidf_(ai), o = sigmoidf_(ao), u = tanh_(au);
+  const float c = i * u, h = o * tanh_(c);
   n.Hs[(size_t)p * H + j] = h;
   n.Cs[(size_t)p * H + j] = c;
   // a leaf has no forget gates: their saved columns are never read

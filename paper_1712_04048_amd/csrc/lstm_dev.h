@@ -57,7 +57,7 @@ __device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const F
     ao += q.po;
     au += q.pu;
   }
-  const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanhf(au);
+  const float ig = sigmoidf_(ai), og = sigmoidf_(ao), ug = tanh_(au);
   float c = ig * ug;
   float f0 = 0.f, f1 = 0.f;
   if (q.cp[0] >= 0) {
@@ -70,7 +70,7 @@ __device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const F
       c += f1 * q.cc[NCH - 1];
     }
   }
-  const float h = og * tanhf(c);
+  const float h = og * tanh_(c);
   n.Hs[(size_t)p * H + j] = h;
   n.Cs[(size_t)p * H + j] = c;
   float* g = n.Gs + (size_t)p * n.GW;
@@ -89,6 +89,112 @@ __device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, fl
   FwdPre<NCH> q;
   lstm_fwd_pre<NCH>(n, p, j, q);
   lstm_fwd_fin<NCH>(n, p, j, q, zi, zo, zu, zf0, zf1);
+}
+
+// Forward epilogue over four consecutive units j0 .. j0+3 of one position
+// (the layout of an MFMA block whose A operand is the weight fragment: lane
+// (r, g) holds units 4g .. 4g+3 of position r).  What depends only on the
+// position, only on the units, or on both is prefetched separately, before
+// the product, so that its latency overlaps the matrix work.
+struct FwdPos {
+  int cp0, cp1, v, pr;  // child positions (-1 absent), vertex id, pull row (-1 none)
+};
+struct Bias4 {
+  float4 i, f, o, u;
+};
+template <int NCH>
+struct FwdCell4 {
+  float4 cc[NCH];       // the children's c at the four units (zero if absent)
+};
+
+template <int NCH>
+__device__ __forceinline__ void lstm_fwd_pos(const Net& n, int p, FwdPos& q) {
+  q.cp0 = n.child_pos[(size_t)p * NCH];
+  q.cp1 = NCH == 2 ? n.child_pos[(size_t)p * NCH + 1] : -1;
+  q.v = n.order[p];
+  q.pr = n.pull_pos[p];
+}
+
+__device__ __forceinline__ void lstm_bias4(const Net& n, int j0, Bias4& b) {
+  const int H = n.H;
+  b.i = ldg4(n.b + G_I * H + j0);
+  b.f = ldg4(n.b + G_F * H + j0);
+  b.o = ldg4(n.b + G_O * H + j0);
+  b.u = ldg4(n.b + G_U * H + j0);
+}
+
+template <int NCH>
+__device__ __forceinline__ void lstm_fwd_cell4(const Net& n, const FwdPos& q, int j0,
+                                               FwdCell4<NCH>& e) {
+  const int H = n.H;
+  e.cc[0] = q.cp0 >= 0 ? ldg4(n.Cs + (size_t)q.cp0 * H + j0) : f4zero();
+  if constexpr (NCH == 2) e.cc[1] = q.cp1 >= 0 ? ldg4(n.Cs + (size_t)q.cp1 * H + j0) : f4zero();
+}
+
+// Gates, cell update and the scatter of (c, h) for units j0 .. j0+3 of
+// position p; z* hold the matrix-product parts of the pre-activations.
+template <int NCH>
+__device__ __forceinline__ void lstm_fwd_fin4(const Net& n, int p, int j0, const FwdPos& q,
+                                              const Bias4& b, const FwdCell4<NCH>& e, v4f zi,
+                                              v4f zo, v4f zu, v4f zf0, v4f zf1) {
+  const int H = n.H;
+  float4 pi = f4zero(), pf = f4zero(), po = f4zero(), pu = f4zero();
+  if (q.pr >= 0) {
+    const float* Pp = n.P + (size_t)p * 4 * H + j0;
+    pi = ldg4(Pp + G_I * H);
+    pf = ldg4(Pp + G_F * H);
+    po = ldg4(Pp + G_O * H);
+    pu = ldg4(Pp + G_U * H);
+  }
+  // same association as the scalar epilogue: (z + b) + pulled term for
+  // i, o, u; z + (b + pulled term) for f
+  const float bi[4] = {b.i.x, b.i.y, b.i.z, b.i.w}, qi[4] = {pi.x, pi.y, pi.z, pi.w};
+  const float bo[4] = {b.o.x, b.o.y, b.o.z, b.o.w}, qo[4] = {po.x, po.y, po.z, po.w};
+  const float bu[4] = {b.u.x, b.u.y, b.u.z, b.u.w}, qu[4] = {pu.x, pu.y, pu.z, pu.w};
+  const float bf[4] = {b.f.x + pf.x, b.f.y + pf.y, b.f.z + pf.z, b.f.w + pf.w};
+  const float c0[4] = {e.cc[0].x, e.cc[0].y, e.cc[0].z, e.cc[0].w};
+  float c1[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (NCH == 2) {
+    c1[0] = e.cc[1].x; c1[1] = e.cc[1].y; c1[2] = e.cc[1].z; c1[3] = e.cc[1].w;
+  }
+  float ig[4], og[4], ug[4], f0[4], f1[4], c[4], h[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float ai = zi[k] + bi[k], ao = zo[k] + bo[k], au = zu[k] + bu[k];
+    if (q.pr >= 0) {
+      ai += qi[k];
+      ao += qo[k];
+      au += qu[k];
+    }
+    ig[k] = sigmoidf_(ai);
+    og[k] = sigmoidf_(ao);
+    ug[k] = tanh_(au);
+    c[k] = ig[k] * ug[k];
+    f0[k] = 0.f;
+    f1[k] = 0.f;
+    if (q.cp0 >= 0) {
+      f0[k] = sigmoidf_(zf0[k] + bf[k]);
+      c[k] += f0[k] * c0[k];
+    }
+    if constexpr (NCH == 2) {
+      if (q.cp1 >= 0) {
+        f1[k] = sigmoidf_(zf1[k] + bf[k]);
+        c[k] += f1[k] * c1[k];
+      }
+    }
+    h[k] = og[k] * tanh_(c[k]);
+  }
+  auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
+  st4(n.Hs + (size_t)p * H + j0, f4(h));
+  st4(n.Cs + (size_t)p * H + j0, f4(c));
+  float* g = n.Gs + (size_t)p * n.GW + j0;
+  st4(g, f4(ig));
+  st4(g + H, f4(f0));
+  st4(g + 2 * H, f4(og));
+  st4(g + 3 * H, f4(ug));
+  if constexpr (NCH == 2) st4(g + 4 * H, f4(f1));
+  st4(n.h_out + (size_t)q.v * H + j0, f4(h));
+  if (n.c_out) st4(n.c_out + (size_t)q.v * H + j0, f4(c));
 }
 
 // ----------------------------------------------------------------- backward
@@ -129,7 +235,7 @@ __device__ __forceinline__ void lstm_gates_fin(const Net& n, int p, int j, float
                                                const GatePre<NCH>& q) {
   const int H = n.H;
   const float gh = gh_parent + q.lg;
-  const float tau = tanhf(q.c);
+  const float tau = tanh_(q.c);
   const float d_o = gh * tau * q.og * (1.f - q.og);
   const float gc = q.gcin + gh * q.og * (1.f - tau * tau);
   const float d_i = gc * q.ug * q.ig * (1.f - q.ig);

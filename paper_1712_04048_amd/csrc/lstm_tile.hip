@@ -69,6 +69,26 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   xcd_tile(H / BU, rt, ut);
   const int row0 = off + rt * BM, rowend = off + M, u0 = ut * BU;
 
+  // Epilogue operands, prefetched before the product.  The weight fragment
+  // is the MFMA's A operand, so in block (tm, tu) lane (r, gq) holds units
+  // j0 .. j0+3 of one position p (four consecutive units: float4 access).
+  FwdPos pos[TM];
+  Bias4 bias[TU];
+  FwdCell4<NCH> cell[TM][TU];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+    pos[tm] = FwdPos{-1, -1, 0, -1};
+    if (p < rowend) lstm_fwd_pos<NCH>(n, p, pos[tm]);
+  }
+#pragma unroll
+  for (int tu = 0; tu < TU; ++tu) lstm_bias4(n, u0 + wu * (BU / 2) + tu * 16 + 4 * gq, bias[tu]);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tu = 0; tu < TU; ++tu)
+      lstm_fwd_cell4<NCH>(n, pos[tm], u0 + wu * (BU / 2) + tu * 16 + 4 * gq, cell[tm][tu]);
+
   // source of each of this lane's copies: LDS rows [0, AROWS) are child
   // rows (child slot ch of position row0 + rr), the rest rows of U^T
   const float* src[IPW];
@@ -103,50 +123,63 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
 #pragma unroll
     for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
   };
-  auto compute = [&](const float* Ls, int) {
-    float bfr[4][TU][8];
+  struct Frag {
+    float a0[TM][8], a1[TM][8], b[4][TU][8];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
       for (int tu = 0; tu < TU; ++tu)
-        frag_sw(Ls, AROWS + g * BU + wu * (BU / 2) + tu * 16 + r, gq, bfr[g][tu]);
+        frag_sw(Ls, AROWS + g * BU + wu * (BU / 2) + tu * 16 + r, gq, f.b[g][tu]);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       const int ra = wr * (BM / 2) + tm * 16 + r;
-      float a0[8], a1[8], ah[8];
-      frag_sw(Ls, ra, gq, a0);
-      if constexpr (NCH == 2) {
-        frag_sw(Ls, BM + ra, gq, a1);
+      frag_sw(Ls, ra, gq, f.a0[tm]);
+      if constexpr (NCH == 2) frag_sw(Ls, BM + ra, gq, f.a1[tm]);
+    }
+  };
+  // A = weight fragment (units), B = child fragment (positions)
+  auto mma = [&](const Frag& f) {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) ah[s] = a0[s] + a1[s];
-      } else {
+    for (int tm = 0; tm < TM; ++tm) {
+      float ah[8];
 #pragma unroll
-        for (int s = 0; s < 8; ++s) ah[s] = a0[s];
-      }
+      for (int s = 0; s < 8; ++s) ah[s] = NCH == 2 ? f.a0[tm][s] + f.a1[tm][s] : f.a0[tm][s];
 #pragma unroll
       for (int tu = 0; tu < TU; ++tu) {
-        acc[tm][tu][0] = mfma_chunk8<BF>(ah, bfr[G_I][tu], acc[tm][tu][0]);
-        acc[tm][tu][1] = mfma_chunk8<BF>(ah, bfr[G_O][tu], acc[tm][tu][1]);
-        acc[tm][tu][2] = mfma_chunk8<BF>(ah, bfr[G_U][tu], acc[tm][tu][2]);
-        acc[tm][tu][3] = mfma_chunk8<BF>(a0, bfr[G_F][tu], acc[tm][tu][3]);
-        if constexpr (NCH == 2) acc[tm][tu][4] = mfma_chunk8<BF>(a1, bfr[G_F][tu], acc[tm][tu][4]);
+        acc[tm][tu][0] = mfma_chunk8<BF>(f.b[G_I][tu], ah, acc[tm][tu][0]);
+        acc[tm][tu][1] = mfma_chunk8<BF>(f.b[G_O][tu], ah, acc[tm][tu][1]);
+        acc[tm][tu][2] = mfma_chunk8<BF>(f.b[G_U][tu], ah, acc[tm][tu][2]);
+        acc[tm][tu][3] = mfma_chunk8<BF>(f.b[G_F][tu], f.a0[tm], acc[tm][tu][3]);
+        if constexpr (NCH == 2)
+          acc[tm][tu][4] = mfma_chunk8<BF>(f.b[G_F][tu], f.a1[tm], acc[tm][tu][4]);
       }
     }
   };
-  ring_loop<S, IPW>(H / kBK, ring, issue, compute);
+  auto sched = [&]() {
+    // one 16-byte LDS read between every few MFMAs of the current chunk
+    constexpr int NR = 2 * (4 * TU + NCH * TM), NM = TM * TU * NACC * (BF ? 1 : 8);
+    constexpr int PER = NM / NR > 0 ? NM / NR : 1;
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, PER, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+  };
+  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, mma, sched);
 
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+    if (p >= rowend) continue;
 #pragma unroll
     for (int tu = 0; tu < TU; ++tu)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = row0 + wr * (BM / 2) + tm * 16 + 4 * gq + i;
-        const int j = u0 + wu * (BU / 2) + tu * 16 + r;
-        if (p < rowend)
-          lstm_fwd_epilogue<NCH>(n, p, j, acc[tm][tu][0][i], acc[tm][tu][1][i], acc[tm][tu][2][i],
-                                 acc[tm][tu][3][i], NCH == 2 ? acc[tm][tu][NACC - 1][i] : 0.f);
-      }
+      lstm_fwd_fin4<NCH>(n, p, u0 + wu * (BU / 2) + tu * 16 + 4 * gq, pos[tm], bias[tu],
+                         cell[tm][tu], acc[tm][tu][0], acc[tm][tu][1], acc[tm][tu][2],
+                         acc[tm][tu][3], NCH == 2 ? acc[tm][tu][NACC - 1] : v4f{0.f, 0.f, 0.f, 0.f});
+  }
 }
 
 template <int NCH, bool BF, int BM, int BN, int S>
@@ -293,7 +326,7 @@ bool lstm_tile_applies(const Net& n, int M) {
 // tiles once a level fills the chip twice over, 32 below.
 void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s) {
   if (M >= 1024) CAVS_TILE_DISPATCH(fwd, 64, 32, 2);
-  else CAVS_TILE_DISPATCH(fwd, 32, 32, 3);
+  else CAVS_TILE_DISPATCH(fwd, 32, 32, 2);
 }
 
 void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s) {
