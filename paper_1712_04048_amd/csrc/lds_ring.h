@@ -106,16 +106,18 @@ __device__ __forceinline__ void ring_loop(int nch, const RingT& ring, Issue&& is
 
 // The same ring with the MFMA fragments double-buffered in registers: while
 // chunk c is multiplied from one register set, the LDS reads of chunk c+1
-// fill the other, and sched() interleaves those reads with the MFMAs so that
+// fill the other, interleaved with the MFMAs (sched_group_barrier) so that
 // they issue while the matrix core is busy.  One barrier per chunk covers
 // both hazards: after it every wavefront holds chunk c's fragments (so the
 // copies of chunk c+S may overwrite its stage) and chunk c+1 has landed.
 //   issue(stage, c): the IPW copies of chunk c;
-//   read(stage ptr, F&): the LDS reads of one chunk's fragments;
-//   mma(const F&): its MFMAs;  sched(): the interleaving directives.
-template <int S, int IPW, class F, class Issue, class Read, class Mma, class Sched, class RingT>
+//   read0(stage ptr, F&): the LDS reads of chunk 0;
+//   body(stage ptr of chunk c+1, F& cur, F& nxt, c): the LDS reads of chunk
+//     c+1 into nxt and the MFMAs of chunk c from cur (past the last chunk the
+//     reads see a stale stage: in bounds, never used).
+template <int S, int IPW, class F, class Issue, class Read0, class Body, class RingT>
 __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&& issue,
-                                             Read&& read, Mma&& mma, Sched&& sched) {
+                                             Read0&& read0, Body&& body) {
   issue(IC<0>{}, 0);
   if (1 < nch) issue(IC<1>{}, 1);
   if constexpr (S > 2) if (2 < nch) issue(IC<2>{}, 2);
@@ -124,17 +126,14 @@ __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&&
   else wait_vmcnt<0>();
   barrier_nofence();
   F f0, f1;
-  read(ring.at(IC<0>{}), f0);
+  read0(ring.at(IC<0>{}), f0);
   auto step = [&](auto sc, F& cur, F& nxt, int c) {
     constexpr int k = decltype(sc)::value;
     if (c + S - 1 < nch) wait_vmcnt_lgkm0<(S - 2) * IPW>();
     else wait_vmcnt_lgkm0<0>();
     barrier_nofence();
     if (c + S < nch) issue(IC<k>{}, c + S);
-    // past the last chunk this reads a stale stage: in bounds, never used
-    read(ring.at(IC<(k + 1) % S>{}), nxt);
-    mma(cur);
-    sched();
+    body(ring.at(IC<(k + 1) % S>{}), cur, nxt, c);
   };
   for (int c = 0; c < nch; c += 2 * S) {
     step(IC<0>{}, f0, f1, c);
@@ -150,6 +149,19 @@ __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&&
       if (c + 7 < nch) step(IC<7 % S>{}, f1, f0, c + 7);
     }
   }
+}
+
+// sched_group_barrier sequence for one chunk: NR LDS reads spread evenly
+// between NM MFMAs.
+template <int NR, int NM>
+__device__ __forceinline__ void interleave_reads() {
+  constexpr int PER = NM / NR > 0 ? NM / NR : 1;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    __builtin_amdgcn_sched_group_barrier(0x008, PER, 0); // PER MFMAs
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
 }
 
 }  // namespace cavs

@@ -157,18 +157,12 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
       }
     }
   };
-  auto sched = [&]() {
-    // one 16-byte LDS read between every few MFMAs of the current chunk
-    constexpr int NR = 2 * (4 * TU + NCH * TM), NM = TM * TU * NACC * (BF ? 1 : 8);
-    constexpr int PER = NM / NR > 0 ? NM / NR : 1;
-#pragma unroll
-    for (int i = 0; i < NR; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, PER, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+    mma(cur);
+    interleave_reads<2 * (4 * TU + NCH * TM), TM * TU * NACC * (BF ? 1 : 8)>();
   };
-  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, mma, sched);
+  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
@@ -203,6 +197,17 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   int rt, ut;
   xcd_tile(H / BN, rt, ut);
   const int row0 = off + rt * BM, rowend = off + M, n0 = ut * BN;
+
+  // The weight fragment is the MFMA's A operand: in block (tm, tn) lane
+  // (r, gq) holds columns 4gq .. 4gq+3 of one position.  Its children's
+  // positions are fetched before the product.
+  int cpos[TM][NCH];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) cpos[tm][k] = p < rowend ? n.child_pos[(size_t)p * NCH + k] : -1;
+  }
 
   // Phase-1 chunks fill rows [0, BM + BN) with IPW1 copies per wavefront,
   // phase-2 chunks all ROWS with IPW; a phase-1 chunk repeats its first
@@ -252,6 +257,7 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
       for (int t = 0; t < IPW; ++t) copy16_to_lds(src2[t] + k0, base + 1024u * t);
     }
   };
+  // A = weight fragment (columns), B = dA fragment (positions)
   auto compute = [&](const float* Ls, int c) {
     float bfr[TN][8];
 #pragma unroll
@@ -262,7 +268,7 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
         float a[8];
         frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, a);
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) acc[tm][tn][0] = mfma_chunk8<BF>(a, bfr[tn], acc[tm][tn][0]);
+        for (int tn = 0; tn < TN; ++tn) acc[tm][tn][0] = mfma_chunk8<BF>(bfr[tn], a, acc[tm][tn][0]);
       }
     } else if constexpr (NCH == 2) {
 #pragma unroll
@@ -273,8 +279,8 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
         frag_sw(Ls, BM + BN + ra, gq, a1);
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
-          acc[tm][tn][1] = mfma_chunk8<BF>(a0, bfr[tn], acc[tm][tn][1]);
-          acc[tm][tn][NACC - 1] = mfma_chunk8<BF>(a1, bfr[tn], acc[tm][tn][NACC - 1]);
+          acc[tm][tn][1] = mfma_chunk8<BF>(bfr[tn], a0, acc[tm][tn][1]);
+          acc[tm][tn][NACC - 1] = mfma_chunk8<BF>(bfr[tn], a1, acc[tm][tn][NACC - 1]);
         }
       }
     }
@@ -282,17 +288,30 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   ring_loop<S, IPW>(nc1 + nc2, ring, issue, compute);
 
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+    if (p >= rowend) continue;
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col0 = n0 + wn * (BN / 2) + tn * 16 + 4 * gq;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = row0 + wr * (BM / 2) + tm * 16 + 4 * gq + i;
-        const int col = n0 + wn * (BN / 2) + tn * 16 + r;
-        if (p < rowend)
-          lstm_bwd_scatter<NCH>(n, p, col, acc[tm][tn][0][i], NCH == 2 ? acc[tm][tn][1][i] : 0.f,
-                                NCH == 2 ? acc[tm][tn][NACC - 1][i] : 0.f);
+      for (int k = 0; k < NCH; ++k) {
+        const int cp = cpos[tm][k];
+        if (cp < 0) continue;
+        v4f gh = acc[tm][tn][0];
+        if constexpr (NCH == 2) gh += acc[tm][tn][1 + k];
+        if (cp < n.fuse_from) {
+          st4(n.dHp + (size_t)cp * H + col0, make_float4(gh[0], gh[1], gh[2], gh[3]));
+        } else {
+          // a child in the fused top levels (levels there never reach tile
+          // size, so this path only keeps the kernel general)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            lstm_gates_elem<NCH>(n, cp, col0 + e, gh[e], n.dCp[(size_t)cp * H + col0 + e]);
+        }
       }
+    }
+  }
 }
 
 }  // namespace
