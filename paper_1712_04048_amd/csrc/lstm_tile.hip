@@ -176,15 +176,21 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   }
 }
 
+// Backward level product, organised like the forward: per 32-deep chunk of
+// the unit index k, the stage holds the dA rows of the tile's positions for
+// every gate block (i, o, u, f_0[, f_1]) and rows n of U for the tile's
+// columns at each gate block, so one chunk feeds 3 + NCH MFMA blocks per
+// 16 x 16 output block:
+//   dL/dh~ += dA_i U_i^T + dA_o U_o^T + dA_u U_u^T,  dL/dh_k += dA_fk U_f^T
+// (one child: the f block joins the single accumulator).
 template <int NCH, bool BF, int BM, int BN, int S>
 __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TN = BN / 32;
-  constexpr int NA = NCH == 2 ? 2 : 1;         // A operands of phase 2
+  constexpr int NGA = 3 + NCH;                 // dA blocks per chunk
   constexpr int NACC = NCH == 2 ? 3 : 1;
-  // stage rows: [0, BM) A0, [BM, BM + BN) B, [BM + BN, ROWS) A1 (phase 2)
-  constexpr int ROWS = NA * BM + BN;
-  constexpr int IPW1 = (BM + BN) / 32, IPW = ROWS / 32;
-  static_assert(IPW1 * 32 == BM + BN && IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  constexpr int AROWS = NGA * BM, ROWS = AROWS + 4 * BN;
+  constexpr int IPW = ROWS / 32;
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
   __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
   __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
@@ -209,31 +215,26 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
     for (int k = 0; k < NCH; ++k) cpos[tm][k] = p < rowend ? n.child_pos[(size_t)p * NCH + k] : -1;
   }
 
-  // Phase-1 chunks fill rows [0, BM + BN) with IPW1 copies per wavefront,
-  // phase-2 chunks all ROWS with IPW; a phase-1 chunk repeats its first
-  // copies so that every chunk issues IPW (same data to the same place),
-  // which keeps the vmcnt bookkeeping of the ring uniform.  Rows past the
-  // level read its last row (their products are never stored).
-  const float* src1[IPW1];
-  const float* src2[IPW];
-#pragma unroll
-  for (int t = 0; t < IPW1; ++t) {
-    const int row = (w * IPW1 + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
-    const float* ptr;
-    if (row < BM) ptr = n.dA + (size_t)min(row0 + row, rowend - 1) * GW;
-    else ptr = n.U + (size_t)(n0 + row - BM) * H4;
-    src1[t] = ptr + 4 * qg;
-  }
+  // Stage rows: [0, AROWS) dA rows, block a (0..NGA-1) for gate i, o, u,
+  // f_0, f_1 (columns 0, 2H, 3H, H, 4H of the dA row; one child: i, o, u,
+  // f); then 4 blocks of BN rows n of U at gate columns i, o, u, f.  Rows
+  // past the level read its last row (their products are never stored).
+  const float* src[IPW];
 #pragma unroll
   for (int t = 0; t < IPW; ++t) {
     const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
     const float* ptr;
-    if (row < BM) ptr = n.dA + (size_t)min(row0 + row, rowend - 1) * GW;             // f_0 at +H
-    else if (row < BM + BN) ptr = n.U + (size_t)(n0 + row - BM) * H4;               // U_f at +H
-    else ptr = n.dA + (size_t)min(row0 + row - BM - BN, rowend - 1) * GW + 3 * H;   // f_1 at +4H
-    src2[t] = ptr + 4 * qg;
+    if (row < AROWS) {
+      const int a = row / BM, p = min(row0 + row % BM, rowend - 1);
+      const int col = a == 0 ? 0 : a == 1 ? 2 * H : a == 2 ? 3 * H : a == 3 ? H : 4 * H;
+      ptr = n.dA + (size_t)p * GW + col;
+    } else {
+      const int b = row - AROWS, g = b / BN, nn = n0 + b % BN;
+      ptr = n.U + (size_t)nn * H4 + (g == 0 ? G_I : g == 1 ? G_O : g == 2 ? G_U : G_F) * H;
+    }
+    src[t] = ptr + 4 * qg;
   }
-  const int nc1 = (NCH == 2 ? 3 * H : H4) / kBK, nc2 = NCH == 2 ? H / kBK : 0;
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
 
   v4f acc[TM][TN][NACC];
 #pragma unroll
@@ -244,48 +245,49 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
       for (int g = 0; g < NACC; ++g) acc[tm][tn][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](auto sc, int c) {
-    const uint32_t stage = lds_addr_of(ring.at(sc));
-    if (c < nc1) {
-      const uint32_t base = __builtin_amdgcn_readfirstlane(stage + 4u * (w * IPW1 * 256));
-      const int k0 = c * kBK, col = (NCH == 2 && k0 >= H) ? k0 + H : k0;
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
 #pragma unroll
-      for (int t = 0; t < IPW; ++t) copy16_to_lds(src1[t % IPW1] + col, base + 1024u * (t % IPW1));
-    } else {
-      const uint32_t base = __builtin_amdgcn_readfirstlane(stage + 4u * (w * IPW * 256));
-      const int k0 = H + (c - nc1) * kBK;
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+  };
+  struct Frag {
+    float a[NGA][TM][8], b[4][TN][8];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
 #pragma unroll
-      for (int t = 0; t < IPW; ++t) copy16_to_lds(src2[t] + k0, base + 1024u * t);
-    }
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        frag_sw(Ls, AROWS + g * BN + wn * (BN / 2) + tn * 16 + r, gq, f.b[g][tn]);
+#pragma unroll
+    for (int a = 0; a < NGA; ++a)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, a * BM + wr * (BM / 2) + tm * 16 + r, gq, f.a[a][tm]);
   };
   // A = weight fragment (columns), B = dA fragment (positions)
-  auto compute = [&](const float* Ls, int c) {
-    float bfr[TN][8];
+  auto mma = [&](const Frag& f) {
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) frag_sw(Ls, BM + wn * (BN / 2) + tn * 16 + r, gq, bfr[tn]);
-    if (c < nc1) {
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        float a[8];
-        frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, a);
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) acc[tm][tn][0] = mfma_chunk8<BF>(bfr[tn], a, acc[tm][tn][0]);
-      }
-    } else if constexpr (NCH == 2) {
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int ra = wr * (BM / 2) + tm * 16 + r;
-        float a0[8], a1[8];
-        frag_sw(Ls, ra, gq, a0);
-        frag_sw(Ls, BM + BN + ra, gq, a1);
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          acc[tm][tn][1] = mfma_chunk8<BF>(bfr[tn], a0, acc[tm][tn][1]);
-          acc[tm][tn][NACC - 1] = mfma_chunk8<BF>(bfr[tn], a1, acc[tm][tn][NACC - 1]);
+      for (int tn = 0; tn < TN; ++tn) {
+        v4f h = acc[tm][tn][0];
+        h = mfma_chunk8<BF>(f.b[0][tn], f.a[0][tm], h);
+        h = mfma_chunk8<BF>(f.b[1][tn], f.a[1][tm], h);
+        h = mfma_chunk8<BF>(f.b[2][tn], f.a[2][tm], h);
+        if constexpr (NCH == 2) {
+          acc[tm][tn][0] = h;
+          acc[tm][tn][1] = mfma_chunk8<BF>(f.b[3][tn], f.a[3][tm], acc[tm][tn][1]);
+          acc[tm][tn][2] = mfma_chunk8<BF>(f.b[3][tn], f.a[4][tm], acc[tm][tn][2]);
+        } else {
+          acc[tm][tn][0] = mfma_chunk8<BF>(f.b[3][tn], f.a[3][tm], h);
         }
       }
-    }
   };
-  ring_loop<S, IPW>(nc1 + nc2, ring, issue, compute);
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+    mma(cur);
+    interleave_reads<2 * (4 * TN + NGA * TM), TM * TN * (3 + NCH) * (BF ? 1 : 8)>();
+  };
+  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
@@ -349,8 +351,8 @@ void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s) {
 }
 
 void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s) {
-  if (M >= 1024) CAVS_TILE_DISPATCH(bwd, 64, 32, 3);
-  else CAVS_TILE_DISPATCH(bwd, 32, 32, 4);
+  if (M >= 1024) CAVS_TILE_DISPATCH(bwd, 64, 32, 2);
+  else CAVS_TILE_DISPATCH(bwd, 32, 32, 2);
 }
 
 }  // namespace cavs
