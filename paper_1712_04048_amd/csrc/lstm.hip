@@ -575,17 +575,19 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
   const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int u0 = ut * 16;
   if (w < KW) {
-    const float* ap[TR][NCH];               // A rows of this lane: row0 + 16 tr + r
+    // A rows of this lane: the children of position row0 + 16 tr + r.  An
+    // absent child (or a row past the level) reads row 0 with weight 0, so
+    // the loads are unconditional.
+    const float* ap[TR][NCH];
+    float am[TR][NCH];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
       const int pa = row0 + 16 * tr + r;
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        ap[tr][c] = nullptr;
-        if (pa < rowend) {
-          const int cp = n.child_pos[(size_t)pa * NCH + c];
-          if (cp >= 0) ap[tr][c] = n.Hs + (size_t)cp * H;
-        }
+        const int cp = pa < rowend ? n.child_pos[(size_t)pa * NCH + c] : -1;
+        ap[tr][c] = n.Hs + (size_t)(cp >= 0 ? cp : 0) * H;
+        am[tr][c] = cp >= 0 ? 1.f : 0.f;
       }
     }
     const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
@@ -605,13 +607,7 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          if (ap[tr][c]) ld8(ap[tr][c] + kk, f.a[tr][c]);
-          else {
-#pragma unroll
-            for (int s = 0; s < 8; ++s) f.a[tr][c][s] = 0.f;
-          }
-        }
+        for (int c = 0; c < NCH; ++c) ld8(ap[tr][c] + kk, f.a[tr][c]);
 #pragma unroll
       for (int g = 0; g < 4; ++g)
 #pragma unroll
@@ -620,16 +616,18 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
     auto compute = [&](const Frag& f) {
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) {
-        float ah[8];
+        float a0[8], a1[8], ah[8];
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-          ah[s] = NCH == 2 ? f.a[tr][0][s] + f.a[tr][NCH - 1][s] : f.a[tr][0][s];
+        for (int s = 0; s < 8; ++s) {
+          a0[s] = f.a[tr][0][s] * am[tr][0];
+          a1[s] = NCH == 2 ? f.a[tr][NCH - 1][s] * am[tr][NCH - 1] : 0.f;
+          ah[s] = NCH == 2 ? a0[s] + a1[s] : a0[s];
+        }
         acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
         acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
         acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
-        acc[tr][3] = mfma_chunk8<BF>(f.a[tr][0], f.b[G_F], acc[tr][3]);
-        if constexpr (NCH == 2)
-          acc[tr][4] = mfma_chunk8<BF>(f.a[tr][NCH - 1], f.b[G_F], acc[tr][4]);
+        acc[tr][3] = mfma_chunk8<BF>(a0, f.b[G_F], acc[tr][3]);
+        if constexpr (NCH == 2) acc[tr][4] = mfma_chunk8<BF>(a1, f.b[G_F], acc[tr][4]);
       }
     };
     // two register buffers: loads of the next chunk overlap the current MFMAs
@@ -637,6 +635,7 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
     load(kbeg, fa);
     for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
       load(k0 + kBK, fb);
+      __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads go out before these MFMAs
       compute(fa);
       if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
       compute(fb);
@@ -719,22 +718,16 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
   const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int n0 = ut * 16;
   if (w < KW) {
+    // rows past the level read its last row: their sums are never used
     const float* da[TR];
 #pragma unroll
-    for (int tr = 0; tr < TR; ++tr) {
-      const int pa = row0 + 16 * tr + r;
-      da[tr] = pa < rowend ? n.dA + (size_t)pa * GW : nullptr;
-    }
+    for (int tr = 0; tr < TR; ++tr) da[tr] = n.dA + (size_t)min(row0 + 16 * tr + r, rowend - 1) * GW;
     const float* ub = n.U + (size_t)(n0 + r) * H4;   // row n0 + r of U: B^T[n][k]
     v4f acc[TR][NACC];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
-    auto zero8 = [](float (&v)[8]) {
-#pragma unroll
-      for (int s = 0; s < 8; ++s) v[s] = 0.f;
-    };
     // phase 1: i|o|u columns (all four blocks with one child slot)
     struct F1 {
       float a[TR][8], b[8];
@@ -743,10 +736,7 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     auto load1 = [&](int c0, F1& f) {
       const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
-      for (int tr = 0; tr < TR; ++tr) {
-        if (da[tr]) ld8(da[tr] + col, f.a[tr]);
-        else zero8(f.a[tr]);
-      }
+      for (int tr = 0; tr < TR; ++tr) ld8(da[tr] + col, f.a[tr]);
       ld8(ub + col, f.b);
     };
     auto comp1 = [&](const F1& f) {
@@ -754,17 +744,20 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
       for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
     };
     // groups of G chunks: all loads of a group are in flight together, so a
-    // small level pays about one memory latency per group, not per chunk
-    constexpr int G1 = 6;
+    // small level pays about one memory latency per group, not per chunk.
+    // A wavefront's share is a whole number of groups (K1 / (32 KW) is a
+    // multiple of 6 with two children and of 8 with one, for the H this
+    // kernel is launched with: H % 512 == 0 at KW = 8, H % 256 == 0 at
+    // KW = 4), so the loads are unconditional.
+    constexpr int G1 = NCH == 2 ? 6 : 8;
     const int end1 = (w + 1) * q1;
     for (int c0 = w * q1; c0 < end1; c0 += G1 * kBK) {
       F1 f[G1];
 #pragma unroll
-      for (int g = 0; g < G1; ++g)
-        if (c0 + g * kBK < end1) load1(c0 + g * kBK, f[g]);
+      for (int g = 0; g < G1; ++g) load1(c0 + g * kBK, f[g]);
+      __builtin_amdgcn_sched_barrier(0);   // keep every load of the group ahead of the MFMAs
 #pragma unroll
-      for (int g = 0; g < G1; ++g)
-        if (c0 + g * kBK < end1) comp1(f[g]);
+      for (int g = 0; g < G1; ++g) comp1(f[g]);
     }
     if constexpr (NCH == 2) {
       struct F2 {
@@ -775,13 +768,8 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
         const int col = c0 + 8 * gq;
 #pragma unroll
         for (int tr = 0; tr < TR; ++tr) {
-          if (da[tr]) {
-            ld8(da[tr] + H + col, f.a0[tr]);
-            ld8(da[tr] + 4 * H + col, f.a1[tr]);
-          } else {
-            zero8(f.a0[tr]);
-            zero8(f.a1[tr]);
-          }
+          ld8(da[tr] + H + col, f.a0[tr]);
+          ld8(da[tr] + 4 * H + col, f.a1[tr]);
         }
         ld8(ub + H + col, f.b);
       };
@@ -792,16 +780,15 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
           acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
         }
       };
-      constexpr int G2 = 4;
+      constexpr int G2 = 2;   // H / (32 KW) is even
       const int end2 = (w + 1) * q2;
       for (int c0 = w * q2; c0 < end2; c0 += G2 * kBK) {
         F2 f[G2];
 #pragma unroll
-        for (int g = 0; g < G2; ++g)
-          if (c0 + g * kBK < end2) load2(c0 + g * kBK, f[g]);
+        for (int g = 0; g < G2; ++g) load2(c0 + g * kBK, f[g]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int g = 0; g < G2; ++g)
-          if (c0 + g * kBK < end2) comp2(f[g]);
+        for (int g = 0; g < G2; ++g) comp2(f[g]);
       }
     }
 #pragma unroll

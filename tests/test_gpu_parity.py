@@ -161,6 +161,21 @@ def test_parity_varlstm_reduced(ctx, seed):
     _parity(ctx, W.config_varlstm(seed, K=6))
 
 
+@pytest.mark.parametrize("H,N", [(256, 2), (256, 1), (768, 2)])
+def test_parity_hidden_widths(ctx, H, N):
+    """Widths that are not multiples of 512 split the small-level products
+    over four wavefronts instead of eight; the forests have levels on both
+    sides of the tile threshold and every vertex labelled."""
+    rng = np.random.default_rng(7 * H + N)
+    if N == 2:
+        trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 40, size=40 if H < 768 else 24)]
+    else:
+        trees = [W.chain(int(L)) for L in rng.integers(5, 60, size=24)]
+    wl = W.make_workload("widths_h%d_n%d" % (H, N), trees, N=N, D=32, H=H, C=5, rng=rng,
+                         labels="all")
+    _parity(ctx, wl)
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_parity_treefc_reduced(ctx, seed):
     _parity(ctx, W.config_treefc(seed, K=2, leaves=64))
