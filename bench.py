@@ -71,6 +71,7 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()),
     }
     base = re.sub(r", (64|128)(, [48])?>", ">", name.replace("_bf", ""))
+    base = re.sub(r"^k_tn_dl<(\w+), .*>$", r"k_tn_gemm<\1>", base)
     return lazy.get(base, 0.0), 0.0
 
 

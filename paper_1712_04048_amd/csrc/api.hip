@@ -57,7 +57,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   };
   L.P = take(lstm ? V * 4 * H : 0);
   L.UT = take(lstm ? 4 * H * H : 0);
-  L.zrow = take(lstm ? H : 0);
+  L.zrow = take(H);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
   L.Gs = take(lstm ? V * GW : 0);

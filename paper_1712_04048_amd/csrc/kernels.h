@@ -28,7 +28,8 @@ struct Net {
   const float* Wx;              // [D, 4H]
   const float* U;               // LSTM [H, 4H]; FC [N*H, H]
   float* UT;                    // LSTM: U transposed, [4H, H] (workspace)
-  float* zrow;                  // LSTM: H zeros (workspace), read for absent children
+  float* zrow;                  // H zeros (workspace): the row an absent operand row reads;
+                                // cleared by the transpose kernel and by the loss kernel
   const float* b;
   const float* Ws;              // [H, C]
   const float* bs;              // [C]

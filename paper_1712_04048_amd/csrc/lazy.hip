@@ -209,6 +209,8 @@ struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = 
   static constexpr const char* kName = "k_tn_gemm<LdDUiou, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDUiou, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";
+  static constexpr const char* kNameDl128 = "k_tn_dl<LdDUiou, 128, 256, 2>";
+  static constexpr const char* kNameDl64 = "k_tn_dl<LdDUiou, 64, 256, 3>";
   struct Idx {
     int c0, c1;
   };
@@ -228,12 +230,28 @@ struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = 
     const int col = (n.N == 2 && c >= n.H) ? c + n.H : c;
     return ldg4(n.dA + (size_t)p * n.GW + col);
   }
+  // row offsets for the direct-to-LDS product: A = h_0 + h_1 (two rows),
+  // B = the dA row; B column n0 of the product is dA column bcol(n0)
+  static constexpr int NA = 2;
+  bool direct() const { return true; }
+  __device__ void offs(int q, int& a0, int& a1, int& b) const {
+    const int p = off1 + q;
+    const int c0 = n.child_pos[(size_t)p * n.N], c1 = n.child_pos[(size_t)p * n.N + n.N - 1];
+    a0 = c0 >= 0 ? c0 * n.H : -1;
+    a1 = (n.N == 2 && c1 >= 0) ? c1 * n.H : -1;
+    b = p * n.GW;
+  }
+  __device__ int bcol(int n0) const { return (n.N == 2 && n0 >= n.H) ? n0 + n.H : n0; }
+  __device__ const float* abase() const { return n.Hs; }
+  __device__ const float* bbase() const { return n.dA; }
 };
 
 struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_fk
   static constexpr const char* kName = "k_tn_gemm<LdDUf, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDUf, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";
+  static constexpr const char* kNameDl128 = "k_tn_dl<LdDUf, 128, 256, 3>";
+  static constexpr const char* kNameDl64 = "k_tn_dl<LdDUf, 64, 256, 3>";
   struct Idx {
     int cp;
   };
@@ -250,12 +268,26 @@ struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_f
     const int k = q >= MI, p = off1 + q - k * MI;
     return ldg4(n.dA + (size_t)p * n.GW + (k ? 4 * n.H : n.H) + c);
   }
+  static constexpr int NA = 1;
+  bool direct() const { return true; }
+  __device__ void offs(int q, int& a0, int& a1, int& b) const {
+    const int k = q >= MI, p = off1 + q - k * MI;
+    const int cp = n.child_pos[(size_t)p * 2 + k];
+    a0 = cp >= 0 ? cp * n.H : -1;
+    a1 = -1;
+    b = p * n.GW + (k ? 4 * n.H : n.H);
+  }
+  __device__ int bcol(int n0) const { return n0; }
+  __device__ const float* abase() const { return n.Hs; }
+  __device__ const float* bbase() const { return n.dA; }
 };
 
 struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1)
   static constexpr const char* kName = "k_tn_gemm<LdDWx, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDWx, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";
+  static constexpr const char* kNameDl128 = "k_tn_dl<LdDWx, 128, 256, 3>";
+  static constexpr const char* kNameDl64 = "k_tn_dl<LdDWx, 64, 256, 3>";
   struct Idx {
     int p, row;
   };
@@ -276,12 +308,27 @@ struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1
     if (n.N == 2 && col >= H && col < 2 * H) v = add4(v, ldg4(row + 3 * H + col));
     return v;
   }
+  // direct-to-LDS only when every B column is a single dA column (the f
+  // block with two children sums f_0 and f_1)
+  static constexpr int NA = 1;
+  bool direct() const { return !(with_f && n.N == 2); }
+  __device__ void offs(int q, int& a0, int& a1, int& b) const {
+    const int p = n.pull_list[q];
+    a0 = n.pull_pos[p] * n.D;
+    a1 = -1;
+    b = p * n.GW;
+  }
+  __device__ int bcol(int n0) const { return (with_f || n0 < n.H) ? n0 : n0 + n.H; }
+  __device__ const float* abase() const { return n.X; }
+  __device__ const float* bbase() const { return n.dA; }
 };
 
 struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   static constexpr const char* kName = "k_tn_gemm<LdFCdW, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdFCdW, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";
+  static constexpr const char* kNameDl128 = "k_tn_dl<LdFCdW, 128, 256, 3>";
+  static constexpr const char* kNameDl64 = "k_tn_dl<LdFCdW, 64, 256, 3>";
   struct Idx {
     int cp;
   };
@@ -296,6 +343,17 @@ struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   __device__ float4 b4(const Idx&, int q, int c) const {
     return ldg4(n.dA + (size_t)(off1 + q) * n.H + c);
   }
+  static constexpr int NA = 1;
+  bool direct() const { return true; }
+  __device__ void offs(int q, int& a0, int& a1, int& b) const {
+    const int cp = n.child_pos[(size_t)(off1 + q) * n.N + slot];
+    a0 = cp >= 0 ? cp * n.H : -1;
+    a1 = -1;
+    b = (off1 + q) * n.H;
+  }
+  __device__ int bcol(int n0) const { return n0; }
+  __device__ const float* abase() const { return n.Hs; }
+  __device__ const float* bbase() const { return n.dA; }
 };
 
 template <class L, int BT, int NW>
@@ -685,6 +743,137 @@ __global__ void k_reduce_splits(const float* __restrict__ part, int S, int Mo, i
   dst[(size_t)m * ldd + col_off + nn + (nn >= gap_start ? gap : 0)] = s;
 }
 
+// Lazy products through direct-to-LDS copies: out[m][n] = sum over q of
+// A[q][m] B[q][n] for q in one split [q_lo, q_hi), with A row q = the sum of
+// the loader's NA source rows (or zero where a row is absent) and B row q a
+// source row starting at the loader's offset plus bcol(n0).  Eight
+// wavefronts own a BM x BN output tile (BM = 128: 2 x 4 wavefronts of
+// 64 x BN/4; BM = 64: 1 x 8 of 64 x BN/8) as 4 x TN MFMA blocks whose rows
+// and columns are interleaved (block b row i is tile row 4i + b, block c
+// column j is column TN j + c), so one 16-byte LDS read gives a lane its A
+// values of all four row blocks.  Stage rows are k (one vertex each) with
+// the tile's columns contiguous, filled by global_load_lds_dwordx4 through
+// an S-stage ring; the source offsets of a segment of rows are computed
+// into LDS first, so issuing a chunk's copies waits on nothing but LDS.
+constexpr int kTnSeg = 1024;
+
+template <class L, int BM, int BN, int S>
+__global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, int No,
+                                               float* out) {
+  constexpr int NA = L::NA, WM = BM / 64, WN = 8 / WM, WTN = BN / WN, TN = WTN / 16;
+  constexpr int ROWS = NA * BM + BN;                 // a stage is 32 k x ROWS floats
+  constexpr int IA = BM * 32 / 256 / 8, IB = BN * 32 / 256 / 8;
+  constexpr int IPW = NA * IA + IB;                  // copies per wavefront per chunk
+  constexpr int APC = 256 / BM, BPC = 256 / BN;      // operand rows per copy
+  static_assert((TN == 2 || TN == 4) && IA >= 1 && IB >= 1 && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  __shared__ int oa0[kTnSeg], oa1[NA == 2 ? kTnSeg : 1], ob[kTnSeg];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, r = lane & 15;
+  const int wr = w / WN, wc = w % WN, ws = __builtin_amdgcn_readfirstlane(w);
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
+  const float* A = ld.abase();
+  const float* B = ld.bbase() + ld.bcol(n0);
+  const float* zero = ld.n.zrow;
+  const int arow = lane / (BM / 4), acol = 4 * (lane % (BM / 4));
+  const int brow = lane / (BN / 4), bcolw = 4 * (lane % (BN / 4));
+  const bool acol_ok = m0 + acol < Mo;
+
+  v4f acc[4][TN];
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int c = 0; c < TN; ++c) acc[b][c] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  for (int seg = q_lo; seg < q_hi; seg += kTnSeg) {
+    const int nq = min(kTnSeg, q_hi - seg);
+    __syncthreads();   // the previous segment's stages and offsets are consumed
+    for (int i = tid; i < nq; i += 512) {
+      int a0, a1, b;
+      ld.offs(seg + i, a0, a1, b);
+      oa0[i] = a0;
+      if constexpr (NA == 2) oa1[i] = a1;
+      ob[i] = b;
+    }
+    __syncthreads();
+    auto issue = [&](auto sc, int c) {
+      const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)));
+      const int q0 = 32 * c;
+      // every offset first, then the copies (a copy's asm statement orders
+      // memory, so interleaving would wait on each LDS read); rows past the
+      // segment read the zero row (A) or the segment's last row (B)
+      int o0[IA], o1[IA], ov[IB];
+#pragma unroll
+      for (int t = 0; t < IA; ++t) {
+        const int qi = q0 + APC * (ws * IA + t) + arow;
+        const bool ok = qi < nq && acol_ok;
+        const int qc = min(qi, nq - 1);
+        o0[t] = ok ? oa0[qc] : -1;
+        if constexpr (NA == 2) o1[t] = ok ? oa1[qc] : -1;
+      }
+#pragma unroll
+      for (int t = 0; t < IB; ++t) ov[t] = ob[min(q0 + BPC * (ws * IB + t) + brow, nq - 1)];
+#pragma unroll
+      for (int t = 0; t < IA; ++t) {
+        const uint32_t j = ws * IA + t;
+        copy16_to_lds(o0[t] >= 0 ? A + o0[t] + m0 + acol : zero, base + 1024u * j);
+        if constexpr (NA == 2)
+          copy16_to_lds(o1[t] >= 0 ? A + o1[t] + m0 + acol : zero, base + 128u * BM + 1024u * j);
+      }
+#pragma unroll
+      for (int t = 0; t < IB; ++t)
+        copy16_to_lds(B + ov[t] + bcolw, base + 128u * NA * BM + 1024u * (ws * IB + t));
+    };
+    auto compute = [&](const float* Ls, int) {
+      const float* A0 = Ls + wr * 64 + 4 * r;
+      const float* A1 = A0 + 32 * BM;
+      const float* Bp = Ls + NA * 32 * BM + wc * WTN + TN * r;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int k = 4 * t + g;
+        float4 a = *reinterpret_cast<const float4*>(A0 + k * BM);
+        if constexpr (NA == 2) {
+          const float4 a1 = *reinterpret_cast<const float4*>(A1 + k * BM);
+          a.x += a1.x; a.y += a1.y; a.z += a1.z; a.w += a1.w;
+        }
+        float bv[TN];
+        if constexpr (TN == 4) {
+          const float4 b4 = *reinterpret_cast<const float4*>(Bp + k * BN);
+          bv[0] = b4.x; bv[1] = b4.y; bv[2] = b4.z; bv[3] = b4.w;
+        } else {
+          const float2 b2 = *reinterpret_cast<const float2*>(Bp + k * BN);
+          bv[0] = b2.x; bv[TN - 1] = b2.y;
+        }
+        const float av[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int c = 0; c < TN; ++c) acc[b][c] = mfma_f32_16x16x4(av[b], bv[c], acc[b][c]);
+      }
+    };
+    ring_loop<S, IPW>((nq + 31) / 32, ring, issue, compute);
+  }
+
+  float* o = out + (size_t)s * Mo * No;
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = m0 + wr * 64 + 16 * g + 4 * e + b;
+      if (m >= Mo) continue;
+      float* dst = o + (size_t)m * No + n0 + wc * WTN + TN * r;
+      if constexpr (TN == 4)
+        st4(dst, make_float4(acc[b][0][e], acc[b][1][e], acc[b][2][e], acc[b][3][e]));
+      else
+        *reinterpret_cast<float2*>(dst) = make_float2(acc[b][0][e], acc[b][TN - 1][e]);
+    }
+}
+
 template <class L>
 void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col_off,
                 int gap_start, int gap, float* part, size_t part_floats, hipStream_t st) {
@@ -692,6 +881,33 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
     // empty contraction: zero output columns
     CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
                        (const float*)part, 0, Mo, No, dst, ldd, col_off, gap_start, gap);
+    return;
+  }
+  // the direct-to-LDS kernel: fp32, 256-column tiles that stay inside one
+  // gate block, row offsets that fit an int, one workgroup per CU
+  const Net& n = ld.n;
+  const long big = (long)n.V * (n.GW > n.H ? n.GW : n.H) + (long)n.V * n.D;
+  if (!n.bf && ld.direct() && n.H % 256 == 0 && No % 256 == 0 && Mo % 4 == 0 && big < (1L << 31)) {
+    const int pad128 = cdiv(Mo, 128) * 128 - Mo, pad64 = cdiv(Mo, 64) * 64 - Mo;
+    const int BM = pad64 < pad128 ? 64 : 128;
+    const int tiles = (No / 256) * cdiv(Mo, BM);
+    int S = 256 / tiles;
+    S = S < 1 ? 1 : S;
+    if (S > cdiv(Q, kBK)) S = cdiv(Q, kBK);
+    while (S > 1 && (size_t)S * Mo * No > part_floats) --S;
+    const int qchunk = cdiv(cdiv(Q, S), kBK) * kBK;
+    S = cdiv(Q, qchunk);
+    const dim3 grid(No / 256, cdiv(Mo, BM), S);
+    // ring depth: the deepest ring whose stages fit in 160 KB of LDS
+    constexpr int S128 = L::NA == 2 ? 2 : 3;
+    if (BM == 64)
+      CAVS_LAUNCH(L::kNameDl64, (k_tn_dl<L, 64, 256, 3>), grid, dim3(512), 0, st, ld, Q, qchunk,
+                  Mo, No, part);
+    else
+      CAVS_LAUNCH(L::kNameDl128, (k_tn_dl<L, 128, 256, S128>), grid, dim3(512), 0, st, ld, Q,
+                  qchunk, Mo, No, part);
+    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0,
+                st, (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
     return;
   }
   const int BT = (!ld.n.bf && No % 128 == 0) ? 128 : 64;
@@ -856,6 +1072,8 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
   const int p0 = blockIdx.x * 16;
   const int H = n.H, C = n.C, CP = n.CP, V = n.V;
+  if (blockIdx.x == 0)   // the zero row the lazy products read for absent rows
+    for (int j = threadIdx.x; j < H; j += 64 * kLossWaves) n.zrow[j] = 0.f;
   const int cm = min(r, C - 1);
   const bool cval = r < C;
   int q[4];
@@ -946,6 +1164,8 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
 __global__ void __launch_bounds__(256) k_loss_l2(Net n) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + w;
+  if (blockIdx.x == 0)   // the zero row the lazy products read for absent rows
+    for (int j = threadIdx.x; j < n.H; j += 256) n.zrow[j] = 0.f;
   if (p >= n.V) return;
   const int q = n.push_pos[p], H = n.H;
   const float* h = n.Hs + (size_t)p * H;
