@@ -39,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, UT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bar, total;
+  size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bar, total;
   size_t part_floats;
 };
 
@@ -57,6 +57,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   };
   L.P = take(lstm ? V * 4 * H : 0);
   L.UT = take(lstm ? 4 * H * H : 0);
+  L.WxT = take(lstm ? 4 * H * (size_t)p->D : 0);
   L.zrow = take(H);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
@@ -146,6 +147,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.P = (float*)(base + L.P);
   n.UT = (float*)(base + L.UT);
   n.zrow = (float*)(base + L.zrow);
+  n.WxT = (float*)(base + L.WxT);
   n.fuse_from = s->V;
   n.f_unread_below = 0;
   n.Hs = (float*)(base + L.Hs);
@@ -293,8 +295,9 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
   if (p->cell == CAVS_TREE_LSTM) {
+    if ((s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) || pull_tile_applies(n, s->n_pull))
+      lstm_transpose_u(n, str);
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, lo[1], str);
-    if (s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) lstm_transpose_u(n, str);
     // fp32: pulled leaves were finished by the pull product
     if (n.bf || s->n_leaf_noinput > 0) lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], !n.bf, str);
     const int ts = persist_first_level(n, lo, s->T);
@@ -371,7 +374,8 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       if (t >= 1) lstm_bwd_level(n, lo[t], M, str);
     }
     const bool with_f = s->n_inner_input > 0;
-    lstm_dU(n, off1, g->dU, part, L.part_floats, str);
+    lstm_dU_iou(n, off1, g->dU, part, L.part_floats, str);
+    lstm_dU_f(n, off1, g->dU, part, L.part_floats, str);
     if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part, L.part_floats, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);

@@ -28,6 +28,7 @@ struct Net {
   const float* Wx;              // [D, 4H]
   const float* U;               // LSTM [H, 4H]; FC [N*H, H]
   float* UT;                    // LSTM: U transposed, [4H, H] (workspace)
+  float* WxT;                   // LSTM: W_x transposed, [4H, D] (workspace)
   float* zrow;                  // H zeros (workspace): the row an absent operand row reads;
                                 // cleared by the transpose kernel and by the loss kernel
   const float* b;
@@ -98,10 +99,18 @@ void fc_bwd_level(const Net& n, int off, int M, hipStream_t s);
 // finished in the same kernel, so lstm_fwd_leaf only handles leaves without
 // input (skip_pulled); in bf16 it writes P for all pulled rows.
 void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s);
+// The pull product runs on the LDS ring (reading n.WxT, written by
+// lstm_transpose_u earlier in the same pass).
+bool pull_tile_applies(const Net& n, int n_pull);
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s);
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s);
 // Lazy weight-gradient products; `part` is split-K scratch of part_floats floats.
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
+// the two halves of lstm_dU: dU_iou (all four blocks with one child) and,
+// with two children, dU_f (a no-op with one child)
+void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
+                 hipStream_t s);
+void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
               size_t part_floats, hipStream_t s);
 void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);

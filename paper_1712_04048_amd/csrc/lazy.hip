@@ -123,6 +123,126 @@ __global__ void __launch_bounds__(256) k_pull_leaf(Net n, int n_pull, int lo1) {
   }
 }
 
+// The same product on the direct-to-LDS ring of the level tiles: a
+// workgroup owns 64 pulled rows x 32 units x NG gate blocks.  Stage rows:
+// the 64 x rows (gathered through pull_list and pull_pos), then the rows of
+// W_x^T for each gate block's 32 units; chunks past D read the zero row.
+// Four wavefronts as 2 x 2 (32 rows x 16 units each); the weight fragment
+// is the MFMA's A operand, so a lane holds four consecutive units of one
+// row (float4 epilogue).  Fragments are double-buffered in registers.
+template <int NG, int S>
+__global__ void __launch_bounds__(256) k_pull_tile(Net n, int n_pull, int lo1) {
+  constexpr int BM = 64, BU = 32, TM = 2;
+  constexpr int ROWS = BM + NG * BU, IPW = ROWS / 32;
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+  const int H = n.H, H4 = 4 * H, D = n.D;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wr = w & 1, wu = w >> 1;
+  int rt, ut;
+  xcd_tile(H / BU, rt, ut);
+  const int m0 = rt * BM, u0 = ut * BU;
+  auto gcol = [](int g) { return NG == 4 ? g : (g == 0 ? G_I : g + 1); };
+
+  // epilogue operands first: the position and vertex of each row, the bias
+  const int j0 = u0 + wu * 16 + 4 * gq;
+  int pos[TM], vid[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int m = m0 + wr * 32 + tm * 16 + r;
+    pos[tm] = m < n_pull ? n.pull_list[m] : -1;
+    vid[tm] = pos[tm] >= 0 && pos[tm] < lo1 ? n.order[pos[tm]] : 0;
+  }
+  Bias4 bias;
+  lstm_bias4(n, j0, bias);
+
+  const float* src[IPW];
+  int kq[IPW];
+#pragma unroll
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    kq[t] = 4 * qg;
+    if (row < BM) {
+      const int p = n.pull_list[min(m0 + row, n_pull - 1)];
+      src[t] = n.X + (size_t)n.pull_pos[p] * D + 4 * qg;
+    } else {
+      const int b = row - BM, g = b / BU, u = b % BU;
+      src[t] = n.WxT + (size_t)(gcol(g) * H + u0 + u) * D + 4 * qg;
+    }
+  }
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
+  v4f acc[TM][NG];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int g = 0; g < NG; ++g) acc[tm][g] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
+    const int k0 = c * kBK;
+#pragma unroll
+    for (int t = 0; t < IPW; ++t)
+      copy16_to_lds(k0 + kq[t] < D ? src[t] + k0 : n.zrow, base + 1024u * t);
+  };
+  struct Frag {
+    float a[TM][8], b[NG][8];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) frag_sw(Ls, BM + g * BU + wu * 16 + r, gq, f.b[g]);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, wr * 32 + tm * 16 + r, gq, f.a[tm]);
+  };
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int g = 0; g < NG; ++g) acc[tm][g] = mfma_chunk8<false>(cur.b[g], cur.a[tm], acc[tm][g]);
+    interleave_reads<2 * (NG + TM), TM * NG * 8>();
+  };
+  ring_loop_db<S, IPW, Frag>((D + kBK - 1) / kBK, ring, issue, read, body);
+
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = pos[tm];
+    if (p < 0) continue;
+    if (p < lo1) {
+      const v4f zi = acc[tm][0], zo = acc[tm][NG == 4 ? 2 : 1], zu = acc[tm][NG == 4 ? 3 : 2];
+      const float bi[4] = {bias.i.x, bias.i.y, bias.i.z, bias.i.w};
+      const float bo[4] = {bias.o.x, bias.o.y, bias.o.z, bias.o.w};
+      const float bu[4] = {bias.u.x, bias.u.y, bias.u.z, bias.u.w};
+      float ig[4], og[4], ug[4], c[4], h[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ig[e] = sigmoidf_(zi[e] + bi[e]);
+        og[e] = sigmoidf_(zo[e] + bo[e]);
+        ug[e] = tanh_(zu[e] + bu[e]);
+        c[e] = ig[e] * ug[e];
+        h[e] = og[e] * tanh_(c[e]);
+      }
+      auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
+      st4(n.Hs + (size_t)p * H + j0, f4(h));
+      st4(n.Cs + (size_t)p * H + j0, f4(c));
+      float* gs = n.Gs + (size_t)p * n.GW + j0;   // a leaf's forget gates are never read
+      st4(gs, f4(ig));
+      st4(gs + 2 * H, f4(og));
+      st4(gs + 3 * H, f4(ug));
+      st4(n.h_out + (size_t)vid[tm] * H + j0, f4(h));
+      if (n.c_out) st4(n.c_out + (size_t)vid[tm] * H + j0, f4(c));
+    } else {
+#pragma unroll
+      for (int g = 0; g < NG; ++g)
+        st4(n.P + (size_t)p * H4 + gcol(g) * H + j0,
+            make_float4(acc[tm][g][0], acc[tm][g][1], acc[tm][g][2], acc[tm][g][3]));
+    }
+  }
+}
+
 // --------------------------------------------------------------- dX GEMM
 // dX[pull_pos[p], d] = sum_k dA_x[p, k] W_x[d, k], k over the gate columns
 // (i,f,o,u or i,o,u); the f column of dA_x is delta_f0 + delta_f1.
@@ -1219,11 +1339,23 @@ void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s) {
     CAVS_LAUNCH("k_pull_gemm_bf", k_pull_gemm_bf, grid, dim3(256), 0, s, n, n_pull, (int)with_f);
     return;
   }
+  if (pull_tile_applies(n, n_pull)) {
+    const dim3 grid(cdiv(n_pull, 64) * (n.H / 32));
+    if (with_f)
+      CAVS_LAUNCH("k_pull_tile<4, 2>", (k_pull_tile<4, 2>), grid, dim3(256), 0, s, n, n_pull, lo1);
+    else
+      CAVS_LAUNCH("k_pull_tile<3, 2>", (k_pull_tile<3, 2>), grid, dim3(256), 0, s, n, n_pull, lo1);
+    return;
+  }
   dim3 grid(cdiv(n_pull, 64), n.H / 32);
   if (with_f)
     CAVS_LAUNCH("k_pull_leaf<4>", k_pull_leaf<4>, grid, dim3(256), 0, s, n, n_pull, lo1);
   else
     CAVS_LAUNCH("k_pull_leaf<3>", k_pull_leaf<3>, grid, dim3(256), 0, s, n, n_pull, lo1);
+}
+
+bool pull_tile_applies(const Net& n, int n_pull) {
+  return !n.bf && n_pull > 0 && n.H % 256 == 0 && n.D > 0 && n.D % 4 == 0;
 }
 
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
@@ -1252,6 +1384,21 @@ void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
   }
   CAVS_LAUNCH("k_loss_sum", k_loss_sum, dim3(1), dim3(1024), 0, s, (const float*)n.lossv, n.V,
                      n.inv_denom, loss_out);
+}
+
+void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
+                 hipStream_t s) {
+  const int H = n.H, MI = n.V - off1;
+  LdDUiou ld{n, off1};
+  if (n.N == 1) tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
+  else tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s);
+}
+
+void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
+  if (n.N != 2) return;
+  const int H = n.H, MI = n.V - off1;
+  LdDUf lf{n, off1, MI};
+  tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s);
 }
 
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {

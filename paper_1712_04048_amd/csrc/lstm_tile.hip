@@ -33,20 +33,29 @@
 namespace cavs {
 namespace {
 
-// UT[c][k] = U[k][c] for the [H, 4H] recurrent weight; block (0, 0) also
-// clears the zero row read for absent children.
+// UT[c][k] = U[k][c] for the [H, 4H] recurrent weight (block rows y < H/32)
+// and WxT[c][k] = W_x[k][c] for the [D, 4H] input weight (the rows above);
+// block (0, 0) also clears the zero row read for absent operand rows.
 __global__ void __launch_bounds__(256) k_transpose_u(const float* __restrict__ U,
                                                      float* __restrict__ UT,
-                                                     float* __restrict__ zrow, int H) {
+                                                     const float* __restrict__ Wx,
+                                                     float* __restrict__ WxT,
+                                                     float* __restrict__ zrow, int H, int D) {
   __shared__ float t[32][33];
-  const int H4 = 4 * H;
-  const int c0 = blockIdx.x * 32, k0 = blockIdx.y * 32;
+  const int H4 = 4 * H, yu = H / 32;
+  const bool wx = (int)blockIdx.y >= yu;
+  const float* src = wx ? Wx : U;
+  float* dst = wx ? WxT : UT;
+  const int K = wx ? D : H;
+  const int c0 = blockIdx.x * 32, k0 = (wx ? blockIdx.y - yu : blockIdx.y) * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   if (blockIdx.x == 0 && blockIdx.y == 0)
     for (int j = threadIdx.x; j < H; j += 256) zrow[j] = 0.f;
-  for (int y = ty; y < 32; y += 8) t[y][tx] = U[(size_t)(k0 + y) * H4 + c0 + tx];
+  for (int y = ty; y < 32; y += 8)
+    if (k0 + y < K) t[y][tx] = src[(size_t)(k0 + y) * H4 + c0 + tx];
   __syncthreads();
-  for (int y = ty; y < 32; y += 8) UT[(size_t)(c0 + y) * H + k0 + tx] = t[tx][y];
+  if (k0 + tx < K)
+    for (int y = ty; y < 32; y += 8) dst[(size_t)(c0 + y) * K + k0 + tx] = t[tx][y];
 }
 
 template <int NCH, bool BF, int BM, int BU, int S>
@@ -319,8 +328,9 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
 }  // namespace
 
 void lstm_transpose_u(const Net& n, hipStream_t s) {
-  CAVS_LAUNCH("k_transpose_u", k_transpose_u, dim3(4 * n.H / 32, n.H / 32), dim3(256), 0, s, n.U,
-              n.UT, n.zrow, n.H);
+  const int yw = n.Wx && n.D > 0 ? cdiv(n.D, 32) : 0;
+  CAVS_LAUNCH("k_transpose_u", k_transpose_u, dim3(4 * n.H / 32, n.H / 32 + yw), dim3(256), 0, s,
+              n.U, n.UT, n.Wx, n.WxT, n.zrow, n.H, n.D);
 }
 
 #define CAVS_TILE_LAUNCH(KIND, NCH, BF, BM, BU, S)                                             \
