@@ -70,6 +70,8 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         "k_tn_gemm<LdDUf>": 2.0 * H * H * float(nc.sum()),
         "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()),
     }
+    if name.startswith(("k_dx_tile", "k_pull_tile")):
+        return 2.0 * n_pull * D * gates_x * H, 0.0
     base = re.sub(r", (64|128)(, [48])?>", ">", name.replace("_bf", ""))
     base = re.sub(r"^k_tn_dl<(\w+), .*>$", r"k_tn_gemm<\1>", base)
     return lazy.get(base, 0.0), 0.0

@@ -602,6 +602,13 @@ __global__ void __launch_bounds__(256) k_dx_tile(Net n, int n_pull, int four, fl
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int wr = w & 1, wn = w >> 1;
   const int m0 = blockIdx.x * BM, d0 = blockIdx.y * BN;
+  // output rows of this lane (one per row block), fetched before the product
+  int orow[TM];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int m = m0 + wr * (BM / 2) + tm * 16 + r;
+    orow[tm] = m < n_pull ? n.pull_pos[n.pull_list[m]] : -1;
+  }
   const float* src[IPW];
 #pragma unroll
   for (int t = 0; t < IPW; ++t) {
@@ -620,32 +627,37 @@ __global__ void __launch_bounds__(256) k_dx_tile(Net n, int n_pull, int four, fl
 #pragma unroll
     for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + col, base + 1024u * t);
   };
-  auto compute = [&](const float* Ls, int) {
-    float b[TN][8];
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) frag_sw(Ls, BM + wn * (BN / 2) + tn * 16 + r, gq, b[tn]);
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      float a[8];
-      frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, a);
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma_chunk8<false>(a, b[tn], acc[tm][tn]);
-    }
+  struct Frag {
+    float a[TM][8], b[TN][8];
   };
-  ring_loop<S, IPW>((four ? H4 : 3 * H) / kBK, ring, issue, compute);
+  auto read = [&](const float* Ls, Frag& f) {
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+    for (int tn = 0; tn < TN; ++tn) frag_sw(Ls, BM + wn * (BN / 2) + tn * 16 + r, gq, f.b[tn]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + wr * (BM / 2) + tm * 16 + 4 * gq + i;
-      if (m >= n_pull) continue;
-      const int row = n.pull_pos[n.pull_list[m]];
+    for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, f.a[tm]);
+  };
+  // A = W_x fragment (d), B = dA fragment (rows): a lane holds four
+  // consecutive d of one row
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int d = d0 + wn * (BN / 2) + tn * 16 + r;
-        if (d < D) dX[(size_t)row * D + d] = acc[tm][tn][i];
-      }
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma_chunk8<false>(cur.b[tn], cur.a[tm], acc[tm][tn]);
+    interleave_reads<2 * (TM + TN), TM * TN * 8>();
+  };
+  ring_loop_db<S, IPW, Frag>((four ? H4 : 3 * H) / kBK, ring, issue, read, body);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    if (orow[tm] < 0) continue;
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int d = d0 + wn * (BN / 2) + tn * 16 + 4 * gq;
+      if (d < D)   // D % 4 == 0: the four d are all in range or all out
+        st4(dX + (size_t)orow[tm] * D + d,
+            make_float4(acc[tm][tn][0], acc[tm][tn][1], acc[tm][tn][2], acc[tm][tn][3]));
     }
+  }
 }
 
 // ------------------------------------------------------------ bf16 variants
@@ -1361,8 +1373,10 @@ bool pull_tile_applies(const Net& n, int n_pull) {
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
   if (n_pull <= 0) return;
   dim3 grid(cdiv(n_pull, 64), cdiv(n.D, 64));
-  if (!n.bf && (!with_f || n.N == 1)) {
-    CAVS_LAUNCH("k_dx_tile<64, 64, 3>", (k_dx_tile<64, 64, 3>), grid, dim3(256), 0, s, n, n_pull,
+  if (!n.bf && (!with_f || n.N == 1) && n.D % 4 == 0) {
+    // 32-row tiles: about three workgroups per CU at the benchmark shapes
+    const dim3 g32(cdiv(n_pull, 32), cdiv(n.D, 64));
+    CAVS_LAUNCH("k_dx_tile<32, 64, 3>", (k_dx_tile<32, 64, 3>), g32, dim3(256), 0, s, n, n_pull,
                 (int)with_f, dX);
     return;
   }
