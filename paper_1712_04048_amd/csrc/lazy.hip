@@ -130,9 +130,9 @@ __global__ void __launch_bounds__(256) k_pull_leaf(Net n, int n_pull, int lo1) {
 // Four wavefronts as 2 x 2 (32 rows x 16 units each); the weight fragment
 // is the MFMA's A operand, so a lane holds four consecutive units of one
 // row (float4 epilogue).  Fragments are double-buffered in registers.
-template <int NG, int S>
+template <int NG, int BM, int S>
 __global__ void __launch_bounds__(256) k_pull_tile(Net n, int n_pull, int lo1) {
-  constexpr int BM = 64, BU = 32, TM = 2;
+  constexpr int BU = 32, TM = BM / 32;
   constexpr int ROWS = BM + NG * BU, IPW = ROWS / 32;
   static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
@@ -153,7 +153,7 @@ __global__ void __launch_bounds__(256) k_pull_tile(Net n, int n_pull, int lo1) {
   int pos[TM], vid[TM];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
-    const int m = m0 + wr * 32 + tm * 16 + r;
+    const int m = m0 + wr * (BM / 2) + tm * 16 + r;
     pos[tm] = m < n_pull ? n.pull_list[m] : -1;
     vid[tm] = pos[tm] >= 0 && pos[tm] < lo1 ? n.order[pos[tm]] : 0;
   }
@@ -195,7 +195,7 @@ __global__ void __launch_bounds__(256) k_pull_tile(Net n, int n_pull, int lo1) {
 #pragma unroll
     for (int g = 0; g < NG; ++g) frag_sw(Ls, BM + g * BU + wu * 16 + r, gq, f.b[g]);
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, wr * 32 + tm * 16 + r, gq, f.a[tm]);
+    for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, f.a[tm]);
   };
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
@@ -1354,9 +1354,11 @@ void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s) {
   if (pull_tile_applies(n, n_pull)) {
     const dim3 grid(cdiv(n_pull, 64) * (n.H / 32));
     if (with_f)
-      CAVS_LAUNCH("k_pull_tile<4, 2>", (k_pull_tile<4, 2>), grid, dim3(256), 0, s, n, n_pull, lo1);
+      CAVS_LAUNCH("k_pull_tile<4, 64, 2>", (k_pull_tile<4, 64, 2>), grid, dim3(256), 0, s, n,
+                  n_pull, lo1);
     else
-      CAVS_LAUNCH("k_pull_tile<3, 2>", (k_pull_tile<3, 2>), grid, dim3(256), 0, s, n, n_pull, lo1);
+      CAVS_LAUNCH("k_pull_tile<3, 64, 2>", (k_pull_tile<3, 64, 2>), grid, dim3(256), 0, s, n,
+                  n_pull, lo1);
     return;
   }
   dim3 grid(cdiv(n_pull, 64), n.H / 32);
