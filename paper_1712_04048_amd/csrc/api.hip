@@ -69,7 +69,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   L.dCp = take(lstm ? V * H : 0);
   L.dA = take(V * GW);
   L.part_floats = lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
-  L.part = take(L.part_floats);
+  L.part = take(3 * L.part_floats);   // dU_iou, dU_f and dW_x split-K sums side by side
   L.bar = take(256);
   L.total = o;
   return L;
@@ -373,10 +373,15 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       if (t < tf) lstm_bwd_gates(n, lo[t], M, str);
       if (t >= 1) lstm_bwd_level(n, lo[t], M, str);
     }
+    // the lazy products keep their split-K sums in separate scratch and share
+    // one reduction launch
     const bool with_f = s->n_inner_input > 0;
-    lstm_dU_iou(n, off1, g->dU, part, L.part_floats, str);
-    lstm_dU_f(n, off1, g->dU, part, L.part_floats, str);
-    if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part, L.part_floats, str);
+    const size_t pf = L.part_floats;
+    SplitJobs jobs;
+    lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
+    lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
+    if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
+    reduce_split_jobs(jobs, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);
   } else {

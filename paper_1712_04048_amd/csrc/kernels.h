@@ -105,14 +105,30 @@ bool pull_tile_applies(const Net& n, int n_pull);
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s);
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s);
 // Lazy weight-gradient products; `part` is split-K scratch of part_floats floats.
+// Split-K sums waiting for their reduction: the lazy products append one
+// job each (their partial sums must then stay in distinct scratch) and one
+// launch reduces them all.
+struct SplitJob {
+  const float* part;
+  float* dst;
+  int S, Mo, No, ldd, col_off, gap_start, gap;
+};
+struct SplitJobs {
+  static constexpr int kMax = 4;
+  SplitJob j[kMax];
+  int n = 0;
+};
+void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s);
+
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
 // the two halves of lstm_dU: dU_iou (all four blocks with one child) and,
 // with two children, dU_f (a no-op with one child)
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
-                 hipStream_t s);
-void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
+                 hipStream_t s, SplitJobs* jobs = nullptr);
+void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s,
+               SplitJobs* jobs = nullptr);
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
-              size_t part_floats, hipStream_t s);
+              size_t part_floats, hipStream_t s, SplitJobs* jobs = nullptr);
 void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);
 // column sums over positions [row0, row1) of the gate gradients -> db
 // db over rows [row0, row1) and, for the CE head, dW_s and db_s over all rows;

@@ -1006,13 +1006,36 @@ __global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, 
     }
 }
 
+// All pending split-K sums in one launch: blockIdx.y picks the job.
+__global__ void k_reduce_jobs(SplitJobs jobs) {
+  const SplitJob& J = jobs.j[blockIdx.y];
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)J.Mo * J.No) return;
+  const int m = (int)(idx / J.No), nn = (int)(idx % J.No);
+  float s = 0.f;
+  for (int k = 0; k < J.S; ++k) s += J.part[(size_t)k * J.Mo * J.No + idx];
+  J.dst[(size_t)m * J.ldd + J.col_off + nn + (nn >= J.gap_start ? J.gap : 0)] = s;
+}
+
+// The reduction of a split-K product: queued on `jobs` when given (the
+// caller then launches reduce_split_jobs), else launched at once.
+void split_sum(const float* part, int S, int Mo, int No, float* dst, int ldd, int col_off,
+               int gap_start, int gap, hipStream_t st, SplitJobs* jobs) {
+  if (jobs && jobs->n < SplitJobs::kMax) {
+    jobs->j[jobs->n++] = SplitJob{part, dst, S, Mo, No, ldd, col_off, gap_start, gap};
+    return;
+  }
+  CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
+              part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
+}
+
 template <class L>
 void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col_off,
-                int gap_start, int gap, float* part, size_t part_floats, hipStream_t st) {
+                int gap_start, int gap, float* part, size_t part_floats, hipStream_t st,
+                SplitJobs* jobs = nullptr) {
   if (Q <= 0) {
     // empty contraction: zero output columns
-    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
-                       (const float*)part, 0, Mo, No, dst, ldd, col_off, gap_start, gap);
+    split_sum(part, 0, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
     return;
   }
   // the direct-to-LDS kernel: fp32, 256-column tiles that stay inside one
@@ -1038,8 +1061,7 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
     else
       CAVS_LAUNCH(L::kNameDl128, (k_tn_dl<L, 128, 256, S128>), grid, dim3(512), 0, st, ld, Q,
                   qchunk, Mo, No, part);
-    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0,
-                st, (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
+    split_sum(part, S, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
     return;
   }
   const int BT = (!ld.n.bf && No % 128 == 0) ? 128 : 64;
@@ -1064,8 +1086,7 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
   else
     CAVS_LAUNCH(L::kName, (k_tn_gemm<L, 64, 4>), dim3(No / 64, cdiv(Mo, 64), S), dim3(256), 0, st,
                 ld, Q, qchunk, Mo, No, part);
-  CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)Mo * No, 256)), dim3(256), 0, st,
-                     (const float*)part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
+  split_sum(part, S, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
 }
 
 // -------------------------------------------------------------- col sums
@@ -1403,18 +1424,29 @@ void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
 }
 
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
-                 hipStream_t s) {
+                 hipStream_t s, SplitJobs* jobs) {
   const int H = n.H, MI = n.V - off1;
   LdDUiou ld{n, off1};
-  if (n.N == 1) tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
-  else tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s);
+  if (n.N == 1) tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s, jobs);
+  else tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s, jobs);
 }
 
-void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
+void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s,
+               SplitJobs* jobs) {
   if (n.N != 2) return;
   const int H = n.H, MI = n.V - off1;
   LdDUf lf{n, off1, MI};
-  tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s);
+  tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s, jobs);
+}
+
+void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s) {
+  if (jobs.n == 0) return;
+  long most = 0;
+  for (int k = 0; k < jobs.n; ++k) {
+    const long e = (long)jobs.j[k].Mo * jobs.j[k].No;
+    most = e > most ? e : most;
+  }
+  CAVS_LAUNCH("k_reduce_jobs", k_reduce_jobs, dim3(cdiv(most, 256), jobs.n), dim3(256), 0, s, jobs);
 }
 
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
@@ -1431,16 +1463,15 @@ void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats,
 }
 
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
-              size_t part_floats, hipStream_t s) {
+              size_t part_floats, hipStream_t s, SplitJobs* jobs) {
   const int H = n.H;
   LdDWx ld{n, (int)with_f};
   if (with_f) {
-    tn_product(ld, n_pull, n.D, 4 * H, dWx, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
+    tn_product(ld, n_pull, n.D, 4 * H, dWx, 4 * H, 0, 1 << 30, 0, part, part_floats, s, jobs);
   } else {
-    tn_product(ld, n_pull, n.D, 3 * H, dWx, 4 * H, 0, H, H, part, part_floats, s);
+    tn_product(ld, n_pull, n.D, 3 * H, dWx, 4 * H, 0, H, H, part, part_floats, s, jobs);
     // the f block of dW_x is exactly zero: no vertex with children pulls
-    CAVS_LAUNCH("k_reduce_splits", k_reduce_splits, dim3(cdiv((long)n.D * H, 256)), dim3(256), 0, s,
-                       (const float*)part, 0, n.D, H, dWx, 4 * H, H, 1 << 30, 0);
+    split_sum(part, 0, n.D, H, dWx, 4 * H, H, 1 << 30, 0, s, jobs);
   }
 }
 
