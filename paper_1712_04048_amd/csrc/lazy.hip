@@ -1006,22 +1006,31 @@ __global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, 
     }
 }
 
-// All pending split-K sums in one launch: blockIdx.y picks the job.
+// All pending split-K sums in one launch: blockIdx.y picks the job; each
+// thread adds four adjacent outputs (every job's No, ldd, col_off,
+// gap_start and gap are multiples of 4, checked on the host).
 __global__ void k_reduce_jobs(SplitJobs jobs) {
   const SplitJob& J = jobs.j[blockIdx.y];
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long idx = 4 * ((long)blockIdx.x * 256 + threadIdx.x);
   if (idx >= (long)J.Mo * J.No) return;
   const int m = (int)(idx / J.No), nn = (int)(idx % J.No);
-  float s = 0.f;
-  for (int k = 0; k < J.S; ++k) s += J.part[(size_t)k * J.Mo * J.No + idx];
-  J.dst[(size_t)m * J.ldd + J.col_off + nn + (nn >= J.gap_start ? J.gap : 0)] = s;
+  float4 s = f4zero();
+  const size_t stride = (size_t)J.Mo * J.No;
+#pragma unroll 4
+  for (int k = 0; k < J.S; ++k) {
+    const float4 v = ldg4(J.part + k * stride + idx);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  st4(J.dst + (size_t)m * J.ldd + J.col_off + nn + (nn >= J.gap_start ? J.gap : 0), s);
 }
 
 // The reduction of a split-K product: queued on `jobs` when given (the
 // caller then launches reduce_split_jobs), else launched at once.
 void split_sum(const float* part, int S, int Mo, int No, float* dst, int ldd, int col_off,
                int gap_start, int gap, hipStream_t st, SplitJobs* jobs) {
-  if (jobs && jobs->n < SplitJobs::kMax) {
+  const bool by4 = No % 4 == 0 && ldd % 4 == 0 && col_off % 4 == 0 && gap % 4 == 0 &&
+                   (gap_start % 4 == 0 || gap_start >= No) && (uintptr_t)dst % 16 == 0;
+  if (jobs && jobs->n < SplitJobs::kMax && by4) {
     jobs->j[jobs->n++] = SplitJob{part, dst, S, Mo, No, ldd, col_off, gap_start, gap};
     return;
   }
@@ -1446,7 +1455,7 @@ void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s) {
     const long e = (long)jobs.j[k].Mo * jobs.j[k].No;
     most = e > most ? e : most;
   }
-  CAVS_LAUNCH("k_reduce_jobs", k_reduce_jobs, dim3(cdiv(most, 256), jobs.n), dim3(256), 0, s, jobs);
+  CAVS_LAUNCH("k_reduce_jobs", k_reduce_jobs, dim3(cdiv(most, 1024), jobs.n), dim3(256), 0, s, jobs);
 }
 
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
