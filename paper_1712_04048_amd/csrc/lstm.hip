@@ -751,15 +751,8 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     // KW = 4), so the loads are unconditional.
     constexpr int G1 = NCH == 2 ? 6 : 8;
     const int end1 = (w + 1) * q1;
-    for (int c0 = w * q1; c0 < end1; c0 += G1 * kBK) {
-      F1 f[G1];
-#pragma unroll
-      for (int g = 0; g < G1; ++g) load1(c0 + g * kBK, f[g]);
-      __builtin_amdgcn_sched_barrier(0);   // keep every load of the group ahead of the MFMAs
-#pragma unroll
-      for (int g = 0; g < G1; ++g) comp1(f[g]);
-    }
     if constexpr (NCH == 2) {
+      // the two phases' loads go out together: one memory latency per level
       struct F2 {
         float a0[TR][8], a1[TR][8], b[8];
       };
@@ -782,13 +775,38 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
       };
       constexpr int G2 = 2;   // H / (32 KW) is even
       const int end2 = (w + 1) * q2;
-      for (int c0 = w * q2; c0 < end2; c0 += G2 * kBK) {
-        F2 f[G2];
+      // per group: the phase-2 chunks and the first half of the phase-1
+      // chunks load together; the second half loads into the registers the
+      // phase-2 fragments free, while the first half is multiplied
+      constexpr int GH = G1 / 2;
+      int c1 = w * q1;
+      for (int c0 = w * q2; c0 < end2; c0 += G2 * kBK, c1 += G1 * kBK) {
+        F2 f2[G2];
+        F1 fa[GH], fb[GH];
 #pragma unroll
-        for (int g = 0; g < G2; ++g) load2(c0 + g * kBK, f[g]);
+        for (int g = 0; g < G2; ++g) load2(c0 + g * kBK, f2[g]);
+#pragma unroll
+        for (int g = 0; g < GH; ++g) load1(c1 + g * kBK, fa[g]);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int g = 0; g < G2; ++g) comp2(f[g]);
+        for (int g = 0; g < G2; ++g) comp2(f2[g]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int g = 0; g < GH; ++g) load1(c1 + (GH + g) * kBK, fb[g]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int g = 0; g < GH; ++g) comp1(fa[g]);
+#pragma unroll
+        for (int g = 0; g < GH; ++g) comp1(fb[g]);
+      }
+    } else {
+      for (int c0 = w * q1; c0 < end1; c0 += G1 * kBK) {
+        F1 f[G1];
+#pragma unroll
+        for (int g = 0; g < G1; ++g) load1(c0 + g * kBK, f[g]);
+        __builtin_amdgcn_sched_barrier(0);   // keep every load of the group ahead of the MFMAs
+#pragma unroll
+        for (int g = 0; g < G1; ++g) comp1(f[g]);
       }
     }
 #pragma unroll
