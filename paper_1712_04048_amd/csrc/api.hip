@@ -180,7 +180,10 @@ cavs_status cavs_create(cavs_ctx** out, int32_t device, void* hip_stream) {
   ctx->stream = (hipStream_t)hip_stream;
   if (hipSetDevice(device) != hipSuccess ||
       hipHostMalloc((void**)&ctx->host_stage, sizeof(int32_t) * kHostStageInts,
-                    hipHostMallocDefault) != hipSuccess) {
+                    hipHostMallocDefault) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->stage_ready, hipEventDisableTiming) != hipSuccess) {
+    if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
+  if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
     delete ctx;
     return CAVS_ERR_HIP;
   }
@@ -197,6 +200,7 @@ cavs_status cavs_set_stream(cavs_ctx* ctx, void* hip_stream) {
 void cavs_destroy(cavs_ctx* ctx) {
   if (!ctx) return;
   if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
+  if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
   for (auto& r : ctx->timed) {
     (void)hipEventDestroy(r.start);
     (void)hipEventDestroy(r.stop);

@@ -25,6 +25,7 @@ struct cavs_ctx {
   bool timing = false;
   std::vector<cavs_timed_launch> timed;   // pending records
   std::vector<hipEvent_t> event_pool;     // reusable events
+  hipEvent_t stage_ready = nullptr;       // the schedule's host stage has arrived
 };
 
 namespace cavs {

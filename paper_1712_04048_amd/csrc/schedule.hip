@@ -509,7 +509,26 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   CAVS_LAUNCH_CHECK(ctx);
   CAVS_HIP_CHECK(ctx, hipMemcpyAsync(ctx->host_stage, stage, sizeof(int) * kHostStageInts,
                                      hipMemcpyDeviceToHost, st));
-  CAVS_HIP_CHECK(ctx, hipStreamSynchronize(st));
+  CAVS_HIP_CHECK(ctx, hipEventRecord(ctx->stage_ready, st));
+  // While the host waits for the stage, the device already sorts assuming
+  // fewer than 256 levels (one radix pass) and remaps; with more levels the
+  // sort and remap run again below and overwrite these results.  On a graph
+  // that fails validation they write only schedule outputs.
+  int* const lvK[2] = {kA, kB};
+  int* const lvV[2] = {vA, vB};
+  auto sort_and_remap = [&](int passes) {
+    cavs_status r = radix_sort(ctx, s->level, nullptr, V, passes, lvK, lvV, s->order, s->pos,
+                               g->pull_idx, s->pull_list, tile_hist, L.ntiles);
+    if (r != CAVS_OK) return r;
+    CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, (const int*)s->order,
+                (const int*)s->pos, g->child, g->parent, g->pull_idx, g->push_idx, s->child_pos,
+                s->parent_pos, s->pull_pos, s->push_pos);
+    CAVS_LAUNCH_CHECK(ctx);
+    return CAVS_OK;
+  };
+  cavs_status r = sort_and_remap(1);
+  if (r != CAVS_OK) return r;
+  CAVS_HIP_CHECK(ctx, hipEventSynchronize(ctx->stage_ready));
   const int* h = ctx->host_stage;
   if (h[F_RANGE]) return fail(ctx, CAVS_ERR_RANGE, "an index array holds an out-of-range value");
   if (h[F_MULTI]) return fail(ctx, CAVS_ERR_MULTIPARENT, "a vertex is a child more than once");
@@ -534,16 +553,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   // levels lie in [0, T): enough 8-bit digits for T - 1
   int passes = 1;
   while (passes < 4 && ((long)(T > 0 ? T - 1 : 0) >> (8 * passes)) > 0) ++passes;
-  int* const lvK[2] = {kA, kB};
-  int* const lvV[2] = {vA, vB};
-  cavs_status r = radix_sort(ctx, s->level, nullptr, V, passes, lvK, lvV, s->order, s->pos,
-                             g->pull_idx, s->pull_list, tile_hist, L.ntiles);
-  if (r != CAVS_OK) return r;
-  CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, (const int*)s->order,
-              (const int*)s->pos, g->child, g->parent, g->pull_idx, g->push_idx, s->child_pos,
-              s->parent_pos, s->pull_pos, s->push_pos);
-  CAVS_LAUNCH_CHECK(ctx);
-  return CAVS_OK;
+  return passes > 1 ? sort_and_remap(passes) : CAVS_OK;
 }
 
 }  // namespace cavs
