@@ -1036,7 +1036,9 @@ void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s) {
     return;
   }
   if (n.H % 256 == 0) {
-    const bool kw8 = (n.H / 8) % 64 == 0 && (3 * n.H / 8) % 64 == 0;
+    // eight K wavefronts at most 128 positions (one round); four above, where
+    // two workgroups per CU keep the whole level co-resident
+    const bool kw8 = (n.H / 8) % 64 == 0 && (3 * n.H / 8) % 64 == 0 && M <= 128;
     dim3 g(cdiv(M, 16) * (n.H / 16));
 #define CAVS_BWD_SK(NCH, BF)                                                                   \
   do {                                                                                         \

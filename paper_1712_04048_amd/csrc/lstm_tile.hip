@@ -353,16 +353,17 @@ bool lstm_tile_applies(const Net& n, int M) {
   return n.H % 256 == 0 && M >= kTileMinRows;
 }
 
-// Tile shapes and ring depths measured on MI355X (H = 512): 64-position
-// tiles once a level fills the chip twice over, 32 below.
+// Tile shapes and ring depths measured on MI355X (H = 512): the forward
+// takes 64-position tiles once a level fills the chip twice over and 32
+// below; the backward, with its larger per-tile stage, measured faster with
+// 32-position tiles at every level size.
 void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s) {
   if (M >= 1024) CAVS_TILE_DISPATCH(fwd, 64, 32, 2);
   else CAVS_TILE_DISPATCH(fwd, 32, 32, 2);
 }
 
 void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s) {
-  if (M >= 1024) CAVS_TILE_DISPATCH(bwd, 64, 32, 2);
-  else CAVS_TILE_DISPATCH(bwd, 32, 32, 2);
+  CAVS_TILE_DISPATCH(bwd, 32, 32, 2);
 }
 
 }  // namespace cavs
