@@ -18,8 +18,12 @@
 //      (their ranks counted the same way over the pulling subset);
 //   6. index remap to positions.
 // Steps 5 and 6 are only enqueued: later calls on the stream see them done.
+// Batches of at most kSmallV vertices run steps 1-4 and steps 5-6 as two
+// one-workgroup launches instead (k_sched_small_levels, k_sched_small_sort).
 #include <stdarg.h>
 #include <stdio.h>
+
+#include <type_traits>
 
 #include "cavs_internal.h"
 
@@ -40,6 +44,7 @@ enum Flag {
   F_LEAF_NOIN = 9,
   F_INNER_IN = 10,
   F_NPULL = 11,
+  F_FALLBACK = 12,   // the one-workgroup scheduler could not finish (more than kSmallT levels)
   F_COUNT = 32
 };
 
@@ -387,6 +392,446 @@ __global__ void k_remap(int V, int N, const int* __restrict__ order, const int* 
 }
 
 // -------------------------------------------------------------------------
+// Small batches: the same steps in two one-workgroup launches
+// -------------------------------------------------------------------------
+// With at most kSmallV vertices the parent links, the arrival counters and
+// the level histogram fit in one workgroup's LDS, so steps 1-4 run as one
+// launch without global atomics or kernel boundaries between them, and steps
+// 5-6 as a second launch that the host does not wait for.  A batch with
+// kSmallT levels or more sets F_FALLBACK and is scheduled again by the
+// general path.
+constexpr int kSmallV = 16384;
+constexpr int kSmallNx = 1 << 18;   // input rows tracked by the LDS bitset
+constexpr int kSmallT = 256;
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallPer = kSmallV / kSmallThreads;
+constexpr int kSmallWaves = kSmallThreads / kWave;
+constexpr int kSmallStageInts = kStageHead + kSmallT + 1;
+
+// Steps 1-4.  Vertex v belongs to thread v % 1024 for the validation.  The
+// levels are then found level-synchronously instead of by walks: round t
+// takes the list of level-t vertices, sets their level and counts each one
+// off its parent's number of children not yet reached; a parent whose count
+// drops to zero has all its children at levels <= t, one of them at t, so it
+// is on level t + 1 and goes into the next list (compacted with a ballot and
+// one LDS atomic per wavefront).  The list lengths are the level histogram.
+// Every round is dense work for the whole workgroup, where leaf-to-root
+// walks would leave most lanes of a wavefront idle.
+__global__ void __launch_bounds__(kSmallThreads) k_sched_small_levels(
+    int V, int N, int n_x, int n_push, const int* __restrict__ child,
+    const int* __restrict__ parent, const int* __restrict__ pull_idx,
+    const int* __restrict__ push_idx, int* __restrict__ level, int* __restrict__ level_offsets,
+    int* __restrict__ stage) {
+  __shared__ short par[kSmallV];              // parent, or -1, or -2 when out of range
+  __shared__ unsigned nrem[kSmallV / 4];      // one byte per vertex: children not yet reached
+  __shared__ int lists[kSmallV];              // two level lists of int16, or reference counts
+  __shared__ unsigned pbits[kSmallNx / 32];   // input rows already pulled
+  __shared__ int fcnt[kSmallT + 1];           // list lengths = the level histogram
+  __shared__ int fl[F_COUNT];
+  __shared__ int red[2];                      // rounds and vertices reached
+  short* const fr0 = reinterpret_cast<short*>(lists);
+  short* const fr1 = fr0 + kSmallV;
+  unsigned char* const nrem8 = reinterpret_cast<unsigned char*>(nrem);
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const unsigned long long lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+
+  // 1. parents into LDS, counters cleared.  The loads are unconditional
+  // (indices clamped to V - 1; the copies past V are never used), so that
+  // each array costs one memory latency.
+  for (int i = tid; i < (n_x + 31) / 32; i += kSmallThreads) pbits[i] = 0;
+  for (int i = tid; i <= kSmallT; i += kSmallThreads) fcnt[i] = 0;
+  if (tid < F_COUNT) fl[tid] = 0;
+  int bad = 0, withp = 0;
+  {
+    int pv[kSmallPer];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) pv[i] = parent[min(tid + i * kSmallThreads, V - 1)];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int v = tid + i * kSmallThreads;
+      if (v < V) {
+        const int p = pv[i];
+        const bool pb = p < -1 || p >= V;
+        bad |= pb;
+        withp += !pb && p >= 0;
+        par[v] = (short)(pb ? -2 : p);
+      }
+    }
+  }
+  __syncthreads();
+
+  // validation counters, the children counts and the leaves (the level-0 list)
+  int links = 0, lab = 0, leafnoin = 0, innerin = 0, npull = 0, multi = 0, dup = 0, mism = 0;
+  unsigned leafmask = 0;   // bit i: vertex tid + 1024 i is a leaf
+  {
+    int cs[kSmallPer][2];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      const size_t v = (size_t)min(tid + i * kSmallThreads, V - 1);
+      cs[i][0] = child[v * N];
+      cs[i][1] = N == 2 ? child[v * N + 1] : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int v = tid + i * kSmallThreads;
+      if (i * kSmallThreads < V && v < V) {   // the first test skips whole trips
+        int nc = 0;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int c = cs[i][k];
+          if (c < -1 || c >= V) {
+            bad = 1;
+          } else if (c >= 0) {
+            mism |= (int)par[c] != v;
+            ++nc;
+          }
+        }
+        // the same child in both slots; a child listed by two different
+        // vertices shows as a mismatch first (see below)
+        multi |= cs[i][0] >= 0 && cs[i][0] < V && cs[i][0] == cs[i][1];
+        nrem8[v] = (unsigned char)nc;
+        if (!nc) leafmask |= 1u << i;
+        links += nc;
+      }
+    }
+  }
+  if (pull_idx) {
+    int rr[kSmallPer];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) rr[i] = pull_idx[min(tid + i * kSmallThreads, V - 1)];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      if (i * kSmallThreads < V && tid + i * kSmallThreads < V) {
+        int r = rr[i];
+        if (r < -1 || r >= n_x) {
+          bad = 1;
+          r = -1;
+        } else if (r >= 0) {
+          ++npull;
+          const unsigned bit = 1u << (r & 31);
+          dup |= (atomicOr(&pbits[r >> 5], bit) & bit) != 0;
+        }
+        const bool leaf = (leafmask >> i) & 1u;
+        leafnoin += leaf && r < 0;
+        innerin += !leaf && r >= 0;
+      }
+    }
+  } else {
+    leafnoin = __popc(leafmask);
+  }
+  if (push_idx) {
+    int qq[kSmallPer];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) qq[i] = push_idx[min(tid + i * kSmallThreads, V - 1)];
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int q = qq[i];
+      if (i * kSmallThreads < V && tid + i * kSmallThreads < V) {
+        if (q < -1 || q >= n_push) bad = 1;
+        else if (q >= 0) ++lab;
+      }
+    }
+  }
+  {
+    // this thread's leaves go to the level-0 list: one LDS atomic per wavefront
+    const int nl = __popc(leafmask);
+    int incl = nl;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int x = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += x;
+    }
+    int base = 0;
+    if (lane == kWave - 1 && incl) base = atomicAdd(&fcnt[0], incl);
+    base = __shfl(base, kWave - 1, kWave) + incl - nl;
+    for (unsigned m = leafmask; m; m &= m - 1) fr0[base++] = (short)(tid + __builtin_ctz(m) * kSmallThreads);
+  }
+  // per-wavefront sums, two 16-bit counts to a word (a thread adds at most
+  // 2 * kSmallPer to each), and the error flags as ballots
+  auto add2 = [&](int idx_lo, int lo, int idx_hi, int hi) {
+    const int x = wave_sum_int(lo | (hi << 16));
+    if (lane == 0 && x) {
+      atomicAdd(&fl[idx_lo], x & 0xFFFF);
+      atomicAdd(&fl[idx_hi], x >> 16);
+    }
+  };
+  auto flag = [&](int idx, int x) {
+    if (__ballot(x != 0) && lane == 0) atomicOr(&fl[idx], 1);
+  };
+  add2(F_LINKS, links, F_WITHPARENT, withp);
+  add2(F_LABELLED, lab, F_NPULL, npull);
+  add2(F_LEAF_NOIN, leafnoin, F_INNER_IN, innerin);
+  flag(F_RANGE, bad);
+  flag(F_MULTI, multi);
+  flag(F_DUP, dup);
+  flag(F_MISMATCH, mism);
+  __syncthreads();
+
+  // A vertex listed as a child by two different vertices has a parent that
+  // differs from at least one of them, so references are only counted
+  // (to tell F_MULTI from F_MISMATCH) when a mismatch was seen.
+  if (fl[F_MISMATCH]) {
+    int* ref = lists;
+    for (int i = tid; i < V; i += kSmallThreads) ref[i] = 0;
+    __syncthreads();
+    int mu = 0;
+    for (int v = tid; v < V; v += kSmallThreads)
+      for (int k = 0; k < N; ++k) {
+        const int c = child[(size_t)v * N + k];
+        if (c >= 0 && c < V) mu |= atomicAdd(&ref[c], 1) != 0;
+      }
+    flag(F_MULTI, mu);
+    __syncthreads();
+  }
+  const bool err = (fl[F_RANGE] | fl[F_MULTI] | fl[F_DUP] | fl[F_MISMATCH]) != 0 ||
+                   fl[F_LINKS] != fl[F_WITHPARENT];
+
+  // 2-3. rounds (skipped on a graph that failed validation: the host reports
+  // the error); at most kSmallT of them, more levels fall back
+  // One round: the list of level T (size entries) in chunks of `stride`
+  // lanes from lane `first`; the completed parents are appended to the next
+  // list (LDS executes each wavefront's atomics in order, so a wavefront's
+  // append is complete before its next round reads the count).
+  auto round = [&](int T, int size, int first, int stride) {
+    const short* cur = (T & 1) ? fr1 : fr0;
+    short* nxt = (T & 1) ? fr0 : fr1;
+    for (int k0 = 0; k0 < size; k0 += stride) {
+      const int k = k0 + first;
+      bool done = false;
+      int p = -1;
+      if (k < size && k < kSmallV) {
+        const int v = cur[k];
+        level[v] = T;
+        p = par[v];
+        if (p >= 0) {
+          const unsigned sh = 8u * (p & 3);
+          done = ((atomicSub(&nrem[p >> 2], 1u << sh) >> sh) & 255u) == 1u;
+        }
+      }
+      const unsigned long long m = __ballot(done);
+      int base = 0;
+      if (lane == 0 && m) base = atomicAdd(&fcnt[T + 1], __popcll(m));
+      base = __builtin_amdgcn_readfirstlane(base) + __popcll(m & lt);
+      if (done && base < kSmallV) nxt[base] = (short)p;
+    }
+  };
+  int T = 0, total = 0;
+  bool deep = false;
+  if (!err) {
+    // whole-workgroup rounds while a list is longer than one wavefront ...
+    for (; T < kSmallT; ++T) {
+      const int size = fcnt[T];   // complete: written before the last barrier
+      if (size <= kWave) break;
+      total += size;
+      round(T, size, tid, kSmallThreads);
+      __syncthreads();
+    }
+    // ... then wavefront 0 alone, without barriers
+    if (tid < kWave) {
+      for (; T < kSmallT; ++T) {
+        const int size = fcnt[T];
+        if (size == 0) break;
+        total += size;
+        round(T, size, lane, kWave);
+      }
+      if (lane == 0) red[0] = T, red[1] = total;
+    }
+    __syncthreads();
+    T = red[0];
+    total = red[1];
+    deep = T == kSmallT && fcnt[kSmallT] > 0;
+  }
+
+  // 4. flags, the offsets scan, and the host stage
+  if (tid == 0) {
+    fl[F_T] = deep ? kSmallT + 1 : T;
+    if (!err && !deep && total < V) fl[F_CYCLE] = 1;   // some vertex was never reached
+    if (deep) fl[F_FALLBACK] = 1;
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    // exclusive scan of the list lengths into offsets 0..T, five entries per lane
+    constexpr int E = (kSmallT + kWave) / kWave;
+    int a[E], sum = 0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int idx = E * lane + j;
+      a[j] = idx < T ? fcnt[idx] : 0;
+      sum += a[j];
+    }
+    int incl = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int x = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += x;
+    }
+    int run = incl - sum;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int idx = E * lane + j;
+      if (idx <= T && idx <= V) {
+        level_offsets[idx] = run;
+        stage[kStageHead + idx] = run;
+      }
+      run += a[j];
+    }
+  } else if (tid < kWave + F_COUNT) {
+    stage[tid - kWave] = fl[tid - kWave];
+  }
+}
+
+// Steps 5-6.  Wavefront w ranks vertices [w S, w S + S) in id order, 64 at a
+// time (chunk j = vertices w S + 64 j ..): the lanes with the same level find
+// each other through a per-level lane mask in LDS, and a per-wavefront
+// running count per level gives each its rank; the counts
+// scanned over levels and wavefronts give the bases.  Pulling vertices are
+// ranked the same way over the pulling lanes.  The ranking is cheap and every
+// workgroup of the launch repeats it (so each holds all positions in LDS);
+// workgroup g then writes the outputs of chunk g of every wavefront, which
+// spreads the scattered stores over as many CUs as there are chunks.  Runs
+// only if steps 1-4 found a valid graph with fewer than kSmallT levels (read
+// from the stage on the device).
+__device__ __forceinline__ int small_sort_span(int V) {
+  return ((V + kSmallWaves - 1) / kSmallWaves + kWave - 1) / kWave * kWave;
+}
+
+__global__ void __launch_bounds__(kSmallThreads) k_sched_small_sort(
+    int V, int N, const int* __restrict__ child, const int* __restrict__ parent,
+    const int* __restrict__ pull_idx, const int* __restrict__ push_idx,
+    const int* __restrict__ level, const int* __restrict__ stage, int* __restrict__ order,
+    int* __restrict__ pos, int* __restrict__ child_pos, int* __restrict__ parent_pos,
+    int* __restrict__ pull_pos, int* __restrict__ push_pos, int* __restrict__ pull_list) {
+  __shared__ int cnt[2][kSmallWaves][kSmallT];   // all vertices, pulling vertices
+  __shared__ int wsum[2][kSmallT / kWave];
+  __shared__ int posl[kSmallV];
+  __shared__ unsigned long long lanes[kSmallWaves][kSmallT];   // per level: lanes of a chunk
+  const int* f = stage;
+  const bool ok = !(f[F_RANGE] | f[F_MULTI] | f[F_DUP] | f[F_MISMATCH] | f[F_CYCLE] |
+                    f[F_FALLBACK]) &&
+                  f[F_LINKS] == f[F_WITHPARENT];
+  if (!ok) return;   // the same for every thread
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1), g = blockIdx.x;
+  for (int i = tid; i < 2 * kSmallWaves * kSmallT; i += kSmallThreads) (&cnt[0][0][0])[i] = 0;
+  for (int i = tid; i < kSmallWaves * kSmallT; i += kSmallThreads) (&lanes[0][0])[i] = 0;
+  const int S = small_sort_span(V);
+  const int nch = S / kWave, v0 = w * S;
+  const unsigned long long lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  // the inputs of this workgroup's own chunk, loaded while it ranks
+  const int vg = v0 + g * kWave + lane, vgc = min(vg, V - 1);
+  const int a0 = child[(size_t)vgc * N], a1 = child[(size_t)vgc * N + N - 1];
+  const int pa = parent[vgc];
+  const int pl = pull_idx ? pull_idx[vgc] : -1, ps = push_idx ? push_idx[vgc] : -1;
+  // unconditional loads (indices clamped to V - 1; copies past V are unused)
+  int lv[kSmallPer], rk[kSmallPer];   // level; rank | pulling rank << 16
+  unsigned pm = 0;                    // bit j: the vertex of chunk j pulls
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) lv[j] = level[min(v0 + j * kWave + lane, V - 1)];
+  if (pull_idx) {
+    int pr[kSmallPer];
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j) pr[j] = pull_idx[min(v0 + j * kWave + lane, V - 1)];
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j) pm |= (unsigned)(pr[j] >= 0) << j;
+  }
+  // the chunk inputs are needed here, so their loads are not moved past the
+  // ranking to their conditional uses
+  asm volatile("" ::"v"(a0), "v"(a1), "v"(pa), "v"(pl), "v"(ps));
+  __syncthreads();
+  // The lanes of a chunk with the same level: every lane ORs its bit into its
+  // level's mask (this wavefront's row), reads the mask back, and the first
+  // lane of each level clears it after the running counts are updated.  The
+  // LDS executes one wavefront's instructions in order.
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    if (j >= nch) continue;   // the same for the whole workgroup
+    const bool valid = v0 + j * kWave + lane < V;
+    const unsigned d = (unsigned)lv[j] & (kSmallT - 1);   // levels of a valid graph are below kSmallT
+    if (valid) atomicOr(&lanes[w][d], 1ull << lane);
+    const unsigned long long peers = valid ? lanes[w][d] : 0ull;
+    const unsigned long long pp = peers & __ballot((pm >> j) & 1u);
+    const int r0 = __popcll(peers & lt), p0 = __popcll(pp & lt);
+    int a = 0, b = 0;
+    if (valid) {
+      a = cnt[0][w][d];
+      b = cnt[1][w][d];
+    }
+    rk[j] = (a + r0) | ((b + p0) << 16);
+    if (valid && r0 == 0) {   // one lane per level in this chunk
+      cnt[0][w][d] = a + __popcll(peers);
+      cnt[1][w][d] = b + __popcll(pp);
+      lanes[w][d] = 0ull;
+    }
+  }
+  __syncthreads();
+  // bases: thread l < kSmallT owns level l
+  int t0 = 0, t1 = 0, i0 = 0, i1 = 0;
+  if (tid < kSmallT) {
+#pragma unroll
+    for (int q = 0; q < kSmallWaves; ++q) {
+      t0 += cnt[0][q][tid];
+      t1 += cnt[1][q][tid];
+    }
+    i0 = t0;
+    i1 = t1;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int x = __shfl_up(i0, o, kWave), y = __shfl_up(i1, o, kWave);
+      if (lane >= o) {
+        i0 += x;
+        i1 += y;
+      }
+    }
+    if (lane == kWave - 1) {
+      wsum[0][w] = i0;
+      wsum[1][w] = i1;
+    }
+  }
+  __syncthreads();
+  if (tid < kSmallT) {
+    int run0 = i0 - t0, run1 = i1 - t1;
+    for (int q = 0; q < w; ++q) {
+      run0 += wsum[0][q];
+      run1 += wsum[1][q];
+    }
+#pragma unroll
+    for (int q = 0; q < kSmallWaves; ++q) {
+      const int c0 = cnt[0][q][tid], c1 = cnt[1][q][tid];
+      cnt[0][q][tid] = run0;
+      cnt[1][q][tid] = run1;
+      run0 += c0;
+      run1 += c1;
+    }
+  }
+  __syncthreads();
+  // every position into LDS; this workgroup's chunk keeps its own
+  int myp = -1, mypp = -1;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int v = v0 + j * kWave + lane;
+    if (j < nch && v < V) {
+      const int d = lv[j] & (kSmallT - 1);
+      const int dst = cnt[0][w][d] + (rk[j] & 0xFFFF);
+      posl[v] = dst;
+      if (j == g) {
+        myp = dst;
+        mypp = cnt[1][w][d] + (rk[j] >> 16);
+      }
+    }
+  }
+  __syncthreads();
+  // 5-6. outputs of chunk g: order, pos, pull_list, and the remap
+  if (vg >= V || (unsigned)myp >= (unsigned)V) return;   // the latter only if the graph was not valid
+  order[myp] = vg;
+  pos[vg] = myp;
+  if (pl >= 0 && (unsigned)mypp < (unsigned)V) pull_list[mypp] = myp;
+  child_pos[(size_t)myp * N] = a0 >= 0 && a0 < V ? posl[a0] : -1;
+  if (N == 2) child_pos[(size_t)myp * N + 1] = a1 >= 0 && a1 < V ? posl[a1] : -1;
+  parent_pos[myp] = pa >= 0 && pa < V ? posl[pa] : -1;
+  pull_pos[myp] = pl;
+  push_pos[myp] = ps;
+}
+
+// -------------------------------------------------------------------------
 // 4. staging for the single device->host copy: done by the offsets scan
 // -------------------------------------------------------------------------
 
@@ -454,6 +899,34 @@ cavs_status radix_sort(cavs_ctx* ctx, const int* keys_in, const int* vals_in, in
   return CAVS_OK;
 }
 
+// The validation result, T, the counts and the level offsets from the host
+// stage; offsets past the first cap come from level_offsets on the device.
+cavs_status read_stage(cavs_ctx* ctx, cavs_sched* s, int cap, const int* level_offsets) {
+  const int* h = ctx->host_stage;
+  if (h[F_RANGE]) return fail(ctx, CAVS_ERR_RANGE, "an index array holds an out-of-range value");
+  if (h[F_MULTI]) return fail(ctx, CAVS_ERR_MULTIPARENT, "a vertex is a child more than once");
+  if (h[F_DUP]) return fail(ctx, CAVS_ERR_DUP_PULL, "two vertices pull the same input row");
+  if (h[F_MISMATCH] || h[F_LINKS] != h[F_WITHPARENT])
+    return fail(ctx, CAVS_ERR_MISMATCH, "child[] and parent[] disagree");
+  if (h[F_CYCLE]) return fail(ctx, CAVS_ERR_CYCLE, "the child links contain a cycle");
+  const int T = h[F_T];
+  s->T = T;
+  s->n_pull = h[F_NPULL];
+  s->n_labelled = h[F_LABELLED];
+  s->n_leaf_noinput = h[F_LEAF_NOIN];
+  s->n_inner_input = h[F_INNER_IN];
+  const int n = T + 1 < cap ? T + 1 : cap;
+  for (int i = 0; i < n; ++i) s->level_offsets_host[i] = h[kStageHead + i];
+  if (T + 1 > cap) {
+    if (!level_offsets) return fail(ctx, CAVS_ERR_HIP, "level offsets past the stage");
+    CAVS_HIP_CHECK(ctx, hipMemcpyAsync(s->level_offsets_host + cap, level_offsets + cap,
+                                       sizeof(int) * (size_t)(T + 1 - cap),
+                                       hipMemcpyDeviceToHost, ctx->stream));
+    CAVS_HIP_CHECK(ctx, hipStreamSynchronize(ctx->stream));
+  }
+  return CAVS_OK;
+}
+
 }  // namespace
 
 size_t schedule_ws_bytes(int32_t V, int32_t N, int32_t n_x) {
@@ -493,6 +966,25 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
     return CAVS_OK;
   }
 
+  if (V <= kSmallV && n_x <= kSmallNx) {
+    CAVS_LAUNCH("k_sched_small_levels", k_sched_small_levels, dim3(1), dim3(kSmallThreads), 0, st,
+                V, N, n_x, g->n_push, g->child, g->parent, g->pull_idx, g->push_idx, s->level,
+                s->level_offsets, stage);
+    CAVS_LAUNCH_CHECK(ctx);
+    CAVS_HIP_CHECK(ctx, hipMemcpyAsync(ctx->host_stage, stage, sizeof(int) * kSmallStageInts,
+                                       hipMemcpyDeviceToHost, st));
+    CAVS_HIP_CHECK(ctx, hipEventRecord(ctx->stage_ready, st));
+    // enqueued before the host has seen the stage: it checks the flags itself
+    const int chunks = cdiv(cdiv(V, kSmallWaves), kWave);
+    CAVS_LAUNCH("k_sched_small_sort", k_sched_small_sort, dim3(chunks), dim3(kSmallThreads), 0, st, V,
+                N, g->child, g->parent, g->pull_idx, g->push_idx, (const int*)s->level,
+                (const int*)stage, s->order, s->pos, s->child_pos, s->parent_pos, s->pull_pos,
+                s->push_pos, s->pull_list);
+    CAVS_LAUNCH_CHECK(ctx);
+    CAVS_HIP_CHECK(ctx, hipEventSynchronize(ctx->stage_ready));
+    if (!ctx->host_stage[F_FALLBACK]) return read_stage(ctx, s, kSmallT + 1, nullptr);
+  }
+
   const int nb = cdiv(V, 256);
   const long zero_ints = (long)(L.zero_end / sizeof(int));
   CAVS_LAUNCH("k_sched_init", k_sched_init, dim3(cdiv(zero_ints > V ? zero_ints : V, 256)),
@@ -529,28 +1021,10 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   cavs_status r = sort_and_remap(1);
   if (r != CAVS_OK) return r;
   CAVS_HIP_CHECK(ctx, hipEventSynchronize(ctx->stage_ready));
-  const int* h = ctx->host_stage;
-  if (h[F_RANGE]) return fail(ctx, CAVS_ERR_RANGE, "an index array holds an out-of-range value");
-  if (h[F_MULTI]) return fail(ctx, CAVS_ERR_MULTIPARENT, "a vertex is a child more than once");
-  if (h[F_DUP]) return fail(ctx, CAVS_ERR_DUP_PULL, "two vertices pull the same input row");
-  if (h[F_MISMATCH] || h[F_LINKS] != h[F_WITHPARENT])
-    return fail(ctx, CAVS_ERR_MISMATCH, "child[] and parent[] disagree");
-  if (h[F_CYCLE]) return fail(ctx, CAVS_ERR_CYCLE, "the child links contain a cycle");
-  const int T = h[F_T];
-  s->T = T;
-  s->n_pull = h[F_NPULL];
-  s->n_labelled = h[F_LABELLED];
-  s->n_leaf_noinput = h[F_LEAF_NOIN];
-  s->n_inner_input = h[F_INNER_IN];
-  int n = T + 1 < cap ? T + 1 : cap;
-  for (int i = 0; i < n; ++i) s->level_offsets_host[i] = h[kStageHead + i];
-  if (T + 1 > cap) {
-    CAVS_HIP_CHECK(ctx, hipMemcpyAsync(s->level_offsets_host + cap, s->level_offsets + cap,
-                                       sizeof(int) * (size_t)(T + 1 - cap),
-                                       hipMemcpyDeviceToHost, st));
-    CAVS_HIP_CHECK(ctx, hipStreamSynchronize(st));
-  }
+  r = read_stage(ctx, s, cap, s->level_offsets);
+  if (r != CAVS_OK) return r;
   // levels lie in [0, T): enough 8-bit digits for T - 1
+  const int T = s->T;
   int passes = 1;
   while (passes < 4 && ((long)(T > 0 ? T - 1 : 0) >> (8 * passes)) > 0) ++passes;
   return passes > 1 ? sort_and_remap(passes) : CAVS_OK;

@@ -97,6 +97,46 @@ def test_schedule_bit_exact_benchmark_shapes(ctx, maker):
     _compare_schedule(got, want)
 
 
+def _forest_of_size(V, seed):
+    """Random binary trees topped up with single-vertex trees to exactly V vertices."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    trees, n = [], 0
+    while True:
+        t = W.random_split_tree(int(rng.integers(2, 80)), rng)
+        if n + len(t) > V:
+            break
+        trees.append(t)
+        n += len(t)
+    trees += [W.chain(1)] * (V - n)
+    wl = W.make_workload("forest%d" % V, trees, N=2, D=4, H=64, C=5, rng=rng, shuffle_ids=True)
+    assert wl.V == V
+    return wl
+
+
+# 16384 vertices is the most the one-workgroup scheduler takes; one more goes
+# through the multi-launch path
+@pytest.mark.parametrize("V", [16384, 16385])
+def test_schedule_bit_exact_at_one_workgroup_limit(ctx, V):
+    wl = _forest_of_size(V, V)
+    print("schedule V=%d" % V, flush=True)
+    _compare_schedule(_gpu_schedule(ctx, wl), oracle.schedule(wl.child, wl.parent, wl.pull_idx,
+                                                              wl.push_idx))
+
+
+def test_schedule_bit_exact_many_input_rows(ctx):
+    # input row ids spread over 300000 rows (more than the one-workgroup
+    # scheduler tracks), so a small batch also takes the multi-launch path
+    wl = _forest(3)
+    pull = np.where(wl.pull_idx >= 0, wl.pull_idx * 250 + 11, -1).astype(np.int32)
+    n_x = 300000
+    assert pull.max() < n_x
+    dev = ctx.torch_device
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+    got = B.schedule(ctx, t(wl.child), t(wl.parent), t(pull), t(wl.push_idx), n_x=n_x,
+                     n_push=wl.n_push).host()
+    _compare_schedule(got, oracle.schedule(wl.child, wl.parent, pull, wl.push_idx))
+
+
 def _raw_schedule_status(ctx, child, parent, pull=None, push=None, n_x=0, n_push=0):
     dev = ctx.torch_device
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
@@ -108,7 +148,9 @@ def _raw_schedule_status(ctx, child, parent, pull=None, push=None, n_x=0, n_push
         return e.status
 
 
-def test_schedule_rejects_invalid_graphs(ctx):
+# pad > 0 appends isolated vertices, past the one-workgroup scheduler's limit
+@pytest.mark.parametrize("pad", [0, 16400])
+def test_schedule_rejects_invalid_graphs(ctx, pad):
     child = np.array([[-1, -1], [-1, -1], [0, 1]])
     parent = np.array([2, 2, -1])
     cases = []
@@ -126,6 +168,11 @@ def test_schedule_rejects_invalid_graphs(ctx):
     cases.append((child, parent, None, np.array([0, 5, -1]), 0, 5))
     cases.append((np.array([[-1, -1], [0, 7], [0, 1]]), parent, None, None, 0, 0))
     for i, (c, p, pl, ps, nx, npush) in enumerate(cases):
+        if pad:
+            c = np.vstack([c, -np.ones((pad, c.shape[1]), np.int64)])
+            p = np.concatenate([p, -np.ones(pad, np.int64)])
+            pl = None if pl is None else np.concatenate([pl, -np.ones(pad, np.int64)])
+            ps = None if ps is None else np.concatenate([ps, -np.ones(pad, np.int64)])
         want = oracle.validate(c, p, pl, nx, ps, npush)
         got = _raw_schedule_status(ctx, c, p, pl, ps, nx, npush)
         assert want != oracle.OK
