@@ -662,8 +662,9 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
     if (w >= KW) {
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) {
-        const int p = row0 + 16 * tr + 4 * gq + i;
-        if (p < rowend) lstm_fwd_pre<NCH>(n, p, u0 + r, pre[tr]);
+        // rows past the level read its last row (unused), so the loads
+        // are unconditional
+        lstm_fwd_pre<NCH>(n, min(row0 + 16 * tr + 4 * gq + i, rowend - 1), u0 + r, pre[tr]);
       }
     }
     __syncthreads();
@@ -831,8 +832,9 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     if (w >= KW) {
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) {
-        const int p = row0 + 16 * tr + 4 * gq + i;
-        if (p < rowend) lstm_bwd_pre<NCH>(n, p, n0 + r, pre[tr]);
+        // rows past the level read its last row (unused), so the loads
+        // are unconditional
+        lstm_bwd_pre<NCH>(n, min(row0 + 16 * tr + 4 * gq + i, rowend - 1), n0 + r, pre[tr]);
       }
     }
     __syncthreads();

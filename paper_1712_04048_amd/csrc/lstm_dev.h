@@ -20,29 +20,39 @@ struct FwdPre {
   int cp[NCH], v, pulled;
 };
 
+// Every load is unconditional (an absent child reads row 0, a position that
+// pulls nothing its own unused row of P; both are masked by selects): a
+// loaded value merged with a constant on a branch makes the compiler wait
+// for that load on its own.
 template <int NCH>
 __device__ __forceinline__ void lstm_fwd_pre(const Net& n, int p, int j, FwdPre<NCH>& q) {
   const int H = n.H;
   const int pr = n.pull_pos[p];
+  int cp[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) cp[k] = n.child_pos[(size_t)p * NCH + k];
+  q.v = n.order[p];
+  const float bi = n.b[G_I * H + j], bo = n.b[G_O * H + j], bu = n.b[G_U * H + j];
+  const float bf = n.b[G_F * H + j];
+  const float* Pp = n.P + (size_t)p * 4 * H;
+  const float pi = Pp[G_I * H + j], po = Pp[G_O * H + j], pu = Pp[G_U * H + j];
+  const float pf = Pp[G_F * H + j];
+  float cc[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) cc[k] = n.Cs[(size_t)max(cp[k], 0) * H + j];
   q.pulled = pr >= 0;
-  q.bi = n.b[G_I * H + j];
-  q.bo = n.b[G_O * H + j];
-  q.bu = n.b[G_U * H + j];
-  q.fb = n.b[G_F * H + j];
-  q.pi = q.po = q.pu = 0.f;
-  if (pr >= 0) {
-    const float* Pp = n.P + (size_t)p * 4 * H;
-    q.pi = Pp[G_I * H + j];
-    q.po = Pp[G_O * H + j];
-    q.pu = Pp[G_U * H + j];
-    q.fb += Pp[G_F * H + j];
-  }
+  q.bi = bi;
+  q.bo = bo;
+  q.bu = bu;
+  q.pi = q.pulled ? pi : 0.f;
+  q.po = q.pulled ? po : 0.f;
+  q.pu = q.pulled ? pu : 0.f;
+  q.fb = q.pulled ? bf + pf : bf;
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
-    q.cp[k] = n.child_pos[(size_t)p * NCH + k];
-    q.cc[k] = q.cp[k] >= 0 ? n.Cs[(size_t)q.cp[k] * H + j] : 0.f;
+    q.cp[k] = cp[k];
+    q.cc[k] = cp[k] >= 0 ? cc[k] : 0.f;
   }
-  q.v = n.order[p];
 }
 
 // Gates, cell update and the scatter of (c, h) for position p, unit j, from
@@ -264,6 +274,36 @@ __device__ __forceinline__ void lstm_gates_elem(const Net& n, int p, int j, floa
   lstm_gates_fin<NCH>(n, p, j, gh, q);
 }
 
+// The same reads with every load unconditional (absent children read row
+// 0 and are masked by selects; see lstm_fwd_pre), including dL/dc from the
+// parent, for the small levels' fused epilogue.
+template <int NCH>
+__device__ __forceinline__ void lstm_gates_pre_all(const Net& n, int p, int j, GatePre<NCH>& q) {
+  const int H = n.H;
+  const float* g = n.Gs + (size_t)p * n.GW;
+  q.lg = n.dHL[(size_t)p * H + j];
+  q.gcin = n.dCp[(size_t)p * H + j];
+  q.ig = g[j];
+  q.og = g[2 * H + j];
+  q.ug = g[3 * H + j];
+  q.c = n.Cs[(size_t)p * H + j];
+  int cp[NCH];
+  float fk[NCH], ck[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    cp[k] = n.child_pos[(size_t)p * NCH + k];
+    fk[k] = g[(k == 0 ? H : 4 * H) + j];
+  }
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) ck[k] = n.Cs[(size_t)max(cp[k], 0) * H + j];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    q.cp[k] = cp[k];
+    q.fk[k] = cp[k] >= 0 ? fk[k] : 0.f;
+    q.ck[k] = cp[k] >= 0 ? ck[k] : 0.f;
+  }
+}
+
 // Backward level epilogue for position p, unit col: child k receives
 // dL/dh_k = zh + zf_k.  p is the child's only parent, so that is the child's
 // whole dL/dh: a child at a position >= n.fuse_from (the small top levels)
@@ -278,11 +318,14 @@ struct BwdPre {
 
 template <int NCH>
 __device__ __forceinline__ void lstm_bwd_pre(const Net& n, int p, int col, BwdPre<NCH>& e) {
+  int cp[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) cp[k] = n.child_pos[(size_t)p * NCH + k];
+  // a child below fuse_from (or absent) reads row 0 here, unused
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
-    const int cp = n.child_pos[(size_t)p * NCH + k];
-    e.cp[k] = cp;
-    if (cp >= n.fuse_from) lstm_gates_pre<NCH>(n, cp, col, n.dCp[(size_t)cp * n.H + col], e.q[k]);
+    e.cp[k] = cp[k];
+    lstm_gates_pre_all<NCH>(n, cp[k] >= n.fuse_from ? cp[k] : 0, col, e.q[k]);
   }
 }
 
