@@ -39,7 +39,7 @@ namespace {
 
 // Workspace of forward + backward, all level-major (row = position).
 struct WsLayout {
-  size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bar, total;
+  size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bpart, bar, total;
   size_t part_floats;
 };
 
@@ -70,6 +70,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   L.dA = take(V * GW);
   L.part_floats = lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
   L.part = take(3 * L.part_floats);   // dU_iou, dU_f and dW_x split-K sums side by side
+  L.bpart = take(bias_part_floats(p->H, p->loss == CAVS_LOSS_CE ? p->C : 0));
   L.bar = take(256);
   L.total = o;
   return L;
@@ -355,6 +356,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   }
   Net n = make_net(p, s, in, ws, L);
   float* part = (float*)((char*)ws + L.part);
+  float* bpart = (float*)((char*)ws + L.bpart);
   const int* lo = s->level_offsets_host;
   const int T = s->T;
   const int off1 = T > 1 ? lo[1] : s->V;
@@ -385,9 +387,9 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
     lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
     if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
+    bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
-    bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);
   } else {
     for (int t = T - 1; t >= 0; --t) {
       const int M = lo[t + 1] - lo[t];
@@ -395,7 +397,9 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       if (t >= 1) fc_bwd_level(n, lo[t], M, str);
     }
     fc_dW(n, off1, g->dU, part, L.part_floats, str);
-    bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, part, L.part_floats, str);
+    SplitJobs jobs;
+    bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
+    reduce_split_jobs(jobs, str);
   }
   CAVS_LAUNCH_CHECK(ctx);
   return CAVS_OK;

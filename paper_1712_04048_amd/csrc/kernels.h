@@ -112,9 +112,10 @@ struct SplitJob {
   const float* part;
   float* dst;
   int S, Mo, No, ldd, col_off, gap_start, gap;
+  int kind;     // 0: float4 sums; 1: Mo = 1, any No, the S partial rows split over 16 wavefronts
 };
 struct SplitJobs {
-  static constexpr int kMax = 4;
+  static constexpr int kMax = 8;
   SplitJob j[kMax];
   int n = 0;
 };
@@ -132,9 +133,11 @@ void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
 void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);
 // column sums over positions [row0, row1) of the gate gradients -> db
 // db over rows [row0, row1) and, for the CE head, dW_s and db_s over all rows;
-// rows below lo1 are level 0 (no children).
+// rows below lo1 are level 0 (no children).  The per-chunk partial sums go
+// to `part` (bias_part_floats floats); their reduction is queued on `jobs`.
+size_t bias_part_floats(int H, int C);
 void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float* dWs, float* dbs,
-                     float* part, size_t part_floats, hipStream_t s);
+                     float* part, hipStream_t s, SplitJobs* jobs);
 size_t lazy_part_floats(int V, int D, int H, int N, int C);
 
 // ---------------------------------------------------------------------------

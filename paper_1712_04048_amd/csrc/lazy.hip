@@ -1006,16 +1006,37 @@ __global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, 
     }
 }
 
-// All pending split-K sums in one launch: blockIdx.y picks the job; each
-// thread adds four adjacent outputs (every job's No, ldd, col_off,
-// gap_start and gap are multiples of 4, checked on the host).
-__global__ void k_reduce_jobs(SplitJobs jobs) {
+// All pending split-K sums in one launch: blockIdx.y picks the job.  Kind 0:
+// each thread adds four adjacent outputs with float4 access (every such
+// job's No, ldd, col_off, gap_start and gap are multiples of 4, checked on
+// the host).  Kind 1 (column sums with many partial rows): see below.
+__global__ void __launch_bounds__(1024) k_reduce_jobs(SplitJobs jobs) {
   const SplitJob& J = jobs.j[blockIdx.y];
-  const long idx = 4 * ((long)blockIdx.x * 256 + threadIdx.x);
-  if (idx >= (long)J.Mo * J.No) return;
+  if (J.kind == 1) {
+    // 64 columns per block; wavefront y adds partial rows y, y + 16, ...,
+    // then the 16 sums are added in order
+    __shared__ float red[16][64];
+    const int x = threadIdx.x & 63, y = threadIdx.x >> 6;
+    const int col = blockIdx.x * 64 + x;
+    if (blockIdx.x * 64 >= J.No) return;   // the whole block
+    float t = 0.f;
+    if (col < J.No)
+      for (int k = y; k < J.S; k += 16) t += J.part[(size_t)k * J.No + col];
+    red[y][x] = t;
+    __syncthreads();
+    if (y != 0 || col >= J.No) return;
+    float u = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) u += red[k][x];
+    J.dst[col] = u;
+    return;
+  }
+  const long idx = 4 * ((long)blockIdx.x * 1024 + threadIdx.x);
+  const long total = (long)J.Mo * J.No;
+  if (idx >= total) return;
+  const size_t stride = (size_t)total;
   const int m = (int)(idx / J.No), nn = (int)(idx % J.No);
   float4 s = f4zero();
-  const size_t stride = (size_t)J.Mo * J.No;
 #pragma unroll 4
   for (int k = 0; k < J.S; ++k) {
     const float4 v = ldg4(J.part + k * stride + idx);
@@ -1103,17 +1124,21 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
 // (lazy batching, Section 3.4): db sums dA (LSTM: 4H columns with
 // f = f_0 + f_1; FC: H columns) over rows [row0, row1); dW_s[j][c] sums
 // h_j dZ_c and db_s[c] sums dZ_c over all rows.  One launch writes per-chunk
-// partials (each thread: 4 adjacent columns, its chunk's rows in order), a
-// second adds the chunks in order, so the result is deterministic.
+// partials (each thread: 4 adjacent columns, its chunk's rows in order); the
+// split-K reduction launch adds the chunks in order, so the result is
+// deterministic.
 constexpr int kBiasChunks = 256;
 
+// Partial sums of chunk y: db columns at part[y * wA + c], dW_s at
+// part[nchunk * wA + y * H C + j C + c], db_s at
+// part[nchunk * (wA + H C) + y C + c]: three arrays whose chunk-major rows
+// are each one split-K reduction job.
 template <int CP4>
 __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, int lo1,
-                                                   int rows_per, int bxA, int wA, int W,
+                                                   int rows_per, int bxA, int wA, int nchunk,
                                                    float* __restrict__ part) {
   const int H = n.H;
   const int lo = blockIdx.y * rows_per, hi = min(n.V, lo + rows_per);
-  float* out = part + (size_t)blockIdx.y * W;
   if ((int)blockIdx.x < bxA) {
     const int c = 4 * (blockIdx.x * 256 + threadIdx.x);
     if (c >= wA) return;
@@ -1141,7 +1166,7 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
         s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
       }
     }
-    *reinterpret_cast<float4*>(out + c) = s;
+    *reinterpret_cast<float4*>(part + (size_t)blockIdx.y * wA + c) = s;
     return;
   }
   // head: columns wA + j*C + c (dW_s row-major), then wA + H*C + c (db_s);
@@ -1176,38 +1201,19 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
       }
     }
   }
-  float* o = out + wA + (size_t)j * C;
+  const size_t HC = (size_t)H * C;
+  float* o = part + (size_t)nchunk * wA + blockIdx.y * HC + (size_t)j * C;
 #pragma unroll
   for (int e = 0; e < 4; ++e)
 #pragma unroll
     for (int c = 0; c < CP; ++c)
       if (c < C) o[e * C + c] = acc[e][c];
-  if (j == 0)
+  if (j == 0) {
+    float* ob = part + (size_t)nchunk * (wA + HC) + (size_t)blockIdx.y * C;
 #pragma unroll
     for (int c = 0; c < CP; ++c)
-      if (c < C) out[wA + H * C + c] = zs[c];
-}
-
-// 16 wavefronts per block: wavefront y adds chunks y, y + 16, ... of 64
-// columns; the 16 sums are then added in order.
-__global__ void __launch_bounds__(1024) k_bias_reduce(const float* __restrict__ part, int nchunk,
-                                                      int W, int wA, int HC, float* db,
-                                                      float* dWs, float* dbs) {
-  __shared__ float red[16][64];
-  const int x = threadIdx.x & 63, y = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + x;
-  float s = 0.f;
-  if (col < W)
-    for (int b = y; b < nchunk; b += 16) s += part[(size_t)b * W + col];
-  red[y][x] = s;
-  __syncthreads();
-  if (y != 0 || col >= W) return;
-  float t = 0.f;
-#pragma unroll
-  for (int k = 0; k < 16; ++k) t += red[k][x];
-  if (col < wA) db[col] = t;
-  else if (col < wA + HC) dWs[col - wA] = t;
-  else dbs[col - wA - HC] = t;
+      if (c < C) ob[c] = zs[c];
+  }
 }
 
 // ---------------------------------------------------------------- loss
@@ -1452,10 +1458,13 @@ void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s) {
   if (jobs.n == 0) return;
   long most = 0;
   for (int k = 0; k < jobs.n; ++k) {
-    const long e = (long)jobs.j[k].Mo * jobs.j[k].No;
+    const SplitJob& J = jobs.j[k];
+    // elements per block: 4096 (four per thread), or 64 columns of a kind-1 job
+    const long e = J.kind == 1 ? (long)cdiv(J.No, 64) * 4096 : (long)J.Mo * J.No;
     most = e > most ? e : most;
   }
-  CAVS_LAUNCH("k_reduce_jobs", k_reduce_jobs, dim3(cdiv(most, 1024), jobs.n), dim3(256), 0, s, jobs);
+  CAVS_LAUNCH("k_reduce_jobs", k_reduce_jobs, dim3(cdiv(most, 4096), jobs.n), dim3(1024), 0, s,
+              jobs);
 }
 
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
@@ -1492,22 +1501,25 @@ void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, h
   }
 }
 
+size_t bias_part_floats(int H, int C) {
+  return (size_t)kBiasChunks * (4 * (size_t)H + (size_t)H * (C > 0 ? C : 0) + (C > 0 ? C : 0));
+}
+
 void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float* dWs, float* dbs,
-                     float* part, size_t part_floats, hipStream_t s) {
+                     float* part, hipStream_t s, SplitJobs* jobs) {
   const int wA = n.GW == n.H ? n.H : 4 * n.H;
   const bool head = n.loss == CAVS_LOSS_CE;
   const int HC = head ? n.H * n.C : 0;
-  const int W = wA + HC + (head ? n.C : 0);
   int nchunk = cdiv(n.V, 16);
   if (nchunk > kBiasChunks) nchunk = kBiasChunks;
   if (nchunk < 1) nchunk = 1;
-  while (nchunk > 1 && (size_t)nchunk * W > part_floats) --nchunk;
   const int rows_per = cdiv(n.V > 0 ? n.V : 1, nchunk);
   nchunk = cdiv(n.V > 0 ? n.V : 1, rows_per);
   const int bxA = cdiv(wA / 4, 256), bxB = head ? cdiv(n.H / 4, 256) : 0;
   const dim3 grid(bxA + bxB, nchunk);
   auto part_launch = [&](auto kern, const char* name) {
-    CAVS_LAUNCH(name, kern, grid, dim3(256), 0, s, n, row0, row1, lo1, rows_per, bxA, wA, W, part);
+    CAVS_LAUNCH(name, kern, grid, dim3(256), 0, s, n, row0, row1, lo1, rows_per, bxA, wA, nchunk,
+                part);
   };
   switch (head ? n.CP / 4 : 1) {
     case 1: part_launch(k_bias_part<1>, "k_bias_part<1>"); break;
@@ -1515,8 +1527,14 @@ void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float
     case 3: part_launch(k_bias_part<3>, "k_bias_part<3>"); break;
     default: part_launch(k_bias_part<4>, "k_bias_part<4>"); break;
   }
-  CAVS_LAUNCH("k_bias_reduce", k_bias_reduce, dim3(cdiv(W, 64)), dim3(1024), 0, s,
-              (const float*)part, nchunk, W, wA, HC, db, dWs, dbs);
+  auto queue = [&](const float* p, int No, float* dst) {
+    jobs->j[jobs->n++] = SplitJob{p, dst, nchunk, 1, No, No, 0, 1 << 30, 0, 1};
+  };
+  queue(part, wA, db);
+  if (head) {
+    queue(part + (size_t)nchunk * wA, HC, dWs);
+    queue(part + (size_t)nchunk * (wA + HC), n.C, dbs);
+  }
 }
 
 }  // namespace cavs
