@@ -1244,9 +1244,13 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
     for (int j = threadIdx.x; j < H; j += 64 * kLossWaves) n.zrow[j] = 0.f;
   const int cm = min(r, C - 1);
   const bool cval = r < C;
+  // loads unconditional (rows past V read row V-1, masked below), so that
+  // they issue together
   int q[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) q[i] = p0 + 4 * g + i < V ? n.push_pos[p0 + 4 * g + i] : -1;
+  for (int i = 0; i < 4; ++i) q[i] = n.push_pos[min(p0 + 4 * g + i, V - 1)];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = p0 + 4 * g + i < V ? q[i] : -1;
   const float bsc = n.bs[cm];
 
   const float* hrow = n.Hs + (size_t)min(p0 + r, V - 1) * H + 8 * g;
@@ -1308,8 +1312,9 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
     for (int u = 0; u < MB; ++u) {
       const float* wrow = n.Ws + (size_t)(min(b0 + NW * u, nb - 1) * 16 + r) * C;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) wb[u][t] = t < KT ? wrow[min(4 * t + g, C - 1)] : 0.f;
+      for (int t = 0; t < 4; ++t) wb[u][t] = wrow[min(4 * t + g, C - 1)];
     }
+    // classes past CP are never multiplied (t < KT below)
 #pragma unroll
     for (int u = 0; u < MB; ++u) {
       const int jb = b0 + NW * u;
