@@ -331,6 +331,7 @@ struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = 
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDUiou, 128, 256, 2>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDUiou, 64, 256, 3>";
+  static constexpr const char* kNameDl128n = "k_tn_dl<LdDUiou, 128, 128, 3>";
   struct Idx {
     int c0, c1;
   };
@@ -372,6 +373,7 @@ struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_f
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDUf, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDUf, 64, 256, 3>";
+  static constexpr const char* kNameDl128n = "k_tn_dl<LdDUf, 128, 128, 4>";
   struct Idx {
     int cp;
   };
@@ -408,6 +410,7 @@ struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDWx, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDWx, 64, 256, 3>";
+  static constexpr const char* kNameDl128n = "k_tn_dl<LdDWx, 128, 128, 4>";
   struct Idx {
     int p, row;
   };
@@ -449,6 +452,7 @@ struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdFCdW, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdFCdW, 64, 256, 3>";
+  static constexpr const char* kNameDl128n = "k_tn_dl<LdFCdW, 128, 128, 4>";
   struct Idx {
     int cp;
   };
@@ -1075,17 +1079,25 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
   if (!n.bf && ld.direct() && n.H % 256 == 0 && No % 256 == 0 && Mo % 4 == 0 && big < (1L << 31)) {
     const int pad128 = cdiv(Mo, 128) * 128 - Mo, pad64 = cdiv(Mo, 64) * 64 - Mo;
     const int BM = pad64 < pad128 ? 64 : 128;
-    const int tiles = (No / 256) * cdiv(Mo, BM);
+    // 128-wide column tiles where the 256-wide ones would be few (16 or
+    // less): half the K splits, so longer K ranges per workgroup and half the
+    // partial sums (measured on dU_f; with more tiles the wider tile's
+    // operand reuse wins)
+    const int BN = BM == 128 && (No / 256) * cdiv(Mo, BM) <= 16 ? 128 : 256;
+    const int tiles = (No / BN) * cdiv(Mo, BM);
     int S = 256 / tiles;
     S = S < 1 ? 1 : S;
     if (S > cdiv(Q, kBK)) S = cdiv(Q, kBK);
     while (S > 1 && (size_t)S * Mo * No > part_floats) --S;
     const int qchunk = cdiv(cdiv(Q, S), kBK) * kBK;
     S = cdiv(Q, qchunk);
-    const dim3 grid(No / 256, cdiv(Mo, BM), S);
+    const dim3 grid(No / BN, cdiv(Mo, BM), S);
     // ring depth: the deepest ring whose stages fit in 160 KB of LDS
-    constexpr int S128 = L::NA == 2 ? 2 : 3;
-    if (BM == 64)
+    constexpr int S128 = L::NA == 2 ? 2 : 3, S128n = L::NA == 2 ? 3 : 4;
+    if (BN == 128)
+      CAVS_LAUNCH(L::kNameDl128n, (k_tn_dl<L, 128, 128, S128n>), grid, dim3(512), 0, st, ld, Q,
+                  qchunk, Mo, No, part);
+    else if (BM == 64)
       CAVS_LAUNCH(L::kNameDl64, (k_tn_dl<L, 64, 256, 3>), grid, dim3(512), 0, st, ld, Q, qchunk,
                   Mo, No, part);
     else
