@@ -179,12 +179,16 @@ cavs_status cavs_create(cavs_ctx** out, int32_t device, void* hip_stream) {
   cavs_ctx* ctx = new cavs_ctx();
   ctx->device = device;
   ctx->stream = (hipStream_t)hip_stream;
+  // The host stage is coherent mapped memory: the scheduler's first kernel
+  // writes it directly (no device->host copy on the stream), and the host
+  // reads it once the event recorded after that kernel has completed.
   if (hipSetDevice(device) != hipSuccess ||
       hipHostMalloc((void**)&ctx->host_stage, sizeof(int32_t) * kHostStageInts,
-                    hipHostMallocDefault) != hipSuccess ||
+                    hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
+      hipHostGetDevicePointer((void**)&ctx->host_stage_dev, ctx->host_stage, 0) != hipSuccess ||
       hipEventCreateWithFlags(&ctx->stage_ready, hipEventDisableTiming) != hipSuccess) {
     if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
-  if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
+    if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
     delete ctx;
     return CAVS_ERR_HIP;
   }

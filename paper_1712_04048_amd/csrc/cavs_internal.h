@@ -20,7 +20,8 @@ struct cavs_timed_launch {
 struct cavs_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
-  int32_t* host_stage = nullptr;  // pinned, kHostStageInts entries
+  int32_t* host_stage = nullptr;  // pinned, kHostStageInts entries (coherent, mapped)
+  int32_t* host_stage_dev = nullptr;  // the same memory as the device sees it
   std::string err;
   bool timing = false;
   std::vector<cavs_timed_launch> timed;   // pending records

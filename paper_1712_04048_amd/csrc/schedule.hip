@@ -406,9 +406,10 @@ constexpr int kSmallT = 256;
 constexpr int kSmallThreads = 1024;
 constexpr int kSmallPer = kSmallV / kSmallThreads;
 constexpr int kSmallWaves = kSmallThreads / kWave;
-constexpr int kSmallStageInts = kStageHead + kSmallT + 1;
 
-// Steps 1-4.  Vertex v belongs to thread v % 1024 for the validation.  The
+// Steps 1-4.  The stage (flags, then offsets) goes both to `stage` in device
+// memory, for the sort kernel, and to `hstage`, the host's coherent mapped
+// copy.  Vertex v belongs to thread v % 1024 for the validation.  The
 // levels are then found level-synchronously instead of by walks: round t
 // takes the list of level-t vertices, sets their level and counts each one
 // off its parent's number of children not yet reached; a parent whose count
@@ -421,7 +422,7 @@ __global__ void __launch_bounds__(kSmallThreads) k_sched_small_levels(
     int V, int N, int n_x, int n_push, const int* __restrict__ child,
     const int* __restrict__ parent, const int* __restrict__ pull_idx,
     const int* __restrict__ push_idx, int* __restrict__ level, int* __restrict__ level_offsets,
-    int* __restrict__ stage) {
+    int* __restrict__ stage, int* __restrict__ hstage) {
   __shared__ short par[kSmallV];              // parent, or -1, or -2 when out of range
   __shared__ unsigned nrem[kSmallV / 4];      // one byte per vertex: children not yet reached
   __shared__ int lists[kSmallV];              // two level lists of int16, or reference counts
@@ -672,11 +673,13 @@ __global__ void __launch_bounds__(kSmallThreads) k_sched_small_levels(
       if (idx <= T && idx <= V) {
         level_offsets[idx] = run;
         stage[kStageHead + idx] = run;
+        hstage[kStageHead + idx] = run;
       }
       run += a[j];
     }
   } else if (tid < kWave + F_COUNT) {
     stage[tid - kWave] = fl[tid - kWave];
+    hstage[tid - kWave] = fl[tid - kWave];
   }
 }
 
@@ -969,10 +972,8 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   if (V <= kSmallV && n_x <= kSmallNx) {
     CAVS_LAUNCH("k_sched_small_levels", k_sched_small_levels, dim3(1), dim3(kSmallThreads), 0, st,
                 V, N, n_x, g->n_push, g->child, g->parent, g->pull_idx, g->push_idx, s->level,
-                s->level_offsets, stage);
+                s->level_offsets, stage, ctx->host_stage_dev);
     CAVS_LAUNCH_CHECK(ctx);
-    CAVS_HIP_CHECK(ctx, hipMemcpyAsync(ctx->host_stage, stage, sizeof(int) * kSmallStageInts,
-                                       hipMemcpyDeviceToHost, st));
     CAVS_HIP_CHECK(ctx, hipEventRecord(ctx->stage_ready, st));
     // enqueued before the host has seen the stage: it checks the flags itself
     const int chunks = cdiv(cdiv(V, kSmallWaves), kWave);
