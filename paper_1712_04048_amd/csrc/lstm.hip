@@ -58,16 +58,76 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int sk
 }
 
 // dA of every position of a level below n.fuse_from (dL/dh, dL/dc stored by
-// the parent; zero at a root).
-__global__ void __launch_bounds__(256) k_lstm_bwd_gates(Net n, int off, int M) {
+// the parent; zero at a root), four consecutive units per thread with
+// 16-byte accesses.  LEAF:
+// the level is the leaves (no children).  Loads are unconditional (a root's
+// parent terms and an absent child's state read stale rows, masked by
+// selects), and each element's arithmetic is that of lstm_gates_fin.
+template <int NCH, bool LEAF>
+__global__ void __launch_bounds__(256) k_lstm_bwd_gates4(Net n, int off, int M) {
+  const int H = n.H, Hq = H / 4;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)M * n.H) return;
-  const int p = off + (int)(idx / n.H), j = (int)(idx % n.H);
+  if (idx >= (long)M * Hq) return;
+  const int p = off + (int)(idx / Hq), j0 = 4 * (int)(idx % Hq);
+  const size_t row = (size_t)p * H + j0;
   const bool root = n.parent_pos[p] < 0;
-  const float gh = root ? 0.f : n.dHp[(size_t)p * n.H + j];
-  const float gc = root ? 0.f : n.dCp[(size_t)p * n.H + j];
-  if (n.N == 2) lstm_gates_elem<2>(n, p, j, gh, gc);
-  else lstm_gates_elem<1>(n, p, j, gh, gc);
+  const float* g = n.Gs + (size_t)p * n.GW + j0;
+  const float4 ig4 = ldg4(g), og4 = ldg4(g + 2 * H), ug4 = ldg4(g + 3 * H);
+  const float4 c4 = ldg4(n.Cs + row), lg4 = ldg4(n.dHL + row);
+  const float4 gh4 = ldg4(n.dHp + row), gi4 = ldg4(n.dCp + row);
+  int cp[NCH];
+  float4 fk4[NCH], ck4[NCH];
+  if constexpr (!LEAF) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) cp[k] = n.child_pos[(size_t)p * NCH + k];
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      fk4[k] = ldg4(g + (k == 0 ? H : 4 * H));
+      ck4[k] = ldg4(n.Cs + (size_t)max(cp[k], 0) * H + j0);
+    }
+  }
+  const float ig[4] = {ig4.x, ig4.y, ig4.z, ig4.w}, og[4] = {og4.x, og4.y, og4.z, og4.w};
+  const float ug[4] = {ug4.x, ug4.y, ug4.z, ug4.w}, cc[4] = {c4.x, c4.y, c4.z, c4.w};
+  const float lg[4] = {lg4.x, lg4.y, lg4.z, lg4.w};
+  const float ghp[4] = {gh4.x, gh4.y, gh4.z, gh4.w}, gci[4] = {gi4.x, gi4.y, gi4.z, gi4.w};
+  float di[4], dO[4], du[4], df[NCH][4], dc[NCH][4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float gh = (root ? 0.f : ghp[e]) + lg[e];
+    const float tau = tanh_(cc[e]);
+    dO[e] = gh * tau * og[e] * (1.f - og[e]);
+    const float gc = (root ? 0.f : gci[e]) + gh * og[e] * (1.f - tau * tau);
+    di[e] = gc * ug[e] * ig[e] * (1.f - ig[e]);
+    du[e] = gc * ig[e] * (1.f - ug[e] * ug[e]);
+    if constexpr (!LEAF) {
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) {
+        const float fk[4] = {fk4[k].x, fk4[k].y, fk4[k].z, fk4[k].w};
+        const float ck[4] = {ck4[k].x, ck4[k].y, ck4[k].z, ck4[k].w};
+        df[k][e] = cp[k] >= 0 ? gc * ck[e] * fk[e] * (1.f - fk[e]) : 0.f;
+        dc[k][e] = gc * fk[e];
+      }
+    }
+  }
+  auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
+  float* da = n.dA + (size_t)p * n.GW + j0;
+  st4(da, f4(di));
+  st4(da + 2 * H, f4(dO));
+  st4(da + 3 * H, f4(du));
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const bool has = !LEAF && cp[k] >= 0;
+    if (has || p >= n.f_unread_below) {
+      float z[4] = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (!LEAF) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z[e] = df[k][e];
+      }
+      st4(da + (k == 0 ? H : 4 * H), f4(z));
+    }
+    if constexpr (!LEAF)
+      if (has) st4(n.dCp + (size_t)cp[k] * H + j0, f4(dc[k]));
+  }
 }
 
 // Roots at positions >= n.fuse_from: one workgroup per position (the others
@@ -1016,8 +1076,19 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates", off, M, k_lstm_bwd_gates, dim3(cdiv((long)M * n.H, 256)),
-                   dim3(256), 0, s, n, off, M);
+  // level 0 (off == 0) holds the leaves, which have no children
+  const dim3 g4(cdiv((long)M * (n.H / 4), 256));
+#define CAVS_G4(NCH, LEAF)                                                                   \
+  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates4", off, M, (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), \
+                   0, s, n, off, M)
+  if (n.N == 2) {
+    if (off == 0) CAVS_G4(2, true);
+    else CAVS_G4(2, false);
+  } else {
+    if (off == 0) CAVS_G4(1, true);
+    else CAVS_G4(1, false);
+  }
+#undef CAVS_G4
 }
 
 void lstm_bwd_roots(const Net& n, hipStream_t s) {
