@@ -56,7 +56,7 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         return float(np.sum(2.0 * c * H * H)), 0.0
     if name == "k_lstm_leaf":          # reads 3 columns of P, writes h, c, 5 gates, h_out, c_out
         return 0.0, rows * H * 4.0 * 12
-    if name in ("k_lstm_bwd_gates", "k_lstm_bwd_gates4"):  # reads dh, dc, 3 gates, c (+ f_k, c_k per child),
+    if name.startswith("k_lstm_bwd_gates"):  # reads dh, dc, 3 gates, c (+ f_k, c_k per child),
         return 0.0, float(np.sum(H * 4.0 * (6 + (3 + N) + 3 * c)))  # writes dA (+ dc_k)
     inner = nc > 0
     lazy = {

@@ -1079,8 +1079,8 @@ void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   // level 0 (off == 0) holds the leaves, which have no children
   const dim3 g4(cdiv((long)M * (n.H / 4), 256));
 #define CAVS_G4(NCH, LEAF)                                                                   \
-  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates4", off, M, (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), \
-                   0, s, n, off, M)
+  CAVS_LAUNCH_ROWS("k_lstm_bwd_gates4<" #NCH ", " #LEAF ">", off, M,                          \
+                   (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), 0, s, n, off, M)
   if (n.N == 2) {
     if (off == 0) CAVS_G4(2, true);
     else CAVS_G4(2, false);
