@@ -902,6 +902,16 @@ cavs_status radix_sort(cavs_ctx* ctx, const int* keys_in, const int* vals_in, in
   return CAVS_OK;
 }
 
+// Waits for the stage by polling the event: the stage is a few hundred bytes
+// that the host needs before it can enqueue the forward pass, and a blocking
+// wait adds the scheduler's wake-up latency to every step.
+hipError_t wait_stage(cavs_ctx* ctx) {
+  hipError_t e;
+  while ((e = hipEventQuery(ctx->stage_ready)) == hipErrorNotReady) {
+  }
+  return e;
+}
+
 // The validation result, T, the counts and the level offsets from the host
 // stage; offsets past the first cap come from level_offsets on the device.
 cavs_status read_stage(cavs_ctx* ctx, cavs_sched* s, int cap, const int* level_offsets) {
@@ -982,7 +992,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
                 (const int*)stage, s->order, s->pos, s->child_pos, s->parent_pos, s->pull_pos,
                 s->push_pos, s->pull_list);
     CAVS_LAUNCH_CHECK(ctx);
-    CAVS_HIP_CHECK(ctx, hipEventSynchronize(ctx->stage_ready));
+    CAVS_HIP_CHECK(ctx, wait_stage(ctx));
     if (!ctx->host_stage[F_FALLBACK]) return read_stage(ctx, s, kSmallT + 1, nullptr);
   }
 
@@ -1021,7 +1031,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   };
   cavs_status r = sort_and_remap(1);
   if (r != CAVS_OK) return r;
-  CAVS_HIP_CHECK(ctx, hipEventSynchronize(ctx->stage_ready));
+  CAVS_HIP_CHECK(ctx, wait_stage(ctx));
   r = read_stage(ctx, s, cap, s->level_offsets);
   if (r != CAVS_OK) return r;
   // levels lie in [0, T): enough 8-bit digits for T - 1
