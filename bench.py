@@ -183,6 +183,29 @@ def main():
     torch.cuda.synchronize()
     fwdbwd_ms = e0.elapsed_time(e1) / args.steps
 
+    # inference (cavs_infer: the forward keeping nothing for a backward) beside
+    # the training forward alone; whole inference steps include the schedule
+    batch.infer()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        batch.forward()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fwd_ms = e0.elapsed_time(e1) / args.steps
+    e0.record(stream)
+    for _ in range(args.steps):
+        batch.infer()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    infer_ms = e0.elapsed_time(e1) / args.steps
+    t3 = time.perf_counter()
+    for _ in range(args.steps):
+        batch.schedule()
+        batch.infer()
+    torch.cuda.synchronize()
+    infer_step_ms = (time.perf_counter() - t3) * 1e3 / args.steps
+
     # per-kernel durations: the same steps again with per-launch HIP events
     ctx.timing(True)
     for _ in range(args.steps):
@@ -269,6 +292,11 @@ def main():
         "schedule_ms": round(sched_ms, 4),
         "fwd_bwd_ms": round(fwdbwd_ms, 4),
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
+        "inference": {"value": wl.V / (infer_step_ms * 1e-3), "unit": "vertices/s",
+                      "step": "cavs_schedule + cavs_infer", "ms_per_step": round(infer_step_ms, 4),
+                      "infer_ms": round(infer_ms, 4), "train_forward_ms": round(fwd_ms, 4),
+                      "workspace_mb": round(batch.ws_infer.numel() / 2 ** 20, 1),
+                      "train_workspace_mb": round(batch.ws.numel() / 2 ** 20, 1)},
         "whole_step_tflops": round(total_flops / (wall_ms * 1e-3) / 1e12, 2),
         "algorithmic_gflop_per_step": round(total_flops / 1e9, 3),
         "kernels": kernels,

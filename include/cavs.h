@@ -15,7 +15,9 @@
  *   cavs_forward   -- F over every task in order, then the lazily batched
  *                     push / loss head (Section 3.5);
  *   cavs_backward  -- dF over the tasks in reverse order, then the lazily
- *                     batched parameter-gradient products (Section 3.5).
+ *                     batched parameter-gradient products (Section 3.5);
+ *   cavs_infer     -- the forward alone, keeping nothing for a backward
+ *                     (inference, timed apart from training in Table 3).
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless marked (host).  Every device buffer
@@ -197,6 +199,20 @@ size_t cavs_workspace_bytes(const cavs_params* params, const cavs_sched* sched);
 cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* params, const cavs_sched* sched,
                          const cavs_inputs* inputs, float* h_out, float* c_out,
                          float* loss_out, void* ws, size_t ws_bytes);
+
+/* Bytes of device workspace cavs_infer needs (states, the pull projection,
+   transposed weights and per-vertex loss terms only).  0 on bad args. */
+size_t cavs_infer_workspace_bytes(const cavs_params* params, const cavs_sched* sched);
+
+/* Inference: the forward of Algorithm 1 over every task, then the loss head,
+   as cavs_forward computes them (bit-identical h_out, c_out and loss_out),
+   but nothing a backward would read is kept -- no saved gates, no gradient
+   of the loss head -- so the workspace is the smaller
+   cavs_infer_workspace_bytes and no cavs_backward may follow.  Arguments,
+   validation and errors as for cavs_forward. */
+cavs_status cavs_infer(cavs_ctx* ctx, const cavs_params* params, const cavs_sched* sched,
+                       const cavs_inputs* inputs, float* h_out, float* c_out,
+                       float* loss_out, void* ws, size_t ws_bytes);
 
 /* Runs dF over the tasks in reverse order (Algorithm 1, Backward), then the
    lazy parameter-gradient products.  Must follow cavs_forward with the same

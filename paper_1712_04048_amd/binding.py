@@ -74,7 +74,8 @@ class cavs_launch_time(ct.Structure):
 
 EXPORTS = ["cavs_create", "cavs_set_stream", "cavs_destroy", "cavs_last_error",
            "cavs_schedule_workspace_bytes", "cavs_schedule", "cavs_workspace_bytes",
-           "cavs_forward", "cavs_backward", "cavs_timing_enable", "cavs_timing_read"]
+           "cavs_forward", "cavs_backward", "cavs_infer_workspace_bytes", "cavs_infer",
+           "cavs_timing_enable", "cavs_timing_read"]
 
 _lib = None
 
@@ -108,6 +109,10 @@ def lib():
         L.cavs_backward.argtypes = [_vp, ct.POINTER(cavs_params), ct.POINTER(cavs_sched),
                                     ct.POINTER(cavs_inputs), _vp, ct.c_size_t,
                                     ct.POINTER(cavs_grads)]
+        L.cavs_infer_workspace_bytes.restype = ct.c_size_t
+        L.cavs_infer_workspace_bytes.argtypes = [ct.POINTER(cavs_params), ct.POINTER(cavs_sched)]
+        L.cavs_infer.restype = _i32
+        L.cavs_infer.argtypes = L.cavs_forward.argtypes
         L.cavs_timing_enable.restype = _i32
         L.cavs_timing_enable.argtypes = [_vp, _i32]
         L.cavs_timing_read.restype = _i32
@@ -275,6 +280,22 @@ def forward(ctx: Context, params: Params, sched: Schedule, X: Optional[torch.Ten
     ctx.check(lib().cavs_forward(ctx._h, ct.byref(p), ct.byref(sched.raw), ct.byref(inp),
                                  _ptr(h_out), _ptr(c_out), _ptr(loss_out), ws.data_ptr(),
                                  ws.numel()))
+
+
+def infer_workspace_bytes(params: Params, sched: Schedule) -> int:
+    p = params.raw()
+    return int(lib().cavs_infer_workspace_bytes(ct.byref(p), ct.byref(sched.raw)))
+
+
+def infer(ctx: Context, params: Params, sched: Schedule, X: Optional[torch.Tensor],
+          Y: Optional[torch.Tensor], ws: torch.Tensor, h_out: torch.Tensor,
+          c_out: Optional[torch.Tensor], loss_out: torch.Tensor) -> None:
+    """cavs_infer (asynchronous on the context's stream)."""
+    p = params.raw()
+    inp = cavs_inputs(_ptr(X), _ptr(Y), int(Y.shape[0]) if Y is not None else 0)
+    ctx.check(lib().cavs_infer(ctx._h, ct.byref(p), ct.byref(sched.raw), ct.byref(inp),
+                               _ptr(h_out), _ptr(c_out), _ptr(loss_out), ws.data_ptr(),
+                               ws.numel()))
 
 
 def backward(ctx: Context, params: Params, sched: Schedule, X: Optional[torch.Tensor],

@@ -37,14 +37,18 @@ cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...) {
 
 namespace {
 
-// Workspace of forward + backward, all level-major (row = position).
+// Workspace of forward + backward, all level-major (row = position).  In
+// inference only the states, the pull projection, the transposed weights and
+// the loss terms are kept: the saved gates and every gradient buffer take no
+// space.
 struct WsLayout {
   size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bpart, bar, total;
   size_t part_floats;
 };
 
-WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
+WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   WsLayout L{};
+  const size_t tr = train ? 1 : 0;
   const size_t V = (size_t)(s->V > 0 ? s->V : 1), H = (size_t)p->H;
   const bool lstm = p->cell == CAVS_TREE_LSTM;
   const size_t GW = lstm ? (size_t)(3 + p->N) * H : H;
@@ -61,16 +65,16 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s) {
   L.zrow = take(H);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
-  L.Gs = take(lstm ? V * GW : 0);
-  L.dZ = take(V * (C > 0 ? C : 1));
+  L.Gs = take(tr * (lstm ? V * GW : 0));
+  L.dZ = take(tr * V * (C > 0 ? C : 1));
   L.lossv = take(V);
-  L.dHL = take(V * H);
-  L.dHp = take(V * H);
-  L.dCp = take(lstm ? V * H : 0);
-  L.dA = take(V * GW);
-  L.part_floats = lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
+  L.dHL = take(tr * V * H);
+  L.dHp = take(tr * V * H);
+  L.dCp = take(tr * (lstm ? V * H : 0));
+  L.dA = take(tr * V * GW);
+  L.part_floats = tr * lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
   L.part = take(3 * L.part_floats);   // dU_iou, dU_f and dW_x split-K sums side by side
-  L.bpart = take(bias_part_floats(p->H, p->loss == CAVS_LOSS_CE ? p->C : 0));
+  L.bpart = take(tr * bias_part_floats(p->H, p->loss == CAVS_LOSS_CE ? p->C : 0));
   L.bar = take(256);
   L.total = o;
   return L;
@@ -119,7 +123,7 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
 }
 
 Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, void* ws,
-             const WsLayout& L) {
+             const WsLayout& L, bool train) {
   Net n{};
   char* base = (char*)ws;
   n.V = s->V;
@@ -160,6 +164,14 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.dHp = (float*)(base + L.dHp);
   n.dCp = (float*)(base + L.dCp);
   n.dA = (float*)(base + L.dA);
+  if (!train) {   // the kernels test these for null and skip what only backward reads
+    n.Gs = nullptr;
+    n.dZ = nullptr;
+    n.dHL = nullptr;
+    n.dHp = nullptr;
+    n.dCp = nullptr;
+    n.dA = nullptr;
+  }
   return n;
 }
 
@@ -278,18 +290,25 @@ cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, vo
 
 size_t cavs_workspace_bytes(const cavs_params* p, const cavs_sched* s) {
   if (!p || !s || p->H <= 0 || p->N <= 0 || s->V < 0) return 0;
-  return ws_layout(p, s).total;
+  return ws_layout(p, s, true).total;
 }
 
-cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
-                         const cavs_inputs* in, float* h_out, float* c_out, float* loss_out,
-                         void* ws, size_t ws_bytes) {
+size_t cavs_infer_workspace_bytes(const cavs_params* p, const cavs_sched* s) {
+  if (!p || !s || p->H <= 0 || p->N <= 0 || s->V < 0) return 0;
+  return ws_layout(p, s, false).total;
+}
+
+// Forward of Algorithm 1 over every task, then the loss head.  train:
+// also keep what the backward reads (saved gates, the head's gradients).
+static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                        const cavs_inputs* in, float* h_out, float* c_out, float* loss_out,
+                        void* ws, size_t ws_bytes, bool train) {
   if (!ctx) return CAVS_ERR_ARG;
   ctx->err.clear();
   cavs_status st = check_args(ctx, p, s, in);
   if (st != CAVS_OK) return st;
   if (!loss_out || (s->V > 0 && !h_out)) return fail(ctx, CAVS_ERR_ARG, "null output");
-  WsLayout L = ws_layout(p, s);
+  WsLayout L = ws_layout(p, s, train);
   if (!ws || ws_bytes < L.total)
     return fail(ctx, CAVS_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, L.total);
   CAVS_HIP_CHECK(ctx, hipSetDevice(ctx->device));
@@ -299,7 +318,7 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
     CAVS_HIP_CHECK(ctx, hipMemsetAsync(loss_out, 0, sizeof(float), str));
     return CAVS_OK;
   }
-  Net n = make_net(p, s, in, ws, L);
+  Net n = make_net(p, s, in, ws, L, train);
   n.h_out = h_out;
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
@@ -323,6 +342,18 @@ cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* 
   return CAVS_OK;
 }
 
+cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                         const cavs_inputs* in, float* h_out, float* c_out, float* loss_out,
+                         void* ws, size_t ws_bytes) {
+  return run_forward(ctx, p, s, in, h_out, c_out, loss_out, ws, ws_bytes, true);
+}
+
+cavs_status cavs_infer(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
+                       const cavs_inputs* in, float* h_out, float* c_out, float* loss_out,
+                       void* ws, size_t ws_bytes) {
+  return run_forward(ctx, p, s, in, h_out, c_out, loss_out, ws, ws_bytes, false);
+}
+
 cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
                           const cavs_inputs* in, void* ws, size_t ws_bytes,
                           const cavs_grads* g) {
@@ -336,7 +367,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   if (p->loss == CAVS_LOSS_CE && (!g->dWs || !g->dbs))
     return fail(ctx, CAVS_ERR_ARG, "dWs / dbs are required for CE");
   if (s->n_x > 0 && !g->dX) return fail(ctx, CAVS_ERR_ARG, "dX is required");
-  WsLayout L = ws_layout(p, s);
+  WsLayout L = ws_layout(p, s, true);
   if (!ws || ws_bytes < L.total)
     return fail(ctx, CAVS_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, L.total);
   CAVS_HIP_CHECK(ctx, hipSetDevice(ctx->device));
@@ -358,7 +389,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
     return CAVS_OK;
   }
-  Net n = make_net(p, s, in, ws, L);
+  Net n = make_net(p, s, in, ws, L, true);
   float* part = (float*)((char*)ws + L.part);
   float* bpart = (float*)((char*)ws + L.bpart);
   const int* lo = s->level_offsets_host;

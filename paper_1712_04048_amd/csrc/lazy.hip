@@ -108,10 +108,12 @@ __global__ void __launch_bounds__(256) k_pull_leaf(Net n, int n_pull, int lo1) {
         const float c = ig * ug, h = og * tanh_(c);
         n.Hs[(size_t)p * H + j] = h;
         n.Cs[(size_t)p * H + j] = c;
-        float* g = n.Gs + (size_t)p * n.GW;   // a leaf's forget gates are never read
-        g[j] = ig;
-        g[2 * H + j] = og;
-        g[3 * H + j] = ug;
+        if (n.Gs) {   // a leaf's forget gates are never read; null in inference
+          float* g = n.Gs + (size_t)p * n.GW;
+          g[j] = ig;
+          g[2 * H + j] = og;
+          g[3 * H + j] = ug;
+        }
         const int v = n.order[p];
         n.h_out[(size_t)v * H + j] = h;
         if (n.c_out) n.c_out[(size_t)v * H + j] = c;
@@ -228,10 +230,12 @@ __global__ void __launch_bounds__(256) k_pull_tile(Net n, int n_pull, int lo1) {
       auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
       st4(n.Hs + (size_t)p * H + j0, f4(h));
       st4(n.Cs + (size_t)p * H + j0, f4(c));
-      float* gs = n.Gs + (size_t)p * n.GW + j0;   // a leaf's forget gates are never read
-      st4(gs, f4(ig));
-      st4(gs + 2 * H, f4(og));
-      st4(gs + 3 * H, f4(ug));
+      if (n.Gs) {   // a leaf's forget gates are never read; null in inference
+        float* gs = n.Gs + (size_t)p * n.GW + j0;
+        st4(gs, f4(ig));
+        st4(gs + 2 * H, f4(og));
+        st4(gs + 3 * H, f4(ug));
+      }
       st4(n.h_out + (size_t)vid[tm] * H + j0, f4(h));
       if (n.c_out) st4(n.c_out + (size_t)vid[tm] * H + j0, f4(c));
     } else {
@@ -1242,6 +1246,7 @@ __global__ void __launch_bounds__(256) k_bias_part(Net n, int row0, int row1, in
 //   rows otherwise (row stride CP, pad columns zero);
 //   dHL = dZ W_s^T, the head's share of dL/dh, on MFMA (K = CP), wavefront w
 //   taking the 16-unit blocks w, w+8, ...
+// Inference (dZ and dHL null) stops after the per-position loss terms.
 constexpr int kLossWaves = 8;
 
 template <int MC>
@@ -1304,11 +1309,12 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
     if (q[i] >= 0 && cval) d = (expf(z - lse) - (r == q[i] ? 1.f : 0.f)) * n.inv_denom;
     dzl[w][4 * g + i][r] = d;
     if (w == 0 && p < V) {
-      if (r < CP) n.dZ[(size_t)p * CP + r] = d;
+      if (r < CP && n.dZ) n.dZ[(size_t)p * CP + r] = d;
       if (q[i] < 0 && r == 0) n.lossv[p] = 0.f;
       if (q[i] >= 0 && r == q[i]) n.lossv[p] = lse - z;
     }
   }
+  if (!n.dHL) return;   // inference: no gradient of the head
   // each wavefront re-reads only its own copy of dZ: its LDS operations
   // complete in order
   __builtin_amdgcn_wave_barrier();
@@ -1345,7 +1351,8 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
 }
 
 // Squared-error head: one wavefront per position; loss 0.5 |h - y|^2 and
-// dHL = (h - y) / |Lambda| (zero rows for unlabelled positions).
+// dHL = (h - y) / |Lambda| (zero rows for unlabelled positions; not written
+// in inference, where dHL is null).
 __global__ void __launch_bounds__(256) k_loss_l2(Net n) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + w;
@@ -1354,10 +1361,11 @@ __global__ void __launch_bounds__(256) k_loss_l2(Net n) {
   if (p >= n.V) return;
   const int q = n.push_pos[p], H = n.H;
   const float* h = n.Hs + (size_t)p * H;
-  float* dh = n.dHL + (size_t)p * H;
+  float* dh = n.dHL ? n.dHL + (size_t)p * H : nullptr;   // null in inference
   if (q < 0) {
     if (lane == 0) n.lossv[p] = 0.f;
-    for (int j = lane; j < H; j += 64) dh[j] = 0.f;
+    if (dh)
+      for (int j = lane; j < H; j += 64) dh[j] = 0.f;
     return;
   }
   const float* y = n.Y + (size_t)q * H;
@@ -1365,7 +1373,7 @@ __global__ void __launch_bounds__(256) k_loss_l2(Net n) {
   for (int j = lane; j < H; j += 64) {
     const float d = h[j] - y[j];
     s += d * d;
-    dh[j] = d * n.inv_denom;
+    if (dh) dh[j] = d * n.inv_denom;
   }
   s = wave_sum(s);
   if (lane == 0) n.lossv[p] = 0.5f * s;

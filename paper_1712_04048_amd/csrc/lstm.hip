@@ -48,10 +48,12 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int sk
   n.Hs[(size_t)p * H + j] = h;
   n.Cs[(size_t)p * H + j] = c;
   // a leaf has no forget gates: their saved columns are never read
-  float* g = n.Gs + (size_t)p * n.GW;
-  g[j] = i;
-  g[2 * H + j] = o;
-  g[3 * H + j] = u;
+  if (n.Gs) {   // null in inference
+    float* g = n.Gs + (size_t)p * n.GW;
+    g[j] = i;
+    g[2 * H + j] = o;
+    g[3 * H + j] = u;
+  }
   const int v = n.order[p];
   n.h_out[(size_t)v * H + j] = h;
   if (n.c_out) n.c_out[(size_t)v * H + j] = c;

@@ -83,12 +83,14 @@ __device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const F
   const float h = og * tanh_(c);
   n.Hs[(size_t)p * H + j] = h;
   n.Cs[(size_t)p * H + j] = c;
-  float* g = n.Gs + (size_t)p * n.GW;
-  g[j] = ig;
-  g[H + j] = f0;
-  g[2 * H + j] = og;
-  g[3 * H + j] = ug;
-  if constexpr (NCH == 2) g[4 * H + j] = f1;
+  if (n.Gs) {   // null in inference: nothing reads the gates back
+    float* g = n.Gs + (size_t)p * n.GW;
+    g[j] = ig;
+    g[H + j] = f0;
+    g[2 * H + j] = og;
+    g[3 * H + j] = ug;
+    if constexpr (NCH == 2) g[4 * H + j] = f1;
+  }
   n.h_out[(size_t)q.v * H + j] = h;
   if (n.c_out) n.c_out[(size_t)q.v * H + j] = c;
 }
@@ -197,12 +199,14 @@ __device__ __forceinline__ void lstm_fwd_fin4(const Net& n, int p, int j0, const
   auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
   st4(n.Hs + (size_t)p * H + j0, f4(h));
   st4(n.Cs + (size_t)p * H + j0, f4(c));
-  float* g = n.Gs + (size_t)p * n.GW + j0;
-  st4(g, f4(ig));
-  st4(g + H, f4(f0));
-  st4(g + 2 * H, f4(og));
-  st4(g + 3 * H, f4(ug));
-  if constexpr (NCH == 2) st4(g + 4 * H, f4(f1));
+  if (n.Gs) {   // null in inference: nothing reads the gates back
+    float* g = n.Gs + (size_t)p * n.GW + j0;
+    st4(g, f4(ig));
+    st4(g + H, f4(f0));
+    st4(g + 2 * H, f4(og));
+    st4(g + 3 * H, f4(ug));
+    if constexpr (NCH == 2) st4(g + 4 * H, f4(f1));
+  }
   st4(n.h_out + (size_t)q.v * H + j0, f4(h));
   if (n.c_out) st4(n.c_out + (size_t)q.v * H + j0, f4(c));
 }

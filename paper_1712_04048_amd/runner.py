@@ -41,6 +41,7 @@ class Batch:
                                bs=f32(wl.bs) if wl.loss == B.LOSS_CE else None)
         self.sched: Optional[B.Schedule] = None
         self.ws = None
+        self.ws_infer = None
 
     def schedule(self) -> B.Schedule:
         """cavs_schedule; reuses the schedule buffers from an earlier call."""
@@ -80,6 +81,24 @@ class Batch:
 
     def backward(self):
         B.backward(self.ctx, self.params, self.sched, self.X, self.Y, self.ws, self.grads)
+
+    def infer(self):
+        """cavs_infer into the same h / c / loss outputs, with its own smaller workspace."""
+        if self.ws_infer is None:
+            nbytes = B.infer_workspace_bytes(self.params, self.sched)
+            self.ws_infer = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=self.dev)
+        B.infer(self.ctx, self.params, self.sched, self.X, self.Y, self.ws_infer, self.h,
+                self.c, self.loss)
+
+    def run_infer(self) -> dict:
+        """Schedule (if needed), cavs_infer, and the outputs as float64 numpy arrays."""
+        if self.sched is None:
+            self.schedule()
+        if self.ws is None:
+            self.alloc()
+        self.infer()
+        torch.cuda.synchronize(self.dev)
+        return self.results(backward=False)
 
     def step(self):
         """One pass of the whole path: schedule, forward, backward (async tail)."""

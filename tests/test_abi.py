@@ -87,3 +87,21 @@ def test_workspace_query_needs_no_gpu():
     s = B.cavs_sched()
     s.V, s.N = 1000, 2
     assert lib.cavs_workspace_bytes(ct.byref(p), ct.byref(s)) > 1000 * 512 * 4
+
+
+def test_infer_workspace_is_the_states_without_saved_gates():
+    """Inference keeps h, c, the pull projection and the transposed weights,
+    but neither the saved gates ((3+N)H per vertex) nor gradient buffers."""
+    _ensure_built()
+    lib = B.lib()
+    V, D, H = 1000, 300, 512
+    p = B.cavs_params(B.TREE_LSTM, B.FP32, B.LOSS_CE, D, H, 2, 5)
+    s = B.cavs_sched()
+    s.V, s.N = V, 2
+    full = lib.cavs_workspace_bytes(ct.byref(p), ct.byref(s))
+    inf = lib.cavs_infer_workspace_bytes(ct.byref(p), ct.byref(s))
+    states = (V * 4 * H + V * H + V * H) * 4          # P, Hs, Cs
+    assert states <= inf < states + (4 * H * H + 4 * H * D + 2 * V + 8 * H) * 4 + 16 * 256
+    assert full - inf >= V * 5 * H * 4                 # at least the saved gates
+    p.H = 0
+    assert lib.cavs_infer_workspace_bytes(ct.byref(p), ct.byref(s)) == 0

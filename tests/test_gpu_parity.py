@@ -294,6 +294,75 @@ def test_full_size_states_on_sampled_graphs(ctx, maker):
     print(errs)
 
 
+# ---------------------------------------------------------------------------
+# Inference (cavs_infer): the forward without anything kept for a backward.
+# Same kernels, so h, c and the loss must equal cavs_forward's bit for bit;
+# against the oracle, the forward's tolerance.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("maker", ["tiny", "sst", "varlstm", "treefc", "deep_bf16"])
+def test_infer_bit_identical_to_forward_full_size(ctx, maker):
+    wl = W.CONFIGS[maker](0)
+    print("infer vs forward %s V=%d" % (maker, wl.V), flush=True)
+    b = Batch(wl, ctx)
+    train = b.run(backward=False)
+    b.h.fill_(float("nan"))
+    if b.c is not None:
+        b.c.fill_(float("nan"))
+    b.loss.fill_(float("nan"))
+    got = b.run_infer()
+    assert b.ws_infer.numel() < b.ws.numel()
+    for k in train:
+        assert np.array_equal(got[k], train[k]), k
+
+
+def _infer_parity(ctx, wl, tol=TOL_FP32, bf16=False, floor=None):
+    print("infer parity %s V=%d H=%d" % (wl.name, wl.V, wl.H), flush=True)
+    got = Batch(wl, ctx).run_infer()
+    want = oracle.run(wl, backward=False, bf16=bf16)
+    keys = [k for k in ("h", "c", "loss") if k in want]
+    kw = {} if floor is None else dict(floor=floor)
+    return check(got, want, keys, tol, "infer_" + wl.name, **kw)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_infer_parity_reduced(ctx, seed):
+    _infer_parity(ctx, W.config_treelstm_sst(seed, K=12))
+    _infer_parity(ctx, W.config_varlstm(seed, K=6))
+    _infer_parity(ctx, W.config_treefc(seed, K=2, leaves=64))
+    _infer_parity(ctx, W.config_tiny_treelstm(seed, shuffle_ids=seed == 1))
+
+
+@pytest.mark.parametrize("case", ["single_vertex_trees", "no_labels", "leaves_without_input",
+                                  "inputs_everywhere"])
+def test_infer_parity_edge_cases(ctx, case):
+    rng = np.random.Generator(np.random.PCG64(12))
+    trees, kw = EDGE[case](rng)
+    args = dict(N=2, D=12, H=64, C=5, sigma=0.3, rng=rng)
+    args.update(kw)
+    wl = W.make_workload(case, trees, **args)
+    _infer_parity(ctx, wl)
+
+
+def test_infer_parity_bf16_reduced(ctx):
+    wl = W.config_treelstm_deep_bf16(0, K=4, D=300, H=1024, lo=8, hi=40)
+    _infer_parity(ctx, wl, tol=TOL_BF16, bf16=True, floor=1.0)
+
+
+def test_infer_rejects_short_workspace(ctx):
+    wl = W.config_tiny_treelstm(0)
+    b = Batch(wl, ctx)
+    b.schedule()
+    b.alloc()
+    need = B.infer_workspace_bytes(b.params, b.sched)
+    assert 0 < need < b.ws.numel()
+    with pytest.raises(B.CavsError) as e:
+        B.infer(ctx, b.params, b.sched, b.X, b.Y, b.ws[:need - 1], b.h, b.c, b.loss)
+    assert e.value.status == B.ERR_WORKSPACE
+    B.infer(ctx, b.params, b.sched, b.X, b.Y, b.ws[:need], b.h, b.c, b.loss)
+    torch.cuda.synchronize()
+    assert np.isfinite(b.loss.item())
+
+
 def test_determinism_bitwise(ctx):
     wl = W.config_treelstm_sst(0, K=24)
     b = Batch(wl, ctx)
