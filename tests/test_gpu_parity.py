@@ -223,6 +223,39 @@ def test_parity_hidden_widths(ctx, H, N):
     _parity(ctx, wl)
 
 
+@pytest.mark.parametrize("case", ["trees_fp32", "chains_fp32", "trees_bf16"])
+def test_parity_tile_levels(ctx, case):
+    """Forests whose internal levels reach the LDS-tiled products (levels of
+    300 positions or more; 64-position forward tiles from 1024): every
+    state, the loss and every gradient against the oracle, so the tiled
+    forward and backward products are checked element by element, not only
+    through properties at full size."""
+    rng = np.random.Generator(np.random.PCG64({"trees_fp32": 31, "chains_fp32": 32,
+                                               "trees_bf16": 33}[case]))
+    if case == "chains_fp32":
+        trees = [W.chain(int(L)) for L in rng.integers(3, 9, size=330)]
+        wl = W.make_workload(case, trees, N=1, D=32, H=256, C=5, rng=rng, inputs="all",
+                             labels="all")
+    elif case == "trees_fp32":
+        trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 14, size=420)]
+        wl = W.make_workload(case, trees, N=2, D=32, H=256, C=5, rng=rng, labels="all")
+    else:
+        # the bf16-emulating oracle rounds every product operand: 300 cherries
+        # keep it to about half a minute and still give one 300-position level
+        wl = W.make_workload(case, [W.complete_tree(2)] * 300, prec=W.PREC_BF16, N=2, D=32,
+                             H=256, C=5, rng=rng, labels="all")
+    sizes = np.diff(oracle.schedule(wl.child, wl.parent, wl.pull_idx, wl.push_idx)["level_offsets"])
+    assert sizes[1] >= 300
+    if case != "trees_bf16":
+        assert sizes[2] >= 300
+    if case == "trees_fp32":
+        assert sizes[1] >= 1024
+    if case == "trees_bf16":
+        _parity_bf16(ctx, wl, case)
+    else:
+        _parity(ctx, wl, label=case)
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_parity_treefc_reduced(ctx, seed):
     _parity(ctx, W.config_treefc(seed, K=2, leaves=64))
@@ -267,6 +300,31 @@ def test_parity_edge_cases(ctx, case):
     wl = W.make_workload(case, trees, **args)
     wl.b[:] = (0.1 * rng.standard_normal(wl.b.shape)).astype(np.float32)
     _parity(ctx, wl, label=case)
+
+
+@pytest.mark.parametrize("cell", [W.CELL_TREE_LSTM, W.CELL_TREE_FC])
+def test_empty_batch(ctx, cell):
+    """No graphs at all: zero levels, loss 0, every gradient overwritten with
+    zeros (the outputs are poisoned first), as the oracle gives."""
+    rng = np.random.Generator(np.random.PCG64(4))
+    kw = dict(N=2, D=12, H=64, C=5) if cell == W.CELL_TREE_LSTM else \
+        dict(cell=cell, loss=W.LOSS_L2, N=2, H=64)
+    wl = W.make_workload("empty", [], rng=rng, **kw)
+    assert wl.V == 0
+    b = Batch(wl, ctx)
+    b.schedule()
+    assert b.sched.T == 0
+    b.alloc()
+    for g in b.grads.values():
+        g.fill_(float("nan"))
+    b.loss.fill_(float("nan"))
+    got = b.run()
+    want = oracle.run(wl)
+    assert got["loss"] == want["loss"] == 0.0
+    for k, v in b.grads.items():
+        assert np.array_equal(got[k], want[k]), k
+    b.loss.fill_(float("nan"))
+    assert b.run_infer()["loss"] == 0.0
 
 
 @pytest.mark.parametrize("maker", ["sst", "varlstm", "treefc"])
