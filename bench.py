@@ -183,6 +183,27 @@ def main():
     torch.cuda.synchronize()
     fwdbwd_ms = e0.elapsed_time(e1) / args.steps
 
+    # engine ablations (fwd+bwd per pass, HIP events): dU formed level by
+    # level instead of lazily, and the persistent loop for the small levels
+    def fwd_bwd_with(var):
+        os.environ[var] = "1"
+        try:
+            batch.forward()
+            batch.backward()
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(args.steps):
+                batch.forward()
+                batch.backward()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / args.steps
+        finally:
+            del os.environ[var]
+
+    eager_ms = fwd_bwd_with("CAVS_EAGER_DW")
+    persist_ms = fwd_bwd_with("CAVS_PERSIST")
+
     # inference (cavs_infer: the forward keeping nothing for a backward) beside
     # the training forward alone; whole inference steps include the schedule
     batch.infer()
@@ -292,6 +313,9 @@ def main():
         "schedule_ms": round(sched_ms, 4),
         "fwd_bwd_ms": round(fwdbwd_ms, 4),
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
+        "ablation": {"unit": "ms per forward + backward pass", "lazy_dw_per_level_launches":
+                     round(fwdbwd_ms, 4), "eager_dw_per_level": round(eager_ms, 4),
+                     "persistent_small_levels": round(persist_ms, 4)},
         "inference": {"value": wl.V / (infer_step_ms * 1e-3), "unit": "vertices/s",
                       "step": "cavs_schedule + cavs_infer", "ms_per_step": round(infer_step_ms, 4),
                       "infer_ms": round(infer_ms, 4), "train_forward_ms": round(fwd_ms, 4),

@@ -3,6 +3,7 @@
 // reverse for dF; Algorithm 2: level-major dynamic tensors).
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include "kernels.h"
 
@@ -120,6 +121,29 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
       return fail(ctx, CAVS_ERR_ARG, "Tree-FC: a vertex must pull an input iff it is a leaf");
   }
   return CAVS_OK;
+}
+
+// Ablation of lazy batching (CAVS_EAGER_DW=1; Tree-LSTM only): the recurrent
+// weight gradients dU are formed level by level, as each task's dA is known,
+// and summed into dU in reverse task order, instead of as one product over
+// every internal vertex after the level loop (Section 3.5).  dW_x, the bias
+// and the loss head stay lazy.  Measured with bench.py; off by default.
+bool eager_dw_enabled() {
+  const char* e = getenv("CAVS_EAGER_DW");
+  return e && e[0] && e[0] != '0';
+}
+
+// dU contributions of the internal positions [off, off + M): queued split-K
+// products whose reductions add into dU (acc) or overwrite it (first level).
+bool lstm_dU_level(const Net& n, int off, int M, float* dU, float* part, size_t pf, bool acc,
+                   hipStream_t str) {
+  SplitJobs jobs;
+  lstm_dU_iou(n, off, dU, part, pf, str, &jobs, M);
+  lstm_dU_f(n, off, dU, part + pf, pf, str, &jobs, M);
+  if (jobs.n != (n.N == 2 ? 2 : 1)) return false;   // a reduction ran unqueued (overwrote dU)
+  for (int k = 0; k < jobs.n; ++k) jobs.j[k].acc = acc;
+  reduce_split_jobs(jobs, str);
+  return true;
 }
 
 Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, void* ws,
@@ -404,8 +428,10 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     const int tf = lstm_fuse_level(lo, T);
     n.fuse_from = lo[tf];
     n.f_unread_below = s->n_inner_input > 0 ? 0 : lo[1];
+    const bool eager = T > 1 && eager_dw_enabled();
+    const size_t pf = L.part_floats;
     lstm_bwd_roots(n, str);
-    int ts = persist_first_level(n, lo, T);
+    int ts = eager ? T : persist_first_level(n, lo, T);
     if (ts < tf) ts = tf;
     int* bar = (int*)((char*)ws + L.bar);
     if (!lstm_bwd_persist(n, s->level_offsets, lo, ts, T, bar, str)) ts = T;
@@ -413,14 +439,18 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       const int M = lo[t + 1] - lo[t];
       if (t < tf) lstm_bwd_gates(n, lo[t], M, str);
       if (t >= 1) lstm_bwd_level(n, lo[t], M, str);
+      // level t's dA is complete once its own product has been enqueued
+      if (eager && t >= 1 && !lstm_dU_level(n, lo[t], M, g->dU, part, pf, t < T - 1, str))
+        return fail(ctx, CAVS_ERR_UNSUPPORTED, "per-level dU reduction could not be queued");
     }
     // the lazy products keep their split-K sums in separate scratch and share
     // one reduction launch
     const bool with_f = s->n_inner_input > 0;
-    const size_t pf = L.part_floats;
     SplitJobs jobs;
-    lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
-    lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
+    if (!eager) {
+      lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
+      lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
+    }
     if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);

@@ -113,6 +113,7 @@ struct SplitJob {
   float* dst;
   int S, Mo, No, ldd, col_off, gap_start, gap;
   int kind;     // 0: float4 sums; 1: Mo = 1, any No, the S partial rows split over 16 wavefronts
+  int acc;      // kind 0: add the sum to what dst holds instead of overwriting it
 };
 struct SplitJobs {
   static constexpr int kMax = 8;
@@ -124,10 +125,12 @@ void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s);
 void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
 // the two halves of lstm_dU: dU_iou (all four blocks with one child) and,
 // with two children, dU_f (a no-op with one child)
+// rows = the positions from off1 the products sum over (-1: every position
+// from off1 to the end)
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
-                 hipStream_t s, SplitJobs* jobs = nullptr);
+                 hipStream_t s, SplitJobs* jobs = nullptr, int rows = -1);
 void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s,
-               SplitJobs* jobs = nullptr);
+               SplitJobs* jobs = nullptr, int rows = -1);
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
               size_t part_floats, hipStream_t s, SplitJobs* jobs = nullptr);
 void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);

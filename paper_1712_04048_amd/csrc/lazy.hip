@@ -1050,7 +1050,12 @@ __global__ void __launch_bounds__(1024) k_reduce_jobs(SplitJobs jobs) {
     const float4 v = ldg4(J.part + k * stride + idx);
     s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
   }
-  st4(J.dst + (size_t)m * J.ldd + J.col_off + nn + (nn >= J.gap_start ? J.gap : 0), s);
+  float* d = J.dst + (size_t)m * J.ldd + J.col_off + nn + (nn >= J.gap_start ? J.gap : 0);
+  if (J.acc) {
+    const float4 o = ldg4(d);
+    s = make_float4(o.x + s.x, o.y + s.y, o.z + s.z, o.w + s.w);
+  }
+  st4(d, s);
 }
 
 // The reduction of a split-K product: queued on `jobs` when given (the
@@ -1464,17 +1469,17 @@ void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
 }
 
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
-                 hipStream_t s, SplitJobs* jobs) {
-  const int H = n.H, MI = n.V - off1;
+                 hipStream_t s, SplitJobs* jobs, int rows) {
+  const int H = n.H, MI = rows >= 0 ? rows : n.V - off1;
   LdDUiou ld{n, off1};
   if (n.N == 1) tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s, jobs);
   else tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s, jobs);
 }
 
 void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s,
-               SplitJobs* jobs) {
+               SplitJobs* jobs, int rows) {
   if (n.N != 2) return;
-  const int H = n.H, MI = n.V - off1;
+  const int H = n.H, MI = rows >= 0 ? rows : n.V - off1;
   LdDUf lf{n, off1, MI};
   tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s, jobs);
 }

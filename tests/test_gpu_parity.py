@@ -526,3 +526,19 @@ def test_persistent_level_loop_opt_in(ctx, monkeypatch):
     wl = W.config_treelstm_deep_bf16(1, K=4, D=300, H=1024, lo=8, hi=40)
     _parity_bf16(ctx, wl, "persistent_bf16")
     monkeypatch.delenv("CAVS_PERSIST")
+
+
+def test_eager_weight_gradients_ablation(ctx, monkeypatch):
+    """The lazy-batching ablation (dU formed level by level and summed into
+    the output, CAVS_EAGER_DW=1) gives the oracle's gradients too."""
+    monkeypatch.setenv("CAVS_EAGER_DW", "1")
+    _parity(ctx, W.config_treelstm_sst(2, K=16), label="eager_dw_fp32")
+    rng = np.random.Generator(np.random.PCG64(34))
+    trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 14, size=420)]
+    _parity(ctx, W.make_workload("eager_dw_tiles", trees, N=2, D=32, H=256, C=5, rng=rng,
+                                 labels="all"))
+    _parity(ctx, W.config_varlstm(1, K=6), label="eager_dw_chains")
+    _parity(ctx, W.config_tiny_treelstm(1), label="eager_dw_tiny")
+    wl = W.config_treelstm_deep_bf16(2, K=4, D=300, H=1024, lo=8, hi=40)
+    _parity_bf16(ctx, wl, "eager_dw_bf16")
+    monkeypatch.delenv("CAVS_EAGER_DW")
