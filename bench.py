@@ -184,7 +184,8 @@ def main():
     fwdbwd_ms = e0.elapsed_time(e1) / args.steps
 
     # engine ablations (fwd+bwd per pass, HIP events): dU formed level by
-    # level instead of lazily, and the persistent loop for the small levels
+    # level instead of lazily, the persistent loop for the small levels, and
+    # the backward's children's gates unfused from the level products
     def fwd_bwd_with(var):
         os.environ[var] = "1"
         try:
@@ -203,6 +204,7 @@ def main():
 
     eager_ms = fwd_bwd_with("CAVS_EAGER_DW")
     persist_ms = fwd_bwd_with("CAVS_PERSIST")
+    unfused_ms = fwd_bwd_with("CAVS_UNFUSED_BWD_GATES")
 
     # inference (cavs_infer: the forward keeping nothing for a backward) beside
     # the training forward alone; whole inference steps include the schedule
@@ -315,7 +317,8 @@ def main():
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
         "ablation": {"unit": "ms per forward + backward pass", "lazy_dw_per_level_launches":
                      round(fwdbwd_ms, 4), "eager_dw_per_level": round(eager_ms, 4),
-                     "persistent_small_levels": round(persist_ms, 4)},
+                     "persistent_small_levels": round(persist_ms, 4),
+                     "unfused_backward_gates": round(unfused_ms, 4)},
         "inference": {"value": wl.V / (infer_step_ms * 1e-3), "unit": "vertices/s",
                       "step": "cavs_schedule + cavs_infer", "ms_per_step": round(infer_step_ms, 4),
                       "infer_ms": round(infer_ms, 4), "train_forward_ms": round(fwd_ms, 4),

@@ -133,6 +133,15 @@ bool eager_dw_enabled() {
   return e && e[0] && e[0] != '0';
 }
 
+// Ablation of kernel fusion in the backward pass (CAVS_UNFUSED_BWD_GATES=1):
+// no child's dA is formed in its parent's product epilogue; every level gets
+// its own elementwise gates kernel, as the levels above 256 positions always
+// do.  Measured with bench.py; off by default.
+bool unfused_bwd_gates() {
+  const char* e = getenv("CAVS_UNFUSED_BWD_GATES");
+  return e && e[0] && e[0] != '0';
+}
+
 // dU contributions of the internal positions [off, off + M): queued split-K
 // products whose reductions add into dU (acc) or overwrite it (first level).
 bool lstm_dU_level(const Net& n, int off, int M, float* dU, float* part, size_t pf, bool acc,
@@ -425,7 +434,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     // Levels tf.. get dA in their parent's level epilogue (roots: one
     // kernel); levels below tf by an elementwise kernel just before their
     // own product, once every parent has stored dL/dh and dL/dc.
-    const int tf = lstm_fuse_level(lo, T);
+    const int tf = unfused_bwd_gates() ? T : lstm_fuse_level(lo, T);
     n.fuse_from = lo[tf];
     n.f_unread_below = s->n_inner_input > 0 ? 0 : lo[1];
     const bool eager = T > 1 && eager_dw_enabled();

@@ -542,3 +542,15 @@ def test_eager_weight_gradients_ablation(ctx, monkeypatch):
     wl = W.config_treelstm_deep_bf16(2, K=4, D=300, H=1024, lo=8, hi=40)
     _parity_bf16(ctx, wl, "eager_dw_bf16")
     monkeypatch.delenv("CAVS_EAGER_DW")
+
+
+def test_unfused_backward_gates_ablation(ctx, monkeypatch):
+    """The fusion ablation (every level's dA from the elementwise kernel,
+    CAVS_UNFUSED_BWD_GATES=1) gives the oracle's gradients too."""
+    monkeypatch.setenv("CAVS_UNFUSED_BWD_GATES", "1")
+    _parity(ctx, W.config_treelstm_sst(0, K=16), label="unfused_fp32")
+    _parity(ctx, W.config_varlstm(2, K=6), label="unfused_chains")
+    _parity(ctx, W.config_tiny_treelstm(2), label="unfused_tiny")
+    wl = W.config_treelstm_deep_bf16(0, K=4, D=300, H=1024, lo=8, hi=40)
+    _parity_bf16(ctx, wl, "unfused_bf16")
+    monkeypatch.delenv("CAVS_UNFUSED_BWD_GATES")
