@@ -32,6 +32,14 @@
  *     non-zero status, cavs_last_error() describes it.  Argument errors are
  *     detected on the host before anything is enqueued.
  *   - Calls on one context must not overlap (one stream, one user at a time).
+ *   - Three environment switches, read at each call and off by default, turn
+ *     the execution engine's optimisations off for ablation measurements;
+ *     results stay within the same tolerance of the exact ones:
+ *       CAVS_EAGER_DW=1           dU formed level by level, not lazily;
+ *       CAVS_UNFUSED_BWD_GATES=1  no child gradient fused into a parent's
+ *                                 backward product;
+ *       CAVS_PERSIST=1            the small levels in one persistent launch
+ *                                 with grid barriers.
  */
 #ifndef CAVS_H
 #define CAVS_H
