@@ -421,6 +421,31 @@ def test_infer_rejects_short_workspace(ctx):
     assert np.isfinite(b.loss.item())
 
 
+def test_runs_on_the_callers_stream():
+    """A context bound to a non-default stream (default priority) enqueues
+    everything there, and set_stream moves it: the outputs equal those of a
+    run on the default stream bit for bit."""
+    wl = W.config_treelstm_sst(1, K=24)
+    c1 = B.Context(0)
+    side = torch.cuda.Stream()
+    c2 = B.Context(0, stream=side)
+    try:
+        ref = Batch(wl, c1).run()
+        b = Batch(wl, c2)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):
+            got = b.run()
+        for k in ref:
+            assert np.array_equal(np.asarray(got[k]), np.asarray(ref[k])), k
+        c2.set_stream(torch.cuda.current_stream())
+        got2 = b.run()
+        for k in ref:
+            assert np.array_equal(np.asarray(got2[k]), np.asarray(ref[k])), k
+    finally:
+        c2.close()
+        c1.close()
+
+
 def test_determinism_bitwise(ctx):
     wl = W.config_treelstm_sst(0, K=24)
     b = Batch(wl, ctx)
