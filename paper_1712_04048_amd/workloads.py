@@ -328,7 +328,7 @@ def config_treelstm_deep_bf16(seed: int = 0, K: int = 256, D: int = 300, H: int 
                          D=D, H=H, C=5, sigma=0.03, rng=rng, inputs="leaves", labels="all")
 
 
-CONFIGS = {
+WORKLOADS = {
     "tiny": config_tiny_treelstm,
     "varlstm": config_varlstm,
     "treefc": config_treefc,

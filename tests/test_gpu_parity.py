@@ -90,7 +90,7 @@ def test_schedule_bit_exact_benchmark_shapes(ctx, maker):
         wl = W.make_workload(maker, trees, N=2, D=4, H=64, C=5, rng=rng, inputs=inputs,
                              shuffle_ids=True)
     else:
-        wl = W.CONFIGS[maker](0)
+        wl = W.WORKLOADS[maker](0)
     print("schedule shape %s V=%d" % (maker, wl.V), flush=True)
     got = _gpu_schedule(ctx, wl)
     want = oracle.schedule(wl.child, wl.parent, wl.pull_idx, wl.push_idx)
@@ -332,7 +332,7 @@ def test_full_size_states_on_sampled_graphs(ctx, maker):
     """Full benchmark-size batch on the GPU (the launch configuration the
     benchmark times); states of sampled graphs against the oracle run on
     those graphs alone (a graph's states depend only on itself)."""
-    wl = W.CONFIGS[maker](0)
+    wl = W.WORKLOADS[maker](0)
     print("full-size %s V=%d" % (maker, wl.V), flush=True)
     b = Batch(wl, ctx)
     got = b.run()
@@ -359,7 +359,7 @@ def test_full_size_states_on_sampled_graphs(ctx, maker):
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("maker", ["tiny", "sst", "varlstm", "treefc", "deep_bf16"])
 def test_infer_bit_identical_to_forward_full_size(ctx, maker):
-    wl = W.CONFIGS[maker](0)
+    wl = W.WORKLOADS[maker](0)
     print("infer vs forward %s V=%d" % (maker, wl.V), flush=True)
     b = Batch(wl, ctx)
     train = b.run(backward=False)
