@@ -455,22 +455,27 @@ def test_determinism_bitwise(ctx):
         assert np.array_equal(np.asarray(r1[k]), np.asarray(r2[k])), k
 
 
-def test_forward_rejects_bad_arguments(ctx):
+@pytest.mark.parametrize("entry", ["forward", "infer"])
+def test_forward_rejects_bad_arguments(ctx, entry):
+    call = B.forward if entry == "forward" else B.infer
     wl = W.config_tiny_treelstm(0)
     b = Batch(wl, ctx)
     b.schedule()
     b.alloc()
     small = torch.empty(16, dtype=torch.uint8, device=ctx.torch_device)
     with pytest.raises(B.CavsError) as e:
-        B.forward(ctx, b.params, b.sched, b.X, b.Y, small, b.h, b.c, b.loss)
+        call(ctx, b.params, b.sched, b.X, b.Y, small, b.h, b.c, b.loss)
     assert e.value.status == B.ERR_WORKSPACE
     p = B.Params(**{**b.params.__dict__, "H": 48})
     with pytest.raises(B.CavsError) as e:
-        B.forward(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
+        call(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
     assert e.value.status in (B.ERR_UNSUPPORTED, B.ERR_WORKSPACE)
     p = B.Params(**{**b.params.__dict__, "N": 1})
     with pytest.raises(B.CavsError) as e:
-        B.forward(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
+        call(ctx, p, b.sched, b.X, b.Y, b.ws, b.h, b.c, b.loss)
+    assert e.value.status == B.ERR_ARG
+    with pytest.raises(B.CavsError) as e:   # no h_out
+        call(ctx, b.params, b.sched, b.X, b.Y, b.ws, None, b.c, b.loss)
     assert e.value.status == B.ERR_ARG
 
 
