@@ -122,9 +122,8 @@ struct SplitJobs {
 };
 void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s);
 
-void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s);
-// the two halves of lstm_dU: dU_iou (all four blocks with one child) and,
-// with two children, dU_f (a no-op with one child)
+// the lazy dU products: dU_iou (all four blocks with one child) and, with
+// two children, dU_f (a no-op with one child)
 // rows = the positions from off1 the products sum over (-1: every position
 // from off1 to the end)
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,

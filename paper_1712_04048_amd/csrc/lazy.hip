@@ -1497,19 +1497,6 @@ void reduce_split_jobs(const SplitJobs& jobs, hipStream_t s) {
               jobs);
 }
 
-void lstm_dU(const Net& n, int off1, float* dU, float* part, size_t part_floats, hipStream_t s) {
-  const int H = n.H, MI = n.V - off1;
-  if (n.N == 1) {
-    LdDUiou ld{n, off1};
-    tn_product(ld, MI, H, 4 * H, dU, 4 * H, 0, 1 << 30, 0, part, part_floats, s);
-  } else {
-    LdDUiou ld{n, off1};
-    tn_product(ld, MI, H, 3 * H, dU, 4 * H, 0, H, H, part, part_floats, s);
-    LdDUf lf{n, off1, MI};
-    tn_product(lf, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part, part_floats, s);
-  }
-}
-
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
               size_t part_floats, hipStream_t s, SplitJobs* jobs) {
   const int H = n.H;
