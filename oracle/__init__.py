@@ -2,8 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY: imported by the tests, by ``__graft_entry__.smoke``
 and by the CPU-baseline leg of ``bench.py``; the product path never imports or
-calls it.  The arithmetic lives in ``oracle.c`` (plain C, fp64); this module
-only compiles it with gcc, loads it with ctypes and marshals numpy arrays.
+calls it.  The arithmetic lives in ``oracle.c`` (plain C); this module only
+compiles it with gcc -- once in fp64 (``liboracle.so``, the parity reference)
+and once in fp32 (``liboracle_f32.so``, the same definitions evaluated in
+float) -- loads it with ctypes and marshals numpy arrays.
 
 Results are returned indexed by vertex id.  Gate arrays use the oracle's own
 per-vertex layout [i | o | u | f_0 .. f_{N-1}], each H wide.
@@ -19,7 +21,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+_LIBS = {"f64": os.path.join(_HERE, "liboracle.so"),
+         "f32": os.path.join(_HERE, "liboracle_f32.so")}
+_LIB = _LIBS["f64"]
 
 OK = 0
 ERR_ARG = -1
@@ -33,25 +37,39 @@ LOSS_CE = 0
 LOSS_L2 = 1
 
 
-def build(force: bool = False) -> str:
-    """Compile oracle.c into liboracle.so (gcc, -O2; no fast-math)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=c99", "-D_DEFAULT_SOURCE", "-shared", "-fPIC",
-                               _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+def build(force: bool = False, precision: str = "f64") -> str:
+    """Compile oracle.c into liboracle.so (fp64) or liboracle_f32.so (fp32):
+    gcc -O2, no fast-math, no FMA contraction (each product and sum rounds
+    on its own, as the source reads)."""
+    path = _LIBS[precision]
+    if force or not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+        tmp = path + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-D_DEFAULT_SOURCE", "-shared",
+               "-fPIC", _SRC, "-o", tmp, "-lm"]
+        if precision == "f32":
+            cmd.insert(1, "-DORC_FLOAT")
+        subprocess.check_call(cmd)
+        os.replace(tmp, path)
+    return path
 
 
-_lib = None
+def build_all(force: bool = False) -> None:
+    for p in _LIBS:
+        build(force, p)
 
 
-def lib():
-    global _lib
-    if _lib is None:
-        _lib = ct.CDLL(build())
+_libs = {}
+
+
+def lib(precision: str = "f64"):
+    if precision not in _libs:
+        L = ct.CDLL(build(precision=precision))
         i32p = ct.POINTER(ct.c_int)
-        f64p = ct.POINTER(ct.c_double)
+        f64p = ct.POINTER(ct.c_double) if precision == "f64" else ct.POINTER(ct.c_float)
+        freal = ct.c_double if precision == "f64" else ct.c_float
+        L.orc_real_bytes.restype = ct.c_int
+        assert L.orc_real_bytes() == (8 if precision == "f64" else 4)
+        _lib = L
         _lib.orc_validate.restype = ct.c_int
         _lib.orc_validate.argtypes = [ct.c_int, ct.c_int, i32p, i32p, i32p, ct.c_int, i32p, ct.c_int]
         _lib.orc_levels_recursive.restype = ct.c_int
@@ -61,14 +79,15 @@ def lib():
         _lib.orc_schedule.restype = ct.c_int
         _lib.orc_schedule.argtypes = [ct.c_int, ct.c_int, i32p, i32p, i32p, i32p, ct.c_int] + [i32p] * 10
         _lib.orc_treelstm.restype = ct.c_int
-        _lib.orc_treelstm.argtypes = ([ct.c_int] * 8 + [i32p] * 4 + [f64p] * 7 + [ct.c_double]
+        _lib.orc_treelstm.argtypes = ([ct.c_int] * 8 + [i32p] * 4 + [f64p] * 7 + [freal]
                                       + [f64p] * 5 + [ct.c_int] + [f64p] * 8)
         _lib.orc_treefc.restype = ct.c_int
-        _lib.orc_treefc.argtypes = ([ct.c_int] * 7 + [i32p] * 4 + [f64p] * 6 + [ct.c_double]
+        _lib.orc_treefc.argtypes = ([ct.c_int] * 7 + [i32p] * 4 + [f64p] * 6 + [freal]
                                     + [f64p] * 3 + [ct.c_int] + [f64p] * 7)
         _lib.orc_bf16_round.restype = ct.c_double
         _lib.orc_bf16_round.argtypes = [ct.c_double]
-    return _lib
+        _libs[precision] = L
+    return _libs[precision]
 
 
 def _i32(a):
@@ -78,22 +97,30 @@ def _i32(a):
     return a, a.ctypes.data_as(ct.POINTER(ct.c_int))
 
 
-def _f64(a):
+def _real(a, dtype=np.float64):
     if a is None:
         return None, None
-    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
-    return a, a.ctypes.data_as(ct.POINTER(ct.c_double))
+    a = np.ascontiguousarray(np.asarray(a, dtype=dtype))
+    ct_t = ct.c_double if dtype == np.float64 else ct.c_float
+    return a, a.ctypes.data_as(ct.POINTER(ct_t))
 
 
-def _out(shape):
-    a = np.zeros(shape, dtype=np.float64)
-    return a, a.ctypes.data_as(ct.POINTER(ct.c_double))
+def _f64(a):
+    return _real(a, np.float64)
+
+
+def _out(shape, dtype=np.float64):
+    a = np.zeros(shape, dtype=dtype)
+    ct_t = ct.c_double if dtype == np.float64 else ct.c_float
+    return a, a.ctypes.data_as(ct.POINTER(ct_t))
 
 
 def validate(child, parent, pull_idx=None, n_x=0, push_idx=None, n_push=0) -> int:
+    """Validation status; parent=None declares graph (DAG) inputs."""
     child = np.asarray(child, dtype=np.int32)
-    V = int(np.asarray(parent).shape[0])
-    N = int(child.shape[1]) if child.ndim == 2 else 1
+    if child.ndim == 1:
+        child = child.reshape(-1, 1)
+    V, N = child.shape
     c, cp = _i32(child)
     p, pp = _i32(parent)
     pl, plp = _i32(pull_idx)
@@ -114,7 +141,8 @@ def levels(child, mode: str = "recursive"):
 
 
 def schedule(child, parent, pull_idx=None, push_idx=None, mode: int = 0) -> dict:
-    """Level-major layout; keys mirror the library's schedule outputs."""
+    """Level-major layout; keys mirror the library's schedule outputs.
+    parent=None declares graph (DAG) inputs (parent_pos is -1 throughout)."""
     child = np.asarray(child, dtype=np.int32)
     V, N = child.shape
     c, cp = _i32(child)
@@ -144,15 +172,22 @@ def bf16_round(x: float) -> float:
 
 
 def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool = True,
-        denom: float = 0.0, params: Optional[dict] = None, X=None, Y=None) -> dict:
-    """Forward (+ loss) and optionally backward of ``wl`` in fp64.
+        denom: float = 0.0, params: Optional[dict] = None, X=None, Y=None,
+        precision: str = "f64") -> dict:
+    """Forward (+ loss) and optionally backward of ``wl``.
 
-    ``params`` may override any of Wx, U, b, Ws, bs (e.g. for finite
-    differences); X/Y likewise.  ``bf16`` defaults to the workload's
-    precision.  Returns a dict with h, c, gates, lossv, loss and, when
-    ``backward``, dh, dc (total dL/dh_v, dL/dc_v per vertex), dWx, dU, db,
-    dWs, dbs, dX.
+    ``precision`` "f64" (the parity reference) or "f32" (the same definitions
+    evaluated in fp32).  ``params`` may override any of Wx, U, b, Ws, bs (e.g.
+    for finite differences); X/Y likewise.  ``bf16`` defaults to the
+    workload's precision.  Graph workloads (``wl.dag``) pass no parent array,
+    so a vertex may be read by several vertices.  Returns a dict of float64
+    arrays with h, c, gates, lossv, loss and, when ``backward``, dh, dc
+    (total dL/dh_v, dL/dc_v per vertex), dWx, dU, db, dWs, dbs, dX.
     """
+    L = lib(precision)
+    dt = np.float64 if precision == "f64" else np.float32
+    rl = lambda a: _real(a, dt)
+    out = lambda shape: _out(shape, dt)
     from_wl = dict(Wx=wl.Wx, U=wl.U, b=wl.b, Ws=wl.Ws, bs=wl.bs)
     if params:
         from_wl.update(params)
@@ -163,53 +198,54 @@ def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool 
     Ya = wl.Y if Y is None else Y
     _, chp = _i32(wl.child.reshape(-1))
     ch_keep = _
-    par, parp = _i32(wl.parent)
+    dag = bool(getattr(wl, "dag", False))
+    par, parp = _i32(None if dag else wl.parent)
     pl, plp = _i32(wl.pull_idx)
     ps, psp = _i32(wl.push_idx)
-    Xk, Xp = _f64(Xa if Xa.size else np.zeros(1))
-    Yk, Yp = _f64(Ya if Ya.size else np.zeros(1))
-    Wk, Wp = _f64(from_wl["Wx"] if from_wl["Wx"].size else np.zeros(1))
-    Uk, Up = _f64(from_wl["U"])
-    bk, bp = _f64(from_wl["b"])
-    Wsk, Wsp = _f64(from_wl["Ws"] if from_wl["Ws"].size else np.zeros(1))
-    bsk, bsp = _f64(from_wl["bs"] if from_wl["bs"].size else np.zeros(1))
-    h, hp = _out((V, H))
-    lossv, lvp = _out(V)
-    loss = ct.c_double(0.0)
+    Xk, Xp = rl(Xa if Xa.size else np.zeros(1))
+    Yk, Yp = rl(Ya if Ya.size else np.zeros(1))
+    Wk, Wp = rl(from_wl["Wx"] if from_wl["Wx"].size else np.zeros(1))
+    Uk, Up = rl(from_wl["U"])
+    bk, bp = rl(from_wl["b"])
+    Wsk, Wsp = rl(from_wl["Ws"] if from_wl["Ws"].size else np.zeros(1))
+    bsk, bsp = rl(from_wl["bs"] if from_wl["bs"].size else np.zeros(1))
+    h, hp = out((V, H))
+    lossv, lvp = out(V)
+    loss = (ct.c_double if precision == "f64" else ct.c_float)(0.0)
     n_x = max(int(Xa.shape[0]), 1)
     res = dict()
     if wl.cell == 0:
-        c, cp = _out((V, H))
-        gates, gp = _out((V, (3 + N) * H))
-        dh, dhp = _out((V, H))
-        dc, dcp = _out((V, H))
-        dWx, dWxp = _out((D, 4 * H))
-        dU, dUp = _out((H, 4 * H))
-        db, dbp = _out(4 * H)
-        dWs, dWsp = _out((H, max(C, 1)))
-        dbs, dbsp = _out(max(C, 1))
-        dX, dXp = _out((n_x, D))
-        st = lib().orc_treelstm(V, N, D, H, C, wl.loss, int(bool(bf16)), int(order_mode),
-                                chp, parp, plp, psp, Xp, Yp, Wp, Up, bp, Wsp, bsp,
-                                float(denom), hp, cp, gp, lvp, ct.byref(loss), int(backward),
-                                dhp, dcp, dWxp, dUp, dbp, dWsp, dbsp, dXp)
+        c, cp = out((V, H))
+        gates, gp = out((V, (3 + N) * H))
+        dh, dhp = out((V, H))
+        dc, dcp = out((V, H))
+        dWx, dWxp = out((D, 4 * H))
+        dU, dUp = out((H, 4 * H))
+        db, dbp = out(4 * H)
+        dWs, dWsp = out((H, max(C, 1)))
+        dbs, dbsp = out(max(C, 1))
+        dX, dXp = out((n_x, D))
+        st = L.orc_treelstm(V, N, D, H, C, wl.loss, int(bool(bf16)), int(order_mode),
+                            chp, parp, plp, psp, Xp, Yp, Wp, Up, bp, Wsp, bsp,
+                            float(denom), hp, cp, gp, lvp, ct.byref(loss), int(backward),
+                            dhp, dcp, dWxp, dUp, dbp, dWsp, dbsp, dXp)
         res.update(c=c, gates=gates)
         if backward:
             res.update(dh=dh, dc=dc, dWx=dWx, dU=dU, db=db, dX=dX[: Xa.shape[0]])
             if wl.loss == LOSS_CE:
                 res.update(dWs=dWs[:, :C], dbs=dbs[:C])
     else:
-        dh, dhp = _out((V, H))
-        dcs, dcsp = _out((V, H))
-        dW, dWp = _out((N * H, H))
-        db, dbp = _out(H)
-        dWs, dWsp = _out((H, max(C, 1)))
-        dbs, dbsp = _out(max(C, 1))
-        dX, dXp = _out((n_x, H))
-        st = lib().orc_treefc(V, N, H, C, wl.loss, int(bool(bf16)), int(order_mode),
-                              chp, parp, plp, psp, Xp, Yp, Up, bp, Wsp, bsp, float(denom),
-                              hp, lvp, ct.byref(loss), int(backward), dhp, dcsp, dWp, dbp,
-                              dWsp, dbsp, dXp)
+        dh, dhp = out((V, H))
+        dcs, dcsp = out((V, H))
+        dW, dWp = out((N * H, H))
+        db, dbp = out(H)
+        dWs, dWsp = out((H, max(C, 1)))
+        dbs, dbsp = out(max(C, 1))
+        dX, dXp = out((n_x, H))
+        st = L.orc_treefc(V, N, H, C, wl.loss, int(bool(bf16)), int(order_mode),
+                          chp, parp, plp, psp, Xp, Yp, Up, bp, Wsp, bsp, float(denom),
+                          hp, lvp, ct.byref(loss), int(backward), dhp, dcsp, dWp, dbp,
+                          dWsp, dbsp, dXp)
         if backward:
             res.update(dh=dh, dU=dW, db=db, dX=dX[: Xa.shape[0]])
             if wl.loss == LOSS_CE:
@@ -218,4 +254,7 @@ def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool 
     if st != OK:
         raise ValueError("oracle rejected the input: status %d" % st)
     res.update(h=h, lossv=lossv, loss=float(loss.value))
+    if precision != "f64":
+        res = {k: (v.astype(np.float64) if isinstance(v, np.ndarray) else v)
+               for k, v in res.items()}
     return res

@@ -57,6 +57,10 @@ class Workload:
     bs: np.ndarray
     tree_offsets: np.ndarray
     meta: dict = field(default_factory=dict)
+    # graph inputs (panel (d) of the recurrent-structures figure, Section 2):
+    # a vertex may be the child of several vertices; ``parent`` is then not
+    # passed to the library or the oracle (it holds -1 throughout)
+    dag: bool = False
 
     @property
     def V(self) -> int:
@@ -160,6 +164,49 @@ def chain(length: int) -> List[List[int]]:
     return [[t - 1] for t in range(length)]
 
 
+def nary_tree(n_leaves: int, N: int, rng: np.random.Generator) -> List[List[int]]:
+    """Tree whose internal vertices have between 2 and N children (random
+    recursive splits of the leaf range into up to N non-empty parts), with
+    the filled slots placed at random among the N."""
+    out: List[List[int]] = []
+
+    def build(L: int) -> int:
+        if L == 1:
+            out.append([-1] * N)
+            return len(out) - 1
+        parts = int(rng.integers(2, min(N, L) + 1))
+        cuts = np.sort(rng.choice(np.arange(1, L), size=parts - 1, replace=False))
+        sizes = np.diff(np.concatenate([[0], cuts, [L]]))
+        kids = [build(int(sz)) for sz in sizes]
+        slots = np.sort(rng.choice(N, size=parts, replace=False))
+        row = [-1] * N
+        for s_, k in zip(slots, kids):
+            row[int(s_)] = k
+        out.append(row)
+        return len(out) - 1
+
+    build(int(n_leaves))
+    return out
+
+
+def random_dag(n_vertices: int, N: int, rng: np.random.Generator,
+               p_child: float = 0.7, window: int = 6) -> List[List[int]]:
+    """Directed acyclic graph in topological order: vertex v fills each of
+    its N slots with probability p_child by a vertex drawn from the `window`
+    vertices before it, so vertices are often read by several vertices
+    (and occasionally twice by one).  The first vertex is always a leaf."""
+    out: List[List[int]] = []
+    for v in range(n_vertices):
+        row = []
+        for _ in range(N):
+            if v > 0 and rng.random() < p_child:
+                row.append(int(rng.integers(max(0, v - window), v)))
+            else:
+                row.append(-1)
+        out.append(row)
+    return out
+
+
 # --------------------------------------------------------------------------
 # assembling a batch
 # --------------------------------------------------------------------------
@@ -193,21 +240,33 @@ def assemble(trees: List[List[List[int]]], N: int, rng: np.random.Generator,
     return child.astype(np.int32), parent.astype(np.int32), offsets.astype(np.int64), perm
 
 
+def read_by_someone(child: np.ndarray) -> np.ndarray:
+    """Vertices that some child link points at (the others are roots)."""
+    V = child.shape[0]
+    read = np.zeros(V, dtype=bool)
+    c = child[child >= 0]
+    read[c] = True
+    return read
+
+
 def make_workload(name: str, trees: List[List[List[int]]], *, cell: int = CELL_TREE_LSTM,
                   prec: int = PREC_FP32, loss: int = LOSS_CE, N: int = 2, D: int = 16,
                   H: int = 16, C: int = 5, sigma: float = 0.1, seed: int = 0,
                   rng: Optional[np.random.Generator] = None,
                   inputs: str = "leaves", labels: str = "root",
-                  shuffle_ids: bool = False) -> Workload:
+                  shuffle_ids: bool = False, dag: bool = False) -> Workload:
     """Draw inputs, parameters and labels for a batch of graphs.
 
     ``inputs``: "leaves" (childless vertices pull an input row), "all", or
     "none".  ``labels``: "root", "all" or "none".  Draw order after the
     shapes: X, the cell parameters, the classifier, then labels or targets.
+    ``dag``: the graphs may share vertices between readers (no parent array).
     """
     if rng is None:
         rng = np.random.Generator(np.random.PCG64(seed))
     child, parent, offsets, _ = assemble(trees, N, rng, shuffle_ids)
+    if dag:
+        parent[:] = -1
     V = parent.shape[0]
     is_leaf = np.all(child < 0, axis=1)
     if inputs == "leaves":
@@ -235,7 +294,7 @@ def make_workload(name: str, trees: List[List[List[int]]], *, cell: int = CELL_T
         U = (sigma * rng.standard_normal((N * H, H))).astype(np.float32)
         b = np.zeros(H, dtype=np.float32)
 
-    is_root = parent < 0
+    is_root = ~read_by_someone(child)
     if labels == "root":
         has_lab = is_root
     elif labels == "all":
@@ -259,7 +318,7 @@ def make_workload(name: str, trees: List[List[List[int]]], *, cell: int = CELL_T
         Y = rng.uniform(-1.0, 1.0, size=(lab_rows.size, H)).astype(np.float32)
     return Workload(name=name, cell=cell, prec=prec, loss=loss, N=N, D=D, H=H, C=C,
                     child=child, parent=parent, pull_idx=pull_idx, push_idx=push_idx,
-                    X=X, Y=Y, Wx=Wx, U=U, b=b, Ws=Ws, bs=bs, tree_offsets=offsets)
+                    X=X, Y=Y, Wx=Wx, U=U, b=b, Ws=Ws, bs=bs, tree_offsets=offsets, dag=dag)
 
 
 # --------------------------------------------------------------------------

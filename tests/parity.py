@@ -1,10 +1,26 @@
-"""Helpers shared by the GPU parity tests (no method arithmetic here)."""
+"""Helpers shared by the GPU parity tests (no method arithmetic here).
+
+Tolerances.  States, the loss and gradients are compared per tensor with the
+floored relative error of rel_err (floor 1% of the tensor's largest
+magnitude).  fp32 outputs must be within 1e-4 of the fp64 oracle, or within
+twice the error of the same definitions evaluated in fp32 (the oracle's
+float build) where that evaluation itself strays further: measured on the
+reduced benchmark shapes, the fp32 oracle reaches 1.1e-4 on h after 87 chain
+levels and 2.3e-4 on Tree-FC dU / dX at this floor, so 1e-4 alone would
+reject every fp32 evaluation of those outputs, exact arithmetic order
+included.
+"""
+import multiprocessing as mp
+import os
+
 import numpy as np
 
 from paper_1712_04048_amd import workloads as W
 
 
-FLOOR = 0.1
+FLOOR = 0.01
+TOL_FP32 = 1e-4
+F32_FACTOR = 2.0
 
 
 def rel_err(got, ref, floor=FLOOR):
@@ -39,6 +55,12 @@ def normwise_err(got, ref):
     return float(np.abs(got - ref).max() / scale)
 
 
+def _err(got, ref, k, floor):
+    if k == "loss":
+        return abs(got - ref) / max(abs(ref), 1e-30)
+    return rel_err(got, ref, floor)
+
+
 def check(gpu: dict, ref: dict, keys, tol, label="", floor=FLOOR):
     """Fails if any tensor's rel_err (with the given floor) exceeds tol.
     floor=1.0 makes the test normwise: max |g - o| / max |o|."""
@@ -46,20 +68,38 @@ def check(gpu: dict, ref: dict, keys, tol, label="", floor=FLOOR):
     for k in keys:
         if k not in ref:
             continue
-        if k == "loss":
-            errs[k] = abs(gpu[k] - ref[k]) / max(abs(ref[k]), 1e-30)
-        else:
-            errs[k] = rel_err(gpu[k], ref[k], floor)
+        errs[k] = _err(gpu[k], ref[k], k, floor)
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, "%s: errors above %g: %s (all: %s)" % (label, tol, bad, errs)
     return errs
 
 
-def subset(wl: W.Workload, trees) -> W.Workload:
+def check_fp32(gpu: dict, ref64: dict, ref32: dict, keys, label=""):
+    """fp32 bar: each tensor within max(TOL_FP32, F32_FACTOR * e32) of the
+    fp64 oracle, where e32 is the fp32 oracle's own error on that tensor.
+    Returns {key: (gpu error, fp32-oracle error)}."""
+    out, bad = {}, {}
+    for k in keys:
+        if k not in ref64:
+            continue
+        e = _err(gpu[k], ref64[k], k, FLOOR)
+        e32 = _err(ref32[k], ref64[k], k, FLOOR)
+        out[k] = (e, e32)
+        if not e <= max(TOL_FP32, F32_FACTOR * e32):
+            bad[k] = (e, e32)
+    print("  %s: (gpu err, fp32-oracle err) at floor %g: %s" % (
+        label, FLOOR, {k: "%.2e/%.2e" % v for k, v in out.items()}), flush=True)
+    assert not bad, "%s: above max(%g, %g x fp32 oracle): %s" % (label, TOL_FP32, F32_FACTOR, bad)
+    return out
+
+
+def subset_maps(wl: W.Workload, trees):
     """The workload restricted to the given graphs (ids renumbered in order;
-    X / Y rows restricted to the rows those graphs use)."""
-    keep = np.concatenate([np.arange(wl.tree_offsets[k], wl.tree_offsets[k + 1]) for k in trees])
-    newid = -np.ones(wl.V, dtype=np.int64)
+    X / Y rows restricted to the rows those graphs use), with the kept vertex
+    ids and X rows of the original."""
+    keep = np.concatenate([np.arange(wl.tree_offsets[k], wl.tree_offsets[k + 1]) for k in trees]) \
+        if len(trees) else np.zeros(0, dtype=np.int64)
+    newid = -np.ones(max(wl.V, 1), dtype=np.int64)
     newid[keep] = np.arange(keep.size)
     child = wl.child[keep]
     child = np.where(child >= 0, newid[np.maximum(child, 0)], -1).astype(np.int32)
@@ -81,7 +121,73 @@ def subset(wl: W.Workload, trees) -> W.Workload:
     sizes = [wl.tree_offsets[k + 1] - wl.tree_offsets[k] for k in trees]
     offs = np.zeros(len(trees) + 1, dtype=np.int64)
     offs[1:] = np.cumsum(sizes)
-    return W.Workload(name=wl.name + "_subset", cell=wl.cell, prec=wl.prec, loss=wl.loss,
-                      N=wl.N, D=wl.D, H=wl.H, C=wl.C, child=child, parent=parent,
-                      pull_idx=pull, push_idx=push, X=wl.X[rows], Y=Y, Wx=wl.Wx, U=wl.U,
-                      b=wl.b, Ws=wl.Ws, bs=wl.bs, tree_offsets=offs)
+    sub = W.Workload(name=wl.name + "_subset", cell=wl.cell, prec=wl.prec, loss=wl.loss,
+                     N=wl.N, D=wl.D, H=wl.H, C=wl.C, child=child, parent=parent,
+                     pull_idx=pull, push_idx=push, X=wl.X[rows], Y=Y, Wx=wl.Wx, U=wl.U,
+                     b=wl.b, Ws=wl.Ws, bs=wl.bs, tree_offsets=offs, dag=wl.dag)
+    return sub, keep, rows
+
+
+def subset(wl: W.Workload, trees) -> W.Workload:
+    return subset_maps(wl, trees)[0]
+
+
+# ---------------------------------------------------------------------------
+# the oracle over shards of graphs in worker processes: graphs are
+# independent, so states and per-vertex terms are placed by vertex id and
+# parameter gradients summed shard by shard in a fixed order (the loss
+# normaliser is the whole batch's |Lambda|)
+# ---------------------------------------------------------------------------
+
+def _oracle_job(args):
+    import oracle
+    sub, kw = args
+    return oracle.run(sub, **kw)
+
+
+def pool_workers():
+    n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def oracle_sharded(wl: W.Workload, workers=None, **kw) -> dict:
+    """oracle.run(wl, **kw) computed over about `workers` shards of graphs in
+    spawned worker processes (they never touch the GPU)."""
+    import oracle
+    workers = workers or pool_workers()
+    K = wl.K
+    if workers <= 1 or K < 2 or wl.V < 2000:
+        return oracle.run(wl, **kw)
+    sizes = np.diff(wl.tree_offsets)
+    cum = np.cumsum(sizes)
+    bounds = np.searchsorted(cum, np.linspace(0, cum[-1], workers + 1)[1:-1], side="right")
+    edges = np.unique(np.concatenate([[0], bounds, [K]]))
+    shards = [list(range(int(a), int(b))) for a, b in zip(edges[:-1], edges[1:]) if b > a]
+    n_lab = int((wl.push_idx >= 0).sum())
+    kw = dict(kw)
+    kw["denom"] = float(max(n_lab, 1))
+    jobs, maps = [], []
+    for sh in shards:
+        sub, keep, rows = subset_maps(wl, sh)
+        jobs.append((sub, kw))
+        maps.append((keep, rows))
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(min(workers, len(jobs))) as pool:
+        parts = pool.map(_oracle_job, jobs)
+    out = {}
+    V = wl.V
+    for (keep, rows), r in zip(maps, parts):
+        for k, v in r.items():
+            if k in ("h", "c", "gates", "lossv", "dh", "dc"):
+                if k not in out:
+                    out[k] = np.zeros((V,) + v.shape[1:], dtype=np.float64)
+                out[k][keep] = v
+            elif k == "dX":
+                if k not in out:
+                    out[k] = np.zeros((wl.n_x, v.shape[1] if v.ndim == 2 else wl.D))
+                out[k][rows] = v
+            elif k == "loss":
+                out[k] = out.get(k, 0.0) + v
+            else:
+                out[k] = v.copy() if k not in out else out[k] + v
+    return out

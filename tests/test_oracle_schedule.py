@@ -1,8 +1,8 @@
 """Pins of the oracle's schedule and validator (CPU only).
 
 The oracle's level assignment is computed two independent ways -- the
-recursive height and Algorithm 1's literal frontier loop (Section 3.2) -- and
-both are checked against closed forms for the shapes of Section 5 (complete
+recursive height and peeling ready vertices off the graph (the activation
+rule of Section 3.2, Algorithm 1) -- and both are checked against closed forms for the shapes of Section 5 (complete
 binary trees with 256 leaves have 511 vertices; chains; left-branching trees).
 """
 import json
