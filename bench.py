@@ -12,6 +12,9 @@ Prints one JSON line with the throughput, a roofline entry for the kernel
 that takes the most time (per-launch algorithmic FLOPs over its mean launch
 duration, from HIP events on the library's stream) and the CPU oracle timed
 on a bounded sample of the same workload.
+
+--workload selects one of the other benchmark-shaped batches (tiny, varlstm,
+treefc, deep_bf16) for the same report; the default is the headline one.
 """
 import argparse
 import json
@@ -35,8 +38,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-trees", type=int, default=256,
-                    help="graphs in the CPU-oracle sample (0 skips the CPU baseline)")
+    ap.add_argument("--workload", default="sst",
+                    choices=["sst", "tiny", "varlstm", "treefc", "deep_bf16"])
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the engine ablations (the persistent variant launches "
+                         "cooperatively) and the inference passes")
     return ap.parse_args()
 
 
@@ -109,22 +116,56 @@ def measured_traffic(workload, kernel):
             k["write_kib"] * rec["copy_bytes"] / rec["copy_write_kib"])
 
 
-def cpu_baseline(wl, n_trees):
-    """The oracle as it stands (fp64, recursive, one thread) on the first
-    n_trees graphs of the batch."""
+# graphs in the CPU-oracle samples: (one thread, all cores), chosen so the
+# baseline costs about 10-30 s of CPU time on the GPU machine
+CPU_SAMPLE = {"sst": (48, 256), "tiny": (8, 8), "varlstm": (12, 64), "treefc": (12, 64),
+              "deep_bf16": (2, 24)}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(wl, key):
+    """The oracle as it stands, in its fp32 build (the same definitions the
+    GPU path computes, in the GPU path's precision; bf16 workloads emulate
+    the rounding), forward + loss + backward: on one thread over the first
+    graphs of the batch, and on all cores (one worker process per core, up
+    to 16, each running the oracle on a shard of graphs; partial gradients
+    summed in a fixed order) over a larger sample."""
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     import oracle
-    from parity import subset
-    n_trees = min(n_trees, wl.K)
-    sub = subset(wl, list(range(n_trees)))
-    oracle.lib()
+    from parity import OraclePool, subset
+    n1, nall = CPU_SAMPLE[key]
+    n1, nall = min(n1, wl.K), min(nall, wl.K)
+    oracle.lib("f32")
+    sub1 = subset(wl, list(range(n1)))
     t0 = time.perf_counter()
-    oracle.run(sub)
-    dt = time.perf_counter() - t0
-    return {"value": sub.V / dt, "unit": "vertices/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d graphs (%d of %d vertices), fp64 recursive oracle, "
-                      "forward + loss + backward, one thread, %.1f s"
-                      % (n_trees, wl.K, sub.V, wl.V, dt)}
+    oracle.run(sub1, precision="f32")
+    dt1 = time.perf_counter() - t0
+    suball = subset(wl, list(range(nall)))
+    with OraclePool() as pool:
+        pool.run(subset(wl, [0]), precision="f32", backward=False)   # workers started
+        t0 = time.perf_counter()
+        pool.run(suball, precision="f32")
+        dta = time.perf_counter() - t0
+        workers = pool.workers
+    return {"value": suball.V / dta, "unit": "vertices/s", "cores": workers, "kind": "oracle",
+            "sample": "first %d of %d graphs (%d of %d vertices), fp32 build of the recursive "
+                      "oracle, forward + loss + backward, %d worker processes (one thread "
+                      "each), %.2f s" % (nall, wl.K, suball.V, wl.V, workers, dta),
+            "single_thread": {"value": sub1.V / dt1, "unit": "vertices/s", "cores": 1,
+                              "sample": "first %d graphs (%d vertices), %.2f s"
+                                        % (n1, sub1.V, dt1)},
+            "nproc": os.cpu_count(), "cpu_model": cpu_model()}
 
 
 def main():
@@ -143,7 +184,8 @@ def main():
     from paper_1712_04048_amd.runner import Batch
 
     torch.cuda.set_device(0)
-    wl = W.config_treelstm_sst(args.seed)
+    wl = W.WORKLOADS[args.workload](args.seed)
+    lstm = wl.cell == W.CELL_TREE_LSTM
     ctx = B.Context(0)
     batch = Batch(wl, ctx)
     batch.schedule()
@@ -152,7 +194,7 @@ def main():
 
     for _ in range(args.warmup):
         batch.step()
-    torch.cuda.synchronize()
+    ctx.sync()
 
     # timed region: K whole steps (schedule + forward + backward)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -191,43 +233,54 @@ def main():
         try:
             batch.forward()
             batch.backward()
-            torch.cuda.synchronize()
+            ctx.sync()
             e0.record(stream)
             for _ in range(args.steps):
                 batch.forward()
                 batch.backward()
             e1.record(stream)
-            torch.cuda.synchronize()
+            ctx.sync()
             return e0.elapsed_time(e1) / args.steps
         finally:
             del os.environ[var]
 
-    eager_ms = fwd_bwd_with("CAVS_EAGER_DW")
-    persist_ms = fwd_bwd_with("CAVS_PERSIST")
-    unfused_ms = fwd_bwd_with("CAVS_UNFUSED_BWD_GATES")
+    ablation = None
+    if lstm and not args.no_ablation:
+        ablation = {"unit": "ms per forward + backward pass",
+                    "lazy_dw_per_level_launches": round(fwdbwd_ms, 4)}
+        ablation["eager_dw_per_level"] = round(fwd_bwd_with("CAVS_EAGER_DW"), 4)
+        ablation["persistent_small_levels"] = round(fwd_bwd_with("CAVS_PERSIST"), 4)
+        ablation["unfused_backward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_BWD_GATES"), 4)
 
     # inference (cavs_infer: the forward keeping nothing for a backward) beside
     # the training forward alone; whole inference steps include the schedule
-    batch.infer()
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        batch.forward()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    fwd_ms = e0.elapsed_time(e1) / args.steps
-    e0.record(stream)
-    for _ in range(args.steps):
+    inference = None
+    if not args.no_ablation:
         batch.infer()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    infer_ms = e0.elapsed_time(e1) / args.steps
-    t3 = time.perf_counter()
-    for _ in range(args.steps):
-        batch.schedule()
-        batch.infer()
-    torch.cuda.synchronize()
-    infer_step_ms = (time.perf_counter() - t3) * 1e3 / args.steps
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            batch.forward()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        fwd_ms = e0.elapsed_time(e1) / args.steps
+        e0.record(stream)
+        for _ in range(args.steps):
+            batch.infer()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        infer_ms = e0.elapsed_time(e1) / args.steps
+        t3 = time.perf_counter()
+        for _ in range(args.steps):
+            batch.schedule()
+            batch.infer()
+        torch.cuda.synchronize()
+        infer_step_ms = (time.perf_counter() - t3) * 1e3 / args.steps
+        inference = {"value": wl.V / (infer_step_ms * 1e-3), "unit": "vertices/s",
+                     "step": "cavs_schedule + cavs_infer", "ms_per_step": round(infer_step_ms, 4),
+                     "infer_ms": round(infer_ms, 4), "train_forward_ms": round(fwd_ms, 4),
+                     "workspace_mb": round(batch.ws_infer.numel() / 2 ** 20, 1),
+                     "train_workspace_mb": round(batch.ws.numel() / 2 ** 20, 1)}
 
     # per-kernel durations: the same steps again with per-launch HIP events
     ctx.timing(True)
@@ -275,7 +328,7 @@ def main():
     if fl > 0:
         per_launch = fl / launches
         achieved = per_launch / (avg_ms * 1e-3) / 1e12
-        bf = "_bf" in dom["name"] or ", true>" in dom["name"]
+        bf = "_bf" in dom["name"] or ", true>" in dom["name"] or ", true," in dom["name"]
         peak = PEAK_BF16_TFLOPS if bf else PEAK_FP32_TFLOPS
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None}
@@ -294,8 +347,12 @@ def main():
     roof["algorithmic_per_launch"] = per_launch
 
     total_flops = sum(a[2] for a in agg.values()) / args.steps
+    loss_desc = ("softmax CE at every vertex" if wl.loss == W.LOSS_CE and
+                 (wl.push_idx >= 0).all() else
+                 "softmax CE at the roots" if wl.loss == W.LOSS_CE else "L2 at the roots")
     out = {
-        "metric": METRIC,
+        "metric": METRIC if args.workload == "sst" else
+        "%s fwd+bwd vertices/sec" % wl.name,
         "value": wl.V / (wall_ms * 1e-3),
         "unit": "vertices/s",
         "n_gpus": 1,
@@ -305,32 +362,29 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16" if wl.prec == W.PREC_BF16 else "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "graphs": wl.K, "vertices": wl.V, "levels": sh["T"],
-                   "D": wl.D, "H": wl.H, "loss": "softmax CE at every vertex",
-                   "seed": args.seed},
+                   "D": wl.D, "H": wl.H, "loss": loss_desc, "seed": args.seed},
         "roofline": roof,
         "gpu_ms_per_step": round(gpu_ms, 4),
         "schedule_ms": round(sched_ms, 4),
         "fwd_bwd_ms": round(fwdbwd_ms, 4),
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
-        "ablation": {"unit": "ms per forward + backward pass", "lazy_dw_per_level_launches":
-                     round(fwdbwd_ms, 4), "eager_dw_per_level": round(eager_ms, 4),
-                     "persistent_small_levels": round(persist_ms, 4),
-                     "unfused_backward_gates": round(unfused_ms, 4)},
-        "inference": {"value": wl.V / (infer_step_ms * 1e-3), "unit": "vertices/s",
-                      "step": "cavs_schedule + cavs_infer", "ms_per_step": round(infer_step_ms, 4),
-                      "infer_ms": round(infer_ms, 4), "train_forward_ms": round(fwd_ms, 4),
-                      "workspace_mb": round(batch.ws_infer.numel() / 2 ** 20, 1),
-                      "train_workspace_mb": round(batch.ws.numel() / 2 ** 20, 1)},
         "whole_step_tflops": round(total_flops / (wall_ms * 1e-3) / 1e12, 2),
         "algorithmic_gflop_per_step": round(total_flops / 1e9, 3),
         "kernels": kernels,
         "levels_us": {"columns": ["rows", "fwd", "bwd_gates", "bwd_gemm"], "rows": level_table},
     }
-    if args.cpu_trees > 0:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_trees)
+    if ablation is not None:
+        out["ablation"] = ablation
+    if inference is not None:
+        out["inference"] = inference
+    ctx.sync()
+    batch = None
+    ctx.close()
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, args.workload)
     print(json.dumps(out), flush=True)
 
 

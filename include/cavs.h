@@ -40,6 +40,13 @@
  *                                 backward product;
  *       CAVS_PERSIST=1            the small levels in one persistent launch
  *                                 with grid barriers.
+ *     A fourth is a failure-injection hook for tests of the error path:
+ *       CAVS_PERSIST_SPIN=n       the persistent loop's grid barrier gives up
+ *                                 after n polls (n < 0: at once) and records
+ *                                 the error that cavs_sync reports.
+ *   - Errors found by kernels after a call has returned (a bounded wait that
+ *     gave up) are kept by the context and returned by the next cavs_sync or
+ *     cavs_timing_read.
  */
 #ifndef CAVS_H
 #define CAVS_H
@@ -86,6 +93,11 @@ void cavs_destroy(cavs_ctx* ctx);
 /* Host string describing the last error on ctx; owned by ctx, valid until
    the next call on ctx.  Never NULL. */
 const char* cavs_last_error(const cavs_ctx* ctx);
+/* Waits for all work enqueued on the context's stream, then returns
+   CAVS_ERR_HIP if a kernel of an earlier call recorded an error (the
+   persistent level loop's bounded grid barrier gave up: that call's outputs
+   are invalid), else CAVS_OK.  The record is cleared by the report. */
+cavs_status cavs_sync(cavs_ctx* ctx);
 
 /* ---------------------------------------------------------------------------
  * Scheduling (Algorithm 1; dynamic tensors of Section 3.3, Algorithm 2)
@@ -248,7 +260,8 @@ cavs_status cavs_timing_enable(cavs_ctx* ctx, int32_t on);
 /* Synchronises the context's stream, writes the pending launch records, in
    launch order, to out[0..max) (host array, caller-owned), clears them, and
    returns the number of records (which may exceed max; only max are
-   written), or a negative status. */
+   written), or a negative status (a kernel error recorded since the last
+   report, as for cavs_sync; the records are still written). */
 int32_t cavs_timing_read(cavs_ctx* ctx, cavs_launch_time* out, int32_t max);
 
 #ifdef __cplusplus

@@ -72,7 +72,7 @@ class cavs_launch_time(ct.Structure):
     _fields_ = [("name", ct.c_char * 96), ("row0", _i32), ("rows", _i32), ("ms", ct.c_double)]
 
 
-EXPORTS = ["cavs_create", "cavs_set_stream", "cavs_destroy", "cavs_last_error",
+EXPORTS = ["cavs_create", "cavs_set_stream", "cavs_destroy", "cavs_last_error", "cavs_sync",
            "cavs_schedule_workspace_bytes", "cavs_schedule", "cavs_workspace_bytes",
            "cavs_forward", "cavs_backward", "cavs_infer_workspace_bytes", "cavs_infer",
            "cavs_timing_enable", "cavs_timing_read"]
@@ -95,6 +95,8 @@ def lib():
         L.cavs_destroy.argtypes = [_vp]
         L.cavs_last_error.restype = ct.c_char_p
         L.cavs_last_error.argtypes = [_vp]
+        L.cavs_sync.restype = _i32
+        L.cavs_sync.argtypes = [_vp]
         L.cavs_schedule_workspace_bytes.restype = ct.c_size_t
         L.cavs_schedule_workspace_bytes.argtypes = [_i32, _i32, _i32]
         L.cavs_schedule.restype = _i32
@@ -160,6 +162,10 @@ class Context:
     def check(self, st: int):
         if st != OK:
             raise CavsError(st, lib().cavs_last_error(self._h).decode())
+
+    def sync(self):
+        """cavs_sync: waits for the context's stream; raises on a kernel-recorded error."""
+        self.check(lib().cavs_sync(self._h))
 
     def set_stream(self, stream: torch.cuda.Stream):
         self.check(lib().cavs_set_stream(self._h, stream.cuda_stream))

@@ -36,6 +36,14 @@ cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...) {
   return st;
 }
 
+cavs_status device_errors(cavs_ctx* ctx) {
+  if (!ctx->dev_err || !ctx->dev_err[0]) return CAVS_OK;
+  ctx->dev_err[0] = 0;
+  return fail(ctx, CAVS_ERR_HIP,
+              "a persistent level loop's grid barrier gave up waiting in an earlier call on "
+              "this context: that call's states and gradients are invalid");
+}
+
 namespace {
 
 // Workspace of forward + backward, all level-major (row = position).  In
@@ -231,12 +239,17 @@ cavs_status cavs_create(cavs_ctx** out, int32_t device, void* hip_stream) {
       hipHostMalloc((void**)&ctx->host_stage, sizeof(int32_t) * kHostStageInts,
                     hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
       hipHostGetDevicePointer((void**)&ctx->host_stage_dev, ctx->host_stage, 0) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->stage_ready, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&ctx->stage_ready, hipEventDisableTiming) != hipSuccess ||
+      hipHostMalloc((void**)&ctx->dev_err, 64, hipHostMallocMapped | hipHostMallocCoherent) !=
+          hipSuccess ||
+      hipHostGetDevicePointer((void**)&ctx->dev_err_dev, ctx->dev_err, 0) != hipSuccess) {
     if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
+    if (ctx->dev_err) (void)hipHostFree(ctx->dev_err);
     if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
     delete ctx;
     return CAVS_ERR_HIP;
   }
+  ctx->dev_err[0] = 0;
   *out = ctx;
   return CAVS_OK;
 }
@@ -250,6 +263,7 @@ cavs_status cavs_set_stream(cavs_ctx* ctx, void* hip_stream) {
 void cavs_destroy(cavs_ctx* ctx) {
   if (!ctx) return;
   if (ctx->host_stage) (void)hipHostFree(ctx->host_stage);
+  if (ctx->dev_err) (void)hipHostFree(ctx->dev_err);
   if (ctx->stage_ready) (void)hipEventDestroy(ctx->stage_ready);
   for (auto& r : ctx->timed) {
     (void)hipEventDestroy(r.start);
@@ -274,6 +288,7 @@ int32_t cavs_timing_read(cavs_ctx* ctx, cavs_launch_time* out, int32_t max) {
   if (!ctx || (max > 0 && !out)) return CAVS_ERR_ARG;
   if (hipStreamSynchronize(ctx->stream) != hipSuccess)
     return fail(ctx, CAVS_ERR_HIP, "hipStreamSynchronize failed");
+  const cavs_status derr = device_errors(ctx);
   int32_t n = 0;
   for (auto& r : ctx->timed) {
     float ms = 0.f;
@@ -290,7 +305,15 @@ int32_t cavs_timing_read(cavs_ctx* ctx, cavs_launch_time* out, int32_t max) {
     ctx->event_pool.push_back(r.stop);
   }
   ctx->timed.clear();
-  return n;
+  return derr != CAVS_OK ? derr : n;
+}
+
+cavs_status cavs_sync(cavs_ctx* ctx) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  CAVS_HIP_CHECK(ctx, hipSetDevice(ctx->device));
+  CAVS_HIP_CHECK(ctx, hipStreamSynchronize(ctx->stream));
+  return device_errors(ctx);
 }
 
 const char* cavs_last_error(const cavs_ctx* ctx) {

@@ -27,6 +27,8 @@ struct cavs_ctx {
   std::vector<cavs_timed_launch> timed;   // pending records
   std::vector<hipEvent_t> event_pool;     // reusable events
   hipEvent_t stage_ready = nullptr;       // the schedule's host stage has arrived
+  int32_t* dev_err = nullptr;             // pinned, coherent, mapped: set by kernels whose
+  int32_t* dev_err_dev = nullptr;         // bounded waits gave up (device view of dev_err)
 };
 
 namespace cavs {
@@ -40,6 +42,9 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // error plumbing
 // ---------------------------------------------------------------------------
 cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...);
+// After the context's stream has been synchronised: CAVS_OK, or the error a
+// kernel recorded in ctx->dev_err since the last check (then cleared).
+cavs_status device_errors(cavs_ctx* ctx);
 
 #define CAVS_HIP_CHECK(ctx, call)                                              \
   do {                                                                         \

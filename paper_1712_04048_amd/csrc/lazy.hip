@@ -1303,20 +1303,26 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
 #pragma unroll
     for (int v = 1; v < NW; ++v) z += zp[v][4 * g + i][r];
     z += bsc;
-    float m = cval ? z : -INFINITY;
+    // log-sum-exp and softmax of the logits in fp64 (C exponentials per
+    // vertex, a negligible cost): with small logits every vertex computes
+    // nearly the same lse, so an fp32 rounding of it would repeat in every
+    // row of dZ and add up coherently in the sums over vertices (db, db_s)
+    const double zd = (double)z;
+    double m = cval ? zd : -INFINITY;
 #pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-    float se = cval ? expf(z - m) : 0.f;
+    for (int o = 8; o >= 1; o >>= 1) m = fmax(m, __shfl_xor(m, o, kWave));
+    double se = cval ? exp(zd - m) : 0.0;
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) se += __shfl_xor(se, o, kWave);
-    const float lse = m + logf(se);
+    const double lse = m + log(se);
     float d = 0.f;
-    if (q[i] >= 0 && cval) d = (expf(z - lse) - (r == q[i] ? 1.f : 0.f)) * n.inv_denom;
+    if (q[i] >= 0 && cval)
+      d = (float)((exp(zd - lse) - (r == q[i] ? 1.0 : 0.0)) * (double)n.inv_denom);
     dzl[w][4 * g + i][r] = d;
     if (w == 0 && p < V) {
       if (r < CP && n.dZ) n.dZ[(size_t)p * CP + r] = d;
       if (q[i] < 0 && r == 0) n.lossv[p] = 0.f;
-      if (q[i] >= 0 && r == q[i]) n.lossv[p] = lse - z;
+      if (q[i] >= 0 && r == q[i]) n.lossv[p] = (float)(lse - zd);
     }
   }
   if (!n.dHL) return;   // inference: no gradient of the head

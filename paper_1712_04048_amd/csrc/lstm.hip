@@ -942,15 +942,25 @@ __global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_bwd_level_sk(Net n, int 
 //
 // Grid barrier: counters only grow (zeroed before the launch).  Barrier e
 // completes when the root counter reaches (e+1) * groups; the last arrival
-// publishes gen = e+1.  Waiting is bounded: after kBarrierSpin polls the
-// barrier records an error flag and returns rather than hang.
+// publishes gen = e+1.  Waiting is bounded: after `spin` polls (kBarrierSpin
+// unless the CAVS_PERSIST_SPIN test hook sets another; a negative value gives
+// up at once) the barrier records an error flag -- in the workspace and in
+// the context's mapped host word, which cavs_sync reports -- and returns
+// rather than hang.  The launch's results are then invalid.
 constexpr int kBarrierSpin = 1 << 24;
 
 struct GridBar {
   int* cnt;   // [1 + groups]: root, then one counter per group of 16 workgroups
   int* gen;
   int* err;
+  int* host_err;   // mapped pinned word of the context (may be null)
+  int spin;
 };
+
+__device__ __forceinline__ void grid_bar_gave_up(const GridBar& b) {
+  atomicOr(b.err, 1);
+  if (b.host_err) __hip_atomic_store(b.host_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
 
 __device__ __forceinline__ void grid_sync(const GridBar& b, int& epoch) {
   __syncthreads();
@@ -967,11 +977,13 @@ __device__ __forceinline__ void grid_sync(const GridBar& b, int& epoch) {
     if (release) {
       __threadfence();
       atomicAdd(b.gen, 1);
+    } else if (b.spin < 0) {
+      grid_bar_gave_up(b);
     } else {
       int it = 0;
       while (__hip_atomic_load(b.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= epoch) {
-        if (++it > kBarrierSpin) {
-          atomicOr(b.err, 1);
+        if (++it > b.spin) {
+          grid_bar_gave_up(b);
           break;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -1187,7 +1199,9 @@ bool launch_persist(const char* name, const void* fn, const Net& n, const int* l
   if (G > 512) G = 512;
   if (G > tiles) G = tiles;
   if (G <= 0) return false;
-  GridBar gb{bar, bar + 64, bar + 65};
+  int spin = kBarrierSpin;
+  if (const char* e = getenv("CAVS_PERSIST_SPIN")) spin = atoi(e);
+  GridBar gb{bar, bar + 64, bar + 65, t_active_ctx ? t_active_ctx->dev_err_dev : nullptr, spin};
   void* args[] = {(void*)&n, (void*)&lo, (void*)&t0, (void*)&t1, (void*)&gb};
   if (hipMemsetAsync(bar, 0, 256 * sizeof(int), s) != hipSuccess) return false;
   TimedScope ts(name, s, lo_host[t0], lo_host[t1] - lo_host[t0], /*bracket=*/true);

@@ -3,6 +3,7 @@
 #pragma once
 
 #include "kernels.h"
+#include "xcd_map.h"
 
 namespace cavs {
 
@@ -381,22 +382,11 @@ __device__ __forceinline__ void ld8(const float* p, float (&v)[8]) {
   v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
 }
 
-// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch), and each
-// XCD has its own L2.  Tiles are mapped so that XCD x only touches unit tiles
-// x, x+8, ...: each L2 then holds 1/8 of the weight columns instead of all.
-// With a unit-tile count that is not a multiple of 8 (narrow layers) the
-// plain row-major order is used: the mapping above needs at least 8 and
-// would otherwise divide by zero.
+// XCD-aware tile order of a launch (xcd_map.h).
 __device__ __forceinline__ void xcd_tile(int n_unit_tiles, int& row_tile, int& unit_tile) {
-  const int bid = blockIdx.x;
-  if (n_unit_tiles & 7) {
-    unit_tile = bid % n_unit_tiles;
-    row_tile = bid / n_unit_tiles;
-    return;
-  }
-  const int xcd = bid & 7, local = bid >> 3, per = n_unit_tiles >> 3;
-  unit_tile = xcd + 8 * (local % per);
-  row_tile = local / per;
+  const TileIdx t = xcd_tile_map(blockIdx.x, n_unit_tiles);
+  row_tile = t.row_tile;
+  unit_tile = t.unit_tile;
 }
 
 }  // namespace cavs

@@ -97,7 +97,7 @@ class Batch:
         if self.ws is None:
             self.alloc()
         self.infer()
-        torch.cuda.synchronize(self.dev)
+        self.ctx.sync()
         return self.results(backward=False)
 
     def step(self):
@@ -114,7 +114,7 @@ class Batch:
         self.forward()
         if backward:
             self.backward()
-        torch.cuda.synchronize(self.dev)
+        self.ctx.sync()
         return self.results(backward)
 
     def results(self, backward: bool = True) -> dict:

@@ -150,44 +150,74 @@ def pool_workers():
     return max(1, min(16, n))
 
 
+class OraclePool:
+    """Worker processes (spawned; they never touch the GPU) that run the
+    oracle over shards of a workload's graphs.  Graphs are independent, so
+    states and per-vertex terms are placed by vertex id and parameter
+    gradients summed shard by shard in a fixed order (the loss normaliser is
+    the whole batch's |Lambda|)."""
+
+    def __init__(self, workers=None):
+        self.workers = workers or pool_workers()
+        self._pool = None
+
+    def __enter__(self):
+        if self.workers > 1:
+            self._pool = mp.get_context("spawn").Pool(self.workers)
+        return self
+
+    def __exit__(self, *exc):
+        if self._pool is not None:
+            self._pool.close()
+            self._pool.join()
+            self._pool = None
+
+    def run(self, wl: W.Workload, **kw) -> dict:
+        import oracle
+        K = wl.K
+        if self._pool is None or K < 2:
+            return oracle.run(wl, **kw)
+        sizes = np.diff(wl.tree_offsets)
+        cum = np.cumsum(sizes)
+        bounds = np.searchsorted(cum, np.linspace(0, cum[-1], self.workers + 1)[1:-1],
+                                 side="right")
+        edges = np.unique(np.concatenate([[0], bounds, [K]]))
+        shards = [list(range(int(a), int(b))) for a, b in zip(edges[:-1], edges[1:]) if b > a]
+        n_lab = int((wl.push_idx >= 0).sum())
+        kw = dict(kw)
+        if not kw.get("denom"):
+            kw["denom"] = float(max(n_lab, 1))
+        jobs, maps = [], []
+        for sh in shards:
+            sub, keep, rows = subset_maps(wl, sh)
+            jobs.append((sub, kw))
+            maps.append((keep, rows))
+        parts = self._pool.map(_oracle_job, jobs)
+        out = {}
+        V = wl.V
+        for (keep, rows), r in zip(maps, parts):
+            for k, v in r.items():
+                if k in ("h", "c", "gates", "lossv", "dh", "dc"):
+                    if k not in out:
+                        out[k] = np.zeros((V,) + v.shape[1:], dtype=np.float64)
+                    out[k][keep] = v
+                elif k == "dX":
+                    if k not in out:
+                        out[k] = np.zeros((wl.n_x, v.shape[1]))
+                    out[k][rows] = v
+                elif k == "loss":
+                    out[k] = out.get(k, 0.0) + v
+                else:
+                    out[k] = v.copy() if k not in out else out[k] + v
+        return out
+
+
 def oracle_sharded(wl: W.Workload, workers=None, **kw) -> dict:
     """oracle.run(wl, **kw) computed over about `workers` shards of graphs in
-    spawned worker processes (they never touch the GPU)."""
+    spawned worker processes (a single process for small batches)."""
     import oracle
     workers = workers or pool_workers()
-    K = wl.K
-    if workers <= 1 or K < 2 or wl.V < 2000:
+    if workers <= 1 or wl.K < 2 or wl.V < 300:
         return oracle.run(wl, **kw)
-    sizes = np.diff(wl.tree_offsets)
-    cum = np.cumsum(sizes)
-    bounds = np.searchsorted(cum, np.linspace(0, cum[-1], workers + 1)[1:-1], side="right")
-    edges = np.unique(np.concatenate([[0], bounds, [K]]))
-    shards = [list(range(int(a), int(b))) for a, b in zip(edges[:-1], edges[1:]) if b > a]
-    n_lab = int((wl.push_idx >= 0).sum())
-    kw = dict(kw)
-    kw["denom"] = float(max(n_lab, 1))
-    jobs, maps = [], []
-    for sh in shards:
-        sub, keep, rows = subset_maps(wl, sh)
-        jobs.append((sub, kw))
-        maps.append((keep, rows))
-    ctx = mp.get_context("spawn")
-    with ctx.Pool(min(workers, len(jobs))) as pool:
-        parts = pool.map(_oracle_job, jobs)
-    out = {}
-    V = wl.V
-    for (keep, rows), r in zip(maps, parts):
-        for k, v in r.items():
-            if k in ("h", "c", "gates", "lossv", "dh", "dc"):
-                if k not in out:
-                    out[k] = np.zeros((V,) + v.shape[1:], dtype=np.float64)
-                out[k][keep] = v
-            elif k == "dX":
-                if k not in out:
-                    out[k] = np.zeros((wl.n_x, v.shape[1] if v.ndim == 2 else wl.D))
-                out[k][rows] = v
-            elif k == "loss":
-                out[k] = out.get(k, 0.0) + v
-            else:
-                out[k] = v.copy() if k not in out else out[k] + v
-    return out
+    with OraclePool(workers) as pool:
+        return pool.run(wl, **kw)
