@@ -165,6 +165,21 @@ size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x);
 cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* graphs, cavs_sched* sched,
                           void* ws, size_t ws_bytes);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc): the same
+   schedule as cavs_schedule, bit for bit, with the scheduler's scratch taken
+   from a static device array of CAVS_SCHEDULE_STATIC_BYTES per GPU (held
+   until the process ends) instead of a workspace argument.  It allocates
+   nothing and calls no allocating routine (with per-launch timing off).
+   Batches whose cavs_schedule_workspace_bytes(V, N, n_x) exceeds
+   CAVS_SCHEDULE_STATIC_BYTES (about 100 000 vertices with as many input
+   rows) are refused with CAVS_ERR_WORKSPACE before anything is enqueued.
+   Every call on one GPU shares that GPU's array: calls that overlap in time
+   on one GPU (contexts on different streams) race and must be serialised by
+   the caller.  Errors and synchronisation as for cavs_schedule. */
+#define CAVS_SCHEDULE_STATIC_BYTES (4u << 20)
+cavs_status cavs_schedule_static(cavs_ctx* ctx, const cavs_graphs* graphs, cavs_sched* sched);
+
 /* ---------------------------------------------------------------------------
  * Forward / backward of F over the scheduled graphs.
  *

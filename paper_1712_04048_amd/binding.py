@@ -73,7 +73,8 @@ class cavs_launch_time(ct.Structure):
 
 
 EXPORTS = ["cavs_create", "cavs_set_stream", "cavs_destroy", "cavs_last_error", "cavs_sync",
-           "cavs_schedule_workspace_bytes", "cavs_schedule", "cavs_workspace_bytes",
+           "cavs_schedule_workspace_bytes", "cavs_schedule", "cavs_schedule_static",
+           "cavs_workspace_bytes",
            "cavs_forward", "cavs_backward", "cavs_infer_workspace_bytes", "cavs_infer",
            "cavs_timing_enable", "cavs_timing_read"]
 
@@ -102,6 +103,8 @@ def lib():
         L.cavs_schedule.restype = _i32
         L.cavs_schedule.argtypes = [_vp, ct.POINTER(cavs_graphs), ct.POINTER(cavs_sched), _vp,
                                     ct.c_size_t]
+        L.cavs_schedule_static.restype = _i32
+        L.cavs_schedule_static.argtypes = [_vp, ct.POINTER(cavs_graphs), ct.POINTER(cavs_sched)]
         L.cavs_workspace_bytes.restype = ct.c_size_t
         L.cavs_workspace_bytes.argtypes = [ct.POINTER(cavs_params), ct.POINTER(cavs_sched)]
         L.cavs_forward.restype = _i32
@@ -238,6 +241,23 @@ def run_schedule(ctx: Context, sched: Schedule, child: torch.Tensor, parent: tor
     nbytes = sched.ws.numel()
     ctx.check(lib().cavs_schedule(ctx._h, ct.byref(g), ct.byref(sched.raw),
                                   sched.ws.data_ptr(), nbytes))
+    return sched
+
+
+SCHEDULE_STATIC_BYTES = 4 << 20   # CAVS_SCHEDULE_STATIC_BYTES
+
+
+def run_schedule_static(ctx: Context, sched: Schedule, child: torch.Tensor, parent: torch.Tensor,
+                        pull_idx: Optional[torch.Tensor] = None,
+                        push_idx: Optional[torch.Tensor] = None, n_x: int = 0, n_push: int = 0):
+    """cavs_schedule_static into a previously allocated Schedule: the
+    scheduler's scratch comes from the library's static device array, so
+    ``sched.ws`` is not used."""
+    V = int(parent.shape[0])
+    N = int(child.shape[1]) if child.dim() == 2 else 1
+    g = cavs_graphs(V, N, int(n_x), int(n_push), _ptr(child), _ptr(parent), _ptr(pull_idx),
+                    _ptr(push_idx))
+    ctx.check(lib().cavs_schedule_static(ctx._h, ct.byref(g), ct.byref(sched.raw)))
     return sched
 
 

@@ -250,6 +250,13 @@ cavs_status cavs_create(cavs_ctx** out, int32_t device, void* hip_stream) {
     return CAVS_ERR_HIP;
   }
   ctx->dev_err[0] = 0;
+  if (static_sched_scratch(ctx, device, &ctx->sched_scratch) != CAVS_OK) {
+    (void)hipHostFree(ctx->host_stage);
+    (void)hipHostFree(ctx->dev_err);
+    (void)hipEventDestroy(ctx->stage_ready);
+    delete ctx;
+    return CAVS_ERR_HIP;
+  }
   *out = ctx;
   return CAVS_OK;
 }
@@ -325,10 +332,7 @@ size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x) {
   return schedule_ws_bytes(V, N, n_x);
 }
 
-cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
-                          size_t ws_bytes) {
-  if (!ctx) return CAVS_ERR_ARG;
-  ctx->err.clear();
+static cavs_status schedule_checks(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s) {
   if (!g || !s) return fail(ctx, CAVS_ERR_ARG, "null graphs / sched");
   if (g->V < 0 || g->n_x < 0 || g->n_push < 0) return fail(ctx, CAVS_ERR_ARG, "negative size");
   if (g->N < 1 || g->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots", g->N);
@@ -338,10 +342,38 @@ cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, vo
                    !s->pull_pos || !s->push_pos || !s->pull_list || !s->level_offsets))
     return fail(ctx, CAVS_ERR_ARG, "schedule output arrays are required");
   if (!s->level_offsets_host) return fail(ctx, CAVS_ERR_ARG, "level_offsets_host is required");
+  return CAVS_OK;
+}
+
+cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
+                          size_t ws_bytes) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  cavs_status st = schedule_checks(ctx, g, s);
+  if (st != CAVS_OK) return st;
   if (g->V > 0 && !ws) return fail(ctx, CAVS_ERR_ARG, "workspace is required");
   if (hipSetDevice(ctx->device) != hipSuccess) return fail(ctx, CAVS_ERR_HIP, "hipSetDevice");
   ActiveCtx active(ctx);
   return schedule_run(ctx, g, s, ws, ws_bytes);
+}
+
+cavs_status cavs_schedule_static(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s) {
+  if (!ctx) return CAVS_ERR_ARG;
+  ctx->err.clear();
+  cavs_status st = schedule_checks(ctx, g, s);
+  if (st != CAVS_OK) return st;
+  if (!ctx->sched_scratch)
+    return fail(ctx, CAVS_ERR_UNSUPPORTED, "no static scheduling scratch for device %d",
+                ctx->device);
+  const size_t need = schedule_ws_bytes(g->V, g->N, g->n_x);
+  if (need > (size_t)CAVS_SCHEDULE_STATIC_BYTES)
+    return fail(ctx, CAVS_ERR_WORKSPACE,
+                "cavs_schedule_static: V=%d, n_x=%d need %zu bytes of scratch, the static "
+                "array holds %zu; use cavs_schedule with a workspace",
+                g->V, g->n_x, need, (size_t)CAVS_SCHEDULE_STATIC_BYTES);
+  if (hipSetDevice(ctx->device) != hipSuccess) return fail(ctx, CAVS_ERR_HIP, "hipSetDevice");
+  ActiveCtx active(ctx);
+  return schedule_run(ctx, g, s, ctx->sched_scratch, (size_t)CAVS_SCHEDULE_STATIC_BYTES);
 }
 
 size_t cavs_workspace_bytes(const cavs_params* p, const cavs_sched* s) {

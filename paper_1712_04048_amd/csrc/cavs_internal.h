@@ -29,6 +29,7 @@ struct cavs_ctx {
   hipEvent_t stage_ready = nullptr;       // the schedule's host stage has arrived
   int32_t* dev_err = nullptr;             // pinned, coherent, mapped: set by kernels whose
   int32_t* dev_err_dev = nullptr;         // bounded waits gave up (device view of dev_err)
+  void* sched_scratch = nullptr;          // this device's static scheduling scratch
 };
 
 namespace cavs {
@@ -185,5 +186,9 @@ struct SchedWs;
 size_t schedule_ws_bytes(int32_t V, int32_t N, int32_t n_x);
 cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, void* ws,
                          size_t ws_bytes);
+// Address of the static scheduling scratch (CAVS_SCHEDULE_STATIC_BYTES) on
+// `device`, which must be current; taken once per device.  *out = NULL for
+// device ids past the supported range.
+cavs_status static_sched_scratch(cavs_ctx* ctx, int device, void** out);
 
 }  // namespace cavs

@@ -23,9 +23,17 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "cavs_internal.h"
+
+// Scratch of the allocation-free entry point cavs_schedule_static: one copy
+// per GPU, alive until the process ends.  Host code never uses this name as
+// an address: static_sched_scratch() takes each device's address of it once
+// (hipGetSymbolAddress, with that device current) and everything else uses
+// that pointer.
+static __device__ __align__(256) unsigned char scratch[CAVS_SCHEDULE_STATIC_BYTES];
 
 namespace cavs {
 
@@ -1039,6 +1047,27 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   int passes = 1;
   while (passes < 4 && ((long)(T > 0 ? T - 1 : 0) >> (8 * passes)) > 0) ++passes;
   return passes > 1 ? sort_and_remap(passes) : CAVS_OK;
+}
+
+// Device address of `scratch` on the current device (`device`), taken once
+// per device and kept for every later context on it.
+cavs_status static_sched_scratch(cavs_ctx* ctx, int device, void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return CAVS_OK;   // the static entry point refuses
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(ctx, CAVS_ERR_HIP, "hipGetSymbolAddress(scratch) failed: %s",
+                  hipGetErrorString(e));
+    addr[device] = p;
+  }
+  *out = addr[device];
+  return CAVS_OK;
 }
 
 }  // namespace cavs
