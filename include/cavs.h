@@ -32,14 +32,17 @@
  *     non-zero status, cavs_last_error() describes it.  Argument errors are
  *     detected on the host before anything is enqueued.
  *   - Calls on one context must not overlap (one stream, one user at a time).
- *   - Three environment switches, read at each call and off by default, turn
- *     the execution engine's optimisations off for ablation measurements;
+ *   - Environment switches, read at each call and off by default, turn the
+ *     execution engine's optimisations off for ablation measurements;
  *     results stay within the same tolerance of the exact ones:
  *       CAVS_EAGER_DW=1           dU formed level by level, not lazily;
  *       CAVS_UNFUSED_BWD_GATES=1  no child gradient fused into a parent's
  *                                 backward product;
  *       CAVS_PERSIST=1            the small levels in one persistent launch
- *                                 with grid barriers.
+ *                                 with grid barriers;
+ *       CAVS_UNFUSED_FWD_GATES=1  the forward gates and cell update in an
+ *                                 elementwise kernel after each level product;
+ *       CAVS_GENERIC=1            trees too run the generic engine.
  *     A fourth is a failure-injection hook for tests of the error path:
  *       CAVS_PERSIST_SPIN=n       the persistent loop's grid barrier gives up
  *                                 after n polls (n < 0: at once) and records
@@ -103,19 +106,23 @@ cavs_status cavs_sync(cavs_ctx* ctx);
  * Scheduling (Algorithm 1; dynamic tensors of Section 3.3, Algorithm 2)
  *
  * The input graphs of one batch.  Vertex ids are global, 0..V-1.  Each vertex
- * has at most N child slots (gather(child_idx), Section 3.1) and at most one
- * parent; a vertex with no children is a leaf.  pull_idx names the row of the
+ * has at most N child slots (gather(child_idx), Section 3.1); a vertex with no
+ * children is a leaf.  Tree inputs give each vertex at most one parent and
+ * list it in parent[].  Graph inputs (the graph-structured cells of Section 2,
+ * panel (d) of the recurrent-structures figure) pass parent = NULL: a vertex
+ * may then be read by several vertices (or by several slots of one), and its
+ * dL/dh and dL/dc are the sums of what each reader sends back.  pull_idx names the row of the
  * external input matrix X that the vertex pulls (pull(), Section 3.1);
  * push_idx names what its pushed state is scored against (push()): a class in
  * [0, C) for CAVS_LOSS_CE or a row of Y for CAVS_LOSS_L2.
  * ------------------------------------------------------------------------- */
 typedef struct {
   int32_t V;                /* number of vertices, >= 0 */
-  int32_t N;                /* child slots per vertex, 1 or 2 */
+  int32_t N;                /* child slots per vertex, 1 .. 4 */
   int32_t n_x;              /* rows of X (pull_idx values lie in [-1, n_x)) */
   int32_t n_push;           /* push_idx values lie in [-1, n_push) */
   const int32_t* child;     /* [V*N] child id of slot k of vertex v, or -1 */
-  const int32_t* parent;    /* [V] parent id, or -1 for a root */
+  const int32_t* parent;    /* [V] parent id, or -1 for a root; NULL = graph inputs */
   const int32_t* pull_idx;  /* [V] row of X, or -1; NULL = no vertex pulls */
   const int32_t* push_idx;  /* [V] label / target row, or -1; NULL = no loss terms */
 } cavs_graphs;
@@ -147,6 +154,13 @@ typedef struct {
   int32_t* level_offsets;   /* [V+1]   T+1 used */
   /* out (host), caller-allocated */
   int32_t* level_offsets_host; /* [V+1] T+1 used; filled by the one synchronisation */
+  /* out (host) */
+  int32_t dag;              /* 1 when the graphs were given without parent[] */
+  /* out (device), caller-allocated; required for graph inputs, else unused:
+     the links e = p*N + k (child slot k of position p) that read position c
+     are in_edges[in_offsets[c] .. in_offsets[c+1]), ascending */
+  int32_t* in_offsets;      /* [V+1] */
+  int32_t* in_edges;        /* [V*N] */
 } cavs_sched;
 
 /* Bytes of device workspace cavs_schedule needs for V vertices, N slots and
@@ -159,8 +173,10 @@ size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x);
    pull_list) are written by work enqueued after that point, so they are
    complete for later work on the same stream (or after a synchronisation).  Graph errors, by priority: CAVS_ERR_RANGE,
    CAVS_ERR_MULTIPARENT, CAVS_ERR_DUP_PULL, CAVS_ERR_MISMATCH, CAVS_ERR_CYCLE;
-   on such an error the device outputs are unspecified.  N outside {1, 2}
-   gives CAVS_ERR_UNSUPPORTED; a null required pointer, CAVS_ERR_ARG; a short
+   on such an error the device outputs are unspecified.  Graph inputs
+   (parent = NULL) are checked for ranges, duplicate pull rows and cycles
+   only.  N outside 1 .. 4 gives CAVS_ERR_UNSUPPORTED; a null required
+   pointer (in_offsets / in_edges for graph inputs), CAVS_ERR_ARG; a short
    workspace, CAVS_ERR_WORKSPACE. */
 cavs_status cavs_schedule(cavs_ctx* ctx, const cavs_graphs* graphs, cavs_sched* sched,
                           void* ws, size_t ws_bytes);
@@ -230,7 +246,12 @@ size_t cavs_workspace_bytes(const cavs_params* params, const cavs_sched* sched);
    receive the states in vertex-id order; loss_out [1] the mean loss.
    Shapes are validated against the schedule on the host: mismatches give
    CAVS_ERR_ARG, shapes this build does not tile (H % 64 != 0, D % 4 != 0,
-   N > 2, BF16 with TREE_FC) give CAVS_ERR_UNSUPPORTED. */
+   N > 4, BF16 with TREE_FC) give CAVS_ERR_UNSUPPORTED.  Trees with at most
+   two child slots run the fused level kernels; graph inputs and wider
+   vertices (TREE_LSTM, fp32 only; else CAVS_ERR_UNSUPPORTED) run the generic
+   engine: per task, separate products and elementwise gate kernels, with
+   each child link's gradient in its own row summed per vertex in a fixed
+   order. */
 cavs_status cavs_forward(cavs_ctx* ctx, const cavs_params* params, const cavs_sched* sched,
                          const cavs_inputs* inputs, float* h_out, float* c_out,
                          float* loss_out, void* ws, size_t ws_bytes);

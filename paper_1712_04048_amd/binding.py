@@ -51,7 +51,8 @@ class cavs_sched(ct.Structure):
                 ("n_inner_input", _i32),
                 ("level", _vp), ("order", _vp), ("pos", _vp), ("child_pos", _vp),
                 ("parent_pos", _vp), ("pull_pos", _vp), ("push_pos", _vp), ("pull_list", _vp),
-                ("level_offsets", _vp), ("level_offsets_host", _vp)]
+                ("level_offsets", _vp), ("level_offsets_host", _vp), ("dag", _i32),
+                ("in_offsets", _vp), ("in_edges", _vp)]
 
 
 class cavs_params(ct.Structure):
@@ -202,7 +203,11 @@ class Schedule:
         return int(self.raw.T)
 
     def host(self) -> dict:
-        d = {k: v.cpu().numpy() for k, v in self.tensors.items()}
+        d = {k: v.cpu().numpy() for k, v in self.tensors.items()
+             if k not in ("in_offsets", "in_edges")}
+        if self.raw.dag:
+            d["in_offsets"] = self.tensors["in_offsets"].cpu().numpy()
+            d["in_edges"] = self.tensors["in_edges"].cpu().numpy()
         d["level_offsets"] = d["level_offsets"][: self.T + 1]
         d["pull_list"] = d["pull_list"][: self.raw.n_pull]
         d["child_pos"] = d["child_pos"].reshape(-1, self.raw.N)
@@ -219,7 +224,8 @@ def alloc_schedule(ctx: Context, V: int, N: int, n_x: int) -> Schedule:
     t = dict(level=torch.empty(V, **i32), order=torch.empty(V, **i32), pos=torch.empty(V, **i32),
              child_pos=torch.empty(V * N, **i32), parent_pos=torch.empty(V, **i32),
              pull_pos=torch.empty(V, **i32), push_pos=torch.empty(V, **i32),
-             pull_list=torch.empty(V, **i32), level_offsets=torch.empty(V + 1, **i32))
+             pull_list=torch.empty(V, **i32), level_offsets=torch.empty(V + 1, **i32),
+             in_offsets=torch.empty(V + 1, **i32), in_edges=torch.empty(V * N, **i32))
     host_off = np.zeros(V + 1, dtype=np.int32)
     s = cavs_sched()
     for k, v in t.items():
@@ -230,11 +236,13 @@ def alloc_schedule(ctx: Context, V: int, N: int, n_x: int) -> Schedule:
     return Schedule(raw=s, tensors=t, level_offsets_host=host_off, ws=ws)
 
 
-def run_schedule(ctx: Context, sched: Schedule, child: torch.Tensor, parent: torch.Tensor,
+def run_schedule(ctx: Context, sched: Schedule, child: torch.Tensor,
+                 parent: Optional[torch.Tensor],
                  pull_idx: Optional[torch.Tensor] = None,
                  push_idx: Optional[torch.Tensor] = None, n_x: int = 0, n_push: int = 0):
-    """cavs_schedule into a previously allocated Schedule (one synchronisation)."""
-    V = int(parent.shape[0])
+    """cavs_schedule into a previously allocated Schedule (one synchronisation).
+    parent=None: graph inputs (a vertex may be read by several vertices)."""
+    V = int(child.shape[0])
     N = int(child.shape[1]) if child.dim() == 2 else 1
     g = cavs_graphs(V, N, int(n_x), int(n_push), _ptr(child), _ptr(parent), _ptr(pull_idx),
                     _ptr(push_idx))
@@ -247,13 +255,14 @@ def run_schedule(ctx: Context, sched: Schedule, child: torch.Tensor, parent: tor
 SCHEDULE_STATIC_BYTES = 4 << 20   # CAVS_SCHEDULE_STATIC_BYTES
 
 
-def run_schedule_static(ctx: Context, sched: Schedule, child: torch.Tensor, parent: torch.Tensor,
+def run_schedule_static(ctx: Context, sched: Schedule, child: torch.Tensor,
+                        parent: Optional[torch.Tensor],
                         pull_idx: Optional[torch.Tensor] = None,
                         push_idx: Optional[torch.Tensor] = None, n_x: int = 0, n_push: int = 0):
     """cavs_schedule_static into a previously allocated Schedule: the
     scheduler's scratch comes from the library's static device array, so
     ``sched.ws`` is not used."""
-    V = int(parent.shape[0])
+    V = int(child.shape[0])
     N = int(child.shape[1]) if child.dim() == 2 else 1
     g = cavs_graphs(V, N, int(n_x), int(n_push), _ptr(child), _ptr(parent), _ptr(pull_idx),
                     _ptr(push_idx))
@@ -261,11 +270,12 @@ def run_schedule_static(ctx: Context, sched: Schedule, child: torch.Tensor, pare
     return sched
 
 
-def schedule(ctx: Context, child: torch.Tensor, parent: torch.Tensor,
+def schedule(ctx: Context, child: torch.Tensor, parent: Optional[torch.Tensor],
              pull_idx: Optional[torch.Tensor] = None, push_idx: Optional[torch.Tensor] = None,
              n_x: int = 0, n_push: int = 0) -> Schedule:
-    """cavs_schedule: int32 device tensors child [V, N], parent [V], ..."""
-    V = int(parent.shape[0])
+    """cavs_schedule: int32 device tensors child [V, N], parent [V] (None for
+    graph inputs), ..."""
+    V = int(child.shape[0])
     N = int(child.shape[1]) if child.dim() == 2 else 1
     sched = alloc_schedule(ctx, V, N, n_x)
     return run_schedule(ctx, sched, child, parent, pull_idx, push_idx, n_x, n_push)

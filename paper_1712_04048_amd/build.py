@@ -18,7 +18,8 @@ LIB = os.path.join(PKG, "libcavs.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "schedule.hip", "lstm.hip", "lstm_tile.hip", "fc.hip", "lazy.hip"]
+SOURCES = ["api.hip", "schedule.hip", "lstm.hip", "lstm_tile.hip", "fc.hip", "lazy.hip",
+           "generic.hip"]
 
 CFLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

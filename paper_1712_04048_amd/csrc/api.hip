@@ -53,10 +53,23 @@ namespace {
 struct WsLayout {
   size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bpart, bar, total;
   size_t part_floats;
+  size_t gHt, gDt, gEh, gEc, gdAx, gpart;   // generic engine
 };
+
+bool env_on(const char* name) {
+  const char* e = getenv(name);
+  return e && e[0] && e[0] != '0';
+}
+
+// Graph inputs and vertices with more than two child slots run the generic
+// engine (generic.hip); CAVS_GENERIC=1 sends trees there too.
+bool generic_mode(const cavs_params* p, const cavs_sched* s) {
+  return s->dag || p->N > 2 || env_on("CAVS_GENERIC");
+}
 
 WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   WsLayout L{};
+  const bool gen = p->cell == CAVS_TREE_LSTM && generic_mode(p, s);
   const size_t tr = train ? 1 : 0;
   const size_t V = (size_t)(s->V > 0 ? s->V : 1), H = (size_t)p->H;
   const bool lstm = p->cell == CAVS_TREE_LSTM;
@@ -74,7 +87,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.zrow = take(H);
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
-  L.Gs = take(tr * (lstm ? V * GW : 0));
+  L.Gs = take((tr || gen) ? (lstm ? V * GW : 0) : 0);   // the generic forward stages in it
   L.dZ = take(tr * V * (C > 0 ? C : 1));
   L.lossv = take(V);
   L.dHL = take(tr * V * H);
@@ -85,6 +98,15 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.part = take(3 * L.part_floats);   // dU_iou, dU_f and dW_x split-K sums side by side
   L.bpart = take(tr * bias_part_floats(p->H, p->loss == CAVS_LOSS_CE ? p->C : 0));
   L.bar = take(256);
+  if (gen) {
+    const size_t N = (size_t)p->N;
+    L.gHt = take(V * H);
+    L.gDt = take(tr * V * H);
+    L.gEh = take(tr * V * N * H);
+    L.gEc = take(tr * V * N * H);
+    L.gdAx = take(tr * V * 4 * H);
+    L.gpart = take(tr * gen_part_floats(p->D, p->H, (int)C));
+  }
   L.total = o;
   return L;
 }
@@ -101,7 +123,18 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
     return fail(ctx, CAVS_ERR_ARG, "unknown precision %d", p->prec);
   if (p->H <= 0 || p->D < 0 || p->N <= 0) return fail(ctx, CAVS_ERR_ARG, "bad D/H/N");
   if (p->N != s->N) return fail(ctx, CAVS_ERR_ARG, "params N=%d != schedule N=%d", p->N, s->N);
-  if (p->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots (max 2)", p->N);
+  if (p->N > kMaxSlots)
+    return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots (max %d)", p->N, kMaxSlots);
+  if (generic_mode(p, s)) {
+    if (p->cell != CAVS_TREE_LSTM)
+      return fail(ctx, CAVS_ERR_UNSUPPORTED,
+                  "graph inputs and more than two child slots are built for the Tree-LSTM only");
+    if (p->prec != CAVS_FP32)
+      return fail(ctx, CAVS_ERR_UNSUPPORTED,
+                  "graph inputs and more than two child slots run in fp32 only");
+    if (s->dag && s->V > 0 && (!s->in_offsets || !s->in_edges))
+      return fail(ctx, CAVS_ERR_ARG, "graph inputs need the schedule's in_offsets / in_edges");
+  }
   if (p->H % 64 != 0) return fail(ctx, CAVS_ERR_UNSUPPORTED, "H=%d not a multiple of 64", p->H);
   if (p->prec == CAVS_BF16 && p->cell != CAVS_TREE_LSTM)
     return fail(ctx, CAVS_ERR_UNSUPPORTED, "bf16 products are built for the Tree-LSTM only");
@@ -136,19 +169,20 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
 // and summed into dU in reverse task order, instead of as one product over
 // every internal vertex after the level loop (Section 3.5).  dW_x, the bias
 // and the loss head stay lazy.  Measured with bench.py; off by default.
-bool eager_dw_enabled() {
-  const char* e = getenv("CAVS_EAGER_DW");
-  return e && e[0] && e[0] != '0';
-}
+bool eager_dw_enabled() { return env_on("CAVS_EAGER_DW"); }
 
 // Ablation of kernel fusion in the backward pass (CAVS_UNFUSED_BWD_GATES=1):
 // no child's dA is formed in its parent's product epilogue; every level gets
 // its own elementwise gates kernel, as the levels above 256 positions always
 // do.  Measured with bench.py; off by default.
-bool unfused_bwd_gates() {
-  const char* e = getenv("CAVS_UNFUSED_BWD_GATES");
-  return e && e[0] && e[0] != '0';
-}
+bool unfused_bwd_gates() { return env_on("CAVS_UNFUSED_BWD_GATES"); }
+
+// Ablation of kernel fusion in the forward pass (CAVS_UNFUSED_FWD_GATES=1):
+// each level's product kernel stores its pre-activation parts and an
+// elementwise kernel applies the gates, cell update and scatter; the leaves
+// too get their cells from that kernel instead of the pull product's
+// epilogue.  Measured with bench.py; off by default.
+bool unfused_fwd_gates() { return env_on("CAVS_UNFUSED_FWD_GATES"); }
 
 // dU contributions of the internal positions [off, off + M): queued split-K
 // products whose reductions add into dU (acc) or overwrite it (first level).
@@ -206,7 +240,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.dCp = (float*)(base + L.dCp);
   n.dA = (float*)(base + L.dA);
   if (!train) {   // the kernels test these for null and skip what only backward reads
-    n.Gs = nullptr;
+    if (!(p->cell == CAVS_TREE_LSTM && generic_mode(p, s))) n.Gs = nullptr;
     n.dZ = nullptr;
     n.dHL = nullptr;
     n.dHp = nullptr;
@@ -214,6 +248,20 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
     n.dA = nullptr;
   }
   return n;
+}
+
+GenBufDev gen_bufs(const cavs_sched* s, void* ws, const WsLayout& L) {
+  char* base = (char*)ws;
+  GenBufDev b{};
+  b.Ht = (float*)(base + L.gHt);
+  b.Dt = (float*)(base + L.gDt);
+  b.Eh = (float*)(base + L.gEh);
+  b.Ec = (float*)(base + L.gEc);
+  b.dAx = (float*)(base + L.gdAx);
+  b.part = (float*)(base + L.gpart);
+  b.in_off = s->dag ? s->in_offsets : nullptr;
+  b.in_edge = s->dag ? s->in_edges : nullptr;
+  return b;
 }
 
 }  // namespace
@@ -335,9 +383,11 @@ size_t cavs_schedule_workspace_bytes(int32_t V, int32_t N, int32_t n_x) {
 static cavs_status schedule_checks(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s) {
   if (!g || !s) return fail(ctx, CAVS_ERR_ARG, "null graphs / sched");
   if (g->V < 0 || g->n_x < 0 || g->n_push < 0) return fail(ctx, CAVS_ERR_ARG, "negative size");
-  if (g->N < 1 || g->N > 2) return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots", g->N);
-  if (g->V > 0 && (!g->child || !g->parent))
-    return fail(ctx, CAVS_ERR_ARG, "child / parent arrays are required");
+  if (g->N < 1 || g->N > kMaxSlots)
+    return fail(ctx, CAVS_ERR_UNSUPPORTED, "N=%d child slots", g->N);
+  if (g->V > 0 && !g->child) return fail(ctx, CAVS_ERR_ARG, "the child array is required");
+  if (g->V > 0 && !g->parent && (!s->in_offsets || !s->in_edges))
+    return fail(ctx, CAVS_ERR_ARG, "graph inputs need in_offsets / in_edges in the schedule");
   if (g->V > 0 && (!s->level || !s->order || !s->pos || !s->child_pos || !s->parent_pos ||
                    !s->pull_pos || !s->push_pos || !s->pull_list || !s->level_offsets))
     return fail(ctx, CAVS_ERR_ARG, "schedule output arrays are required");
@@ -410,7 +460,22 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
   n.h_out = h_out;
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
-  if (p->cell == CAVS_TREE_LSTM) {
+  if (p->cell == CAVS_TREE_LSTM && generic_mode(p, s)) {
+    lstm_transpose_u(n, str);
+    pull_gemm(n, s->n_pull, s->n_inner_input > 0, 0, str);   // P for every pulling row
+    lstm_fwd_gates(n, lo[0], lo[1] - lo[0], false, str);
+    gen_forward_levels(n, gen_bufs(s, ws, L), lo, s->T, str);
+  } else if (p->cell == CAVS_TREE_LSTM && train && unfused_fwd_gates()) {
+    n.fwd_unfused = 1;
+    if ((s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) || pull_tile_applies(n, s->n_pull))
+      lstm_transpose_u(n, str);
+    pull_gemm(n, s->n_pull, s->n_inner_input > 0, 0, str);
+    lstm_fwd_gates(n, lo[0], lo[1] - lo[0], false, str);
+    for (int t = 1; t < s->T; ++t) {
+      lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+      lstm_fwd_gates(n, lo[t], lo[t + 1] - lo[t], true, str);
+    }
+  } else if (p->cell == CAVS_TREE_LSTM) {
     if ((s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) || pull_tile_applies(n, s->n_pull))
       lstm_transpose_u(n, str);
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, lo[1], str);
@@ -485,7 +550,10 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   const int off1 = T > 1 ? lo[1] : s->V;
   if (s->n_x > 0 && s->n_pull < s->n_x)
     CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
-  if (lstm) {
+  if (lstm && generic_mode(p, s)) {
+    gen_backward(n, gen_bufs(s, ws, L), lo, T, s->n_pull, g->dU, g->db, g->dWx, g->dX, g->dWs,
+                 g->dbs, str);
+  } else if (lstm) {
     // Levels tf.. get dA in their parent's level epilogue (roots: one
     // kernel); levels below tf by an elementwise kernel just before their
     // own product, once every parent has stored dL/dh and dL/dc.

@@ -17,6 +17,9 @@ struct Net {
   int fuse_from;                // LSTM backward: positions >= this get dA in the parent's epilogue
   int f_unread_below;           // LSTM backward: rows below this (leaves, when no vertex with
                                 // children pulls) skip their dA forget columns: nothing reads them
+  int fwd_unfused;              // LSTM forward: the level products store their pre-activation
+                                // parts in the saved-gate rows and lstm_fwd_gates finishes
+                                // (the fusion ablation)
   // schedule
   const int* child_pos;         // [V*N]
   const int* parent_pos;        // [V]
@@ -55,6 +58,23 @@ struct Net {
 // gate column blocks of Wx / U / b (each H wide)
 enum { G_I = 0, G_F = 1, G_O = 2, G_U = 3 };
 
+// Most child slots the generic engine (generic.hip) takes; the fused engine
+// takes two.
+constexpr int kMaxSlots = 4;
+
+// Workspace buffers of the generic engine (level-major; a link e = p * N + k
+// is child slot k of position p).
+struct GenBufDev {
+  float* Ht;          // [V, H]     h~ = sum of the present children's h
+  float* Dt;          // [V, H]     dL/dh~
+  float* Eh;          // [V*N, H]   dL/dh sent back along each child link
+  float* Ec;          // [V*N, H]   dL/dc sent back along each child link
+  float* dAx;         // [V, 4H]    (d_i, sum_k d_fk, d_o, d_u): input and bias gradients
+  float* part;        // split-K partial sums (gen_part_floats)
+  const int* in_off;  // graph inputs: [V+1] offsets into in_edge per position; null for trees
+  const int* in_edge; // graph inputs: links reading each position, ascending
+};
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -89,6 +109,16 @@ bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, i
                       hipStream_t s);
 // First level >= 1 small enough for the persistent loop (T if none).
 int persist_first_level(const Net& n, const int* lo_host, int T);
+// generic.hip
+// Forward gates of positions [off, off + M) from the pre-activation parts in
+// the saved-gate rows (has_product false: none, as for leaves).
+void lstm_fwd_gates(const Net& n, int off, int M, bool has_product, hipStream_t s);
+void gen_forward_levels(const Net& n, const GenBufDev& b, const int* lo_host, int T,
+                        hipStream_t s);
+void gen_backward(const Net& n, const GenBufDev& b, const int* lo_host, int T, int n_pull,
+                  float* dU, float* db, float* dWx, float* dX, float* dWs, float* dbs,
+                  hipStream_t s);
+size_t gen_part_floats(int D, int H, int CP);
 // fc.hip
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);

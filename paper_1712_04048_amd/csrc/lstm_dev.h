@@ -62,6 +62,15 @@ template <int NCH>
 __device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const FwdPre<NCH>& q,
                                              float zi, float zo, float zu, float zf0, float zf1) {
   const int H = n.H;
+  if (n.fwd_unfused) {   // fusion ablation: the gates run in their own kernel
+    float* g = n.Gs + (size_t)p * n.GW;
+    g[j] = zi;
+    g[H + j] = zf0;
+    g[2 * H + j] = zo;
+    g[3 * H + j] = zu;
+    if constexpr (NCH == 2) g[4 * H + j] = zf1;
+    return;
+  }
   float ai = zi + q.bi, ao = zo + q.bo, au = zu + q.bu;
   if (q.pulled) {
     ai += q.pi;
@@ -151,6 +160,16 @@ __device__ __forceinline__ void lstm_fwd_fin4(const Net& n, int p, int j0, const
                                               const Bias4& b, const FwdCell4<NCH>& e, v4f zi,
                                               v4f zo, v4f zu, v4f zf0, v4f zf1) {
   const int H = n.H;
+  if (n.fwd_unfused) {   // fusion ablation: the gates run in their own kernel
+    float* g = n.Gs + (size_t)p * n.GW + j0;
+    auto v2f = [](v4f v) { return make_float4(v[0], v[1], v[2], v[3]); };
+    st4(g, v2f(zi));
+    st4(g + H, v2f(zf0));
+    st4(g + 2 * H, v2f(zo));
+    st4(g + 3 * H, v2f(zu));
+    if constexpr (NCH == 2) st4(g + 4 * H, v2f(zf1));
+    return;
+  }
   float4 pi = f4zero(), pf = f4zero(), po = f4zero(), pu = f4zero();
   if (q.pr >= 0) {
     const float* Pp = n.P + (size_t)p * 4 * H + j0;

@@ -86,7 +86,7 @@ __global__ void k_scan_edges(int V, int N, int n_x, int n_push, const int* __res
         ++nc;
       }
     }
-    int p = parent[v];
+    int p = parent ? parent[v] : -1;
     if (p < -1 || p >= V) bad = 1;
     else if (p >= 0) withp = 1;
     int r = pull_idx ? pull_idx[v] : -1;
@@ -183,6 +183,121 @@ __global__ void k_sched_init(int* zero_base, long zero_ints, int* level, int V) 
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < zero_ints) zero_base[i] = 0;
   if (i < V) level[i] = -1;
+}
+
+// -------------------------------------------------------------------------
+// 2'. levels of graph inputs (no parent array: a vertex may be read by
+// several vertices) and of trees with more than two child slots, by peeling:
+// a vertex is ready once every vertex it reads has its level.  The readers
+// of each vertex are listed first (rd_off, from the reference counts, and
+// rd_list); one workgroup then takes the ready vertices round by round: the
+// round-t list gets level t, and each of its vertices counts itself off
+// every reader's number of unfinished children (once per link); a reader
+// whose count reaches zero goes into the next list.  The list lengths are
+// the level histogram.  A vertex never reached lies on a cycle.
+// -------------------------------------------------------------------------
+__global__ void k_check_links(int V, int N, int n_x, const int* __restrict__ child,
+                              const int* __restrict__ parent, const int* __restrict__ ref_cnt,
+                              const int* __restrict__ pull_cnt, int* flags) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (parent) check_links_of(v, V, N, n_x, child, parent, ref_cnt, pull_cnt, flags);
+  else if (v < n_x && pull_cnt[v] > 1) atomicOr(&flags[F_DUP], 1);
+}
+
+__global__ void k_graph_readers(int V, int N, const int* __restrict__ child,
+                                const int* __restrict__ rd_off, int* rd_cur, int* rd_list) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V) return;
+  for (int k = 0; k < N; ++k) {
+    const int c = child[(size_t)v * N + k];
+    if (c >= 0 && c < V) rd_list[rd_off[c] + atomicAdd(&rd_cur[c], 1)] = v;
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_graph_levels(int V, const int* __restrict__ nchild,
+                                                       const int* __restrict__ rd_off,
+                                                       const int* __restrict__ rd_list,
+                                                       int* nrem, int* listA, int* listB,
+                                                       int* level, int* hist, int* flags) {
+  __shared__ int cur_n, next_n, done_n;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    cur_n = 0;
+    next_n = 0;
+    done_n = 0;
+  }
+  __syncthreads();
+  for (int v = tid; v < V; v += 1024) {
+    const int c = nchild[v];
+    nrem[v] = c;
+    if (c == 0) listA[atomicAdd(&cur_n, 1)] = v;
+  }
+  __syncthreads();
+  int* cur = listA;
+  int* nxt = listB;
+  int t = 0;
+  while (cur_n > 0 && t < V) {
+    const int n = cur_n;
+    for (int i = tid; i < n; i += 1024) {
+      const int v = cur[i];
+      level[v] = t;
+      for (int e = rd_off[v]; e < rd_off[v + 1]; ++e) {
+        const int r = rd_list[e];
+        if (atomicSub(&nrem[r], 1) == 1) nxt[atomicAdd(&next_n, 1)] = r;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      hist[t] = n;
+      done_n += n;
+      cur_n = next_n;
+      next_n = 0;
+    }
+    int* sw = cur;
+    cur = nxt;
+    nxt = sw;
+    ++t;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    flags[F_T] = t;
+    if (done_n != V) flags[F_CYCLE] = 1;
+  }
+}
+
+// In-link lists by position (graph inputs): the links e = p * N + k whose
+// child is position c, ascending, in in_edge[in_off[c] .. in_off[c+1]).
+__global__ void k_in_count(int E, const int* __restrict__ child_pos, int* in_cnt) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < E && child_pos[e] >= 0) atomicAdd(&in_cnt[child_pos[e]], 1);
+}
+
+__global__ void k_in_fill(int E, const int* __restrict__ child_pos,
+                          const int* __restrict__ in_off, int* in_cur, int* in_edge) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int c = child_pos[e];
+  if (c >= 0) in_edge[in_off[c] + atomicAdd(&in_cur[c], 1)] = e;
+}
+
+__global__ void k_in_sort(int V, const int* __restrict__ in_off, int* in_edge) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= V) return;
+  const int a = in_off[c], b = in_off[c + 1];
+  for (int i = a + 1; i < b; ++i) {   // insertion sort: lists are short
+    const int x = in_edge[i];
+    int j = i - 1;
+    while (j >= a && in_edge[j] > x) {
+      in_edge[j + 1] = in_edge[j];
+      --j;
+    }
+    in_edge[j + 1] = x;
+  }
+}
+
+__global__ void k_zero_ints(int* p, long n) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
 }
 
 // -------------------------------------------------------------------------
@@ -392,7 +507,7 @@ __global__ void k_remap(int V, int N, const int* __restrict__ order, const int* 
     int c = child[(size_t)v * N + k];
     child_pos[(size_t)p * N + k] = (c >= 0 && c < V) ? pos[c] : -1;
   }
-  int q = parent[v];
+  int q = parent ? parent[v] : -1;
   parent_pos[p] = (q >= 0 && q < V) ? pos[q] : -1;
   int r = pull_idx ? pull_idx[v] : -1;
   pull_pos[p] = r;
@@ -847,13 +962,13 @@ __global__ void __launch_bounds__(kSmallThreads) k_sched_small_sort(
 // -------------------------------------------------------------------------
 
 struct Layout {
-  size_t flags, ref_cnt, arrive, pull_cnt, hist, zero_end;
+  size_t flags, ref_cnt, arrive, pull_cnt, hist, rd_cur, zero_end;
+  size_t rd_off, rd_list, nrem, listA, listB, in_cnt;
   size_t nchild, keysA, valsA, keysB, valsB, tile_hist, stage, total;
   int ntiles;
 };
 
 Layout layout(int32_t V, int32_t N, int32_t n_x) {
-  (void)N;
   Layout L;
   size_t o = 0;
   auto take = [&](size_t ints) {
@@ -867,7 +982,14 @@ Layout layout(int32_t V, int32_t N, int32_t n_x) {
   L.arrive = take(2 * ((size_t)V + 1));   // 64-bit words
   L.pull_cnt = take((size_t)n_x + 1);
   L.hist = take((size_t)(V + 2 > 256 ? V + 2 : 256));
+  L.rd_cur = take((size_t)V + 1);
   L.zero_end = o;
+  L.rd_off = take((size_t)V + 1);
+  L.rd_list = take((size_t)V * N + 1);
+  L.nrem = take((size_t)V + 1);
+  L.listA = take((size_t)V + 1);
+  L.listB = take((size_t)V + 1);
+  L.in_cnt = take(2 * ((size_t)V + 1));   // counts, then fill cursors
   L.nchild = take((size_t)V + 1);
   L.keysA = take((size_t)V + 1);
   L.valsA = take((size_t)V + 1);
@@ -922,12 +1044,13 @@ hipError_t wait_stage(cavs_ctx* ctx) {
 
 // The validation result, T, the counts and the level offsets from the host
 // stage; offsets past the first cap come from level_offsets on the device.
-cavs_status read_stage(cavs_ctx* ctx, cavs_sched* s, int cap, const int* level_offsets) {
+cavs_status read_stage(cavs_ctx* ctx, cavs_sched* s, int cap, const int* level_offsets,
+                       bool dag = false) {
   const int* h = ctx->host_stage;
   if (h[F_RANGE]) return fail(ctx, CAVS_ERR_RANGE, "an index array holds an out-of-range value");
   if (h[F_MULTI]) return fail(ctx, CAVS_ERR_MULTIPARENT, "a vertex is a child more than once");
   if (h[F_DUP]) return fail(ctx, CAVS_ERR_DUP_PULL, "two vertices pull the same input row");
-  if (h[F_MISMATCH] || h[F_LINKS] != h[F_WITHPARENT])
+  if (!dag && (h[F_MISMATCH] || h[F_LINKS] != h[F_WITHPARENT]))
     return fail(ctx, CAVS_ERR_MISMATCH, "child[] and parent[] disagree");
   if (h[F_CYCLE]) return fail(ctx, CAVS_ERR_CYCLE, "the child links contain a cycle");
   const int T = h[F_T];
@@ -976,10 +1099,14 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
   int* tile_hist = (int*)(base + L.tile_hist);
   int* stage = (int*)(base + L.stage);
   hipStream_t st = ctx->stream;
+  const bool dag = g->parent == nullptr && V > 0;
+  // graph inputs and more than two slots: levels by peeling (k_graph_levels)
+  const bool peel = dag || N > 2;
   s->V = V;
   s->N = N;
   s->n_x = n_x;
   s->n_push = g->n_push;
+  s->dag = dag ? 1 : 0;
   if (V == 0) {  // nothing to schedule: no launches, no device access
     s->T = 0;
     s->n_pull = s->n_labelled = s->n_leaf_noinput = s->n_inner_input = 0;
@@ -987,7 +1114,7 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
     return CAVS_OK;
   }
 
-  if (V <= kSmallV && n_x <= kSmallNx) {
+  if (!peel && V <= kSmallV && n_x <= kSmallNx) {
     CAVS_LAUNCH("k_sched_small_levels", k_sched_small_levels, dim3(1), dim3(kSmallThreads), 0, st,
                 V, N, n_x, g->n_push, g->child, g->parent, g->pull_idx, g->push_idx, s->level,
                 s->level_offsets, stage, ctx->host_stage_dev);
@@ -1010,10 +1137,27 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
               dim3(256), 0, st, (int*)base, zero_ints, s->level, V);
   CAVS_LAUNCH("k_scan_edges", k_scan_edges, dim3(nb), dim3(256), 0, st, V, N, n_x, g->n_push,
               g->child, g->parent, g->pull_idx, g->push_idx, ref_cnt, pull_cnt, nchild, flags);
-  CAVS_LAUNCH("k_links_levels", k_links_levels, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256), 0,
-              st, V, N, n_x, g->child, g->parent, (const int*)ref_cnt, (const int*)pull_cnt,
-              (const int*)nchild, arrive, s->level, flags);
-  CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist, flags);
+  if (!peel) {
+    CAVS_LAUNCH("k_links_levels", k_links_levels, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256),
+                0, st, V, N, n_x, g->child, g->parent, (const int*)ref_cnt,
+                (const int*)pull_cnt, (const int*)nchild, arrive, s->level, flags);
+    CAVS_LAUNCH("k_level_hist", k_level_hist, dim3(nb), dim3(256), 0, st, V, s->level, hist,
+                flags);
+  } else {
+    int* rd_off = (int*)(base + L.rd_off);
+    int* rd_list = (int*)(base + L.rd_list);
+    CAVS_LAUNCH("k_check_links", k_check_links, dim3(cdiv(V > n_x ? V : n_x, 256)), dim3(256),
+                0, st, V, N, n_x, g->child, g->parent, (const int*)ref_cnt, (const int*)pull_cnt,
+                flags);
+    CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, (const int*)ref_cnt,
+                rd_off, V + 1, (const int*)nullptr, (const int*)nullptr, 0, (int*)nullptr);
+    CAVS_LAUNCH("k_graph_readers", k_graph_readers, dim3(nb), dim3(256), 0, st, V, N, g->child,
+                (const int*)rd_off, (int*)(base + L.rd_cur), rd_list);
+    CAVS_LAUNCH("k_graph_levels", k_graph_levels, dim3(1), dim3(1024), 0, st, V,
+                (const int*)nchild, (const int*)rd_off, (const int*)rd_list,
+                (int*)(base + L.nrem), (int*)(base + L.listA), (int*)(base + L.listB), s->level,
+                hist, flags);
+  }
   const int cap = kHostStageInts - kStageHead;
   CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, hist, s->level_offsets, 0,
               (const int*)(flags + F_T), (const int*)flags, cap, stage);
@@ -1034,13 +1178,29 @@ cavs_status schedule_run(cavs_ctx* ctx, const cavs_graphs* g, cavs_sched* s, voi
     CAVS_LAUNCH("k_remap", k_remap, dim3(nb), dim3(256), 0, st, V, N, (const int*)s->order,
                 (const int*)s->pos, g->child, g->parent, g->pull_idx, g->push_idx, s->child_pos,
                 s->parent_pos, s->pull_pos, s->push_pos);
+    if (dag) {   // the links reading each position, for the backward's sums
+      int* in_cnt = (int*)(base + L.in_cnt);
+      int* in_cur = in_cnt + V + 1;
+      const int E = V * N;
+      CAVS_LAUNCH("k_zero_ints", k_zero_ints, dim3(cdiv(2L * (V + 1), 256)), dim3(256), 0, st,
+                  in_cnt, 2L * (V + 1));
+      CAVS_LAUNCH("k_in_count", k_in_count, dim3(cdiv(E, 256)), dim3(256), 0, st, E,
+                  (const int*)s->child_pos, in_cnt);
+      CAVS_LAUNCH("k_scan_excl", k_scan_excl, dim3(1), dim3(1024), 0, st, (const int*)in_cnt,
+                  s->in_offsets, V + 1, (const int*)nullptr, (const int*)nullptr, 0,
+                  (int*)nullptr);
+      CAVS_LAUNCH("k_in_fill", k_in_fill, dim3(cdiv(E, 256)), dim3(256), 0, st, E,
+                  (const int*)s->child_pos, (const int*)s->in_offsets, in_cur, s->in_edges);
+      CAVS_LAUNCH("k_in_sort", k_in_sort, dim3(nb), dim3(256), 0, st, V,
+                  (const int*)s->in_offsets, s->in_edges);
+    }
     CAVS_LAUNCH_CHECK(ctx);
     return CAVS_OK;
   };
   cavs_status r = sort_and_remap(1);
   if (r != CAVS_OK) return r;
   CAVS_HIP_CHECK(ctx, wait_stage(ctx));
-  r = read_stage(ctx, s, cap, s->level_offsets);
+  r = read_stage(ctx, s, cap, s->level_offsets, dag);
   if (r != CAVS_OK) return r;
   // levels lie in [0, T): enough 8-bit digits for T - 1
   const int T = s->T;

@@ -28,7 +28,8 @@ class Batch:
             return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
         self.child = i32(wl.child.reshape(wl.V, wl.N))
-        self.parent = i32(wl.parent)
+        # graph inputs pass no parent array
+        self.parent = None if getattr(wl, "dag", False) else i32(wl.parent)
         self.pull_idx = i32(wl.pull_idx)
         self.push_idx = i32(wl.push_idx)
         self.X = f32(wl.X)

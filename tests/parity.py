@@ -150,6 +150,17 @@ def pool_workers():
     return max(1, min(16, n))
 
 
+def graphs_contiguous(wl: W.Workload) -> bool:
+    """True when graph k occupies exactly the ids [tree_offsets[k],
+    tree_offsets[k+1]) (not so after shuffle_ids), so graphs can be split
+    by offsets."""
+    gid = np.repeat(np.arange(wl.K), np.diff(wl.tree_offsets))
+    if gid.size != wl.V:
+        return False
+    v, k = np.nonzero(wl.child >= 0)
+    return bool(np.all(gid[wl.child[v, k]] == gid[v]))
+
+
 class OraclePool:
     """Worker processes (spawned; they never touch the GPU) that run the
     oracle over shards of a workload's graphs.  Graphs are independent, so
@@ -175,7 +186,7 @@ class OraclePool:
     def run(self, wl: W.Workload, **kw) -> dict:
         import oracle
         K = wl.K
-        if self._pool is None or K < 2:
+        if self._pool is None or K < 2 or not graphs_contiguous(wl):
             return oracle.run(wl, **kw)
         sizes = np.diff(wl.tree_offsets)
         cum = np.cumsum(sizes)
@@ -217,7 +228,7 @@ def oracle_sharded(wl: W.Workload, workers=None, **kw) -> dict:
     spawned worker processes (a single process for small batches)."""
     import oracle
     workers = workers or pool_workers()
-    if workers <= 1 or wl.K < 2 or wl.V < 300:
+    if workers <= 1 or wl.K < 2 or wl.V < 300 or not graphs_contiguous(wl):
         return oracle.run(wl, **kw)
     with OraclePool(workers) as pool:
         return pool.run(wl, **kw)

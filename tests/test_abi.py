@@ -52,6 +52,7 @@ int main(void) {
          sizeof(cavs_grads), sizeof(cavs_launch_time));
   F(cavs_graphs, child) F(cavs_graphs, push_idx)
   F(cavs_sched, n_inner_input) F(cavs_sched, level) F(cavs_sched, level_offsets_host)
+  F(cavs_sched, dag) F(cavs_sched, in_offsets) F(cavs_sched, in_edges)
   F(cavs_params, C) F(cavs_params, Wx) F(cavs_params, bs)
   F(cavs_inputs, n_y) F(cavs_grads, dX) F(cavs_launch_time, rows) F(cavs_launch_time, ms)
   return 0;
