@@ -228,9 +228,12 @@ def main():
     # engine ablations (fwd+bwd per pass, HIP events): dU formed level by
     # level instead of lazily, the persistent loop for the small levels, and
     # the backward's children's gates unfused from the level products
-    def fwd_bwd_with(var):
-        os.environ[var] = "1"
+    def fwd_bwd_with(*variables):
+        for var in variables:
+            os.environ[var] = "1"
         try:
+            if "CAVS_GENERIC" in variables:   # the generic engine's larger workspace
+                batch.alloc()
             batch.forward()
             batch.backward()
             ctx.sync()
@@ -242,7 +245,39 @@ def main():
             ctx.sync()
             return e0.elapsed_time(e1) / args.steps
         finally:
-            del os.environ[var]
+            for var in variables:
+                del os.environ[var]
+
+    def graph_replay():
+        """forward + backward captured once into a HIP graph (through torch's
+        stream capture of the library's launches on a side stream), then
+        replayed; returns (ms per replay, ms to capture and instantiate)."""
+        side = torch.cuda.Stream()
+        ctx.set_stream(side)
+        try:
+            with torch.cuda.stream(side):
+                batch.forward()
+                batch.backward()
+            ctx.sync()
+            g = torch.cuda.CUDAGraph()
+            tc = time.perf_counter()
+            with torch.cuda.graph(g, stream=side):
+                batch.forward()
+                batch.backward()
+            torch.cuda.synchronize()
+            cap_ms = (time.perf_counter() - tc) * 1e3
+            with torch.cuda.stream(side):
+                g.replay()
+                e0.record(side)
+                for _ in range(args.steps):
+                    g.replay()
+                e1.record(side)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            del g
+            return ms, cap_ms
+        finally:
+            ctx.set_stream(stream)
 
     ablation = None
     if lstm and not args.no_ablation:
@@ -251,6 +286,14 @@ def main():
         ablation["eager_dw_per_level"] = round(fwd_bwd_with("CAVS_EAGER_DW"), 4)
         ablation["persistent_small_levels"] = round(fwd_bwd_with("CAVS_PERSIST"), 4)
         ablation["unfused_backward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_BWD_GATES"), 4)
+        ablation["unfused_forward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_FWD_GATES"), 4)
+        ablation["unfused_gates_both"] = round(
+            fwd_bwd_with("CAVS_UNFUSED_FWD_GATES", "CAVS_UNFUSED_BWD_GATES"), 4)
+        if wl.prec == W.PREC_FP32:
+            ablation["generic_engine"] = round(fwd_bwd_with("CAVS_GENERIC"), 4)
+        g_ms, cap_ms = graph_replay()
+        ablation["graph_captured_replay"] = round(g_ms, 4)
+        ablation["graph_capture_instantiate_ms"] = round(cap_ms, 3)
 
     # inference (cavs_infer: the forward keeping nothing for a backward) beside
     # the training forward alone; whole inference steps include the schedule

@@ -36,6 +36,22 @@ cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...) {
   return st;
 }
 
+// Zero fill by a kernel rather than hipMemsetAsync, so that a caller may
+// capture the calls into a HIP graph (memset nodes in captured graphs have
+// given wrong results on replay on this platform).
+__global__ void k_zero_words(uint32_t* p, long long n) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+hipError_t zero_async(void* p, size_t bytes, hipStream_t s) {
+  const long long n = (long long)(bytes / 4);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_words, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     (uint32_t*)p, n);
+  return hipGetLastError();
+}
+
 cavs_status device_errors(cavs_ctx* ctx) {
   if (!ctx->dev_err || !ctx->dev_err[0]) return CAVS_OK;
   ctx->dev_err[0] = 0;
@@ -453,7 +469,7 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
   ActiveCtx active(ctx);
   hipStream_t str = ctx->stream;
   if (s->V == 0) {
-    CAVS_HIP_CHECK(ctx, hipMemsetAsync(loss_out, 0, sizeof(float), str));
+    CAVS_HIP_CHECK(ctx, zero_async(loss_out, sizeof(float), str));
     return CAVS_OK;
   }
   Net n = make_net(p, s, in, ws, L, train);
@@ -530,16 +546,16 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   const bool lstm = p->cell == CAVS_TREE_LSTM;
   if (s->V == 0) {
     const size_t nU = lstm ? (size_t)H * 4 * H : (size_t)p->N * H * H;
-    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dU, 0, nU * sizeof(float), str));
-    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->db, 0, (lstm ? 4 * H : H) * sizeof(float), str));
+    CAVS_HIP_CHECK(ctx, zero_async(g->dU, nU * sizeof(float), str));
+    CAVS_HIP_CHECK(ctx, zero_async(g->db, (lstm ? 4 * H : H) * sizeof(float), str));
     if (lstm && D > 0)
-      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dWx, 0, (size_t)D * 4 * H * sizeof(float), str));
+      CAVS_HIP_CHECK(ctx, zero_async(g->dWx, (size_t)D * 4 * H * sizeof(float), str));
     if (p->loss == CAVS_LOSS_CE) {
-      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dWs, 0, (size_t)H * p->C * sizeof(float), str));
-      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dbs, 0, (size_t)p->C * sizeof(float), str));
+      CAVS_HIP_CHECK(ctx, zero_async(g->dWs, (size_t)H * p->C * sizeof(float), str));
+      CAVS_HIP_CHECK(ctx, zero_async(g->dbs, (size_t)p->C * sizeof(float), str));
     }
     if (s->n_x > 0)
-      CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
+      CAVS_HIP_CHECK(ctx, zero_async(g->dX, (size_t)s->n_x * D * sizeof(float), str));
     return CAVS_OK;
   }
   Net n = make_net(p, s, in, ws, L, true);
@@ -549,7 +565,7 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
   const int T = s->T;
   const int off1 = T > 1 ? lo[1] : s->V;
   if (s->n_x > 0 && s->n_pull < s->n_x)
-    CAVS_HIP_CHECK(ctx, hipMemsetAsync(g->dX, 0, (size_t)s->n_x * D * sizeof(float), str));
+    CAVS_HIP_CHECK(ctx, zero_async(g->dX, (size_t)s->n_x * D * sizeof(float), str));
   if (lstm && generic_mode(p, s)) {
     gen_backward(n, gen_bufs(s, ws, L), lo, T, s->n_pull, g->dU, g->db, g->dWx, g->dX, g->dWs,
                  g->dbs, str);

@@ -46,6 +46,8 @@ cavs_status fail(cavs_ctx* ctx, cavs_status st, const char* fmt, ...);
 // After the context's stream has been synchronised: CAVS_OK, or the error a
 // kernel recorded in ctx->dev_err since the last check (then cleared).
 cavs_status device_errors(cavs_ctx* ctx);
+// Clears `bytes` (a multiple of 4) at p with a kernel on stream s.
+hipError_t zero_async(void* p, size_t bytes, hipStream_t s);
 
 #define CAVS_HIP_CHECK(ctx, call)                                              \
   do {                                                                         \

@@ -1203,7 +1203,7 @@ bool launch_persist(const char* name, const void* fn, const Net& n, const int* l
   if (const char* e = getenv("CAVS_PERSIST_SPIN")) spin = atoi(e);
   GridBar gb{bar, bar + 64, bar + 65, t_active_ctx ? t_active_ctx->dev_err_dev : nullptr, spin};
   void* args[] = {(void*)&n, (void*)&lo, (void*)&t0, (void*)&t1, (void*)&gb};
-  if (hipMemsetAsync(bar, 0, 256 * sizeof(int), s) != hipSuccess) return false;
+  if (zero_async(bar, 256 * sizeof(int), s) != hipSuccess) return false;
   TimedScope ts(name, s, lo_host[t0], lo_host[t1] - lo_host[t0], /*bracket=*/true);
   return hipLaunchCooperativeKernel(fn, dim3(G), dim3(256), args, 0, s) == hipSuccess;
 }

@@ -444,6 +444,43 @@ def test_runs_on_the_callers_stream():
         c1.close()
 
 
+def test_graph_captured_replays_match_eager():
+    """forward + backward captured into a HIP graph (torch's stream capture
+    of the library's launches on a side stream) and replayed three times,
+    with eager runs and synchronisations in between: every replay gives the
+    eager run's outputs bit for bit."""
+    wl = W.config_treelstm_sst(3, K=24)
+    side = torch.cuda.Stream()
+    c = B.Context(0, stream=side)
+    try:
+        b = Batch(wl, c)
+        with torch.cuda.stream(side):
+            ref = b.run()
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            b.forward()
+            b.backward()
+        torch.cuda.synchronize()
+        for rep in range(3):
+            for t in b.grads.values():
+                t.fill_(float("nan"))
+            b.h.fill_(float("nan"))
+            with torch.cuda.stream(side):
+                g.replay()
+            torch.cuda.synchronize()
+            got = b.results()
+            for k in ref:
+                assert np.array_equal(np.asarray(got[k]), np.asarray(ref[k])), (rep, k)
+            with torch.cuda.stream(side):
+                b.forward()
+                b.backward()
+            c.sync()
+        del g
+    finally:
+        c.close()
+
+
 def test_determinism_bitwise(ctx):
     wl = W.config_treelstm_sst(0, K=24)
     b = Batch(wl, ctx)
