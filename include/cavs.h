@@ -82,6 +82,8 @@ typedef int32_t cavs_status;
 /* loss heads attached through push */
 #define CAVS_LOSS_CE 0    /* softmax cross-entropy over C classes, mean over labelled vertices */
 #define CAVS_LOSS_L2 1    /* 0.5 * ||h - y||^2, mean over labelled vertices */
+#define CAVS_LOSS_NONE 2  /* no loss head: the states go to an external consumer (push
+                             connector), whose gradient comes back as inputs.dH_ext */
 
 typedef struct cavs_ctx cavs_ctx;
 
@@ -210,6 +212,12 @@ cavs_status cavs_schedule_static(cavs_ctx* ctx, const cavs_graphs* graphs, cavs_
  *   U holds W as [N*H, H] (rows k*H .. k*H+H-1 = W_k); b [H]; Wx unused.
  * Loss (the lazily batched push, Section 3.5): CE z = h Ws + bs, Ws [H, C],
  *   bs [C]; or L2 against rows of Y [n_y, H].  L = mean over labelled vertices.
+ *   CE with more than 16 classes (a language-model vocabulary at every
+ *   vertex) runs on matrix-core products and needs C % 4 == 0.
+ *   CAVS_LOSS_NONE: no head (L = 0); with inputs.dH_ext the backward is that
+ *   of an external loss whose gradient w.r.t. the pushed states is dH_ext --
+ *   the connector that stacks layers (layer l+1 pulls layer l's h_out as X,
+ *   layer l gets layer l+1's dX as dH_ext) or joins an encoder to a decoder.
  * ------------------------------------------------------------------------- */
 typedef struct {
   int32_t cell;             /* CAVS_TREE_LSTM or CAVS_TREE_FC */
@@ -219,14 +227,17 @@ typedef struct {
   const float* Wx;          /* TREE_LSTM: [D, 4H]; TREE_FC: unused (may be NULL) */
   const float* U;           /* TREE_LSTM: [H, 4H]; TREE_FC: [N*H, H] */
   const float* b;           /* TREE_LSTM: [4H];    TREE_FC: [H] */
-  const float* Ws;          /* CE: [H, C]; L2: unused */
-  const float* bs;          /* CE: [C];    L2: unused */
+  const float* Ws;          /* CE: [H, C]; L2, NONE: unused */
+  const float* bs;          /* CE: [C];    L2, NONE: unused */
 } cavs_params;
 
 typedef struct {
   const float* X;           /* [n_x, D] pulled inputs (may be NULL when n_x = 0) */
   const float* Y;           /* L2: [n_y, H] targets; CE: unused */
   int32_t n_y;              /* rows of Y */
+  const float* dH_ext;      /* [V, H] vertex-id order, or NULL: gradient of the pushed
+                               states from an external consumer, added to every vertex's
+                               dL/dh by cavs_backward (cavs_forward ignores it) */
 } cavs_inputs;
 
 typedef struct {            /* outputs of cavs_backward, overwritten (not accumulated) */

@@ -35,6 +35,7 @@ ERR_DUP_PULL = -9
 
 LOSS_CE = 0
 LOSS_L2 = 1
+LOSS_NONE = 2
 
 
 def build(force: bool = False, precision: str = "f64") -> str:
@@ -80,10 +81,10 @@ def lib(precision: str = "f64"):
         _lib.orc_schedule.argtypes = [ct.c_int, ct.c_int, i32p, i32p, i32p, i32p, ct.c_int] + [i32p] * 10
         _lib.orc_treelstm.restype = ct.c_int
         _lib.orc_treelstm.argtypes = ([ct.c_int] * 8 + [i32p] * 4 + [f64p] * 7 + [freal]
-                                      + [f64p] * 5 + [ct.c_int] + [f64p] * 8)
+                                      + [f64p] * 5 + [ct.c_int] + [f64p] * 9)
         _lib.orc_treefc.restype = ct.c_int
         _lib.orc_treefc.argtypes = ([ct.c_int] * 7 + [i32p] * 4 + [f64p] * 6 + [freal]
-                                    + [f64p] * 3 + [ct.c_int] + [f64p] * 7)
+                                    + [f64p] * 3 + [ct.c_int] + [f64p] * 8)
         _lib.orc_bf16_round.restype = ct.c_double
         _lib.orc_bf16_round.argtypes = [ct.c_double]
         _libs[precision] = L
@@ -173,13 +174,15 @@ def bf16_round(x: float) -> float:
 
 def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool = True,
         denom: float = 0.0, params: Optional[dict] = None, X=None, Y=None,
-        precision: str = "f64") -> dict:
+        precision: str = "f64", dH_ext=None) -> dict:
     """Forward (+ loss) and optionally backward of ``wl``.
 
     ``precision`` "f64" (the parity reference) or "f32" (the same definitions
     evaluated in fp32).  ``params`` may override any of Wx, U, b, Ws, bs (e.g.
     for finite differences); X/Y likewise.  ``bf16`` defaults to the
-    workload's precision.  Graph workloads (``wl.dag``) pass no parent array,
+    workload's precision.  ``dH_ext`` [V, H] (vertex-id rows) is the gradient
+    of the pushed states from an external consumer, added to every dL/dh.
+    Graph workloads (``wl.dag``) pass no parent array,
     so a vertex may be read by several vertices.  Returns a dict of float64
     arrays with h, c, gates, lossv, loss and, when ``backward``, dh, dc
     (total dL/dh_v, dL/dc_v per vertex), dWx, dU, db, dWs, dbs, dX.
@@ -211,6 +214,7 @@ def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool 
     bsk, bsp = rl(from_wl["bs"] if from_wl["bs"].size else np.zeros(1))
     h, hp = out((V, H))
     lossv, lvp = out(V)
+    ext, extp = rl(dH_ext) if dH_ext is not None else (None, None)
     loss = (ct.c_double if precision == "f64" else ct.c_float)(0.0)
     n_x = max(int(Xa.shape[0]), 1)
     res = dict()
@@ -228,7 +232,7 @@ def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool 
         st = L.orc_treelstm(V, N, D, H, C, wl.loss, int(bool(bf16)), int(order_mode),
                             chp, parp, plp, psp, Xp, Yp, Wp, Up, bp, Wsp, bsp,
                             float(denom), hp, cp, gp, lvp, ct.byref(loss), int(backward),
-                            dhp, dcp, dWxp, dUp, dbp, dWsp, dbsp, dXp)
+                            dhp, dcp, dWxp, dUp, dbp, dWsp, dbsp, dXp, extp)
         res.update(c=c, gates=gates)
         if backward:
             res.update(dh=dh, dc=dc, dWx=dWx, dU=dU, db=db, dX=dX[: Xa.shape[0]])
@@ -245,12 +249,12 @@ def run(wl, *, order_mode: int = 0, bf16: Optional[bool] = None, backward: bool 
         st = L.orc_treefc(V, N, H, C, wl.loss, int(bool(bf16)), int(order_mode),
                           chp, parp, plp, psp, Xp, Yp, Up, bp, Wsp, bsp, float(denom),
                           hp, lvp, ct.byref(loss), int(backward), dhp, dcsp, dWp, dbp,
-                          dWsp, dbsp, dXp)
+                          dWsp, dbsp, dXp, extp)
         if backward:
             res.update(dh=dh, dU=dW, db=db, dX=dX[: Xa.shape[0]])
             if wl.loss == LOSS_CE:
                 res.update(dWs=dWs[:, :C], dbs=dbs[:C])
-    del ch_keep
+    del ch_keep, ext
     if st != OK:
         raise ValueError("oracle rejected the input: status %d" % st)
     res.update(h=h, lossv=lossv, loss=float(loss.value))

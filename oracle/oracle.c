@@ -65,6 +65,7 @@ typedef double real;
 
 #define LOSS_CE 0
 #define LOSS_L2 1
+#define LOSS_NONE 2   /* no loss head: the state is pushed to an external consumer */
 
 /* ------------------------------------------------------------------------ */
 /* bf16 emulation: round x to 8 significant bits, ties to even.              */
@@ -288,6 +289,8 @@ typedef struct {
   /* forward results */
   real *h, *c, *gates, *lossv;
   /* backward */
+  const real* dh_ext;   /* [V, H] or NULL: gradient of the pushed states from an
+                           external consumer (push connector), added to dL/dh */
   real *dh, *dc;
   real *dWx, *dU, *db, *dWs, *dbs, *dX;
   int do_bwd;
@@ -306,7 +309,7 @@ static void loss_vertex(model_t* m, int v) {
   int H = m->H, C = m->C;
   int y = m->push_idx ? m->push_idx[v] : -1;
   m->lossv[v] = R(0);
-  if (y < 0) return;
+  if (y < 0 || m->loss_kind == LOSS_NONE) return;
   const real* hv = m->h + (size_t)v * H;
   if (m->loss_kind == LOSS_CE) {
     real* z = (real*)malloc(sizeof(real) * C);
@@ -664,6 +667,8 @@ static int run_model(model_t* m, int order_mode, real* loss_out) {
     L += m->lossv[v];
   }
   *loss_out = L / m->denom;
+  if (m->do_bwd && m->dh_ext)
+    for (size_t i = 0; i < (size_t)V * H; ++i) m->dh[i] += m->dh_ext[i];
   if (m->do_bwd) {
     if (order_mode == 1) {
       for (int t = T - 1; t >= 0; --t)
@@ -684,9 +689,10 @@ int orc_treelstm(int V, int N, int D, int H, int C, int loss_kind, int bf16, int
                  const real* b, const real* Ws, const real* bs, real denom,
                  real* h, real* c, real* gates, real* lossv, real* loss,
                  int do_bwd, real* dh, real* dc, real* dWx, real* dU, real* db,
-                 real* dWs, real* dbs, real* dX) {
+                 real* dWs, real* dbs, real* dX, const real* dh_ext) {
   model_t m;
   memset(&m, 0, sizeof m);
+  m.dh_ext = dh_ext;
   m.V = V; m.N = N; m.D = D; m.H = H; m.C = C; m.loss_kind = loss_kind; m.cell = 0;
   m.child = child; m.parent = parent; m.pull_idx = pull_idx; m.push_idx = push_idx;
   m.X = X; m.Y = Y; m.Wx = Wx; m.U = U; m.b = b; m.Ws = Ws; m.bs = bs; m.denom = denom;
@@ -717,9 +723,10 @@ int orc_treefc(int V, int N, int H, int C, int loss_kind, int bf16, int order_mo
                const real* Ws, const real* bs, real denom,
                real* h, real* lossv, real* loss,
                int do_bwd, real* dh, real* dc_scratch, real* dW, real* db,
-               real* dWs, real* dbs, real* dX) {
+               real* dWs, real* dbs, real* dX, const real* dh_ext) {
   model_t m;
   memset(&m, 0, sizeof m);
+  m.dh_ext = dh_ext;
   m.V = V; m.N = N; m.D = H; m.H = H; m.C = C; m.loss_kind = loss_kind; m.cell = 1;
   m.child = child; m.parent = parent; m.pull_idx = pull_idx; m.push_idx = push_idx;
   m.X = X; m.Y = Y; m.U = W; m.b = b; m.Ws = Ws; m.bs = bs; m.denom = denom;

@@ -35,6 +35,7 @@ FP32 = 0
 BF16 = 1
 LOSS_CE = 0
 LOSS_L2 = 1
+LOSS_NONE = 2
 
 _i32 = ct.c_int32
 _vp = ct.c_void_p
@@ -62,7 +63,7 @@ class cavs_params(ct.Structure):
 
 
 class cavs_inputs(ct.Structure):
-    _fields_ = [("X", _vp), ("Y", _vp), ("n_y", _i32)]
+    _fields_ = [("X", _vp), ("Y", _vp), ("n_y", _i32), ("dH_ext", _vp)]
 
 
 class cavs_grads(ct.Structure):
@@ -335,10 +336,14 @@ def infer(ctx: Context, params: Params, sched: Schedule, X: Optional[torch.Tenso
 
 
 def backward(ctx: Context, params: Params, sched: Schedule, X: Optional[torch.Tensor],
-             Y: Optional[torch.Tensor], ws: torch.Tensor, grads: dict) -> None:
-    """cavs_backward (asynchronous); ``grads`` holds dWx, dU, db, dWs, dbs, dX tensors."""
+             Y: Optional[torch.Tensor], ws: torch.Tensor, grads: dict,
+             dH_ext: Optional[torch.Tensor] = None) -> None:
+    """cavs_backward (asynchronous); ``grads`` holds dWx, dU, db, dWs, dbs, dX
+    tensors; ``dH_ext`` [V, H] (vertex-id rows) is an external gradient of the
+    pushed states."""
     p = params.raw()
-    inp = cavs_inputs(_ptr(X), _ptr(Y), int(Y.shape[0]) if Y is not None else 0)
+    inp = cavs_inputs(_ptr(X), _ptr(Y), int(Y.shape[0]) if Y is not None else 0,
+                      _ptr(dH_ext))
     g = cavs_grads(*[_ptr(grads.get(k)) for k in ("dWx", "dU", "db", "dWs", "dbs", "dX")])
     ctx.check(lib().cavs_backward(ctx._h, ct.byref(p), ct.byref(sched.raw), ct.byref(inp),
                                   ws.data_ptr(), ws.numel(), ct.byref(g)))

@@ -70,7 +70,11 @@ struct WsLayout {
   size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bpart, bar, total;
   size_t part_floats;
   size_t gHt, gDt, gEh, gEc, gdAx, gpart;   // generic engine
+  size_t WsT, dHLx;
+  size_t gpart_floats;
 };
+
+bool lm_head(const cavs_params* p) { return p->loss == CAVS_LOSS_CE && p->C > kSmallHeadC; }
 
 bool env_on(const char* name) {
   const char* e = getenv(name);
@@ -91,6 +95,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   const bool lstm = p->cell == CAVS_TREE_LSTM;
   const size_t GW = lstm ? (size_t)(3 + p->N) * H : H;
   const size_t C = p->loss == CAVS_LOSS_CE ? (size_t)(p->C + 3) / 4 * 4 : 0;
+  const bool lm = lm_head(p);
   size_t o = 0;
   auto take = [&](size_t floats) {
     size_t r = o;
@@ -104,7 +109,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.Hs = take(V * H);
   L.Cs = take(lstm ? V * H : 0);
   L.Gs = take((tr || gen) ? (lstm ? V * GW : 0) : 0);   // the generic forward stages in it
-  L.dZ = take(tr * V * (C > 0 ? C : 1));
+  L.dZ = take((tr || lm) ? V * (C > 0 ? C : 1) : 0);   // the LM head's logits in inference
   L.lossv = take(V);
   L.dHL = take(tr * V * H);
   L.dHp = take(tr * V * H);
@@ -112,8 +117,14 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.dA = take(tr * V * GW);
   L.part_floats = tr * lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
   L.part = take(3 * L.part_floats);   // dU_iou, dU_f and dW_x split-K sums side by side
-  L.bpart = take(tr * bias_part_floats(p->H, p->loss == CAVS_LOSS_CE ? p->C : 0));
+  L.bpart = take(tr * bias_part_floats(p->H, (p->loss == CAVS_LOSS_CE && !lm) ? p->C : 0));
   L.bar = take(256);
+  L.WsT = take(lm ? C * H : 0);
+  L.dHLx = take(tr * V * H);
+  if (lm && !gen) {
+    L.gpart_floats = tr * gen_part_floats(p->D, p->H, (int)C);
+    L.gpart = take(L.gpart_floats);
+  }
   if (gen) {
     const size_t N = (size_t)p->N;
     L.gHt = take(V * H);
@@ -121,7 +132,8 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
     L.gEh = take(tr * V * N * H);
     L.gEc = take(tr * V * N * H);
     L.gdAx = take(tr * V * 4 * H);
-    L.gpart = take(tr * gen_part_floats(p->D, p->H, (int)C));
+    L.gpart_floats = tr * gen_part_floats(p->D, p->H, (int)C);
+    L.gpart = take(L.gpart_floats);
   }
   L.total = o;
   return L;
@@ -133,7 +145,7 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
   if (!p || !s || !in) return fail(ctx, CAVS_ERR_ARG, "null params / sched / inputs");
   if (p->cell != CAVS_TREE_LSTM && p->cell != CAVS_TREE_FC)
     return fail(ctx, CAVS_ERR_ARG, "unknown cell %d", p->cell);
-  if (p->loss != CAVS_LOSS_CE && p->loss != CAVS_LOSS_L2)
+  if (p->loss != CAVS_LOSS_CE && p->loss != CAVS_LOSS_L2 && p->loss != CAVS_LOSS_NONE)
     return fail(ctx, CAVS_ERR_ARG, "unknown loss %d", p->loss);
   if (p->prec != CAVS_FP32 && p->prec != CAVS_BF16)
     return fail(ctx, CAVS_ERR_ARG, "unknown precision %d", p->prec);
@@ -161,10 +173,13 @@ cavs_status check_args(cavs_ctx* ctx, const cavs_params* p, const cavs_sched* s,
     return fail(ctx, CAVS_ERR_ARG, "schedule arrays missing");
   if (!p->U || !p->b) return fail(ctx, CAVS_ERR_ARG, "U and b are required");
   if (p->loss == CAVS_LOSS_CE) {
-    if (p->C <= 0 || p->C > 16) return fail(ctx, CAVS_ERR_UNSUPPORTED, "C=%d (1..16)", p->C);
+    if (p->C <= 0) return fail(ctx, CAVS_ERR_ARG, "C=%d classes", p->C);
+    if (p->C > kSmallHeadC && p->C % 4 != 0)
+      return fail(ctx, CAVS_ERR_UNSUPPORTED, "C=%d: more than %d classes must be a multiple of 4",
+                  p->C, kSmallHeadC);
     if (s->n_push != p->C) return fail(ctx, CAVS_ERR_ARG, "schedule n_push != C");
     if (!p->Ws || !p->bs) return fail(ctx, CAVS_ERR_ARG, "Ws and bs are required for CE");
-  } else {
+  } else if (p->loss == CAVS_LOSS_L2) {
     if (s->n_push != in->n_y) return fail(ctx, CAVS_ERR_ARG, "schedule n_push != n_y");
     if (s->n_labelled > 0 && !in->Y) return fail(ctx, CAVS_ERR_ARG, "Y is required for L2");
   }
@@ -238,6 +253,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.b = p->b;
   n.Ws = p->Ws;
   n.bs = p->bs;
+  n.WsT = (float*)((char*)ws + L.WsT);
   n.X = in->X;
   n.Y = in->Y;
   n.P = (float*)(base + L.P);
@@ -257,7 +273,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.dA = (float*)(base + L.dA);
   if (!train) {   // the kernels test these for null and skip what only backward reads
     if (!(p->cell == CAVS_TREE_LSTM && generic_mode(p, s))) n.Gs = nullptr;
-    n.dZ = nullptr;
+    if (!lm_head(p)) n.dZ = nullptr;
     n.dHL = nullptr;
     n.dHp = nullptr;
     n.dCp = nullptr;
@@ -275,6 +291,7 @@ GenBufDev gen_bufs(const cavs_sched* s, void* ws, const WsLayout& L) {
   b.Ec = (float*)(base + L.gEc);
   b.dAx = (float*)(base + L.gdAx);
   b.part = (float*)(base + L.gpart);
+  b.part_cap = L.gpart_floats;
   b.in_off = s->dag ? s->in_offsets : nullptr;
   b.in_edge = s->dag ? s->in_edges : nullptr;
   return b;
@@ -559,6 +576,11 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     return CAVS_OK;
   }
   Net n = make_net(p, s, in, ws, L, true);
+  if (in->dH_ext) {   // the push connector's gradient joins the loss head's term
+    float* dhlx = (float*)((char*)ws + L.dHLx);
+    add_external_grad(n, in->dH_ext, dhlx, str);
+    n.dHL = dhlx;
+  }
   float* part = (float*)((char*)ws + L.part);
   float* bpart = (float*)((char*)ws + L.bpart);
   const int* lo = s->level_offsets_host;
@@ -602,6 +624,8 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);
+    if (lm_head(p))
+      lm_head_grads(n, g->dWs, g->dbs, (float*)((char*)ws + L.gpart), L.gpart_floats, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
   } else {
     for (int t = T - 1; t >= 0; --t) {
@@ -613,6 +637,8 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     SplitJobs jobs;
     bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);
+    if (lm_head(p))
+      lm_head_grads(n, g->dWs, g->dbs, (float*)((char*)ws + L.gpart), L.gpart_floats, str);
   }
   CAVS_LAUNCH_CHECK(ctx);
   return CAVS_OK;

@@ -406,6 +406,65 @@ __global__ void __launch_bounds__(256) k_gen_bwd_gates(Net n, GenBufDev b, int o
   st4(dx + G_U * H, f4(du));
 }
 
+// ---------------------------------------------------------- the LM head
+// A softmax loss over a large vocabulary at every labelled vertex (the LM
+// models of Section 5): logits Z = h W_s + b_s by an NT product into the dZ
+// rows, then one workgroup per position forms the log-sum-exp and dZ in
+// fp64, and dL/dh = dZ W_s^T by a second NT product.
+
+// dst[c][r] = src[r][c] for an R x Cc row-major src.
+__global__ void __launch_bounds__(256) k_gen_transpose(const float* __restrict__ src, int R,
+                                                       int Cc, float* __restrict__ dst) {
+  __shared__ float t[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int y = ty; y < 32; y += 8)
+    if (r0 + y < R && c0 + tx < Cc) t[y][tx] = src[(size_t)(r0 + y) * Cc + c0 + tx];
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8)
+    if (c0 + y < Cc && r0 + tx < R) dst[(size_t)(c0 + y) * R + r0 + tx] = t[tx][y];
+}
+
+__device__ __forceinline__ double block_reduce(double v, bool is_max, double* red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const double x = __shfl_xor(v, o, kWave);
+    v = is_max ? fmax(v, x) : v + x;
+  }
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double r = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) r = is_max ? fmax(r, red[i]) : r + red[i];
+  return r;
+}
+
+// Position p = blockIdx.x: its logits row (dZ[p], C wide) plus b_s; labelled:
+// lossv = lse - z_y and (with write_dz) dZ = (softmax - e_y) / |Lambda|;
+// unlabelled: lossv = 0, dZ = 0.
+__global__ void __launch_bounds__(256) k_lm_softmax(Net n, int write_dz) {
+  __shared__ double red[4];
+  const int p = blockIdx.x, C = n.C, tid = threadIdx.x;
+  float* row = n.dZ + (size_t)p * C;
+  const int y = n.push_pos[p];
+  const double zy = y >= 0 ? (double)row[y] + (double)n.bs[y] : 0.0;
+  double m = -INFINITY;
+  for (int c = tid; c < C; c += 256) m = fmax(m, (double)row[c] + (double)n.bs[c]);
+  m = block_reduce(m, true, red);
+  double se = 0.0;
+  for (int c = tid; c < C; c += 256) se += exp((double)row[c] + (double)n.bs[c] - m);
+  se = block_reduce(se, false, red);
+  const double lse = m + log(se);
+  if (tid == 0) n.lossv[p] = y >= 0 ? (float)(lse - zy) : 0.f;
+  if (!write_dz) return;
+  const double inv = (double)n.inv_denom;
+  for (int c = tid; c < C; c += 256) {
+    const double z = (double)row[c] + (double)n.bs[c];
+    row[c] = y >= 0 ? (float)((exp(z - lse) - (c == y ? 1.0 : 0.0)) * inv) : 0.f;
+  }
+}
+
 // ----------------------------------------------------------------- launchers
 GenIdx gen_idx(const Net& n) { return GenIdx{n.child_pos, n.pull_list, n.pull_pos, n.N, n.H}; }
 RowSel sel(const float* base, int ld, int mode = RM_DIRECT, int row0 = 0) {
@@ -429,9 +488,14 @@ int gen_splits(int R, int tiles) {
 
 // C (ldc; columns < Nb_out) (= or +=) sum_r A_r^T B_r
 void gen_tn(const char* name, const Net& n, int R, int Ka, int Nb, int Nb_out, RowSel ra,
-            RowSel rb, float* C, int ldc, bool accumulate, float* part, hipStream_t s) {
+            RowSel rb, float* C, int ldc, bool accumulate, float* part, hipStream_t s,
+            size_t part_cap = 0) {
   const int tiles = cdiv(Ka, kGT) * cdiv(Nb, kGT);
-  const int S = gen_splits(R, tiles);
+  int S = gen_splits(R, tiles);
+  if (part_cap) {   // at least one split always fits (the scratch is sized for it)
+    const size_t fit = part_cap / ((size_t)Ka * Nb);
+    if ((size_t)S > fit) S = fit > 0 ? (int)fit : 1;
+  }
   const int per = (R > 0 ? cdiv(cdiv(R, S), kGK) : 1) * kGK;
   CAVS_LAUNCH(name, k_gen_tn, dim3(cdiv(Ka, kGT), cdiv(Nb, kGT), S), dim3(256), 0, s, R, Ka, Nb,
               ra, rb, gen_idx(n), per, part);
@@ -551,7 +615,7 @@ void gen_backward(const Net& n, const GenBufDev& b, const int* lo, int T, int n_
   gen_colsum(n, V, 4 * H, 4 * H, sel(b.dAx, 4 * H), db, part, s);
   if (n.loss == CAVS_LOSS_CE) {
     gen_tn("k_gen_tn<dWs>", n, V, H, n.CP, n.C, sel(n.Hs, H), sel(n.dZ, n.CP), dWs, n.C, false,
-           part, s);
+           part, s, b.part_cap);
     gen_colsum(n, V, n.CP, n.C, sel(n.dZ, n.CP), dbs, part, s);
   }
 }
@@ -559,9 +623,35 @@ void gen_backward(const Net& n, const GenBufDev& b, const int* lo, int T, int n_
 size_t gen_part_floats(int D, int H, int CP) {
   size_t m = (size_t)2 * H * H;
   if ((size_t)D * 4 * H > m) m = (size_t)D * 4 * H;
-  if ((size_t)H * (CP > 4 ? CP : 4) > m) m = (size_t)H * (CP > 4 ? CP : 4);
+  const int cs = CP < 4 ? 4 : (CP > 16 ? 16 : CP);
+  if ((size_t)H * cs > m) m = (size_t)H * cs;
   if ((size_t)4 * H > m) m = (size_t)4 * H;
-  return m * kMaxSplits;
+  size_t total = m * kMaxSplits;
+  if (CP > 16) {   // LM head: dW_s in one split, db_s in up to kMaxSplits
+    const size_t lm = (size_t)H * CP + (size_t)kMaxSplits * CP;
+    if (lm > total) total = lm;
+  }
+  return total;
+}
+
+void lm_head_fwd(const Net& n, hipStream_t s) {
+  const int H = n.H, C = n.C, V = n.V;
+  const RowSel none = sel(nullptr, 0);
+  CAVS_LAUNCH("k_gen_transpose", k_gen_transpose, dim3(cdiv(C, 32), cdiv(H, 32)), dim3(256), 0,
+              s, n.Ws, H, C, n.WsT);
+  gen_nt("k_gen_nt<lm_logits>", n, V, C, H, sel(n.Hs, H), n.WsT, H, sel(n.dZ, C), none, false,
+         s);
+  CAVS_LAUNCH("k_lm_softmax", k_lm_softmax, dim3(V), dim3(256), 0, s, n, (int)(n.dHL != nullptr));
+  if (n.dHL)
+    gen_nt("k_gen_nt<lm_dh>", n, V, H, C, sel(n.dZ, C), n.Ws, C, sel(n.dHL, H), none, false, s);
+}
+
+void lm_head_grads(const Net& n, float* dWs, float* dbs, float* part, size_t part_cap,
+                   hipStream_t s) {
+  const int H = n.H, C = n.C, V = n.V;
+  gen_tn("k_gen_tn<lm_dWs>", n, V, H, C, C, sel(n.Hs, H), sel(n.dZ, C), dWs, C, false, part, s,
+         part_cap);
+  gen_colsum(n, V, C, C, sel(n.dZ, C), dbs, part, s);
 }
 
 }  // namespace cavs

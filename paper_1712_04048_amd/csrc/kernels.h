@@ -36,6 +36,7 @@ struct Net {
                                 // cleared by the transpose kernel and by the loss kernel
   const float* b;
   const float* Ws;              // [H, C]
+  float* WsT;                   // [C, H] W_s transposed (workspace; the LM head)
   const float* bs;              // [C]
   const float* X;               // [n_x, D]
   const float* Y;               // [n_y, H]
@@ -71,6 +72,7 @@ struct GenBufDev {
   float* Ec;          // [V*N, H]   dL/dc sent back along each child link
   float* dAx;         // [V, 4H]    (d_i, sum_k d_fk, d_o, d_u): input and bias gradients
   float* part;        // split-K partial sums (gen_part_floats)
+  size_t part_cap;    // floats in part
   const int* in_off;  // graph inputs: [V+1] offsets into in_edge per position; null for trees
   const int* in_edge; // graph inputs: links reading each position, ascending
 };
@@ -119,6 +121,13 @@ void gen_backward(const Net& n, const GenBufDev& b, const int* lo_host, int T, i
                   float* dU, float* db, float* dWx, float* dX, float* dWs, float* dbs,
                   hipStream_t s);
 size_t gen_part_floats(int D, int H, int CP);
+// Softmax heads with more than kSmallHeadC classes (a language-model
+// vocabulary): logits, log-sum-exp, dZ and dL/dh on the generic products.
+constexpr int kSmallHeadC = 16;
+// per-vertex loss terms into lossv (and dZ, dL/dh when training)
+void lm_head_fwd(const Net& n, hipStream_t s);
+void lm_head_grads(const Net& n, float* dWs, float* dbs, float* part, size_t part_cap,
+                   hipStream_t s);
 // fc.hip
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);
@@ -133,6 +142,9 @@ void pull_gemm(const Net& n, int n_pull, bool with_f, int lo1, hipStream_t s);
 // lstm_transpose_u earlier in the same pass).
 bool pull_tile_applies(const Net& n, int n_pull);
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s);
+// dhlx = the loss head's dL/dh plus an external gradient of the pushed
+// states (vertex-id rows).
+void add_external_grad(const Net& n, const float* ext, float* dhlx, hipStream_t s);
 void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s);
 // Lazy weight-gradient products; `part` is split-K scratch of part_floats floats.
 // Split-K sums waiting for their reduction: the lazy products append one

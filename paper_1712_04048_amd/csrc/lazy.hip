@@ -1460,8 +1460,34 @@ void dx_gemm(const Net& n, int n_pull, bool with_f, float* dX, hipStream_t s) {
     CAVS_LAUNCH("k_dx_gemm", k_dx_gemm, grid, dim3(256), 0, s, n, n_pull, (int)with_f, dX);
 }
 
+// dhlx[p] = dHL[p] + ext[vertex of p]: the gradient an external consumer of
+// the pushed states sends back (vertex-id rows), joined to the loss head's.
+__global__ void __launch_bounds__(256) k_add_ext(Net n, const float* __restrict__ ext,
+                                                 float* __restrict__ dhlx) {
+  const int q = n.H / 4;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)n.V * q) return;
+  const int p = (int)(i / q), j0 = 4 * (int)(i % q);
+  const int v = n.order[p];
+  st4(dhlx + (size_t)p * n.H + j0,
+      add4(ldg4(n.dHL + (size_t)p * n.H + j0), ldg4(ext + (size_t)v * n.H + j0)));
+}
+
+void add_external_grad(const Net& n, const float* ext, float* dhlx, hipStream_t s) {
+  if (n.V <= 0) return;
+  CAVS_LAUNCH("k_add_ext", k_add_ext, dim3(cdiv((long)n.V * (n.H / 4), 256)), dim3(256), 0, s, n,
+              ext, dhlx);
+}
+
 void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
-  if (n.loss == CAVS_LOSS_CE) {
+  if (n.loss == CAVS_LOSS_NONE || (n.loss == CAVS_LOSS_CE && n.C > kSmallHeadC))
+    (void)zero_async(n.zrow, (size_t)n.H * sizeof(float), s);   // the small heads' kernels clear it
+  if (n.loss == CAVS_LOSS_NONE) {   // states pushed to an external consumer only
+    (void)zero_async(n.lossv, (size_t)n.V * sizeof(float), s);
+    if (n.dHL) (void)zero_async(n.dHL, (size_t)n.V * n.H * sizeof(float), s);
+  } else if (n.loss == CAVS_LOSS_CE && n.C > kSmallHeadC) {
+    lm_head_fwd(n, s);
+  } else if (n.loss == CAVS_LOSS_CE) {
     const int per = cdiv(n.H / kBK, kLossWaves);  // K chunks per wavefront
     const dim3 grid(cdiv(n.V, 16)), block(64 * kLossWaves);
     if (per <= 1) CAVS_LAUNCH("k_loss_ce<1>", k_loss_ce<1>, grid, block, 0, s, n);
@@ -1531,7 +1557,7 @@ size_t bias_part_floats(int H, int C) {
 void bias_head_grads(const Net& n, int row0, int row1, int lo1, float* db, float* dWs, float* dbs,
                      float* part, hipStream_t s, SplitJobs* jobs) {
   const int wA = n.GW == n.H ? n.H : 4 * n.H;
-  const bool head = n.loss == CAVS_LOSS_CE;
+  const bool head = n.loss == CAVS_LOSS_CE && n.C <= kSmallHeadC;   // the LM head has its own
   const int HC = head ? n.H * n.C : 0;
   int nchunk = cdiv(n.V, 16);
   if (nchunk > kBiasChunks) nchunk = kBiasChunks;

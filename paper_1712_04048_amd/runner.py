@@ -40,6 +40,7 @@ class Batch:
                                U=f32(wl.U), b=f32(wl.b),
                                Ws=f32(wl.Ws) if wl.loss == B.LOSS_CE else None,
                                bs=f32(wl.bs) if wl.loss == B.LOSS_CE else None)
+        self.dH_ext: Optional[torch.Tensor] = None   # [V, H] external gradient of h_out
         self.sched: Optional[B.Schedule] = None
         self.ws = None
         self.ws_infer = None
@@ -81,7 +82,8 @@ class Batch:
                   self.loss)
 
     def backward(self):
-        B.backward(self.ctx, self.params, self.sched, self.X, self.Y, self.ws, self.grads)
+        B.backward(self.ctx, self.params, self.sched, self.X, self.Y, self.ws, self.grads,
+                   self.dH_ext)
 
     def infer(self):
         """cavs_infer into the same h / c / loss outputs, with its own smaller workspace."""

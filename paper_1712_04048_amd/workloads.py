@@ -32,6 +32,7 @@ PREC_FP32 = 0
 PREC_BF16 = 1
 LOSS_CE = 0
 LOSS_L2 = 1
+LOSS_NONE = 2     # no loss head: the pushed states go to an external consumer
 
 
 @dataclass
@@ -304,7 +305,11 @@ def make_workload(name: str, trees: List[List[List[int]]], *, cell: int = CELL_T
     else:
         raise ValueError(labels)
     push_idx = np.full(V, -1, dtype=np.int32)
-    if loss == LOSS_CE:
+    if loss == LOSS_NONE:
+        Ws = np.zeros((0, 0), dtype=np.float32)
+        bs = np.zeros(0, dtype=np.float32)
+        Y = np.zeros((0, H), dtype=np.float32)
+    elif loss == LOSS_CE:
         Ws = (sigma * rng.standard_normal((H, C))).astype(np.float32)
         bs = np.zeros(C, dtype=np.float32)
         lab_rows = np.nonzero(has_lab)[0]
