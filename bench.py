@@ -75,7 +75,8 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         "k_tn_gemm<LdDWx>": 2.0 * n_pull * D * gates_x * H,
         "k_tn_gemm<LdDUiou>": 2.0 * H * (3 if N == 2 else 4) * H * int(inner.sum()),
         "k_tn_gemm<LdDUf>": 2.0 * H * H * float(nc.sum()),
-        "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()),
+        # one launch per child slot: each carries its share of the links
+        "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()) / N,
     }
     if name.startswith(("k_dx_tile", "k_pull_tile")):
         return 2.0 * n_pull * D * gates_x * H, 0.0
