@@ -59,8 +59,10 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
     if name.startswith(("k_lstm_fwd_level", "k_lstm_bwd_level", "k_lstm_fwd_persist",
                         "k_lstm_bwd_persist", "k_lstm_fwd_tile", "k_lstm_bwd_tile")):
         return float(np.sum(2.0 * H * (3 * H + c * H))), 0.0
-    if name.startswith(("k_fc_fwd_level", "k_fc_bwd_level")):
+    if name.startswith(("k_fc_fwd_tile", "k_fc_bwd_tile", "k_fc_fwd_sk", "k_fc_bwd_sk")):
         return float(np.sum(2.0 * c * H * H)), 0.0
+    if name == "k_fc_leaf":            # reads x, writes h and h_out
+        return 0.0, rows * H * 4.0 * 3
     if name == "k_lstm_leaf":          # reads 3 columns of P, writes h, c, 5 gates, h_out, c_out
         return 0.0, rows * H * 4.0 * 12
     if name.startswith("k_lstm_bwd_gates"):  # reads dh, dc, 3 gates, c (+ f_k, c_k per child),

@@ -103,7 +103,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
     return r;
   };
   L.P = take(lstm ? V * 4 * H : 0);
-  L.UT = take(lstm ? 4 * H * H : 0);
+  L.UT = take(lstm ? 4 * H * H : (size_t)p->N * H * H);
   L.WxT = take(lstm ? 4 * H * (size_t)p->D : 0);
   L.zrow = take(H);
   L.Hs = take(V * H);
@@ -112,7 +112,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.dZ = take((tr || lm) ? V * (C > 0 ? C : 1) : 0);   // the LM head's logits in inference
   L.lossv = take(V);
   L.dHL = take(tr * V * H);
-  L.dHp = take(tr * V * H);
+  L.dHp = take(tr * (lstm ? V * H : 0));
   L.dCp = take(tr * (lstm ? V * H : 0));
   L.dA = take(tr * V * GW);
   L.part_floats = tr * lazy_part_floats(s->V, p->D, p->H, p->N, p->C);
@@ -520,6 +520,7 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
     if (!lstm_fwd_persist(n, s->level_offsets, lo, ts, s->T, bar, str))
       for (int t = ts; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
   } else {
+    if (s->T > 1) fc_transpose(n, str);
     fc_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
     for (int t = 1; t < s->T; ++t) fc_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
   }
@@ -628,11 +629,12 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       lm_head_grads(n, g->dWs, g->dbs, (float*)((char*)ws + L.gpart), L.gpart_floats, str);
     dx_gemm(n, s->n_pull, with_f, g->dX, str);
   } else {
-    for (int t = T - 1; t >= 0; --t) {
-      const int M = lo[t + 1] - lo[t];
-      fc_bwd_gates(n, lo[t], M, t == 0, g->dX, str);
-      if (t >= 1) fc_bwd_level(n, lo[t], M, str);
-    }
+    // roots first; every other vertex's delta (or a leaf's input gradient)
+    // comes from its parent's level product
+    n.dX = g->dX;
+    n.leaf_end = off1;
+    fc_bwd_roots(n, str);
+    for (int t = T - 1; t >= 1; --t) fc_bwd_level(n, lo[t], lo[t + 1] - lo[t], str);
     fc_dW(n, off1, g->dU, part, L.part_floats, str);
     SplitJobs jobs;
     bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);

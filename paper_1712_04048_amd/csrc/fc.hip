@@ -1,238 +1,473 @@
 // Tree-FC vertex function (Section 5, Tree-FC: a single fully-connected layer
 // as the cell): internal vertex h = tanh(h_0 W_0 + h_1 W_1 + b); a leaf's
 // state is its pulled input.  One batching task (level) per launch.
-#include "kernels.h"
+//
+// Level products.  Levels of at least kTileMinRows positions run LDS-ring
+// tiles (the staging scheme of the Tree-LSTM tiles, lds_ring.h): per 32-deep
+// chunk of the hidden index, a stage holds the tile's child rows of every
+// slot and the matching rows of each slot's weight block, so the K = N H
+// contraction runs as H / 32 chunks with one MFMA block per slot.  Smaller
+// levels run split-K kernels (16 x 16 outputs per workgroup, the contraction
+// split over its wavefronts).  In both the weight fragment is the MFMA's A
+// operand, so lane (r, gq) ends up holding four consecutive columns of one
+// position (float4 epilogue accesses).
+//
+// Backward: a vertex has one parent, so the parent's level product is its
+// whole dL/dh from above; the product's epilogue adds the child's loss term
+// and stores the child's delta (or a leaf's input gradient) directly.  Roots
+// get theirs from one elementwise kernel before the first level.
+#include "lds_ring.h"
+#include "lstm_dev.h"
 
 namespace cavs {
 namespace {
 
 __global__ void __launch_bounds__(256) k_fc_leaf(Net n, int off, int M) {
-  const int H = n.H;
+  const int H4 = n.H / 4;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)M * H) return;
-  const int p = off + (int)(idx / H), j = (int)(idx % H);
-  const float h = n.X[(size_t)n.pull_pos[p] * H + j];
-  n.Hs[(size_t)p * H + j] = h;
-  n.h_out[(size_t)n.order[p] * H + j] = h;
+  if (idx >= (long)M * H4) return;
+  const int p = off + (int)(idx / H4), j = 4 * (int)(idx % H4);
+  const float4 h = ldg4(n.X + (size_t)n.pull_pos[p] * n.H + j);
+  st4(n.Hs + (size_t)p * n.H + j, h);
+  st4(n.h_out + (size_t)n.order[p] * n.H + j, h);
 }
 
-// z = [h_0, h_1] W + b over a tile of BM positions x 64 units; K = 2H runs
-// through child slot 0's rows then slot 1's (gathered from the state buffer).
-template <int BM>
-__global__ void __launch_bounds__(256) k_fc_fwd_level(Net n, int off, int M) {
-  constexpr int BN = 64;
-  constexpr int WRW = BM == 64 ? 2 : 1, WCW = 4 / WRW;
-  constexpr int TM = BM / 16 / WRW, TN = BN / 16 / WCW;
-  constexpr int LDA = kBK + 4, LDB = BN + 2;
-  constexpr int A_N = BM * 8, A_PER = (A_N + 255) / 256;
-  constexpr int B_PER = kBK * (BN / 4) / 256;
-  __shared__ __attribute__((aligned(16))) float As[BM * LDA];
-  __shared__ float Bs[kBK * LDB];
-  const int H = n.H, N = n.N;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int wrow = (w / WCW) * TM * 16, wcol = (w % WCW) * TN * 16;
-  const int row0 = off + blockIdx.x * BM, rowend = off + M;
-  const int n0 = blockIdx.y * BN;
-
-  int arow[A_PER], aq[A_PER];
-  bool aval[A_PER];
-#pragma unroll
-  for (int a = 0; a < A_PER; ++a) {
-    const int idx = tid + 256 * a;
-    arow[a] = idx / 8;
-    aq[a] = idx % 8;
-    aval[a] = idx < A_N && row0 + arow[a] < rowend;
+// dL/dh of position p from above is g; with p's own loss term it gives
+// delta = dL/dh (1 - h^2), or, for a leaf (h = x), the gradient of its
+// input row.
+__device__ __forceinline__ void fc_finish_grad(const Net& n, int p, int col0, float4 g) {
+  const size_t e = (size_t)p * n.H + col0;
+  const float4 l = ldg4(n.dHL + e);
+  g.x += l.x; g.y += l.y; g.z += l.z; g.w += l.w;
+  if (p < n.leaf_end) {
+    st4(n.dX + (size_t)n.pull_pos[p] * n.H + col0, g);
+    return;
   }
-  // child rows of this thread's A row, looked up once (slots 0 and 1)
-  const float* crow[A_PER][2];
+  const float4 h = ldg4(n.Hs + e);
+  st4(n.dA + e, make_float4(g.x * (1.f - h.x * h.x), g.y * (1.f - h.y * h.y),
+                            g.z * (1.f - h.z * h.z), g.w * (1.f - h.w * h.w)));
+}
+
+// Roots (no parent, at any level): the gradient from the loss term alone,
+// four units per thread.
+__global__ void __launch_bounds__(256) k_fc_bwd_roots(Net n) {
+  const int H4 = n.H / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)n.V * H4) return;
+  const int p = (int)(idx / H4);
+  if (n.parent_pos[p] >= 0) return;
+  fc_finish_grad(n, p, 4 * (int)(idx % H4), make_float4(0.f, 0.f, 0.f, 0.f));
+}
+
+// WT[k][n][j] = U[k H + j][n]: each slot's [H, H] block of the Tree-FC
+// weight transposed, so that the forward's weight rows are contiguous in the
+// contraction index.  Block (0, 0) also clears the zero row read for absent
+// children and for rows past a level.
+__global__ void __launch_bounds__(256) k_fc_transpose(const float* __restrict__ U,
+                                                      float* __restrict__ WT,
+                                                      float* __restrict__ zrow, int H) {
+  __shared__ float t[32][33];
+  const int n0 = blockIdx.x * 32, r0 = blockIdx.y * 32;   // r0: row of U in [0, N H)
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int j = threadIdx.x; j < H; j += 256) zrow[j] = 0.f;
+  for (int y = ty; y < 32; y += 8) t[y][tx] = U[(size_t)(r0 + y) * H + n0 + tx];
+  __syncthreads();
+  const int k = r0 / H, j0 = r0 % H;   // 32 | H: a block stays inside one slot
+  for (int y = ty; y < 32; y += 8) WT[((size_t)k * H + n0 + y) * H + j0 + tx] = t[tx][y];
+}
+
+// Forward tile: BM positions x BN units; per chunk the stage holds, for each
+// slot k, the BM child rows h_k (a zero row where a child is absent or past
+// the level) and the BN rows of W_k^T; z = sum_k h_k W_k, then tanh(z + b).
+template <int NCH, int BM, int BN, int S>
+__global__ void __launch_bounds__(256) k_fc_fwd_tile(Net n, int off, int M) {
+  constexpr int TM = BM / 32, TN = BN / 32;    // 16 x 16 blocks per wavefront
+  constexpr int AROWS = NCH * BM, ROWS = AROWS + NCH * BN;
+  constexpr int IPW = ROWS / 32;               // copies per wavefront per chunk
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+
+  const int H = n.H;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  const int wr = w & 1, wn = w >> 1;
+  int rt, ut;
+  xcd_tile(H / BN, rt, ut);
+  const int row0 = off + rt * BM, rowend = off + M, n0 = ut * BN;
+
+  // epilogue operands, fetched before the product
+  int vout[TM];
 #pragma unroll
-  for (int a = 0; a < A_PER; ++a)
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+    vout[tm] = p < rowend ? n.order[p] : -1;
+  }
+  float4 bias[TN];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      crow[a][k] = nullptr;
-      if (aval[a] && k < N) {
-        const int cp = n.child_pos[(size_t)(row0 + arow[a]) * N + k];
-        if (cp >= 0) crow[a][k] = n.Hs + (size_t)cp * H + 4 * aq[a];
+  for (int tn = 0; tn < TN; ++tn) bias[tn] = ldg4(n.b + n0 + wn * (BN / 2) + tn * 16 + 4 * gq);
+
+  // LDS rows [0, AROWS): child rows, slot k of position row0 + rr at k BM + rr;
+  // then NCH blocks of BN rows of W_k^T
+  const float* src[IPW];
+#pragma unroll
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const float* ptr;
+    if (row < AROWS) {
+      const int k = row / BM, p = row0 + row % BM;
+      ptr = n.zrow;
+      if (p < rowend) {
+        const int cp = n.child_pos[(size_t)p * NCH + k];
+        if (cp >= 0) ptr = n.Hs + (size_t)cp * H;
       }
+    } else {
+      const int b = row - AROWS, k = b / BN, u = n0 + b % BN;
+      ptr = n.UT + ((size_t)k * H + u) * H;
     }
-  float4 ra[A_PER], rb[B_PER];
-  auto gload = [&](int kc) {
-    const int k0 = kc * kBK, slot = k0 / H, r0 = k0 % H;
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a) {
-      const float* src = slot == 0 ? crow[a][0] : crow[a][1];
-      ra[a] = src ? ldg4(src + r0) : f4zero();
-    }
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) {
-      const int idx = tid + 256 * b, kk = idx / (BN / 4), q = idx % (BN / 4);
-      rb[b] = ldg4(n.U + (size_t)(k0 + kk) * H + n0 + 4 * q);
-    }
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a)
-      if (tid + 256 * a < A_N) st4(&As[arow[a] * LDA + 4 * aq[a]], ra[a]);
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) {
-      const int idx = tid + 256 * b, kk = idx / (BN / 4), q = idx % (BN / 4);
-      st4_scalar(&Bs[kk * LDB + 4 * q], rb[b]);
-    }
-  };
+    src[t] = ptr + 4 * qg;
+  }
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
+
   v4f acc[TM][TN];
-  zero_acc(acc);
-  const int nk = N * H / kBK;
-  gload(0);
-  for (int kc = 0; kc < nk; ++kc) {
-    __syncthreads();
-    sstore();
-    __syncthreads();
-    if (kc + 1 < nk) gload(kc + 1);
-    mfma_chunk<TM, TN, true, false, LDA, LDB>(As, Bs, wrow, wcol, acc);
-  }
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int p = row0 + wrow + tm * 16 + 4 * gq + i;
-      if (p >= rowend) continue;
-      const int v = n.order[p];
+    for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int col = n0 + wcol + tn * 16 + r;
-        const float h = tanh_(acc[tm][tn][i] + n.b[col]);
-        n.Hs[(size_t)p * H + col] = h;
-        n.h_out[(size_t)v * H + col] = h;
-      }
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+  };
+  struct Frag {
+    float a[NCH][TM][8], b[NCH][TN][8];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        frag_sw(Ls, AROWS + k * BN + wn * (BN / 2) + tn * 16 + r, gq, f.b[k][tn]);
+#pragma unroll
+    for (int k = 0; k < NCH; ++k)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, k * BM + wr * (BM / 2) + tm * 16 + r, gq, f.a[k][tm]);
+  };
+  // A = weight fragment (units), B = child fragment (positions)
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int k = 0; k < NCH; ++k) acc[tm][tn] = mfma_chunk8<false>(f.b[k][tn], f.a[k][tm], acc[tm][tn]);
+  };
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+    mma(cur);
+    interleave_reads<2 * NCH * (TN + TM), TM * TN * NCH * 8>();
+  };
+  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+    if (p >= rowend) continue;
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col0 = n0 + wn * (BN / 2) + tn * 16 + 4 * gq;
+      const float4 h = make_float4(tanh_(acc[tm][tn][0] + bias[tn].x), tanh_(acc[tm][tn][1] + bias[tn].y),
+                                   tanh_(acc[tm][tn][2] + bias[tn].z), tanh_(acc[tm][tn][3] + bias[tn].w));
+      st4(n.Hs + (size_t)p * H + col0, h);
+      st4(n.h_out + (size_t)vout[tm] * H + col0, h);
     }
+  }
 }
 
-// delta = dL/dh * (1 - h^2) for internal vertices; a leaf passes dL/dh to
-// its input row (h = x).
-__global__ void __launch_bounds__(256) k_fc_bwd_gates(Net n, int off, int M, int leaf,
-                                                      float* dX) {
+// Backward tile: dL/dh_k = delta W_k^T over BM positions x BN columns j of
+// every slot; per chunk of the unit index the stage holds the BM delta rows
+// (rows past the level repeat its last row; their products are never
+// stored) and, for each slot k, rows k H + j of U (contiguous in the unit
+// index).  Each slot's result finishes its child's gradient (trees: one
+// writer per row).
+template <int NCH, int BM, int BN, int S>
+__global__ void __launch_bounds__(256) k_fc_bwd_tile(Net n, int off, int M) {
+  constexpr int TM = BM / 32, TN = BN / 32;
+  constexpr int ROWS = BM + NCH * BN;
+  constexpr int IPW = ROWS / 32;
+  static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+
   const int H = n.H;
-  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long)M * H) return;
-  const int p = off + (int)(idx / H), j = (int)(idx % H);
-  const int par = n.parent_pos[p];
-  float gh = par >= 0 ? n.dHp[(size_t)p * H + j] : 0.f;
-  const float h = n.Hs[(size_t)p * H + j];
-  gh += n.dHL[(size_t)p * H + j];
-  if (leaf) dX[(size_t)n.pull_pos[p] * H + j] = gh;
-  else n.dA[(size_t)p * H + j] = gh * (1.f - h * h);
-}
-
-// dL/dh_k = delta W_k^T for both child slots; tile BM positions x 64 units.
-template <int BM>
-__global__ void __launch_bounds__(256) k_fc_bwd_level(Net n, int off, int M) {
-  constexpr int BN = 64;
-  constexpr int WRW = BM == 64 ? 2 : 1, WCW = 4 / WRW;
-  constexpr int TM = BM / 16 / WRW, TN = BN / 16 / WCW;
-  constexpr int LDA = kBK + 4, LDB = kBK + 4;
-  constexpr int A_N = BM * 8, A_PER = (A_N + 255) / 256;
-  constexpr int B_PER = BN * 8 / 256;
-  __shared__ __attribute__((aligned(16))) float As[BM * LDA];
-  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDB];
-  const int H = n.H, N = n.N;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int wrow = (w / WCW) * TM * 16, wcol = (w % WCW) * TN * 16;
-  const int row0 = off + blockIdx.x * BM, rowend = off + M;
-  const int n0 = blockIdx.y * BN;
-  int arow[A_PER], aq[A_PER];
-  bool aval[A_PER];
+  const int wr = w & 1, wn = w >> 1;
+  int rt, ut;
+  xcd_tile(H / BN, rt, ut);
+  const int row0 = off + rt * BM, rowend = off + M, n0 = ut * BN;
+
+  int cpos[TM][NCH];
 #pragma unroll
-  for (int a = 0; a < A_PER; ++a) {
-    const int idx = tid + 256 * a;
-    arow[a] = idx / 8;
-    aq[a] = idx % 8;
-    aval[a] = idx < A_N && row0 + arow[a] < rowend;
+  for (int tm = 0; tm < TM; ++tm) {
+    const int p = row0 + wr * (BM / 2) + tm * 16 + r;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) cpos[tm][k] = p < rowend ? n.child_pos[(size_t)p * NCH + k] : -1;
   }
-  float4 ra[A_PER], rb[2][B_PER];
-  auto gload = [&](int k0) {
+
+  const float* src[IPW];
 #pragma unroll
-    for (int a = 0; a < A_PER; ++a)
-      ra[a] = aval[a] ? ldg4(n.dA + (size_t)(row0 + arow[a]) * H + k0 + 4 * aq[a]) : f4zero();
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) {
-      const int idx = tid + 256 * b, nr = idx / 8, q = idx % 8;
-#pragma unroll
-      for (int k = 0; k < 2; ++k)
-        rb[k][b] = k < N ? ldg4(n.U + (size_t)(k * H + n0 + nr) * H + k0 + 4 * q) : f4zero();
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const float* ptr;
+    if (row < BM) {
+      ptr = n.dA + (size_t)min(row0 + row, rowend - 1) * H;
+    } else {
+      const int b = row - BM, k = b / BN, j = n0 + b % BN;
+      ptr = n.U + ((size_t)k * H + j) * H;
     }
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int a = 0; a < A_PER; ++a)
-      if (tid + 256 * a < A_N) st4(&As[arow[a] * LDA + 4 * aq[a]], ra[a]);
-#pragma unroll
-    for (int b = 0; b < B_PER; ++b) {
-      const int idx = tid + 256 * b, nr = idx / 8, q = idx % 8;
-      st4(&Bs[0][nr * LDB + 4 * q], rb[0][b]);
-      st4(&Bs[1][nr * LDB + 4 * q], rb[1][b]);
-    }
-  };
-  v4f acc0[TM][TN], acc1[TM][TN];
-  zero_acc(acc0);
-  zero_acc(acc1);
-  const int nk = H / kBK;
-  gload(0);
-  for (int kc = 0; kc < nk; ++kc) {
-    __syncthreads();
-    sstore();
-    __syncthreads();
-    if (kc + 1 < nk) gload((kc + 1) * kBK);
-    mfma_chunk<TM, TN, true, true, LDA, LDB>(As, Bs[0], wrow, wcol, acc0);
-    mfma_chunk<TM, TN, true, true, LDA, LDB>(As, Bs[1], wrow, wcol, acc1);
+    src[t] = ptr + 4 * qg;
   }
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
+
+  v4f acc[TM][TN][NCH];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int p = row0 + wrow + tm * 16 + 4 * gq + i;
-      if (p >= rowend) continue;
-      const int cp0 = n.child_pos[(size_t)p * N];
-      const int cp1 = N == 2 ? n.child_pos[(size_t)p * N + 1] : -1;
+    for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int col = n0 + wcol + tn * 16 + r;
-        if (cp0 >= 0) n.dHp[(size_t)cp0 * H + col] = acc0[tm][tn][i];
-        if (cp1 >= 0) n.dHp[(size_t)cp1 * H + col] = acc1[tm][tn][i];
+      for (int k = 0; k < NCH; ++k) acc[tm][tn][k] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+  };
+  struct Frag {
+    float a[TM][8], b[NCH][TN][8];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        frag_sw(Ls, BM + k * BN + wn * (BN / 2) + tn * 16 + r, gq, f.b[k][tn]);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, wr * (BM / 2) + tm * 16 + r, gq, f.a[tm]);
+  };
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int k = 0; k < NCH; ++k)
+          acc[tm][tn][k] = mfma_chunk8<false>(f.b[k][tn], f.a[tm], acc[tm][tn][k]);
+  };
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+    mma(cur);
+    interleave_reads<2 * (NCH * TN + TM), TM * TN * NCH * 8>();
+  };
+  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col0 = n0 + wn * (BN / 2) + tn * 16 + 4 * gq;
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) {
+        const int cp = cpos[tm][k];
+        if (cp >= 0)
+          fc_finish_grad(n, cp, col0,
+                         make_float4(acc[tm][tn][k][0], acc[tm][tn][k][1], acc[tm][tn][k][2], acc[tm][tn][k][3]));
       }
     }
+}
+
+// Split-K kernels for levels below the tile threshold: a workgroup owns 16
+// positions x 16 units (forward) or 16 positions x 16 columns of every slot
+// (backward); wavefront w multiplies the w-th share of the 32-deep chunks of
+// the contraction with fragments loaded straight from global memory (the
+// weight rows k-contiguous: W^T for the forward, U for the backward), and
+// wavefront 0 sums the KW partial blocks in a fixed order (deterministic)
+// and finishes.
+template <int NCH, int KW>
+__global__ void __launch_bounds__(64 * KW) k_fc_fwd_sk(Net n, int off, int M) {
+  __shared__ float4 red[KW][64];
+  const int H = n.H;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  int rt, ut;
+  xcd_tile(H / 16, rt, ut);
+  const int row0 = off + rt * 16, rowend = off + M, u0 = ut * 16;
+  const int p = row0 + r;
+  const float* ap[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int cp = p < rowend ? n.child_pos[(size_t)p * NCH + k] : -1;
+    ap[k] = cp >= 0 ? n.Hs + (size_t)cp * H : n.zrow;
+  }
+  const float* bp = n.UT + (size_t)(u0 + r) * H;
+  const int nch = NCH * H / kBK, c0 = w * nch / KW, c1 = (w + 1) * nch / KW;
+  struct Frag {
+    float a[8], b[8];
+  };
+  auto load = [&](int c, Frag& f) {
+    const int k = c * kBK, slot = k / H, kk = k - slot * H + 8 * gq;
+    ld8((slot == 0 ? ap[0] : ap[NCH - 1]) + kk, f.a);
+    ld8(bp + (size_t)slot * H * H + kk, f.b);
+  };
+  v4f acc{0.f, 0.f, 0.f, 0.f};
+  Frag fa, fb;
+  if (c0 < c1) load(c0, fa);
+  for (int c = c0; c < c1; c += 2) {
+    if (c + 1 < c1) load(c + 1, fb);
+    __builtin_amdgcn_sched_barrier(0);
+    acc = mfma_chunk8<false>(fa.b, fa.a, acc);
+    if (c + 1 >= c1) break;
+    if (c + 2 < c1) load(c + 2, fa);
+    acc = mfma_chunk8<false>(fb.b, fb.a, acc);
+  }
+  red[w][lane] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  __syncthreads();
+  if (w != 0 || p >= rowend) return;
+  float4 z = red[0][lane];
+#pragma unroll
+  for (int q = 1; q < KW; ++q) {
+    const float4 t = red[q][lane];
+    z.x += t.x; z.y += t.y; z.z += t.z; z.w += t.w;
+  }
+  const int col0 = u0 + 4 * gq;
+  const float4 bias = ldg4(n.b + col0);
+  const float4 h = make_float4(tanh_(z.x + bias.x), tanh_(z.y + bias.y), tanh_(z.z + bias.z),
+                               tanh_(z.w + bias.w));
+  st4(n.Hs + (size_t)p * H + col0, h);
+  st4(n.h_out + (size_t)n.order[p] * H + col0, h);
+}
+
+template <int NCH, int KW>
+__global__ void __launch_bounds__(64 * KW) k_fc_bwd_sk(Net n, int off, int M) {
+  __shared__ float4 red[KW][NCH][64];
+  const int H = n.H;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
+  int rt, ut;
+  xcd_tile(H / 16, rt, ut);
+  const int row0 = off + rt * 16, rowend = off + M, j0 = ut * 16;
+  const int p = row0 + r;
+  // rows past the level read its last delta row (never stored)
+  const float* ap = n.dA + (size_t)min(p, rowend - 1) * H;
+  const float* bp[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) bp[k] = n.U + ((size_t)k * H + j0 + r) * H;
+  const int nch = H / kBK, c0 = w * nch / KW, c1 = (w + 1) * nch / KW;
+  struct Frag {
+    float a[8], b[NCH][8];
+  };
+  auto load = [&](int c, Frag& f) {
+    const int kk = c * kBK + 8 * gq;
+    ld8(ap + kk, f.a);
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) ld8(bp[k] + kk, f.b[k]);
+  };
+  v4f acc[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) acc[k] = v4f{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) acc[k] = mfma_chunk8<false>(f.b[k], f.a, acc[k]);
+  };
+  Frag fa, fb;
+  if (c0 < c1) load(c0, fa);
+  for (int c = c0; c < c1; c += 2) {
+    if (c + 1 < c1) load(c + 1, fb);
+    __builtin_amdgcn_sched_barrier(0);
+    mma(fa);
+    if (c + 1 >= c1) break;
+    if (c + 2 < c1) load(c + 2, fa);
+    mma(fb);
+  }
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) red[w][k][lane] = make_float4(acc[k][0], acc[k][1], acc[k][2], acc[k][3]);
+  __syncthreads();
+  if (w != 0 || p >= rowend) return;
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int cp = n.child_pos[(size_t)p * NCH + k];
+    if (cp < 0) continue;
+    float4 z = red[0][k][lane];
+#pragma unroll
+    for (int q = 1; q < KW; ++q) {
+      const float4 t = red[q][k][lane];
+      z.x += t.x; z.y += t.y; z.z += t.z; z.w += t.w;
+    }
+    fc_finish_grad(n, cp, j0 + 4 * gq, z);
+  }
 }
 
 }  // namespace
 
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  CAVS_LAUNCH_ROWS("k_fc_leaf", off, M, k_fc_leaf, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M);
+  CAVS_LAUNCH_ROWS("k_fc_leaf", off, M, k_fc_leaf, dim3(cdiv((long)M * (n.H / 4), 256)), dim3(256), 0, s,
+                   n, off, M);
 }
+
+void fc_transpose(const Net& n, hipStream_t s) {
+  CAVS_LAUNCH("k_fc_transpose", k_fc_transpose, dim3(n.H / 32, n.N * n.H / 32), dim3(256), 0, s, n.U,
+              n.UT, n.zrow, n.H);
+}
+
+#define CAVS_FC_TILE(KIND, NCH, BM, BN, S)                                                  \
+  CAVS_LAUNCH_ROWS("k_fc_" #KIND "_tile<" #NCH ", " #BM ", " #BN ", " #S ">", off, M,        \
+                   (k_fc_##KIND##_tile<NCH, BM, BN, S>), dim3(cdiv(M, BM) * (n.H / BN)),     \
+                   dim3(256), 0, s, n, off, M)
+
+#define CAVS_FC_SK(KIND, NCH, KW)                                                           \
+  CAVS_LAUNCH_ROWS("k_fc_" #KIND "_sk<" #NCH ", " #KW ">", off, M, (k_fc_##KIND##_sk<NCH, KW>), \
+                   dim3(cdiv(M, 16) * (n.H / 16)), dim3(64 * KW), 0, s, n, off, M)
+
+// Variant by level size, measured on MI355X (H = 512): split-K below
+// kTileMinRows positions, 32 x 32 tiles up to 4096, 64 x 64 tiles above.
+// 0: split-K, 1: 32 x 32 tile, 2: 64 x 64 tile
+static int fc_variant(int M) {
+  return M > 4096 ? 2 : M >= kTileMinRows ? 1 : 0;
+}
+
+#define CAVS_FC_LEVEL(KIND)                                                                 \
+  do {                                                                                      \
+    const int var = fc_variant(M);                                                          \
+    if (n.N == 2) {                                                                         \
+      if (var == 2) CAVS_FC_TILE(KIND, 2, 64, 64, 2);                                       \
+      else if (var == 1) CAVS_FC_TILE(KIND, 2, 32, 32, 2);                                  \
+      else CAVS_FC_SK(KIND, 2, 8);                                                          \
+    } else {                                                                                \
+      if (var == 2) CAVS_FC_TILE(KIND, 1, 64, 64, 2);                                       \
+      else if (var == 1) CAVS_FC_TILE(KIND, 1, 32, 32, 2);                                  \
+      else CAVS_FC_SK(KIND, 1, 8);                                                          \
+    }                                                                                       \
+  } while (0)
 
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  if (M <= 32)
-    CAVS_LAUNCH_ROWS("k_fc_fwd_level<16>", off, M, (k_fc_fwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
-                       M);
-  else
-    CAVS_LAUNCH_ROWS("k_fc_fwd_level<64>", off, M, (k_fc_fwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
-                       M);
+  CAVS_FC_LEVEL(fwd);
 }
 
-void fc_bwd_gates(const Net& n, int off, int M, int leaf, float* dX, hipStream_t s) {
-  if (M <= 0) return;
-  CAVS_LAUNCH_ROWS("k_fc_bwd_gates", off, M, k_fc_bwd_gates, dim3(cdiv((long)M * n.H, 256)), dim3(256), 0, s, n, off, M,
-                     leaf, dX);
+void fc_bwd_roots(const Net& n, hipStream_t s) {
+  if (n.V <= 0) return;
+  CAVS_LAUNCH("k_fc_bwd_roots", k_fc_bwd_roots, dim3(cdiv((long)n.V * (n.H / 4), 256)), dim3(256), 0,
+              s, n);
 }
 
 void fc_bwd_level(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  if (M <= 32)
-    CAVS_LAUNCH_ROWS("k_fc_bwd_level<16>", off, M, (k_fc_bwd_level<16>), dim3(cdiv(M, 16), n.H / 64), dim3(256), 0, s, n, off,
-                       M);
-  else
-    CAVS_LAUNCH_ROWS("k_fc_bwd_level<64>", off, M, (k_fc_bwd_level<64>), dim3(cdiv(M, 64), n.H / 64), dim3(256), 0, s, n, off,
-                       M);
+  CAVS_FC_LEVEL(bwd);
 }
 
 }  // namespace cavs

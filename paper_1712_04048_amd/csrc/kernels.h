@@ -30,7 +30,8 @@ struct Net {
   // parameters and inputs
   const float* Wx;              // [D, 4H]
   const float* U;               // LSTM [H, 4H]; FC [N*H, H]
-  float* UT;                    // LSTM: U transposed, [4H, H] (workspace)
+  float* UT;                    // LSTM: U transposed, [4H, H]; FC: each slot's block
+                                // transposed, [N, H, H] (workspace)
   float* WxT;                   // LSTM: W_x transposed, [4H, D] (workspace)
   float* zrow;                  // H zeros (workspace): the row an absent operand row reads;
                                 // cleared by the transpose kernel and by the loss kernel
@@ -48,10 +49,12 @@ struct Net {
   float* dZ;                    // [V, CP] d loss / d logits (columns >= C are zero)
   float* dHL;                   // [V, H]  the loss head's share of dL/dh (zero if unlabelled)
   float* lossv;                 // [V]     per-vertex loss terms
-  float* dHp;                   // [V, H]  dL/dh contributed by the parent
+  float* dHp;                   // [V, H]  dL/dh contributed by the parent (LSTM)
   float* dCp;                   // [V, H]  dL/dc contributed by the parent
   float* dA;                    // [V, GW] pre-activation gradients, same layout as Gs
   // outputs in vertex-id order
+  float* dX;                    // [n_x, D] input gradient (FC backward)
+  int leaf_end;                 // FC backward: positions below this are leaves (level 0)
   float* h_out;
   float* c_out;
 };
@@ -131,8 +134,13 @@ void lm_head_grads(const Net& n, float* dWs, float* dbs, float* part, size_t par
 // fc.hip
 void fc_fwd_leaf(const Net& n, int off, int M, hipStream_t s);
 void fc_fwd_level(const Net& n, int off, int M, hipStream_t s);
-void fc_bwd_gates(const Net& n, int off, int M, int leaf, float* dX, hipStream_t s);
+// backward: fc_bwd_roots, then fc_bwd_level for t = T-1 .. 1 (needs n.dX,
+// n.leaf_end)
+void fc_bwd_roots(const Net& n, hipStream_t s);
 void fc_bwd_level(const Net& n, int off, int M, hipStream_t s);
+// fc_fwd_level reads n.UT and n.zrow, written by fc_transpose earlier in the
+// same pass
+void fc_transpose(const Net& n, hipStream_t s);
 // lazy.hip
 // Pull projection; in fp32 the cell of every pulled leaf (position < lo1) is
 // finished in the same kernel, so lstm_fwd_leaf only handles leaves without

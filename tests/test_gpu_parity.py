@@ -274,6 +274,29 @@ def test_parity_treefc_cross_entropy(ctx):
     _parity(ctx, wl)
 
 
+@pytest.mark.parametrize("case", ["forest_n2_h128", "chains_n1_h192", "unary_slots_h64"])
+def test_parity_treefc_tiles(ctx, case):
+    """Tree-FC levels of >= 300 positions (the LDS-ring tiles) with a ragged
+    last row tile: binary forests, one-slot chains at H = 192 (three unit
+    tiles), and vertices with only slot 0 or only slot 1 filled."""
+    rng = np.random.Generator(np.random.PCG64(21))
+    if case == "forest_n2_h128":
+        trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 13, size=450)]
+        kw = dict(N=2, H=128)
+    elif case == "chains_n1_h192":
+        trees = [W.chain(int(n)) for n in rng.integers(2, 11, size=400)]
+        kw = dict(N=1, H=192)
+    else:
+        trees = [[[-1, -1], [0, -1], [-1, -1], [1, 2]]] * 331 + [[[-1, -1], [-1, 0]]] * 70
+        kw = dict(N=2, H=64)
+    wl = W.make_workload("fc_" + case, trees, cell=W.CELL_TREE_FC, loss=W.LOSS_L2, D=kw["H"],
+                         C=0, sigma=0.1, rng=rng, inputs="leaves", labels="all", **kw)
+    wl.b[:] = (0.1 * rng.standard_normal(wl.b.shape)).astype(np.float32)
+    sizes = np.diff(oracle.schedule(wl.child, wl.parent)["level_offsets"])
+    assert sizes[1] >= 300 and sizes[1] % 64 != 0
+    _parity(ctx, wl, label=case)
+
+
 EDGE = {
     "single_vertex_trees": lambda rng: ([[[-1, -1]]] * 37, dict()),
     "chain_len1_and_mixed": lambda rng: ([W.chain(1), W.chain(3), W.chain(1), W.chain(70)],
