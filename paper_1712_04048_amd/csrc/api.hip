@@ -618,11 +618,14 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     // one reduction launch
     const bool with_f = s->n_inner_input > 0;
     SplitJobs jobs;
-    if (!eager) {
+    if (eager) {
+      if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
+    } else if (!lstm_lazy_grouped(n, off1, s->n_pull, with_f, g->dU, g->dWx, part, pf, str,
+                                  &jobs)) {
       lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
       lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
+      if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     }
-    if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);
     if (lm_head(p))
@@ -635,8 +638,8 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     n.leaf_end = off1;
     fc_bwd_roots(n, str);
     for (int t = T - 1; t >= 1; --t) fc_bwd_level(n, lo[t], lo[t + 1] - lo[t], str);
-    fc_dW(n, off1, g->dU, part, L.part_floats, str);
     SplitJobs jobs;
+    fc_dW(n, off1, g->dU, part, L.part_floats, str, &jobs);
     bias_head_grads(n, off1, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
     reduce_split_jobs(jobs, str);
     if (lm_head(p))

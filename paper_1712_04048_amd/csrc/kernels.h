@@ -182,7 +182,16 @@ void lstm_dU_f(const Net& n, int off1, float* dU, float* part, size_t part_float
                SplitJobs* jobs = nullptr, int rows = -1);
 void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
               size_t part_floats, hipStream_t s, SplitJobs* jobs = nullptr);
-void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s);
+// the lazy weight-gradient products of the fused Tree-LSTM path: dU_iou,
+// then dU_f and dW_x in one grouped launch, reductions queued on jobs;
+// false (and nothing launched or queued) where the grouped kernel does not
+// apply (one child slot, no inputs, bf16)
+bool lstm_lazy_grouped(const Net& n, int off1, int n_pull, bool with_f, float* dU, float* dWx,
+                       float* part, size_t pf, hipStream_t s, SplitJobs* jobs);
+// part holds 3 part_floats (the slots' partials side by side); reductions
+// are queued on jobs
+void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s,
+           SplitJobs* jobs);
 // column sums over positions [row0, row1) of the gate gradients -> db
 // db over rows [row0, row1) and, for the CE head, dW_s and db_s over all rows;
 // rows below lo1 are level 0 (no children).  The per-chunk partial sums go

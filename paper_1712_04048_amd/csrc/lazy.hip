@@ -5,6 +5,9 @@
 //   - push:   the loss head over every labelled vertex (z = h W_s + b_s);
 //   - dF:     dW_x, dU, db, dX, dW_s, db_s as long-K products over all
 //             vertices, with deterministic split-K (fixed-order reduction).
+#include <algorithm>
+#include <vector>
+
 #include "lds_ring.h"
 #include "lstm_dev.h"
 
@@ -897,25 +900,36 @@ __global__ void k_reduce_splits(const float* __restrict__ part, int S, int Mo, i
 // into LDS first, so issuing a chunk's copies waits on nothing but LDS.
 constexpr int kTnSeg = 1024;
 
+// LDS of one tile shape: S stages of 32 k x ROWS floats, then the segment's
+// row offsets (NA A rows and one B row per k).
 template <class L, int BM, int BN, int S>
-__global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, int No,
-                                               float* out) {
+struct TnShape {
+  static constexpr int ROWS = L::NA * BM + BN;
+  static constexpr int FLOATS = S * ROWS * 32;
+  static constexpr int INTS = (L::NA + 1) * kTnSeg;
+};
+
+// Output tile (bx, by) of split s; lds holds TnShape::FLOATS floats
+// (1 KB-aligned), offs TnShape::INTS ints.
+template <class L, int BM, int BN, int S>
+__device__ __forceinline__ void tn_dl_tile(const L& ld, int Q, int qchunk, int Mo, int No,
+                                           float* out, int bx, int by, int s, float* lds,
+                                           int* offs) {
   constexpr int NA = L::NA, WM = BM / 64, WN = 8 / WM, WTN = BN / WN, TN = WTN / 16;
   constexpr int ROWS = NA * BM + BN;                 // a stage is 32 k x ROWS floats
   constexpr int IA = BM * 32 / 256 / 8, IB = BN * 32 / 256 / 8;
   constexpr int IPW = NA * IA + IB;                  // copies per wavefront per chunk
   constexpr int APC = 256 / BM, BPC = 256 / BN;      // operand rows per copy
   static_assert((TN == 2 || TN == 4) && IA >= 1 && IB >= 1 && S >= 2 && S <= 4, "tile shape");
-  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
-  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
-  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
-  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
-  __shared__ int oa0[kTnSeg], oa1[NA == 2 ? kTnSeg : 1], ob[kTnSeg];
-  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+  const Ring<ROWS, S> ring{lds, lds + ROWS * 32, lds + (S > 2 ? 2 : 0) * ROWS * 32,
+                           lds + (S > 3 ? 3 : 0) * ROWS * 32};
+  int* oa0 = offs;
+  int* oa1 = offs + kTnSeg;
+  int* ob = offs + NA * kTnSeg;
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, r = lane & 15;
   const int wr = w / WN, wc = w % WN, ws = __builtin_amdgcn_readfirstlane(w);
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int n0 = bx * BN, m0 = by * BM;
   const int q_lo = s * qchunk, q_hi = min(Q, q_lo + qchunk);
   const float* A = ld.abase();
   const float* B = ld.bbase() + ld.bcol(n0);
@@ -1014,6 +1028,63 @@ __global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, 
     }
 }
 
+template <class L, int BM, int BN, int S>
+__global__ void __launch_bounds__(512) k_tn_dl(L ld, int Q, int qchunk, int Mo, int No,
+                                               float* out) {
+  using T = TnShape<L, BM, BN, S>;
+  __shared__ __attribute__((aligned(1024))) float lds[T::FLOATS];
+  __shared__ int offs[T::INTS];
+  tn_dl_tile<L, BM, BN, S>(ld, Q, qchunk, Mo, No, out, blockIdx.x, blockIdx.y, blockIdx.z, lds,
+                           offs);
+}
+
+// Up to three lazy products in one launch (the lazy batching of Section
+// 3.5 taken one step further: the parameter-gradient products of a pass are
+// independent, so they share one grid).  Workgroups [0, j[0].wg_end) run
+// product A, then B, then C; inside a product, workgroup i is output tile
+// (i % tx, i / tx % ty) of split i / (tx ty).  The split counts are chosen
+// on the host so that every workgroup carries about the same MFMA work.
+struct TnJob {
+  int Q, qchunk, Mo, No, tx, ty, wg_end;
+  float* out;
+};
+
+template <class LA, class LB, class LC>
+struct TnGroupArgs {
+  LA a;
+  LB b;
+  LC c;
+  TnJob j[3];
+};
+
+constexpr int cmax3(int a, int b, int c) { return a > b ? (a > c ? a : c) : (b > c ? b : c); }
+
+template <class LA, int BMA, int BNA, int SA, class LB, int BMB, int BNB, int SB, class LC,
+          int BMC, int BNC, int SC>
+__global__ void __launch_bounds__(512) k_tn_group(TnGroupArgs<LA, LB, LC> g) {
+  using TA = TnShape<LA, BMA, BNA, SA>;
+  using TB = TnShape<LB, BMB, BNB, SB>;
+  using TC = TnShape<LC, BMC, BNC, SC>;
+  __shared__ __attribute__((aligned(1024))) float lds[cmax3(TA::FLOATS, TB::FLOATS, TC::FLOATS)];
+  __shared__ int offs[cmax3(TA::INTS, TB::INTS, TC::INTS)];
+  const int b = blockIdx.x;
+  if (b < g.j[0].wg_end) {
+    const TnJob& J = g.j[0];
+    tn_dl_tile<LA, BMA, BNA, SA>(g.a, J.Q, J.qchunk, J.Mo, J.No, J.out, b % J.tx, b / J.tx % J.ty,
+                                 b / (J.tx * J.ty), lds, offs);
+  } else if (b < g.j[1].wg_end) {
+    const TnJob& J = g.j[1];
+    const int i = b - g.j[0].wg_end;
+    tn_dl_tile<LB, BMB, BNB, SB>(g.b, J.Q, J.qchunk, J.Mo, J.No, J.out, i % J.tx, i / J.tx % J.ty,
+                                 i / (J.tx * J.ty), lds, offs);
+  } else {
+    const TnJob& J = g.j[2];
+    const int i = b - g.j[1].wg_end;
+    tn_dl_tile<LC, BMC, BNC, SC>(g.c, J.Q, J.qchunk, J.Mo, J.No, J.out, i % J.tx, i / J.tx % J.ty,
+                                 i / (J.tx * J.ty), lds, offs);
+  }
+}
+
 // All pending split-K sums in one launch: blockIdx.y picks the job.  Kind 0:
 // each thread adds four adjacent outputs with float4 access (every such
 // job's No, ldd, col_off, gap_start and gap are multiples of 4, checked on
@@ -1072,6 +1143,13 @@ void split_sum(const float* part, int S, int Mo, int No, float* dst, int ldd, in
               part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
 }
 
+// The direct-to-LDS kernel applies: fp32, 256-column tiles that stay inside
+// one gate block, row offsets that fit an int.
+bool tn_direct_ok(const Net& n, bool direct, int Mo, int No) {
+  const long big = (long)n.V * (n.GW > n.H ? n.GW : n.H) + (long)n.V * n.D;
+  return !n.bf && direct && n.H % 256 == 0 && No % 256 == 0 && Mo % 4 == 0 && big < (1L << 31);
+}
+
 template <class L>
 void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col_off,
                 int gap_start, int gap, float* part, size_t part_floats, hipStream_t st,
@@ -1081,11 +1159,9 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
     split_sum(part, 0, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
     return;
   }
-  // the direct-to-LDS kernel: fp32, 256-column tiles that stay inside one
-  // gate block, row offsets that fit an int, one workgroup per CU
+  // the direct-to-LDS kernel, one workgroup per CU
   const Net& n = ld.n;
-  const long big = (long)n.V * (n.GW > n.H ? n.GW : n.H) + (long)n.V * n.D;
-  if (!n.bf && ld.direct() && n.H % 256 == 0 && No % 256 == 0 && Mo % 4 == 0 && big < (1L << 31)) {
+  if (tn_direct_ok(n, ld.direct(), Mo, No)) {
     const int pad128 = cdiv(Mo, 128) * 128 - Mo, pad64 = cdiv(Mo, 64) * 64 - Mo;
     const int BM = pad64 < pad128 ? 64 : 128;
     // 128-wide column tiles where the 256-wide ones would be few (16 or
@@ -1500,6 +1576,110 @@ void loss_fwd(const Net& n, float* loss_out, hipStream_t s) {
                      n.inv_denom, loss_out);
 }
 
+// One product of a grouped launch: out[:, cols] = sum over q < Q of
+// A(q)^T B(q) ([Mo, No]), reduced from its split-K partials (part) into dst
+// as split_sum does; BM x BN is the tile shape the kernel instantiation
+// gives it.
+struct TnPlan {
+  bool on;
+  int Q, Mo, No;
+  float* dst;
+  int ldd, col_off, gap_start, gap;
+  float* part;
+  size_t part_floats;
+  int BM, BN;
+};
+
+// At most this many workgroups per grouped launch: one round, one per CU (a
+// product workgroup holds 120-156 KB of LDS).
+constexpr int kTnGroupWGs = 256;
+
+// Split counts: the smallest per-workgroup MFMA work u (32-deep chunks x
+// tile area, in 128 x 256 units) for which every product, split so that no
+// workgroup carries more than u, fits the launch in one round.
+template <class K, class LA, class LB, class LC>
+void tn_group_launch(K kernel, const char* name, TnGroupArgs<LA, LB, LC>& g, const TnPlan (&P)[3],
+                     hipStream_t st, SplitJobs* jobs) {
+  int nch[3] = {0, 0, 0}, tiles[3] = {0, 0, 0}, area[3] = {0, 0, 0}, cap[3] = {0, 0, 0};
+  std::vector<long> cand;
+  for (int k = 0; k < 3; ++k) {
+    if (!P[k].on || P[k].Q <= 0) continue;
+    nch[k] = cdiv(P[k].Q, kBK);
+    tiles[k] = (P[k].No / P[k].BN) * cdiv(P[k].Mo, P[k].BM);
+    area[k] = P[k].BM * P[k].BN / (64 * 128);   // 1, 2 or 4
+    cap[k] = nch[k];
+    while (cap[k] > 1 && (size_t)cap[k] * P[k].Mo * P[k].No > P[k].part_floats) --cap[k];
+    for (int c = 1; c <= nch[k]; ++c) cand.push_back((long)c * area[k]);
+  }
+  auto splits = [&](int k, long u) {   // fewest splits with at most u per workgroup
+    const long per = u / area[k];
+    int sk = per < 1 ? cap[k] : (int)cdiv(nch[k], (int)(per < nch[k] ? per : nch[k]));
+    return sk > cap[k] ? cap[k] : sk;
+  };
+  auto wgs = [&](long u) {
+    long t = 0;
+    for (int k = 0; k < 3; ++k)
+      if (nch[k] > 0) t += (long)tiles[k] * splits(k, u);
+    return t;
+  };
+  long u = 0;
+  if (!cand.empty()) {
+    std::sort(cand.begin(), cand.end());
+    cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
+    size_t lo = 0, hi = cand.size() - 1;   // wgs() does not increase with u
+    while (lo < hi) {
+      const size_t mid = (lo + hi) / 2;
+      if (wgs(cand[mid]) <= kTnGroupWGs) hi = mid;
+      else lo = mid + 1;
+    }
+    u = cand[lo];
+  }
+  int end = 0, S[3] = {0, 0, 0};
+  for (int k = 0; k < 3; ++k) {
+    TnJob& J = g.j[k];
+    J = TnJob{0, 0, 0, 0, 1, 1, end, nullptr};
+    if (nch[k] == 0) continue;
+    const int qchunk = cdiv(cdiv(P[k].Q, splits(k, u)), kBK) * kBK;
+    S[k] = cdiv(P[k].Q, qchunk);
+    end += tiles[k] * S[k];
+    J = TnJob{P[k].Q, qchunk, P[k].Mo, P[k].No, P[k].No / P[k].BN, cdiv(P[k].Mo, P[k].BM), end,
+              P[k].part};
+  }
+  if (end > 0) CAVS_LAUNCH(name, kernel, dim3(end), dim3(512), 0, st, g);
+  for (int k = 0; k < 3; ++k)
+    if (P[k].on)
+      split_sum(P[k].part, S[k], P[k].Mo, P[k].No, P[k].dst, P[k].ldd, P[k].col_off,
+                P[k].gap_start, P[k].gap, st, jobs);
+}
+
+bool lstm_lazy_grouped(const Net& n, int off1, int n_pull, bool with_f, float* dU, float* dWx,
+                       float* part, size_t pf, hipStream_t s, SplitJobs* jobs) {
+  const int H = n.H, D = n.D, MI = n.V - off1;
+  if (n.N != 2 || D <= 0) return false;
+  TnGroupArgs<LdDUf, LdDWx, LdDWx> g{LdDUf{n, off1, MI}, LdDWx{n, (int)with_f},
+                                     LdDWx{n, (int)with_f}, {}};
+  const int NoC = with_f ? 4 * H : 3 * H;
+  if (!tn_direct_ok(n, g.a.direct(), H, H) || !tn_direct_ok(n, g.b.direct(), D, NoC)) return false;
+  // dU_iou (the largest) alone fills the chip; dU_f and dW_x share a launch
+  lstm_dU_iou(n, off1, dU, part, pf, s, jobs);
+  // dW_x: 64-row tiles where they waste fewer rows of D
+  const bool c64 = cdiv(D, 64) * 64 - D < cdiv(D, 128) * 128 - D;
+  const TnPlan P[3] = {
+      {true, 2 * MI, H, H, dU, 4 * H, H, 1 << 30, 0, part + pf, pf, 128, 128},
+      {true, n_pull, D, NoC, dWx, 4 * H, 0, with_f ? 1 << 30 : H, with_f ? 0 : H, part + 2 * pf,
+       pf, c64 ? 64 : 128, 256},
+      {false, 0, 0, 0, nullptr, 0, 0, 0, 0, nullptr, 0, 128, 256}};
+  if (c64)
+    tn_group_launch(k_tn_group<LdDUf, 128, 128, 4, LdDWx, 64, 256, 3, LdDWx, 64, 256, 3>,
+                    "k_tn_group<dUf, dWx64>", g, P, s, jobs);
+  else
+    tn_group_launch(k_tn_group<LdDUf, 128, 128, 4, LdDWx, 128, 256, 3, LdDWx, 128, 256, 3>,
+                    "k_tn_group<dUf, dWx128>", g, P, s, jobs);
+  // the f block of dW_x is exactly zero when no vertex with children pulls
+  if (!with_f) split_sum(part + 2 * pf, 0, D, H, dWx, 4 * H, H, 1 << 30, 0, s, jobs);
+  return true;
+}
+
 void lstm_dU_iou(const Net& n, int off1, float* dU, float* part, size_t part_floats,
                  hipStream_t s, SplitJobs* jobs, int rows) {
   const int H = n.H, MI = rows >= 0 ? rows : n.V - off1;
@@ -1542,8 +1722,22 @@ void lstm_dWx(const Net& n, int n_pull, bool with_f, float* dWx, float* part,
   }
 }
 
-void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s) {
+void fc_dW(const Net& n, int off1, float* dW, float* part, size_t part_floats, hipStream_t s,
+           SplitJobs* jobs) {
   const int H = n.H, MI = n.V - off1;
+  TnGroupArgs<LdFCdW, LdFCdW, LdFCdW> g{LdFCdW{n, off1, 0}, LdFCdW{n, off1, 1}, LdFCdW{n, off1, 0},
+                                        {}};
+  if (n.N <= 2 && tn_direct_ok(n, g.a.direct(), H, H)) {
+    // both child slots' products share one launch; their split-K partials
+    // sit side by side
+    TnPlan P[3];
+    for (int k = 0; k < 3; ++k)
+      P[k] = TnPlan{k < n.N, MI, H, H, dW + (size_t)k * H * H, H, 0, 1 << 30, 0,
+                    part + k * part_floats, part_floats, 128, 128};
+    tn_group_launch(k_tn_group<LdFCdW, 128, 128, 4, LdFCdW, 128, 128, 4, LdFCdW, 128, 128, 4>,
+                    "k_tn_group<FCdW>", g, P, s, jobs);
+    return;
+  }
   for (int k = 0; k < n.N; ++k) {
     LdFCdW ld{n, off1, k};
     tn_product(ld, MI, H, H, dW + (size_t)k * H * H, H, 0, 1 << 30, 0, part, part_floats, s);
