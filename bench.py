@@ -84,6 +84,16 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         return 2.0 * n_pull * D * gates_x * H, 0.0
     base = re.sub(r", (64|128)(, [48])?>", ">", name.replace("_bf", ""))
     base = re.sub(r"^k_tn_dl<(\w+), .*>$", r"k_tn_gemm<\1>", base)
+    base = re.sub(r"^k_nt<(\w+)>$", r"k_tn_gemm<\1>", base)   # k_nt_bf, "_bf" dropped
+    if name.startswith("k_pack_bf<"):   # bf16 operand packs: fp32 reads, bf16 writes
+        MI, nL = int(inner.sum()), float(nc.sum())
+        No = 3 * H if N == 2 else 4 * H
+        pad = lambda q, m: -(-q // m) * m
+        pk = {"LdDUiou": (nL * H + MI * No) * 4.0 + (pad(H, 128) + No) * pad(MI, 64) * 2.0,
+              "LdDUf": (nL + 2 * MI) * H * 4.0 + (pad(H, 128) + H) * pad(2 * MI, 64) * 2.0,
+              "LdDWx": n_pull * (D + gates_x * H) * 4.0
+              + (pad(D, 128) + gates_x * H) * pad(n_pull, 64) * 2.0}
+        return 0.0, pk.get(name[len("k_pack_bf<"):-1], 0.0)
     return lazy.get(base, 0.0), 0.0
 
 

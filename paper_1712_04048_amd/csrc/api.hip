@@ -4,10 +4,11 @@
 #include <stdarg.h>
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
 
 #include "kernels.h"
-
-#include <string.h>
 
 namespace cavs {
 
@@ -72,9 +73,25 @@ struct WsLayout {
   size_t gHt, gDt, gEh, gEc, gdAx, gpart;   // generic engine
   size_t WsT, dHLx;
   size_t gpart_floats;
+  size_t pack, pack_elems;                  // bf16 lazy products: packed operands
 };
 
 bool lm_head(const cavs_params* p) { return p->loss == CAVS_LOSS_CE && p->C > kSmallHeadC; }
+
+// bf16 values of the largest packed lazy product of the fused Tree-LSTM
+// path (rows: the A columns padded to the product tile, then the B columns;
+// each row the contraction length padded to the pack segment)
+size_t bf_pack_elems(const cavs_params* p, const cavs_sched* s) {
+  if (p->prec != CAVS_BF16 || p->cell != CAVS_TREE_LSTM || s->V <= 0) return 0;
+  const size_t H = (size_t)p->H, D = (size_t)p->D;
+  const size_t MI = s->T > 1 ? (size_t)(s->V - s->level_offsets_host[1]) : 0;
+  auto qp = [](size_t q) { return (q + kPackSeg - 1) / kPackSeg * kPackSeg; };
+  auto mp = [](size_t m) { return (m + kPackTile - 1) / kPackTile * kPackTile; };
+  size_t e = (mp(H) + 4 * H) * qp(MI);                              // dU_iou
+  if (p->N == 2) e = std::max(e, (mp(H) + H) * qp(2 * MI));         // dU_f
+  if (D > 0) e = std::max(e, (mp(D) + 4 * H) * qp((size_t)s->n_pull));  // dW_x
+  return e;
+}
 
 bool env_on(const char* name) {
   const char* e = getenv(name);
@@ -121,6 +138,8 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.bar = take(256);
   L.WsT = take(lm ? C * H : 0);
   L.dHLx = take(tr * V * H);
+  L.pack_elems = (tr && !gen) ? bf_pack_elems(p, s) : 0;
+  L.pack = take((L.pack_elems + 1) / 2);
   if (lm && !gen) {
     L.gpart_floats = tr * gen_part_floats(p->D, p->H, (int)C);
     L.gpart = take(L.gpart_floats);
@@ -271,6 +290,8 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.dHp = (float*)(base + L.dHp);
   n.dCp = (float*)(base + L.dCp);
   n.dA = (float*)(base + L.dA);
+  n.pack = L.pack_elems > 0 ? (unsigned short*)(base + L.pack) : nullptr;
+  n.pack_elems = L.pack_elems;
   if (!train) {   // the kernels test these for null and skip what only backward reads
     if (!(p->cell == CAVS_TREE_LSTM && generic_mode(p, s))) n.Gs = nullptr;
     if (!lm_head(p)) n.dZ = nullptr;

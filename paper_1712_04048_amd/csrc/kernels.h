@@ -52,6 +52,8 @@ struct Net {
   float* dHp;                   // [V, H]  dL/dh contributed by the parent (LSTM)
   float* dCp;                   // [V, H]  dL/dc contributed by the parent
   float* dA;                    // [V, GW] pre-activation gradients, same layout as Gs
+  unsigned short* pack;         // bf16 lazy products: operands packed q-contiguous (workspace;
+  size_t pack_elems;            // null: the unpacked kernels), capacity in bf16 values
   // outputs in vertex-id order
   float* dX;                    // [n_x, D] input gradient (FC backward)
   int leaf_end;                 // FC backward: positions below this are leaves (level 0)
@@ -281,6 +283,10 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
 // accumulation is fp32.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+// packed bf16 lazy products: q per 128-byte pack segment (the product's
+// chunk) and the output tile of the packed product (both sides)
+constexpr int kPackSeg = 64;
+constexpr int kPackTile = 128;
 typedef unsigned short u16;
 constexpr int kLDH = kBK + 8;   // 40 bf16 = 80 bytes per row (16-byte aligned)
 

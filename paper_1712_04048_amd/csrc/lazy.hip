@@ -336,6 +336,8 @@ struct LdDUiou {  // dU[:, i|o|u] (or all four blocks when N == 1): A = h~, B = 
   static constexpr const char* kName = "k_tn_gemm<LdDUiou, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDUiou, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUiou>";
+  static constexpr const char* kNamePack = "k_pack_bf<LdDUiou>";
+  static constexpr const char* kNameNt = "k_nt_bf<LdDUiou>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDUiou, 128, 256, 2>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDUiou, 64, 256, 3>";
   static constexpr const char* kNameDl128n = "k_tn_dl<LdDUiou, 128, 128, 3>";
@@ -378,6 +380,8 @@ struct LdDUf {  // dU[:, f] with two children: q in [0, 2 MI), A = h_k, B = dA_f
   static constexpr const char* kName = "k_tn_gemm<LdDUf, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDUf, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDUf>";
+  static constexpr const char* kNamePack = "k_pack_bf<LdDUf>";
+  static constexpr const char* kNameNt = "k_nt_bf<LdDUf>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDUf, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDUf, 64, 256, 3>";
   static constexpr const char* kNameDl128n = "k_tn_dl<LdDUf, 128, 128, 4>";
@@ -415,6 +419,8 @@ struct LdDWx {  // dW_x: q over pulling vertices, A = x, B = dA_x (f = f_0 + f_1
   static constexpr const char* kName = "k_tn_gemm<LdDWx, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdDWx, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdDWx>";
+  static constexpr const char* kNamePack = "k_pack_bf<LdDWx>";
+  static constexpr const char* kNameNt = "k_nt_bf<LdDWx>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdDWx, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdDWx, 64, 256, 3>";
   static constexpr const char* kNameDl128n = "k_tn_dl<LdDWx, 128, 128, 4>";
@@ -457,6 +463,8 @@ struct LdFCdW {  // Tree-FC dW_k: A = h_k, B = delta, q over internal vertices
   static constexpr const char* kName = "k_tn_gemm<LdFCdW, 64, 4>";
   static constexpr const char* kName128 = "k_tn_gemm<LdFCdW, 128, 8>";
   static constexpr const char* kNameBf = "k_tn_gemm_bf<LdFCdW>";
+  static constexpr const char* kNamePack = "k_pack_bf<LdFCdW>";
+  static constexpr const char* kNameNt = "k_nt_bf<LdFCdW>";
   static constexpr const char* kNameDl128 = "k_tn_dl<LdFCdW, 128, 256, 3>";
   static constexpr const char* kNameDl64 = "k_tn_dl<LdFCdW, 64, 256, 3>";
   static constexpr const char* kNameDl128n = "k_tn_dl<LdFCdW, 128, 128, 4>";
@@ -1143,6 +1151,130 @@ void split_sum(const float* part, int S, int Mo, int No, float* dst, int ldd, in
               part, S, Mo, No, dst, ldd, col_off, gap_start, gap);
 }
 
+// ------------------------------------------- bf16 lazy products, packed
+// With bf16 matrix-product operands a lazy product first packs both
+// operands, rounded to bf16 (nearest-even) where the fp32 path would feed
+// them to the matrix core, into rows that are contiguous in the contraction
+// index q: pack row c < Mp is column m = c of A (zero for m >= Mo), row
+// Mp + n is column n of B; every row holds Qp values (zero for q >= Q).  The
+// product is then an "A B^T" over those rows, staged straight into LDS.
+constexpr int kPackQ = kPackSeg;
+constexpr int kNtTile = kPackTile;
+
+template <class L>
+__global__ void __launch_bounds__(256) k_pack_bf(L ld, int Q, int Qp, int Mo, int Mp,
+                                                 u16* __restrict__ pk) {
+  __shared__ u16 t[64][kPackQ + 8];   // [column][q]
+  const int c0 = blockIdx.x * 64, q0 = blockIdx.y * kPackQ;
+  const int tid = threadIdx.x, c4 = tid & 15, qr = tid >> 4;
+  const bool aside = c0 < Mp;        // 64 | Mp: a block is all A or all B columns
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ql = qr + 16 * i, q = q0 + ql;
+    float4 v = f4zero();
+    if (q < Q) {
+      const auto x = ld.idx(q);
+      if (aside) {
+        const int m = c0 + 4 * c4;
+        if (m < Mo) v = ld.a4(x, q, m);
+      } else {
+        v = ld.b4(x, q, c0 - Mp + 4 * c4);
+      }
+    }
+    t[4 * c4 + 0][ql] = f2bf(v.x);
+    t[4 * c4 + 1][ql] = f2bf(v.y);
+    t[4 * c4 + 2][ql] = f2bf(v.z);
+    t[4 * c4 + 3][ql] = f2bf(v.w);
+  }
+  __syncthreads();
+  // 64 columns x 64 q: thread (row, seg) writes 16 q (32 bytes) of one row
+  const int row = tid >> 2, seg = tid & 3;
+  const uint4* sp = reinterpret_cast<const uint4*>(&t[row][16 * seg]);
+  uint4* dp = reinterpret_cast<uint4*>(pk + (size_t)(c0 + row) * Qp + q0 + 16 * seg);
+  dp[0] = sp[0];
+  dp[1] = sp[1];
+}
+
+// out[s][m][n] = sum over q in split s of pack[m][q] pack[Mp + n][q] for
+// m < Mo: a 128 x 128 tile, four wavefronts of 64 x 64 (4 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16), 64-deep chunks through an S-stage ring of
+// 128-byte LDS rows (quads XOR-swizzled by row & 7).  The n fragment is the
+// MFMA's A operand, so lane (r, g) holds four consecutive n of one m.
+__device__ __forceinline__ bf16x8 quad_sw(const float* L, int row, int q) {
+  return *reinterpret_cast<const bf16x8*>(L + row * 32 + 4 * (q ^ (row & 7)));
+}
+
+template <int S>
+__global__ void __launch_bounds__(256) k_nt_bf(const u16* __restrict__ pk, int Qp, int qchunk,
+                                               int Mo, int Mp, int No, float* __restrict__ out) {
+  constexpr int BM = kNtTile, BN = kNtTile, ROWS = BM + BN, IPW = ROWS / 32;
+  __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L1[ROWS * 32];
+  __shared__ __attribute__((aligned(1024))) float L2[S > 2 ? ROWS * 32 : 4];
+  __shared__ __attribute__((aligned(1024))) float L3[S > 3 ? ROWS * 32 : 4];
+  const Ring<ROWS, S> ring{L0, L1, L2, L3};
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, r = lane & 15;
+  const int wm = w & 1, wn = w >> 1;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, s = blockIdx.z;
+  const int q_lo = s * qchunk, nch = (min(Qp, q_lo + qchunk) - q_lo) / kPackQ;
+  // LDS rows [0, BM): pack rows m0 + row; [BM, ROWS): pack rows Mp + n0 + row - BM
+  const char* src[IPW];
+#pragma unroll
+  for (int t = 0; t < IPW; ++t) {
+    const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
+    const int prow = row < BM ? m0 + row : Mp + n0 + row - BM;
+    src[t] = reinterpret_cast<const char*>(pk + (size_t)prow * Qp + q_lo) + 16 * qg;
+  }
+  const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
+  v4f acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = v4f{0.f, 0.f, 0.f, 0.f};
+  auto issue = [&](auto sc, int c) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
+#pragma unroll
+    for (int t = 0; t < IPW; ++t)
+      copy16_to_lds(reinterpret_cast<const float*>(src[t] + 128 * c), base + 1024u * t);
+  };
+  struct Frag {
+    bf16x8 m[4][2], n[4][2];
+  };
+  auto read = [&](const float* Ls, Frag& f) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        f.n[b][h] = quad_sw(Ls, BM + wn * 64 + b * 16 + r, 4 * h + g);
+        f.m[b][h] = quad_sw(Ls, wm * 64 + b * 16 + r, 4 * h + g);
+      }
+  };
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = mfma_bf16_16x16x32(f.n[b][h], f.m[a][h], acc[a][b]);
+  };
+  auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
+    read(Lnext, nxt);
+    mma(cur);
+    interleave_reads<16, 32>();
+  };
+  if (nch > 0) ring_loop_db<S, IPW, Frag>(nch, ring, issue, read, body);
+  float* o = out + (size_t)s * Mo * No;
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const int m = m0 + wm * 64 + a * 16 + r;
+    if (m >= Mo) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      st4(o + (size_t)m * No + n0 + wn * 64 + b * 16 + 4 * g,
+          make_float4(acc[a][b][0], acc[a][b][1], acc[a][b][2], acc[a][b][3]));
+  }
+}
+
 // The direct-to-LDS kernel applies: fp32, 256-column tiles that stay inside
 // one gate block, row offsets that fit an int.
 bool tn_direct_ok(const Net& n, bool direct, int Mo, int No) {
@@ -1188,6 +1320,23 @@ void tn_product(const L& ld, int Q, int Mo, int No, float* dst, int ldd, int col
     else
       CAVS_LAUNCH(L::kNameDl128, (k_tn_dl<L, 128, 256, S128>), grid, dim3(512), 0, st, ld, Q,
                   qchunk, Mo, No, part);
+    split_sum(part, S, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
+    return;
+  }
+  // bf16: pack, then the packed product
+  const int Mp = cdiv(Mo, kNtTile) * kNtTile, Qp = cdiv(Q, kPackQ) * kPackQ;
+  if (n.bf && n.pack && No % kNtTile == 0 && (size_t)(Mp + No) * Qp <= n.pack_elems) {
+    CAVS_LAUNCH(L::kNamePack, k_pack_bf<L>, dim3((Mp + No) / 64, Qp / kPackQ), dim3(256), 0, st, ld,
+                Q, Qp, Mo, Mp, n.pack);
+    const int tiles = (No / kNtTile) * (Mp / kNtTile);
+    int S = 256 / tiles;
+    S = S < 1 ? 1 : S;
+    if (S > Qp / kPackQ) S = Qp / kPackQ;
+    while (S > 1 && (size_t)S * Mo * No > part_floats) --S;
+    const int qchunk = cdiv(cdiv(Qp, S), kPackQ) * kPackQ;
+    S = cdiv(Qp, qchunk);
+    CAVS_LAUNCH(L::kNameNt, k_nt_bf<3>, dim3(No / kNtTile, Mp / kNtTile, S), dim3(256), 0, st,
+                n.pack, Qp, qchunk, Mo, Mp, No, part);
     split_sum(part, S, Mo, No, dst, ldd, col_off, gap_start, gap, st, jobs);
     return;
   }
