@@ -74,6 +74,7 @@ struct WsLayout {
   size_t WsT, dHLx;
   size_t gpart_floats;
   size_t pack, pack_elems;                  // bf16 lazy products: packed operands
+  size_t Ub, UTb;                           // bf16 copies of U and U^T
 };
 
 bool lm_head(const cavs_params* p) { return p->loss == CAVS_LOSS_CE && p->C > kSmallHeadC; }
@@ -140,6 +141,9 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.dHLx = take(tr * V * H);
   L.pack_elems = (tr && !gen) ? bf_pack_elems(p, s) : 0;
   L.pack = take((L.pack_elems + 1) / 2);
+  const bool ubf = lstm && !gen && p->prec == CAVS_BF16;
+  L.Ub = take(ubf ? 2 * H * H : 0);    // 4 H^2 bf16 values each
+  L.UTb = take(ubf ? 2 * H * H : 0);
   if (lm && !gen) {
     L.gpart_floats = tr * gen_part_floats(p->D, p->H, (int)C);
     L.gpart = take(L.gpart_floats);
@@ -291,6 +295,9 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   n.dCp = (float*)(base + L.dCp);
   n.dA = (float*)(base + L.dA);
   n.pack = L.pack_elems > 0 ? (unsigned short*)(base + L.pack) : nullptr;
+  const bool ubf = p->cell == CAVS_TREE_LSTM && p->prec == CAVS_BF16 && !generic_mode(p, s);
+  n.Ub = ubf ? (unsigned short*)(base + L.Ub) : nullptr;
+  n.UTb = ubf ? (unsigned short*)(base + L.UTb) : nullptr;
   n.pack_elems = L.pack_elems;
   if (!train) {   // the kernels test these for null and skip what only backward reads
     if (!(p->cell == CAVS_TREE_LSTM && generic_mode(p, s))) n.Gs = nullptr;
@@ -514,6 +521,7 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
   n.h_out = h_out;
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
+  if (n.Ub && s->T > 1) lstm_round_u(n, str);   // bf16 weight operands of the level products
   if (p->cell == CAVS_TREE_LSTM && generic_mode(p, s)) {
     lstm_transpose_u(n, str);
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, 0, str);   // P for every pulling row

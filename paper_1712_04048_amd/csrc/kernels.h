@@ -33,6 +33,8 @@ struct Net {
   float* UT;                    // LSTM: U transposed, [4H, H]; FC: each slot's block
                                 // transposed, [N, H, H] (workspace)
   float* WxT;                   // LSTM: W_x transposed, [4H, D] (workspace)
+  unsigned short* Ub;           // LSTM bf16: U rounded to bf16, [H, 4H] (workspace; null in
+  unsigned short* UTb;          // fp32) and U^T rounded to bf16, [4H, H]; written per pass
   float* zrow;                  // H zeros (workspace): the row an absent operand row reads;
                                 // cleared by the transpose kernel and by the loss kernel
   const float* b;
@@ -102,6 +104,8 @@ int lstm_fuse_level(const int* lo_host, int T);
 constexpr int kTileMinRows = 300;
 bool lstm_tile_applies(const Net& n, int M);
 void lstm_transpose_u(const Net& n, hipStream_t s);
+// bf16: n.Ub and n.UTb from n.U (before any level product of the pass)
+void lstm_round_u(const Net& n, hipStream_t s);
 void lstm_fwd_tile(const Net& n, int off, int M, hipStream_t s);
 void lstm_bwd_tile(const Net& n, int off, int M, hipStream_t s);
 // Persistent loop over levels [t0, t1) (forward) or t1-1 .. t0 (backward:

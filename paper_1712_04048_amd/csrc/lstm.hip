@@ -660,20 +660,30 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
+    // bf16: the weight fragment comes pre-rounded from n.UTb (U^T, one
+    // 16-byte load per gate); fp32: eight loads down a column of U
     struct Frag {
       float a[TR][NCH][8];
-      float b[4][8];
+      float b[BF ? 1 : 4][8];
+      bf16x8 bq[BF ? 4 : 1];
     };
+    const u16* utb = BF ? n.UTb + (size_t)(u0 + r) * H : nullptr;
     auto load = [&](int k0, Frag& f) {
       const int kk = k0 + 8 * gq;
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
         for (int c = 0; c < NCH; ++c) ld8(ap[tr][c] + kk, f.a[tr][c]);
+      if constexpr (BF) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < 4; ++g)
+          f.bq[g] = *reinterpret_cast<const bf16x8*>(utb + (size_t)g * H * H + kk);
+      } else {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
+      }
     };
     auto compute = [&](const Frag& f) {
 #pragma unroll
@@ -685,11 +695,20 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
           a1[s] = NCH == 2 ? f.a[tr][NCH - 1][s] * am[tr][NCH - 1] : 0.f;
           ah[s] = NCH == 2 ? a0[s] + a1[s] : a0[s];
         }
-        acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
-        acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
-        acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
-        acc[tr][3] = mfma_chunk8<BF>(a0, f.b[G_F], acc[tr][3]);
-        if constexpr (NCH == 2) acc[tr][4] = mfma_chunk8<BF>(a1, f.b[G_F], acc[tr][4]);
+        if constexpr (BF) {
+          const bf16x8 hb = to_bf8(ah), b0 = to_bf8(a0);
+          acc[tr][0] = mfma_bf16_16x16x32(hb, f.bq[G_I], acc[tr][0]);
+          acc[tr][1] = mfma_bf16_16x16x32(hb, f.bq[G_O], acc[tr][1]);
+          acc[tr][2] = mfma_bf16_16x16x32(hb, f.bq[G_U], acc[tr][2]);
+          acc[tr][3] = mfma_bf16_16x16x32(b0, f.bq[G_F], acc[tr][3]);
+          if constexpr (NCH == 2) acc[tr][4] = mfma_bf16_16x16x32(to_bf8(a1), f.bq[G_F], acc[tr][4]);
+        } else {
+          acc[tr][0] = mfma_chunk8<BF>(ah, f.b[G_I], acc[tr][0]);
+          acc[tr][1] = mfma_chunk8<BF>(ah, f.b[G_O], acc[tr][1]);
+          acc[tr][2] = mfma_chunk8<BF>(ah, f.b[G_U], acc[tr][2]);
+          acc[tr][3] = mfma_chunk8<BF>(a0, f.b[G_F], acc[tr][3]);
+          if constexpr (NCH == 2) acc[tr][4] = mfma_chunk8<BF>(a1, f.b[G_F], acc[tr][4]);
+        }
       }
     };
     // two register buffers: loads of the next chunk overlap the current MFMAs
@@ -792,19 +811,26 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
     // phase 1: i|o|u columns (all four blocks with one child slot)
+    // bf16: the U fragment comes pre-rounded from n.Ub (one 16-byte load)
+    const u16* ubb = BF ? n.Ub + (size_t)(n0 + r) * H4 : nullptr;
     struct F1 {
-      float a[TR][8], b[8];
+      float a[TR][8], b[BF ? 1 : 8];
+      bf16x8 bq;
     };
     const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / KW;
     auto load1 = [&](int c0, F1& f) {
       const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) ld8(da[tr] + col, f.a[tr]);
-      ld8(ub + col, f.b);
+      if constexpr (BF) f.bq = *reinterpret_cast<const bf16x8*>(ubb + col);
+      else ld8(ub + col, f.b);
     };
     auto comp1 = [&](const F1& f) {
 #pragma unroll
-      for (int tr = 0; tr < TR; ++tr) acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
+      for (int tr = 0; tr < TR; ++tr) {
+        if constexpr (BF) acc[tr][0] = mfma_bf16_16x16x32(to_bf8(f.a[tr]), f.bq, acc[tr][0]);
+        else acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
+      }
     };
     // groups of G chunks: all loads of a group are in flight together, so a
     // small level pays about one memory latency per group, not per chunk.
@@ -817,7 +843,8 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     if constexpr (NCH == 2) {
       // the two phases' loads go out together: one memory latency per level
       struct F2 {
-        float a0[TR][8], a1[TR][8], b[8];
+        float a0[TR][8], a1[TR][8], b[BF ? 1 : 8];
+        bf16x8 bq;
       };
       const int q2 = H / KW;
       auto load2 = [&](int c0, F2& f) {
@@ -827,13 +854,19 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
           ld8(da[tr] + H + col, f.a0[tr]);
           ld8(da[tr] + 4 * H + col, f.a1[tr]);
         }
-        ld8(ub + H + col, f.b);
+        if constexpr (BF) f.bq = *reinterpret_cast<const bf16x8*>(ubb + H + col);
+        else ld8(ub + H + col, f.b);
       };
       auto comp2 = [&](const F2& f) {
 #pragma unroll
         for (int tr = 0; tr < TR; ++tr) {
-          acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
-          acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
+          if constexpr (BF) {
+            acc[tr][1] = mfma_bf16_16x16x32(to_bf8(f.a0[tr]), f.bq, acc[tr][1]);
+            acc[tr][2] = mfma_bf16_16x16x32(to_bf8(f.a1[tr]), f.bq, acc[tr][2]);
+          } else {
+            acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
+            acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
+          }
         }
       };
       constexpr int G2 = 2;   // H / (32 KW) is even

@@ -395,6 +395,14 @@ __device__ __forceinline__ v4f mfma_chunk8(const float (&a)[8], const float (&b)
   }
 }
 
+// eight values rounded to bf16 (nearest-even), as one MFMA operand
+__device__ __forceinline__ bf16x8 to_bf8(const float (&v)[8]) {
+  bf16x8 b;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) b[s] = __builtin_bit_cast(__bf16, f2bf(v[s]));
+  return b;
+}
+
 __device__ __forceinline__ void ld8(const float* p, float (&v)[8]) {
   const float4 x = ldg4(p), y = ldg4(p + 4);
   v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;

@@ -58,6 +58,23 @@ __global__ void __launch_bounds__(256) k_transpose_u(const float* __restrict__ U
     for (int y = ty; y < 32; y += 8) dst[(size_t)(c0 + y) * K + k0 + tx] = t[tx][y];
 }
 
+// Ub[k][c] = bf16(U[k][c]) and UTb[c][k] = bf16(U[k][c]) for the [H, 4H]
+// recurrent weight: the bf16 operands of the split-K level products, rounded
+// once per pass (nearest-even, as every other bf16 operand).
+__global__ void __launch_bounds__(256) k_round_u(const float* __restrict__ U, u16* __restrict__ Ub,
+                                                 u16* __restrict__ UTb, int H) {
+  __shared__ u16 t[32][34];
+  const int H4 = 4 * H, c0 = blockIdx.x * 32, k0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int y = ty; y < 32; y += 8) {
+    const u16 v = f2bf(U[(size_t)(k0 + y) * H4 + c0 + tx]);
+    Ub[(size_t)(k0 + y) * H4 + c0 + tx] = v;
+    t[y][tx] = v;
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) UTb[(size_t)(c0 + y) * H + k0 + tx] = t[tx][y];
+}
+
 template <int NCH, bool BF, int BM, int BU, int S>
 __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TU = BU / 32;   // 16 x 16 blocks per wavefront
@@ -331,6 +348,11 @@ void lstm_transpose_u(const Net& n, hipStream_t s) {
   const int yw = n.Wx && n.D > 0 ? cdiv(n.D, 32) : 0;
   CAVS_LAUNCH("k_transpose_u", k_transpose_u, dim3(4 * n.H / 32, n.H / 32 + yw), dim3(256), 0, s,
               n.U, n.UT, n.Wx, n.WxT, n.zrow, n.H, n.D);
+}
+
+void lstm_round_u(const Net& n, hipStream_t s) {
+  CAVS_LAUNCH("k_round_u", k_round_u, dim3(4 * n.H / 32, n.H / 32), dim3(256), 0, s, n.U, n.Ub,
+              n.UTb, n.H);
 }
 
 #define CAVS_TILE_LAUNCH(KIND, NCH, BF, BM, BU, S)                                             \
