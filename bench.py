@@ -300,6 +300,7 @@ def main():
         ablation["persistent_small_levels"] = round(fwd_bwd_with("CAVS_PERSIST"), 4)
         ablation["unfused_backward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_BWD_GATES"), 4)
         ablation["unfused_forward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_FWD_GATES"), 4)
+        ablation["two_stream_lazy_products"] = round(fwd_bwd_with("CAVS_TWO_STREAM"), 4)
         ablation["unfused_gates_both"] = round(
             fwd_bwd_with("CAVS_UNFUSED_FWD_GATES", "CAVS_UNFUSED_BWD_GATES"), 4)
         if wl.prec == W.PREC_FP32:

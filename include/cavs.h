@@ -42,8 +42,12 @@
  *                                 with grid barriers;
  *       CAVS_UNFUSED_FWD_GATES=1  the forward gates and cell update in an
  *                                 elementwise kernel after each level product;
- *       CAVS_GENERIC=1            trees too run the generic engine.
- *     A fourth is a failure-injection hook for tests of the error path:
+ *       CAVS_GENERIC=1            trees too run the generic engine;
+ *       CAVS_TWO_STREAM=1         the backward's input-side lazy products
+ *                                 (dW_x, dX) on a second stream of the
+ *                                 context beside dU, joined by events before
+ *                                 the split-K reductions.
+ *     Another is a failure-injection hook for tests of the error path:
  *       CAVS_PERSIST_SPIN=n       the persistent loop's grid barrier gives up
  *                                 after n polls (n < 0: at once) and records
  *                                 the error that cavs_sync reports.

@@ -238,6 +238,20 @@ bool unfused_bwd_gates() { return env_on("CAVS_UNFUSED_BWD_GATES"); }
 // epilogue.  Measured with bench.py; off by default.
 bool unfused_fwd_gates() { return env_on("CAVS_UNFUSED_FWD_GATES"); }
 
+// Ablation of the single-stream lazy phase (CAVS_TWO_STREAM=1; fused
+// Tree-LSTM path with inputs): the input-side products (dW_x, dX) run on a
+// second stream beside the recurrent ones (dU), joined before the split-K
+// reductions.  The second stream keeps the default priority.
+bool two_stream_lazy() { return env_on("CAVS_TWO_STREAM"); }
+
+hipError_t side_stream(cavs_ctx* ctx) {
+  if (ctx->side) return hipSuccess;
+  hipError_t e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->join_ev, hipEventDisableTiming);
+  return e;
+}
+
 // dU contributions of the internal positions [off, off + M): queued split-K
 // products whose reductions add into dU (acc) or overwrite it (first level).
 bool lstm_dU_level(const Net& n, int off, int M, float* dU, float* part, size_t pf, bool acc,
@@ -386,6 +400,9 @@ void cavs_destroy(cavs_ctx* ctx) {
     (void)hipEventDestroy(r.stop);
   }
   for (auto e : ctx->event_pool) (void)hipEventDestroy(e);
+  if (ctx->side) (void)hipStreamDestroy(ctx->side);
+  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
+  if (ctx->join_ev) (void)hipEventDestroy(ctx->join_ev);
   delete ctx;
 }
 
@@ -647,7 +664,17 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     // one reduction launch
     const bool with_f = s->n_inner_input > 0;
     SplitJobs jobs;
-    if (eager) {
+    const bool two = !eager && D > 0 && two_stream_lazy();
+    if (two) {
+      CAVS_HIP_CHECK(ctx, side_stream(ctx));
+      CAVS_HIP_CHECK(ctx, hipEventRecord(ctx->fork_ev, str));
+      CAVS_HIP_CHECK(ctx, hipStreamWaitEvent(ctx->side, ctx->fork_ev, 0));
+      lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, ctx->side, &jobs);
+      dx_gemm(n, s->n_pull, with_f, g->dX, ctx->side);
+      CAVS_HIP_CHECK(ctx, hipEventRecord(ctx->join_ev, ctx->side));
+      lstm_dU_iou(n, off1, g->dU, part, pf, str, &jobs);
+      lstm_dU_f(n, off1, g->dU, part + pf, pf, str, &jobs);
+    } else if (eager) {
       if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     } else if (!lstm_lazy_grouped(n, off1, s->n_pull, with_f, g->dU, g->dWx, part, pf, str,
                                   &jobs)) {
@@ -656,10 +683,11 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
       if (D > 0) lstm_dWx(n, s->n_pull, with_f, g->dWx, part + 2 * pf, pf, str, &jobs);
     }
     bias_head_grads(n, 0, s->V, off1, g->db, g->dWs, g->dbs, bpart, str, &jobs);
+    if (two) CAVS_HIP_CHECK(ctx, hipStreamWaitEvent(str, ctx->join_ev, 0));
     reduce_split_jobs(jobs, str);
     if (lm_head(p))
       lm_head_grads(n, g->dWs, g->dbs, (float*)((char*)ws + L.gpart), L.gpart_floats, str);
-    dx_gemm(n, s->n_pull, with_f, g->dX, str);
+    if (!two) dx_gemm(n, s->n_pull, with_f, g->dX, str);
   } else {
     // roots first; every other vertex's delta (or a leaf's input gradient)
     // comes from its parent's level product

@@ -30,6 +30,9 @@ struct cavs_ctx {
   int32_t* dev_err = nullptr;             // pinned, coherent, mapped: set by kernels whose
   int32_t* dev_err_dev = nullptr;         // bounded waits gave up (device view of dev_err)
   void* sched_scratch = nullptr;          // this device's static scheduling scratch
+  hipStream_t side = nullptr;             // the two-stream ablation's second stream and its
+  hipEvent_t fork_ev = nullptr;           // fork / join events (created on first use)
+  hipEvent_t join_ev = nullptr;
 };
 
 namespace cavs {

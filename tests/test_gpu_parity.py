@@ -665,6 +665,26 @@ def test_eager_weight_gradients_ablation(ctx, monkeypatch):
     monkeypatch.delenv("CAVS_EAGER_DW")
 
 
+def test_two_stream_lazy_products_ablation(ctx, monkeypatch):
+    """The two-stream variant (dW_x and dX on a second stream beside dU,
+    CAVS_TWO_STREAM=1) gives the oracle's gradients; its states and loss are
+    the single-stream ones bit for bit (only the backward's lazy phase
+    changes streams)."""
+    wl = W.config_treelstm_sst(3, K=16)
+    base = Batch(wl, ctx).run()
+    monkeypatch.setenv("CAVS_TWO_STREAM", "1")
+    got = Batch(wl, ctx).run()
+    for k in ("h", "c", "loss", "dX"):
+        assert np.array_equal(got[k], base[k]), k
+    _parity(ctx, wl, label="two_stream_sst")
+    _parity(ctx, W.config_varlstm(2, K=6), label="two_stream_chains")
+    rng = np.random.Generator(np.random.PCG64(36))
+    trees = [W.random_split_tree(int(L), rng) for L in rng.integers(2, 14, size=420)]
+    _parity(ctx, W.make_workload("two_stream_tiles", trees, N=2, D=32, H=256, C=5, rng=rng,
+                                 labels="all", inputs="all"))
+    monkeypatch.delenv("CAVS_TWO_STREAM")
+
+
 def test_unfused_backward_gates_ablation(ctx, monkeypatch):
     """The fusion ablation (every level's dA from the elementwise kernel,
     CAVS_UNFUSED_BWD_GATES=1) gives the oracle's gradients too."""
