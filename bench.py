@@ -57,7 +57,8 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
     c = nc[row0:row0 + rows]
     gates_x = 4 if with_f else 3
     if name.startswith(("k_lstm_fwd_level", "k_lstm_bwd_level", "k_lstm_fwd_persist",
-                        "k_lstm_bwd_persist", "k_lstm_fwd_tile", "k_lstm_bwd_tile")):
+                        "k_lstm_bwd_persist", "k_lstm_fwd_tile", "k_lstm_bwd_tile",
+                        "k_lstm_fwd_xcd", "k_lstm_bwd_xcd")):
         return float(np.sum(2.0 * H * (3 * H + c * H))), 0.0
     if name.startswith(("k_fc_fwd_tile", "k_fc_bwd_tile", "k_fc_fwd_sk", "k_fc_bwd_sk")):
         return float(np.sum(2.0 * c * H * H)), 0.0

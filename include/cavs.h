@@ -47,9 +47,20 @@
  *                                 (dW_x, dX) on a second stream of the
  *                                 context beside dU, joined by events before
  *                                 the split-K reductions.
+ *     One switch chooses an engine path that is on by default where it
+ *     measured faster: child-sum Tree-LSTM at H = 512 whose small levels (at
+ *     most 256 vertices each, at most 16384 in all) number 24 or more run
+ *     them in one cooperative launch per direction, each XCD of the device
+ *     taking the top levels of the trees rooted on it, with barriers among
+ *     that XCD's workgroups only:
+ *       CAVS_XCD_LOOP=0 / =1      never take it / take it wherever it applies
+ *                                 (H a multiple of 256, at most 16384 vertices
+ *                                 from the first small level up).
+ *     Its barriers are bounded waits: a wait that gives up records the error
+ *     that cavs_sync reports.
  *     Another is a failure-injection hook for tests of the error path:
- *       CAVS_PERSIST_SPIN=n       the persistent loop's grid barrier gives up
- *                                 after n polls (n < 0: at once) and records
+ *       CAVS_PERSIST_SPIN=n       the persistent and XCD loops' barriers give up
+ *                                 after n polls (n < 0: at once) and record
  *                                 the error that cavs_sync reports.
  *   - Errors found by kernels after a call has returned (a bounded wait that
  *     gave up) are kept by the context and returned by the next cavs_sync or

@@ -57,7 +57,8 @@ cavs_status device_errors(cavs_ctx* ctx) {
   if (!ctx->dev_err || !ctx->dev_err[0]) return CAVS_OK;
   ctx->dev_err[0] = 0;
   return fail(ctx, CAVS_ERR_HIP,
-              "a persistent level loop's grid barrier gave up waiting in an earlier call on "
+              "a persistent or XCD-local level loop's grid barrier gave up waiting in an "
+              "earlier call on "
               "this context: that call's states and gradients are invalid");
 }
 
@@ -75,6 +76,7 @@ struct WsLayout {
   size_t gpart_floats;
   size_t pack, pack_elems;                  // bf16 lazy products: packed operands
   size_t Ub, UTb;                           // bf16 copies of U and U^T
+  size_t xcd;                               // the XCD-local level loop's words and owners
 };
 
 bool lm_head(const cavs_params* p) { return p->loss == CAVS_LOSS_CE && p->C > kSmallHeadC; }
@@ -141,6 +143,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   L.dHLx = take(tr * V * H);
   L.pack_elems = (tr && !gen) ? bf_pack_elems(p, s) : 0;
   L.pack = take((L.pack_elems + 1) / 2);
+  L.xcd = take(lstm && !gen ? xcd_ws_bytes(s->V) / 4 + 1 : 0);
   const bool ubf = lstm && !gen && p->prec == CAVS_BF16;
   L.Ub = take(ubf ? 2 * H * H : 0);    // 4 H^2 bf16 values each
   L.UTb = take(ubf ? 2 * H * H : 0);
@@ -560,11 +563,16 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, lo[1], str);
     // fp32: pulled leaves were finished by the pull product
     if (n.bf || s->n_leaf_noinput > 0) lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], !n.bf, str);
-    const int ts = persist_first_level(n, lo, s->T);
+    const int tx = xcd_first_level(n, lo, s->T);
+    const int ts = tx < s->T ? tx : persist_first_level(n, lo, s->T);
     for (int t = 1; t < ts; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
     int* bar = (int*)((char*)ws + L.bar);
-    if (!lstm_fwd_persist(n, s->level_offsets, lo, ts, s->T, bar, str))
+    if (tx < s->T) {
+      if (!lstm_fwd_xcd(n, s->level_offsets, lo, tx, s->T, (char*)ws + L.xcd, str))
+        for (int t = tx; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+    } else if (!lstm_fwd_persist(n, s->level_offsets, lo, ts, s->T, bar, str)) {
       for (int t = ts; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
+    }
   } else {
     if (s->T > 1) fc_transpose(n, str);
     fc_fwd_leaf(n, lo[0], lo[1] - lo[0], str);
@@ -648,10 +656,18 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     const bool eager = T > 1 && eager_dw_enabled();
     const size_t pf = L.part_floats;
     lstm_bwd_roots(n, str);
-    int ts = eager ? T : persist_first_level(n, lo, T);
-    if (ts < tf) ts = tf;
-    int* bar = (int*)((char*)ws + L.bar);
-    if (!lstm_bwd_persist(n, s->level_offsets, lo, ts, T, bar, str)) ts = T;
+    // the XCD-local loop takes fused levels only (every child of its levels
+    // is finished in the parent's epilogue or left dL/dh below fuse_from)
+    const int tx = eager ? T : xcd_first_level(n, lo, T);
+    int ts = T;
+    if (tx < T && tf <= tx) {
+      if (lstm_bwd_xcd(n, s->level_offsets, lo, tx, T, (char*)ws + L.xcd, str)) ts = tx;
+    } else {
+      ts = eager ? T : persist_first_level(n, lo, T);
+      if (ts < tf) ts = tf;
+      int* bar = (int*)((char*)ws + L.bar);
+      if (!lstm_bwd_persist(n, s->level_offsets, lo, ts, T, bar, str)) ts = T;
+    }
     for (int t = ts - 1; t >= 0; --t) {
       const int M = lo[t + 1] - lo[t];
       if (t < tf) lstm_bwd_gates(n, lo[t], M, str);

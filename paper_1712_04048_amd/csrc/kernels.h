@@ -98,6 +98,8 @@ void lstm_bwd_level(const Net& n, int off, int M, hipStream_t s);
 // First level whose rows (and those of every level above) get their dA in
 // the parent's epilogue: levels of at most kFuseRows positions.
 constexpr int kFuseRows = 256;
+// the hidden width the weight-stationary XCD-local level loop is built for
+constexpr int kXcdWsH = 512;
 int lstm_fuse_level(const int* lo_host, int T);
 // lstm_tile.hip: LDS-tiled level products for levels of >= kTileMinRows
 // positions (needs n.UT, written by lstm_transpose_u in the same pass).
@@ -120,6 +122,15 @@ bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, i
                       hipStream_t s);
 // First level >= 1 small enough for the persistent loop (T if none).
 int persist_first_level(const Net& n, const int* lo_host, int T);
+// XCD-local small-level loop (CAVS_XCD_LOOP=1): the first level it would
+// take (T: none), its workspace, and the forward launch (false: nothing
+// suitable launched, run the levels one by one)
+int xcd_first_level(const Net& n, const int* lo_host, int T);
+size_t xcd_ws_bytes(int V);
+bool lstm_fwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
+                  hipStream_t s);
+bool lstm_bwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
+                  hipStream_t s);
 // generic.hip
 // Forward gates of positions [off, off + M) from the pre-activation parts in
 // the saved-gate rows (has_product false: none, as for leaves).

@@ -627,31 +627,41 @@ struct FwdRed {
 // besides the product (bias, pulled term, children's c) while the others
 // multiply, then finish element i = w - KW of every row tile.  Without EPI
 // (persistent loop, 64*KW threads) the contraction wavefronts finish it.
-template <int NCH, bool BF, int TR, int KW, bool EPI>
-__device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
-                                                 FwdRed<NCH, TR, KW>& R) {
+// Rows: the positions of the tile's 16*TR rows (RangeRows or ListRows).
+// COH: the children's rows may have been written earlier in the same launch
+// (the XCD-local level loop), so they are read with coherent loads.
+// WL: the weight columns of this unit tile are resident in LDS (wl: column
+// c = 16 g + r of the tile, k-contiguous, row stride WLD elements; fp32, or
+// bf16 pre-rounded); otherwise they are read from global memory.
+template <int NCH, bool BF, int TR, int KW, bool EPI, class Rows = RangeRows, bool COH = false,
+          int WLD = 0>
+__device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, const Rows& rows, int ut,
+                                                 FwdRed<NCH, TR, KW>& R,
+                                                 const void* wl = nullptr) {
   constexpr int NACC = 3 + NCH;
   auto& red = R.v;
   const int H = n.H, H4 = 4 * H;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int u0 = ut * 16;
   if (w < KW) {
-    // A rows of this lane: the children of position row0 + 16 tr + r.  An
-    // absent child (or a row past the level) reads row 0 with weight 0, so
-    // the loads are unconditional.
+    // A rows of this lane: the children of the position of tile row 16 tr + r.
+    // An absent child (or a row past the level) reads row 0 with weight 0,
+    // so the loads are unconditional.
     const float* ap[TR][NCH];
+    size_t aoff[TR][NCH];
     float am[TR][NCH];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
-      const int pa = row0 + 16 * tr + r;
+      const int pa = rows.pos(16 * tr + r);
 #pragma unroll
       for (int c = 0; c < NCH; ++c) {
-        const int cp = pa < rowend ? n.child_pos[(size_t)pa * NCH + c] : -1;
-        ap[tr][c] = n.Hs + (size_t)(cp >= 0 ? cp : 0) * H;
+        const int cp = pa >= 0 ? n.child_pos[(size_t)pa * NCH + c] : -1;
+        aoff[tr][c] = (size_t)(cp >= 0 ? cp : 0) * H;
+        ap[tr][c] = n.Hs + aoff[tr][c];
         am[tr][c] = cp >= 0 ? 1.f : 0.f;
       }
     }
+    const CohBuf hb = COH ? coh_buf(n.Hs, (size_t)n.V * H) : CohBuf{};
     const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
     const int kq = H / KW, kbeg = w * kq, kend = kbeg + kq;
     v4f acc[TR][NACC];
@@ -668,13 +678,39 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
       bf16x8 bq[BF ? 4 : 1];
     };
     const u16* utb = BF ? n.UTb + (size_t)(u0 + r) * H : nullptr;
-    auto load = [&](int k0, Frag& f) {
+    auto load_a = [&](int k0, Frag& f) {
       const int kk = k0 + 8 * gq;
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) ld8(ap[tr][c] + kk, f.a[tr][c]);
-      if constexpr (BF) {
+        for (int c = 0; c < NCH; ++c) {
+          if constexpr (COH) {
+            const float4 x = coh_ld4(hb, aoff[tr][c] + kk), y = coh_ld4(hb, aoff[tr][c] + kk + 4);
+            float* d = f.a[tr][c];
+            d[0] = x.x; d[1] = x.y; d[2] = x.z; d[3] = x.w;
+            d[4] = y.x; d[5] = y.y; d[6] = y.z; d[7] = y.w;
+          } else {
+            ld8(ap[tr][c] + kk, f.a[tr][c]);
+          }
+        }
+    };
+    auto load_b = [&](int k0, Frag& f) {
+      const int kk = k0 + 8 * gq;
+      if constexpr (WLD > 0 && BF) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          f.bq[g] = *reinterpret_cast<const bf16x8*>(static_cast<const u16*>(wl) +
+                                                     (16 * g + r) * WLD + kk);
+      } else if constexpr (WLD > 0) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float* bp = static_cast<const float*>(wl) + (16 * g + r) * WLD + kk;
+          const float4 x = *reinterpret_cast<const float4*>(bp);
+          const float4 y = *reinterpret_cast<const float4*>(bp + 4);
+          f.b[g][0] = x.x; f.b[g][1] = x.y; f.b[g][2] = x.z; f.b[g][3] = x.w;
+          f.b[g][4] = y.x; f.b[g][5] = y.y; f.b[g][6] = y.z; f.b[g][7] = y.w;
+        }
+      } else if constexpr (BF) {
 #pragma unroll
         for (int g = 0; g < 4; ++g)
           f.bq[g] = *reinterpret_cast<const bf16x8*>(utb + (size_t)g * H * H + kk);
@@ -684,6 +720,10 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
 #pragma unroll
           for (int s = 0; s < 8; ++s) f.b[g][s] = ub[(size_t)(kk + s) * H4 + g * H];
       }
+    };
+    auto load = [&](int k0, Frag& f) {
+      load_a(k0, f);
+      load_b(k0, f);
     };
     auto compute = [&](const Frag& f) {
 #pragma unroll
@@ -711,15 +751,30 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
         }
       }
     };
-    // two register buffers: loads of the next chunk overlap the current MFMAs
-    Frag fa, fb;
-    load(kbeg, fa);
-    for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
-      load(k0 + kBK, fb);
-      __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads go out before these MFMAs
-      compute(fa);
-      if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
-      compute(fb);
+    if constexpr (WLD > 0) {
+      // weights in LDS: every chunk's child rows are requested at once (one
+      // memory latency); the weight fragments are read chunk by chunk
+      constexpr int NCK = kXcdWsH / KW / kBK;
+      Frag f[NCK];
+#pragma unroll
+      for (int c = 0; c < NCK; ++c) load_a(kbeg + c * kBK, f[c]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < NCK; ++c) {
+        load_b(kbeg + c * kBK, f[c]);
+        compute(f[c]);
+      }
+    } else {
+      // two register buffers: loads of the next chunk overlap the current MFMAs
+      Frag fa, fb;
+      load(kbeg, fa);
+      for (int k0 = kbeg; k0 < kend; k0 += 2 * kBK) {
+        load(k0 + kBK, fb);
+        __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads go out before these MFMAs
+        compute(fa);
+        if (k0 + 2 * kBK < kend) load(k0 + 2 * kBK, fa);
+        compute(fb);
+      }
     }
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr)
@@ -745,15 +800,15 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
       for (int tr = 0; tr < TR; ++tr) {
         // rows past the level read its last row (unused), so the loads
         // are unconditional
-        lstm_fwd_pre<NCH>(n, min(row0 + 16 * tr + 4 * gq + i, rowend - 1), u0 + r, pre[tr]);
+        lstm_fwd_pre<NCH, COH>(n, rows.clamp(16 * tr + 4 * gq + i), u0 + r, pre[tr]);
       }
     }
     __syncthreads();
     if (w < KW) return;
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
-      const int p = row0 + 16 * tr + 4 * gq + i;
-      if (p >= rowend) continue;
+      const int p = rows.pos(16 * tr + 4 * gq + i);
+      if (p < 0) continue;
       float z[NACC];
       zsum(tr, i, z);
       lstm_fwd_fin<NCH>(n, p, u0 + r, pre[tr], z[0], z[1], z[2], z[3],
@@ -765,11 +820,12 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, int off, int M, i
     const int i = w & 3;
 #pragma unroll
     for (int tr = w >> 2; tr < TR; tr += KW / 4) {
-      const int p = row0 + 16 * tr + 4 * gq + i;
-      if (p >= rowend) continue;
+      const int p = rows.pos(16 * tr + 4 * gq + i);
+      if (p < 0) continue;
       float z[NACC];
       zsum(tr, i, z);
-      lstm_fwd_epilogue<NCH>(n, p, u0 + r, z[0], z[1], z[2], z[3], NCH == 2 ? z[NACC - 1] : 0.f);
+      lstm_fwd_epilogue<NCH, COH>(n, p, u0 + r, z[0], z[1], z[2], z[3],
+                                  NCH == 2 ? z[NACC - 1] : 0.f);
     }
   }
 }
@@ -779,7 +835,7 @@ __global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_fwd_level_sk(Net n, int 
   __shared__ FwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_fwd_sk_tile<NCH, BF, TR, KW, true>(n, off, M, rt, ut, red);
+  lstm_fwd_sk_tile<NCH, BF, TR, KW, true>(n, RangeRows{off + rt * 16 * TR, off + M}, ut, red);
 }
 
 template <int NCH, int TR, int KW = 4>
@@ -790,29 +846,60 @@ struct BwdRed {
 // One 16*TR-position x 16-column backward tile (row tile rt, column tile ut);
 // wavefront roles as in the forward tile (EPI: four epilogue wavefronts
 // that prefetch the children's saved state while the others multiply).
-template <int NCH, bool BF, int TR, int KW, bool EPI>
-__device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, int rt, int ut,
-                                                 BwdRed<NCH, TR, KW>& R) {
+// Rows, COH and WL (rows n0 .. n0+15 of U resident in LDS, row stride WLD)
+// as in the forward tile; COH also covers the dA rows of the level (written
+// by the parents' epilogues in the same launch).
+template <int NCH, bool BF, int TR, int KW, bool EPI, class Rows = RangeRows, bool COH = false,
+          int WLD = 0>
+__device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows, int ut,
+                                                 BwdRed<NCH, TR, KW>& R,
+                                                 const void* wl = nullptr) {
   constexpr int NACC = 1 + (NCH == 2 ? 2 : 0);
   auto& red = R.v;
   const int H = n.H, H4 = 4 * H, GW = n.GW;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
-  const int row0 = off + rt * 16 * TR, rowend = off + M;
   const int n0 = ut * 16;
   if (w < KW) {
     // rows past the level read its last row: their sums are never used
     const float* da[TR];
+    size_t daoff[TR];
 #pragma unroll
-    for (int tr = 0; tr < TR; ++tr) da[tr] = n.dA + (size_t)min(row0 + 16 * tr + r, rowend - 1) * GW;
-    const float* ub = n.U + (size_t)(n0 + r) * H4;   // row n0 + r of U: B^T[n][k]
+    for (int tr = 0; tr < TR; ++tr) {
+      daoff[tr] = (size_t)rows.clamp(16 * tr + r) * GW;
+      da[tr] = n.dA + daoff[tr];
+    }
+    const CohBuf ab = COH ? coh_buf(n.dA, (size_t)n.V * GW) : CohBuf{};
+    auto lda = [&](int tr, int col, float (&v)[8]) {
+      if constexpr (COH) {
+        const float4 x = coh_ld4(ab, daoff[tr] + col), y = coh_ld4(ab, daoff[tr] + col + 4);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+        v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+      } else {
+        ld8(da[tr] + col, v);
+      }
+    };
+    // the U fragment: row n0 + r of U at columns col .. col+7
+    auto ldu = [&](int col, float (&v)[8], bf16x8& q) {
+      if constexpr (WLD > 0 && BF) {
+        q = *reinterpret_cast<const bf16x8*>(static_cast<const u16*>(wl) + r * WLD + col);
+      } else if constexpr (WLD > 0) {
+        const float* bp = static_cast<const float*>(wl) + r * WLD + col;
+        const float4 x = *reinterpret_cast<const float4*>(bp);
+        const float4 y = *reinterpret_cast<const float4*>(bp + 4);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+        v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+      } else if constexpr (BF) {
+        q = *reinterpret_cast<const bf16x8*>(n.Ub + (size_t)(n0 + r) * H4 + col);
+      } else {
+        ld8(n.U + (size_t)(n0 + r) * H4 + col, v);
+      }
+    };
     v4f acc[TR][NACC];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
       for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
     // phase 1: i|o|u columns (all four blocks with one child slot)
-    // bf16: the U fragment comes pre-rounded from n.Ub (one 16-byte load)
-    const u16* ubb = BF ? n.Ub + (size_t)(n0 + r) * H4 : nullptr;
     struct F1 {
       float a[TR][8], b[BF ? 1 : 8];
       bf16x8 bq;
@@ -821,9 +908,10 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     auto load1 = [&](int c0, F1& f) {
       const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
-      for (int tr = 0; tr < TR; ++tr) ld8(da[tr] + col, f.a[tr]);
-      if constexpr (BF) f.bq = *reinterpret_cast<const bf16x8*>(ubb + col);
-      else ld8(ub + col, f.b);
+      for (int tr = 0; tr < TR; ++tr) lda(tr, col, f.a[tr]);
+      float dummy[8];
+      if constexpr (BF) ldu(col, dummy, f.bq);
+      else ldu(col, f.b, f.bq);
     };
     auto comp1 = [&](const F1& f) {
 #pragma unroll
@@ -851,11 +939,12 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
         const int col = c0 + 8 * gq;
 #pragma unroll
         for (int tr = 0; tr < TR; ++tr) {
-          ld8(da[tr] + H + col, f.a0[tr]);
-          ld8(da[tr] + 4 * H + col, f.a1[tr]);
+          lda(tr, H + col, f.a0[tr]);
+          lda(tr, 4 * H + col, f.a1[tr]);
         }
-        if constexpr (BF) f.bq = *reinterpret_cast<const bf16x8*>(ubb + H + col);
-        else ld8(ub + H + col, f.b);
+        float dummy[8];
+        if constexpr (BF) ldu(H + col, dummy, f.bq);
+        else ldu(H + col, f.b, f.bq);
       };
       auto comp2 = [&](const F2& f) {
 #pragma unroll
@@ -929,15 +1018,15 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
       for (int tr = 0; tr < TR; ++tr) {
         // rows past the level read its last row (unused), so the loads
         // are unconditional
-        lstm_bwd_pre<NCH>(n, min(row0 + 16 * tr + 4 * gq + i, rowend - 1), n0 + r, pre[tr]);
+        lstm_bwd_pre<NCH, COH>(n, rows.clamp(16 * tr + 4 * gq + i), n0 + r, pre[tr]);
       }
     }
     __syncthreads();
     if (w < KW) return;
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
-      const int p = row0 + 16 * tr + 4 * gq + i;
-      if (p >= rowend) continue;
+      const int p = rows.pos(16 * tr + 4 * gq + i);
+      if (p < 0) continue;
       float z[NACC];
       zsum(tr, i, z);
       lstm_bwd_fin<NCH>(n, n0 + r, pre[tr], z[0], NCH == 2 ? z[1] : 0.f,
@@ -948,12 +1037,12 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, int off, int M, i
     const int i = w & 3;
 #pragma unroll
     for (int tr = w >> 2; tr < TR; tr += KW / 4) {
-      const int p = row0 + 16 * tr + 4 * gq + i;
-      if (p >= rowend) continue;
+      const int p = rows.pos(16 * tr + 4 * gq + i);
+      if (p < 0) continue;
       float z[NACC];
       zsum(tr, i, z);
-      lstm_bwd_scatter<NCH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f,
-                            NCH == 2 ? z[NACC - 1] : 0.f);
+      lstm_bwd_scatter<NCH, COH>(n, p, n0 + r, z[0], NCH == 2 ? z[1] : 0.f,
+                                 NCH == 2 ? z[NACC - 1] : 0.f);
     }
   }
 }
@@ -963,7 +1052,7 @@ __global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_bwd_level_sk(Net n, int 
   __shared__ BwdRed<NCH, TR, KW> red;
   int rt, ut;
   xcd_tile(n.H / 16, rt, ut);
-  lstm_bwd_sk_tile<NCH, BF, TR, KW, true>(n, off, M, rt, ut, red);
+  lstm_bwd_sk_tile<NCH, BF, TR, KW, true>(n, RangeRows{off + rt * 16 * TR, off + M}, ut, red);
 }
 
 // ----------------------------------------------- persistent small-level loop
@@ -1038,7 +1127,8 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_persist(Net n, const int* lo, 
     const int off = lo[t], M = lo[t + 1] - off;
     const int tiles = cdiv_dev(M, 16) * ut;
     for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-      lstm_fwd_sk_tile<NCH, BF, 1, 4, false>(n, off, M, tile / ut, tile % ut, red);
+      lstm_fwd_sk_tile<NCH, BF, 1, 4, false>(n, RangeRows{off + tile / ut * 16, off + M}, tile % ut,
+                                             red);
       __syncthreads();
     }
     if (t + 1 < t1) grid_sync(bar, epoch);
@@ -1057,7 +1147,8 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_persist(Net n, const int* lo, 
     const int off = lo[t], M = lo[t + 1] - off;
     const int tiles = cdiv_dev(M, 16) * ut;
     for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-      lstm_bwd_sk_tile<NCH, BF, 1, 4, false>(n, off, M, tile / ut, tile % ut, red);
+      lstm_bwd_sk_tile<NCH, BF, 1, 4, false>(n, RangeRows{off + tile / ut * 16, off + M}, tile % ut,
+                                             red);
       __syncthreads();
     }
     if (t > t0) grid_sync(bar, epoch);
@@ -1243,6 +1334,392 @@ bool launch_persist(const char* name, const void* fn, const Net& n, const int* l
 
 }  // namespace
 
+// ------------------------------------------ XCD-local small-level loop
+// The small levels near the roots in one launch per direction, without
+// grid-wide barriers.  The graphs of a batch are independent, so the top of
+// every tree (its positions in the suffix of small levels) is given to one
+// of the eight XCDs, and the workgroups running on an XCD (its hardware id
+// read from XCC_ID) process only their XCD's positions, level by level,
+// separated by a barrier among themselves.  Everything one level writes and
+// the next reads then stays inside one XCD: its CUs share one L2, stores
+// reach it through the write-through L1, and the readers' device-scope
+// loads (sc1) miss their own L1 and read it.  No level needs the L2
+// write-back and invalidation that make a grid-wide barrier cost as much as
+// a kernel launch.
+constexpr int kXcdRows = 256;          // levels of at most this many positions
+constexpr int kXcdMaxSuffix = 16384;   // suffix positions the owner kernel holds
+constexpr int kXcdWords = 1024;        // barrier words
+constexpr int kXcdSpin = 1 << 21;      // bounded waits (polls) before giving up
+
+// Barrier words: [0] grid arrivals, [1] grid generation, [32 + x] the
+// ticket (rank counter) of XCD x, [64 + 32 x] arrivals at XCD x's barrier,
+// [64 + 32 x + 16] its generation.  Counters return to zero by themselves
+// (the last arriver resets them); the owner kernel zeroes them first.
+struct XcdLoop {
+  int* w;
+  const unsigned char* own;   // owner XCD of suffix position p (indexed p - base)
+  int base;
+  int spin;
+  int* host_err;              // mapped pinned error word of the context (may be null)
+};
+
+__device__ __forceinline__ int xcc_id() {
+  int v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 7;
+}
+
+__device__ __forceinline__ int ld_sc1(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void xcd_gave_up(const XcdLoop& xl) {
+  atomicOr(&xl.w[2], 1);
+  if (xl.host_err) __hip_atomic_store(xl.host_err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Owner of every suffix position: the rank of its tree's root among the
+// suffix roots (in position order), modulo 8.  Roots by pointer doubling in
+// LDS (a parent always lies in the suffix: it is on a higher level).  One
+// workgroup; also clears the barrier words.
+__global__ void __launch_bounds__(1024) k_xcd_owner(const int* __restrict__ parent_pos, int base,
+                                                    int S, unsigned char* __restrict__ own,
+                                                    int* __restrict__ words) {
+  __shared__ short ra[kXcdMaxSuffix], rb[kXcdMaxSuffix];
+  __shared__ int wcnt[16], changed[2];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  for (int i = tid; i < kXcdWords; i += 1024) words[i] = 0;
+  for (int q = tid; q < S; q += 1024) {
+    const int pp = parent_pos[base + q];
+    ra[q] = (short)(pp >= base && pp < base + S ? pp - base : q);
+  }
+  if (tid < 2) changed[tid] = 0;
+  __syncthreads();
+  short* a = ra;
+  short* b = rb;
+  for (int it = 0; it < 16; ++it) {   // 2^15 > kXcdMaxSuffix: enough rounds
+    int ch = 0;
+    for (int q = tid; q < S; q += 1024) {
+      const short v = a[a[q]];
+      b[q] = v;
+      ch |= v != a[q];
+    }
+    if (ch) changed[it & 1] = 1;
+    __syncthreads();
+    const bool more = changed[it & 1] != 0;
+    if (tid == 0) changed[(it + 1) & 1] = 0;
+    short* t = a;
+    a = b;
+    b = t;
+    __syncthreads();
+    if (!more) break;
+  }
+  // ranks of the roots (a[q] == q) in position order: each thread a
+  // contiguous chunk, a block-wide exclusive scan of the chunk counts
+  const int per = (S + 1023) / 1024, q0 = min(S, tid * per), q1 = min(S, q0 + per);
+  int c = 0;
+  for (int q = q0; q < q1; ++q) c += a[q] == q;
+  int incl = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wcnt[wv] = incl;
+  __syncthreads();
+  int rank = incl - c;
+  for (int k = 0; k < wv; ++k) rank += wcnt[k];
+  for (int q = q0; q < q1; ++q)
+    if (a[q] == q) b[q] = (short)(rank++);
+  __syncthreads();
+  for (int q = tid; q < S; q += 1024) own[q] = (unsigned char)(b[a[q]] & 7);
+}
+
+// Group formation: rank of this workgroup among those on its XCD (s[1],
+// known at once), then, after a one-time grid-wide arrival, their number
+// (s[2]: every ticket is final).  Work that needs only the rank can run
+// between the two halves.
+__device__ __forceinline__ void xcd_arrive(const XcdLoop& xl, int* s) {
+  if (threadIdx.x == 0) {
+    const int x = xcc_id();
+    const int rank = atomicAdd(&xl.w[32 + x], 1);
+    const int g0 = ld_sc1(&xl.w[1]);
+    __builtin_amdgcn_s_waitcnt(0);
+    const int old = atomicAdd(&xl.w[0], 1);
+    if (old == (int)gridDim.x - 1) {
+      atomicExch(&xl.w[0], 0);
+      __builtin_amdgcn_s_waitcnt(0);
+      atomicAdd(&xl.w[1], 1);
+      s[5] = -1;   // released the grid: nothing to wait for
+    } else {
+      s[5] = g0;
+    }
+    s[0] = x;
+    s[1] = rank;
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void xcd_wait(const XcdLoop& xl, int* s) {
+  if (threadIdx.x == 0) {
+    const int x = s[0], g0 = s[5];
+    if (g0 != -1) {
+      int it = 0;
+      while (ld_sc1(&xl.w[1]) == g0) {
+        if (++it > xl.spin || ld_sc1(&xl.w[2])) {
+          xcd_gave_up(xl);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    s[2] = ld_sc1(&xl.w[32 + x]);
+    s[3] = ld_sc1(&xl.w[64 + 32 * x + 16]);
+    s[4] = ld_sc1(&xl.w[2]);
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void xcd_begin(const XcdLoop& xl, int* s) {
+  xcd_arrive(xl, s);
+  xcd_wait(xl, s);
+}
+
+// Barrier among the gs workgroups of XCD x; s[3] is the generation this
+// workgroup waits to see change, s[4] set when a wait gave up.  touch()
+// runs between arriving and leaving: loads of the next level's static
+// operands (schedule rows, saved state), issued while the barrier is
+// pending so that the next tile finds them in cache.
+template <class Touch>
+__device__ __forceinline__ void xcd_sync(const XcdLoop& xl, int x, int gs, int* s, Touch&& touch) {
+  __builtin_amdgcn_s_waitcnt(0);   // this wavefront's stores have reached the L2
+  __syncthreads();
+  int* cnt = &xl.w[64 + 32 * x];
+  int* gen = cnt + 16;
+  bool last = false;
+  if (threadIdx.x == 0) {
+    last = atomicAdd(cnt, 1) == gs - 1;
+    if (last) {
+      atomicExch(cnt, 0);
+      __builtin_amdgcn_s_waitcnt(0);
+      atomicAdd(gen, 1);
+    }
+  }
+  const float keep = touch();
+  if (threadIdx.x == 0) {
+    const int g0 = s[3];
+    if (!last) {
+      int it = 0;
+      while (ld_sc1(gen) == g0) {
+        if (++it > xl.spin || ld_sc1(&xl.w[2])) {
+          xcd_gave_up(xl);
+          s[4] = 1;
+          break;
+        }
+      }
+    }
+    s[3] = g0 + 1;
+  }
+  if (keep == 1.5e-44f) s[6] = 1;   // never true; keeps the touch loads
+  __syncthreads();
+}
+
+__device__ __forceinline__ void xcd_sync(const XcdLoop& xl, int x, int gs, int* s) {
+  xcd_sync(xl, x, gs, s, [] { return 0.f; });
+}
+
+// The static operands of the first row tile of a level (positions
+// base + lst[0 .. m)) for unit / column tile u0, as the split-K tiles with
+// KW = 4 read them: the contraction wavefronts' child positions, the
+// epilogue wavefronts' prefetch (forward: lstm_fwd_pre; backward:
+// lstm_bwd_pre, whose dL/dc word may be stale here and is read again
+// coherently by the tile).
+template <int NCH, bool FWD>
+__device__ __forceinline__ float xcd_touch(const Net& n, const short* lst, int m, int base, int u0) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, gq = lane >> 4, r = lane & 15;
+  if (m <= 0) return 0.f;
+  float acc = 0.f;
+  if (w < 4) {
+    const int p = base + lst[min(r, m - 1)];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc += (float)n.child_pos[(size_t)p * NCH + c];
+  } else if (w < 8) {
+    const int p = base + lst[min(4 * gq + (w - 4), m - 1)];
+    if constexpr (FWD) {
+      FwdPre<NCH> q;
+      lstm_fwd_pre<NCH, false>(n, p, u0 + r, q);
+      acc += q.bi + q.pi + q.fb + q.cc[0];
+    } else {
+      BwdPre<NCH> e;
+      lstm_bwd_pre<NCH, false>(n, p, u0 + r, e);
+      acc += e.q[0].ig + e.q[0].c + e.q[0].ck[0] + e.q[0].lg;
+    }
+  }
+  return acc;
+}
+
+// This XCD's positions of the level [l0, l1) (offsets from l0, in order)
+// into lst and their number into *m; wavefront 0.
+__device__ __forceinline__ void xcd_level_list(const XcdLoop& xl, int x, int l0, int l1,
+                                               short* lst, int* m) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int cnt = 0;
+    for (int i0 = l0; i0 < l1; i0 += 64) {
+      const int p = i0 + lane;
+      const bool mine = p < l1 && xl.own[p - xl.base] == x;
+      const unsigned long long bal = __ballot(mine);
+      if (mine) lst[cnt + __popcll(bal & ((1ull << lane) - 1ull))] = (short)(p - l0);
+      cnt += __popcll(bal);
+    }
+    if (lane == 0) *m = cnt;
+  }
+}
+
+template <int NCH, bool BF>
+__global__ void __launch_bounds__(768) k_lstm_fwd_xcd(Net n, const int* lo, int t0, int t1,
+                                                      XcdLoop xl) {
+  __shared__ FwdRed<NCH, 1, 8> red;
+  __shared__ short lst[2][kXcdRows];
+  __shared__ int s[8];
+  __shared__ int sm[2];
+  xcd_begin(xl, s);
+  const int x = s[0], rank = s[1], gs = s[2];
+  const int nut = n.H / 16;
+  xcd_level_list(xl, x, lo[t0], lo[t0 + 1], lst[0], &sm[0]);
+  __syncthreads();
+  for (int t = t0; t < t1 && !s[4]; ++t) {
+    const int cur = (t - t0) & 1, m = sm[cur], base = lo[t];
+    const int jobs = cdiv_dev(m, 16) * nut;
+    for (int j = rank; j < jobs; j += gs) {
+      const int rt = j / nut;
+      lstm_fwd_sk_tile<NCH, BF, 1, 8, true, ListRows, true>(
+          n, ListRows{lst[cur] + 16 * rt, m - 16 * rt, base}, j % nut, red);
+      __syncthreads();
+    }
+    if (t + 1 < t1) xcd_level_list(xl, x, lo[t + 1], lo[t + 2], lst[cur ^ 1], &sm[cur ^ 1]);
+    // the last barrier also tells every workgroup of the XCD that the
+    // ticket (read at the start) can be cleared
+    xcd_sync(xl, x, gs, s);
+  }
+  if (threadIdx.x == 0 && rank == 0 && !s[4]) atomicExch(&xl.w[32 + x], 0);
+}
+
+// Weight-stationary variant: with H = 16 x (workgroups per XCD), workgroup
+// `rank` of an XCD owns unit tile `rank` for the whole loop and keeps that
+// tile's weight columns (H x 64: four gates x 16 units) in LDS, so a level
+// reads only the children's rows; every workgroup of an XCD runs every row
+// tile of its XCD's positions at its unit tile.
+template <bool BF>
+struct WsLds {
+  static constexpr int LD = kXcdWsH + (BF ? 8 : 4);   // padded row: conflict-free 16-byte reads
+  static constexpr int BYTES = 64 * LD * (BF ? 2 : 4);
+};
+
+template <int NCH, bool BF>
+__global__ void __launch_bounds__(512) k_lstm_fwd_xcd_ws(Net n, const int* lo, int t0, int t1,
+                                                         XcdLoop xl) {
+  using WS = WsLds<BF>;
+  __shared__ __attribute__((aligned(16))) unsigned char wl[WS::BYTES];
+  __shared__ FwdRed<NCH, 1, 4> red;
+  __shared__ short lst[2][kXcdRows];
+  __shared__ int s[8];
+  __shared__ int sm[2];
+  xcd_arrive(xl, s);
+  const int H = n.H, ut = min(s[1], H / 16 - 1);
+  // this unit tile's weight columns (while the grid-wide arrival completes):
+  // column c = 16 g + r is column g H + 16 ut + r of U
+  for (int i = threadIdx.x; i < 64 * (H / 4); i += 512) {
+    const int c = i / (H / 4), k4 = 4 * (i % (H / 4));
+    const int col = (c >> 4) * H + 16 * ut + (c & 15);
+    if constexpr (BF) {
+      const u16* src = n.UTb + (size_t)col * H + k4;
+      u16* d = reinterpret_cast<u16*>(wl) + c * WS::LD + k4;
+      d[0] = src[0]; d[1] = src[1]; d[2] = src[2]; d[3] = src[3];
+    } else {   // n.UT: U transposed, k-contiguous (written earlier in the pass)
+      *reinterpret_cast<float4*>(reinterpret_cast<float*>(wl) + c * WS::LD + k4) =
+          ldg4(n.UT + (size_t)col * H + k4);
+    }
+  }
+  xcd_wait(xl, s);
+  const int x = s[0], rank = s[1], gs = s[2];
+  if (gs * 16 != H) {   // the host launches this only when it holds; record, do nothing
+    if (threadIdx.x == 0) xcd_gave_up(xl);
+    return;
+  }
+  xcd_level_list(xl, x, lo[t0], lo[t0 + 1], lst[0], &sm[0]);
+  __syncthreads();
+  for (int t = t0; t < t1 && !s[4]; ++t) {
+    const int cur = (t - t0) & 1, m = sm[cur], base = lo[t];
+    for (int rt = 0; rt < cdiv_dev(m, 16); ++rt) {
+      lstm_fwd_sk_tile<NCH, BF, 1, 4, true, ListRows, true, WS::LD>(
+          n, ListRows{lst[cur] + 16 * rt, m - 16 * rt, base}, ut, red, wl);
+      __syncthreads();
+    }
+    if (t + 1 < t1) xcd_level_list(xl, x, lo[t + 1], lo[t + 2], lst[cur ^ 1], &sm[cur ^ 1]);
+    __syncthreads();
+    const int nb = t + 1 < t1 ? lo[t + 1] : 0, nm = t + 1 < t1 ? sm[cur ^ 1] : 0;
+    xcd_sync(xl, x, gs, s,
+             [&] { return xcd_touch<NCH, true>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
+  }
+  if (threadIdx.x == 0 && rank == 0 && !s[4]) atomicExch(&xl.w[32 + x], 0);
+}
+
+template <bool BF>
+struct WsLdsB {
+  static constexpr int LD = 4 * kXcdWsH + (BF ? 8 : 4);   // rows n0 .. n0+15 of U, padded
+  static constexpr int BYTES = 16 * LD * (BF ? 2 : 4);
+};
+
+// Backward, top level first: workgroup `rank` of an XCD owns output column
+// tile `rank` (rows 16 rank .. 16 rank + 15 of U resident in LDS) and runs
+// every row tile of its XCD's positions of a level; each child's dA (or,
+// below the loop, its dL/dh) is finished in the epilogue.
+template <int NCH, bool BF>
+__global__ void __launch_bounds__(512) k_lstm_bwd_xcd_ws(Net n, const int* lo, int t0, int t1,
+                                                         XcdLoop xl) {
+  using WS = WsLdsB<BF>;
+  __shared__ __attribute__((aligned(16))) unsigned char wl[WS::BYTES];
+  __shared__ BwdRed<NCH, 1, 4> red;
+  __shared__ short lst[2][kXcdRows];
+  __shared__ int s[8];
+  __shared__ int sm[2];
+  xcd_arrive(xl, s);
+  const int H = n.H, H4 = 4 * H, ut = min(s[1], H / 16 - 1);
+  for (int i = threadIdx.x; i < 16 * (H4 / 4); i += 512) {
+    const int row = i / (H4 / 4), c4 = 4 * (i % (H4 / 4));
+    const size_t src = (size_t)(16 * ut + row) * H4 + c4;
+    if constexpr (BF) {
+      u16* d = reinterpret_cast<u16*>(wl) + row * WS::LD + c4;
+      d[0] = n.Ub[src]; d[1] = n.Ub[src + 1]; d[2] = n.Ub[src + 2]; d[3] = n.Ub[src + 3];
+    } else {
+      *reinterpret_cast<float4*>(reinterpret_cast<float*>(wl) + row * WS::LD + c4) = ldg4(n.U + src);
+    }
+  }
+  xcd_wait(xl, s);
+  const int x = s[0], rank = s[1], gs = s[2];
+  if (gs * 16 != H) {
+    if (threadIdx.x == 0) xcd_gave_up(xl);
+    return;
+  }
+  xcd_level_list(xl, x, lo[t1 - 1], lo[t1], lst[0], &sm[0]);
+  __syncthreads();
+  for (int t = t1 - 1; t >= t0 && !s[4]; --t) {
+    const int cur = (t1 - 1 - t) & 1, m = sm[cur], base = lo[t];
+    for (int rt = 0; rt < cdiv_dev(m, 16); ++rt) {
+      lstm_bwd_sk_tile<NCH, BF, 1, 4, true, ListRows, true, WS::LD>(
+          n, ListRows{lst[cur] + 16 * rt, m - 16 * rt, base}, ut, red, wl);
+      __syncthreads();
+    }
+    if (t > t0) xcd_level_list(xl, x, lo[t - 1], lo[t], lst[cur ^ 1], &sm[cur ^ 1]);
+    __syncthreads();
+    const int nb = t > t0 ? lo[t - 1] : 0, nm = t > t0 ? sm[cur ^ 1] : 0;
+    xcd_sync(xl, x, gs, s,
+             [&] { return xcd_touch<NCH, false>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
+  }
+  if (threadIdx.x == 0 && rank == 0 && !s[4]) atomicExch(&xl.w[32 + x], 0);
+}
+
 int persist_first_level(const Net& n, const int* lo_host, int T) {
   if (!persist_enabled() || n.H % 256 != 0) return T;
   for (int t = 1; t < T; ++t)
@@ -1261,6 +1738,90 @@ bool lstm_fwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, i
   if (n.N == 2) return n.bf ? CAVS_FP(2, true) : CAVS_FP(2, false);
   return n.bf ? CAVS_FP(1, true) : CAVS_FP(1, false);
 #undef CAVS_FP
+}
+
+// On by default where it measured faster than per-level launches: weights
+// resident in LDS and a long suffix of small levels (each level then costs
+// a tile and an XCD barrier instead of a launch, against a fixed start of
+// about 10 us).  CAVS_XCD_LOOP=1 takes it wherever it applies, =0 never.
+constexpr int kXcdMinLevels = 24;
+
+int xcd_mode() {
+  const char* e = getenv("CAVS_XCD_LOOP");
+  return e && e[0] ? (e[0] == '0' ? 0 : 1) : -1;
+}
+
+int xcd_first_level(const Net& n, const int* lo_host, int T) {
+  const int mode = xcd_mode();
+  if (mode == 0 || n.H % 256 != 0 || (n.H / 8) % 64 != 0) return T;
+  if ((size_t)n.V * n.GW >= (1u << 29)) return T;   // 32-bit offsets of the coherent loads
+  for (int t = 1; t < T; ++t)
+    if (lo_host[t + 1] - lo_host[t] <= kXcdRows) {
+      if (n.V - lo_host[t] > kXcdMaxSuffix) return T;
+      for (int u = t + 1; u < T; ++u)   // every level of the loop fits its position lists
+        if (lo_host[u + 1] - lo_host[u] > kXcdRows) return T;
+      if (mode < 0 && (T - t < kXcdMinLevels || n.H != kXcdWsH)) return T;
+      return t;
+    }
+  return T;
+}
+
+size_t xcd_ws_bytes(int V) { return (size_t)kXcdWords * 4 + (size_t)V; }
+
+namespace {
+
+template <int NCH, bool BF>
+const void* xcd_kernel(bool fwd, bool ws) {
+  if (fwd) return ws ? reinterpret_cast<const void*>(&k_lstm_fwd_xcd_ws<NCH, BF>)
+                     : reinterpret_cast<const void*>(&k_lstm_fwd_xcd<NCH, BF>);
+  return ws ? reinterpret_cast<const void*>(&k_lstm_bwd_xcd_ws<NCH, BF>) : nullptr;
+}
+
+// Owner kernel, then the cooperative launch of the forward or backward loop
+// over levels [t0, T); false when none could be launched.
+bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t0, int T,
+                void* xws, hipStream_t s) {
+  if (t0 >= T) return true;
+  int* words = (int*)xws;
+  unsigned char* own = (unsigned char*)xws + (size_t)kXcdWords * 4;
+  const int base = lo_host[t0], S = n.V - base;
+  int dev = 0, ncu = 0, per = 0, coop = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop)
+    return false;
+  const int G = ncu / 8 * 8;   // one workgroup per CU, the same number on every XCD
+  // weight-stationary: one unit (column) tile per workgroup of an XCD
+  const bool ws = n.H == kXcdWsH && G / 8 * 16 == n.H;
+  if (!ws && xcd_mode() < 0) return false;   // the default takes only the weight-stationary loop
+  const void* fn = n.N == 2 ? (n.bf ? xcd_kernel<2, true>(fwd, ws) : xcd_kernel<2, false>(fwd, ws))
+                            : (n.bf ? xcd_kernel<1, true>(fwd, ws) : xcd_kernel<1, false>(fwd, ws));
+  const int threads = ws ? 512 : 768;
+  if (!fn || G < 8 ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, threads, 0) != hipSuccess || per < 1)
+    return false;
+  CAVS_LAUNCH("k_xcd_owner", k_xcd_owner, dim3(1), dim3(1024), 0, s, n.parent_pos, base, S, own,
+              words);
+  int spin = kXcdSpin;
+  if (const char* e = getenv("CAVS_PERSIST_SPIN")) spin = atoi(e);
+  XcdLoop xl{words, own, base, spin, t_active_ctx ? t_active_ctx->dev_err_dev : nullptr};
+  int a0 = t0, a1 = T;
+  void* args[] = {(void*)&n, (void*)&lo, (void*)&a0, (void*)&a1, (void*)&xl};
+  const char* name = fwd ? (ws ? "k_lstm_fwd_xcd_ws" : "k_lstm_fwd_xcd") : "k_lstm_bwd_xcd_ws";
+  TimedScope ts(name, s, lo_host[t0], lo_host[T] - lo_host[t0], /*bracket=*/true);
+  return hipLaunchCooperativeKernel(fn, dim3(G), dim3(threads), args, 0, s) == hipSuccess;
+}
+
+}  // namespace
+
+bool lstm_fwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
+                  hipStream_t s) {
+  return xcd_launch(true, n, lo, lo_host, t0, T, xws, s);
+}
+
+bool lstm_bwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
+                  hipStream_t s) {
+  return xcd_launch(false, n, lo, lo_host, t0, T, xws, s);
 }
 
 bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,

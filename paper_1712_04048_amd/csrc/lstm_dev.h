@@ -21,11 +21,37 @@ struct FwdPre {
   int cp[NCH], v, pulled;
 };
 
+// Loads of rows that other workgroups of the same launch wrote (the
+// XCD-local level loop): device-scope buffer loads (sc1), which miss the
+// CU's L1 and read the XCD's L2, where the writers' stores have landed.
+// Offsets are 32-bit: the buffers hold fewer than 2^29 floats (checked on
+// the host before such a launch).
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit elements
+constexpr int kLoadSc1 = 1 << 4;         // cache policy: device scope
+struct CohBuf {
+  __amdgpu_buffer_rsrc_t rs;
+};
+__device__ __forceinline__ CohBuf coh_buf(const float* base, size_t floats) {
+  const size_t bytes = floats * 4;
+  return CohBuf{__builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0,
+                                                   (int)(bytes < 0x7fffffffu ? bytes : 0x7fffffffu),
+                                                   kRsrcWord3)};
+}
+__device__ __forceinline__ float4 coh_ld4(const CohBuf& b, size_t idx) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(b.rs, (int)(idx * 4), 0,
+                                                                         kLoadSc1));
+}
+__device__ __forceinline__ float coh_ld1(const CohBuf& b, size_t idx) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(b.rs, (int)(idx * 4), 0,
+                                                                       kLoadSc1));
+}
+
 // Every load is unconditional (an absent child reads row 0, a position that
 // pulls nothing its own unused row of P; both are masked by selects): a
 // loaded value merged with a constant on a branch makes the compiler wait
-// for that load on its own.
-template <int NCH>
+// for that load on its own.  COH: the children's c rows may have been
+// written by this launch (coherent loads).
+template <int NCH, bool COH = false>
 __device__ __forceinline__ void lstm_fwd_pre(const Net& n, int p, int j, FwdPre<NCH>& q) {
   const int H = n.H;
   const int pr = n.pull_pos[p];
@@ -39,8 +65,14 @@ __device__ __forceinline__ void lstm_fwd_pre(const Net& n, int p, int j, FwdPre<
   const float pi = Pp[G_I * H + j], po = Pp[G_O * H + j], pu = Pp[G_U * H + j];
   const float pf = Pp[G_F * H + j];
   float cc[NCH];
+  if constexpr (COH) {
+    const CohBuf cb = coh_buf(n.Cs, (size_t)n.V * H);
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) cc[k] = n.Cs[(size_t)max(cp[k], 0) * H + j];
+    for (int k = 0; k < NCH; ++k) cc[k] = coh_ld1(cb, (size_t)max(cp[k], 0) * H + j);
+  } else {
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) cc[k] = n.Cs[(size_t)max(cp[k], 0) * H + j];
+  }
   q.pulled = pr >= 0;
   q.bi = bi;
   q.bo = bo;
@@ -105,11 +137,11 @@ __device__ __forceinline__ void lstm_fwd_fin(const Net& n, int p, int j, const F
   if (n.c_out) n.c_out[(size_t)q.v * H + j] = c;
 }
 
-template <int NCH>
+template <int NCH, bool COH = false>
 __device__ __forceinline__ void lstm_fwd_epilogue(const Net& n, int p, int j, float zi, float zo,
                                                   float zu, float zf0, float zf1) {
   FwdPre<NCH> q;
-  lstm_fwd_pre<NCH>(n, p, j, q);
+  lstm_fwd_pre<NCH, COH>(n, p, j, q);
   lstm_fwd_fin<NCH>(n, p, j, q, zi, zo, zu, zf0, zf1);
 }
 
@@ -301,12 +333,14 @@ __device__ __forceinline__ void lstm_gates_elem(const Net& n, int p, int j, floa
 // The same reads with every load unconditional (absent children read row
 // 0 and are masked by selects; see lstm_fwd_pre), including dL/dc from the
 // parent, for the small levels' fused epilogue.
-template <int NCH>
+// COH: dL/dc from the parent may have been written in the same launch.
+template <int NCH, bool COH = false>
 __device__ __forceinline__ void lstm_gates_pre_all(const Net& n, int p, int j, GatePre<NCH>& q) {
   const int H = n.H;
   const float* g = n.Gs + (size_t)p * n.GW;
   q.lg = n.dHL[(size_t)p * H + j];
-  q.gcin = n.dCp[(size_t)p * H + j];
+  if constexpr (COH) q.gcin = coh_ld1(coh_buf(n.dCp, (size_t)n.V * H), (size_t)p * H + j);
+  else q.gcin = n.dCp[(size_t)p * H + j];
   q.ig = g[j];
   q.og = g[2 * H + j];
   q.ug = g[3 * H + j];
@@ -340,7 +374,7 @@ struct BwdPre {
   int cp[NCH];
 };
 
-template <int NCH>
+template <int NCH, bool COH = false>
 __device__ __forceinline__ void lstm_bwd_pre(const Net& n, int p, int col, BwdPre<NCH>& e) {
   int cp[NCH];
 #pragma unroll
@@ -349,7 +383,7 @@ __device__ __forceinline__ void lstm_bwd_pre(const Net& n, int p, int col, BwdPr
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     e.cp[k] = cp[k];
-    lstm_gates_pre_all<NCH>(n, cp[k] >= n.fuse_from ? cp[k] : 0, col, e.q[k]);
+    lstm_gates_pre_all<NCH, COH>(n, cp[k] >= n.fuse_from ? cp[k] : 0, col, e.q[k]);
   }
 }
 
@@ -366,13 +400,29 @@ __device__ __forceinline__ void lstm_bwd_fin(const Net& n, int col, const BwdPre
   }
 }
 
-template <int NCH>
+template <int NCH, bool COH = false>
 __device__ __forceinline__ void lstm_bwd_scatter(const Net& n, int p, int col, float zh, float zf0,
                                                  float zf1) {
   BwdPre<NCH> e;
-  lstm_bwd_pre<NCH>(n, p, col, e);
+  lstm_bwd_pre<NCH, COH>(n, p, col, e);
   lstm_bwd_fin<NCH>(n, col, e, zh, zf0, zf1);
 }
+
+// Rows of a small-level tile: tile row i is position pos(i), or none (-1);
+// clamp(i) is a valid position for the unconditional loads of row i.
+// A contiguous range of a level ...
+struct RangeRows {
+  int row0, rowend;
+  __device__ int pos(int i) const { return row0 + i < rowend ? row0 + i : -1; }
+  __device__ int clamp(int i) const { return min(row0 + i, rowend - 1); }
+};
+// ... or m entries of a list of positions (relative to base) in LDS.
+struct ListRows {
+  const short* list;
+  int m, base;
+  __device__ int pos(int i) const { return i < m ? base + list[i] : -1; }
+  __device__ int clamp(int i) const { return base + list[min(i, m - 1)]; }
+};
 
 // Register-direct MFMA chunk: a[s], b[s] hold k = 8g + s of a 32-deep chunk
 // (lane group g), so eight fp32 16x16x4 steps (or one bf16 16x16x32 step
