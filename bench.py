@@ -81,6 +81,10 @@ def launch_cost(wl, nc, name, row0, rows, n_pull, with_f):
         # one launch per child slot: each carries its share of the links
         "k_tn_gemm<LdFCdW>": 2.0 * H * H * float(nc.sum()) / N,
     }
+    if name.startswith("k_tn_group<dUf, dWx"):   # dU_f and dW_x in one grid
+        return lazy["k_tn_gemm<LdDUf>"] + lazy["k_tn_gemm<LdDWx>"], 0.0
+    if name == "k_tn_group<FCdW>":                  # both child slots in one grid
+        return 2.0 * H * H * float(nc.sum()), 0.0
     if name.startswith(("k_dx_tile", "k_pull_tile")):
         return 2.0 * n_pull * D * gates_x * H, 0.0
     base = re.sub(r", (64|128)(, [48])?>", ">", name.replace("_bf", ""))

@@ -41,3 +41,22 @@ def test_step_flops_match_the_closed_form():
     assert np.all(nc[nc > 0] == 2) and n_pull == wl.V - v_int
     H, D = wl.H, wl.D
     assert total == 30.0 * H * H * v_int + 18.0 * D * H * n_pull
+
+
+def test_grouped_and_loop_launches_cost_what_their_parts_do():
+    """The grouped lazy launch (dU_f with dW_x) costs the sum of the two
+    products, and the XCD loop kernels cost what per-level launches over the
+    same rows would."""
+    wl = W.config_treelstm_sst(0, K=24)
+    s = oracle.schedule(wl.child, wl.parent, wl.pull_idx, wl.push_idx)
+    nc = (s["child_pos"] >= 0).sum(axis=1)
+    lo = s["level_offsets"]
+    n_pull = int((wl.pull_idx >= 0).sum())
+    cost = lambda k, r0=0, r=wl.V: bench.launch_cost(wl, nc, k, r0, r, n_pull, False)[0]
+    assert cost("k_tn_group<dUf, dWx64>") == (cost("k_tn_dl<LdDUf, 128, 128, 4>") +
+                                              cost("k_tn_dl<LdDWx, 64, 256, 3>")) > 0
+    t0 = len(lo) - 4
+    per_level = sum(cost("k_lstm_fwd_level_sk<2, false, 1, 8>", int(lo[t]), int(lo[t + 1] - lo[t]))
+                    for t in range(t0, len(lo) - 1))
+    assert cost("k_lstm_fwd_xcd_ws", int(lo[t0]), wl.V - int(lo[t0])) == per_level > 0
+    assert cost("k_lstm_bwd_xcd_ws", int(lo[t0]), wl.V - int(lo[t0])) == per_level
