@@ -1807,7 +1807,15 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
   XcdLoop xl{words, own, base, spin, t_active_ctx ? t_active_ctx->dev_err_dev : nullptr};
   int a0 = t0, a1 = T;
   void* args[] = {(void*)&n, (void*)&lo, (void*)&a0, (void*)&a1, (void*)&xl};
-  const char* name = fwd ? (ws ? "k_lstm_fwd_xcd_ws" : "k_lstm_fwd_xcd") : "k_lstm_bwd_xcd_ws";
+  // timing names carry the template arguments, as the kernels' symbols do
+  static const char* const kNames[3][2][2] = {
+      {{"k_lstm_fwd_xcd<1, false>", "k_lstm_fwd_xcd<1, true>"},
+       {"k_lstm_fwd_xcd<2, false>", "k_lstm_fwd_xcd<2, true>"}},
+      {{"k_lstm_fwd_xcd_ws<1, false>", "k_lstm_fwd_xcd_ws<1, true>"},
+       {"k_lstm_fwd_xcd_ws<2, false>", "k_lstm_fwd_xcd_ws<2, true>"}},
+      {{"k_lstm_bwd_xcd_ws<1, false>", "k_lstm_bwd_xcd_ws<1, true>"},
+       {"k_lstm_bwd_xcd_ws<2, false>", "k_lstm_bwd_xcd_ws<2, true>"}}};
+  const char* name = kNames[fwd ? (ws ? 1 : 0) : 2][n.N == 2 ? 1 : 0][n.bf ? 1 : 0];
   TimedScope ts(name, s, lo_host[t0], lo_host[T] - lo_host[t0], /*bracket=*/true);
   return hipLaunchCooperativeKernel(fn, dim3(G), dim3(threads), args, 0, s) == hipSuccess;
 }
