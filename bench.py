@@ -246,9 +246,13 @@ def main():
     # engine ablations (fwd+bwd per pass, HIP events): dU formed level by
     # level instead of lazily, the persistent loop for the small levels, and
     # the backward's children's gates unfused from the level products
-    def fwd_bwd_with(*variables):
-        for var in variables:
-            os.environ[var] = "1"
+    def fwd_bwd_with(*settings):
+        # each setting is NAME (set to 1) or NAME=VALUE
+        variables = []
+        for st in settings:
+            var, _, val = st.partition("=")
+            os.environ[var] = val or "1"
+            variables.append(var)
         try:
             if "CAVS_GENERIC" in variables:   # the generic engine's larger workspace
                 batch.alloc()
@@ -300,12 +304,15 @@ def main():
     ablation = None
     if lstm and not args.no_ablation:
         ablation = {"unit": "ms per forward + backward pass",
-                    "lazy_dw_per_level_launches": round(fwdbwd_ms, 4)}
+                    "default_engine": round(fwdbwd_ms, 4)}
         ablation["eager_dw_per_level"] = round(fwd_bwd_with("CAVS_EAGER_DW"), 4)
-        ablation["persistent_small_levels"] = round(fwd_bwd_with("CAVS_PERSIST"), 4)
+        ablation["persistent_small_levels"] = round(fwd_bwd_with("CAVS_PERSIST",
+                                                                 "CAVS_XCD_LOOP=0"), 4)
         ablation["unfused_backward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_BWD_GATES"), 4)
         ablation["unfused_forward_gates"] = round(fwd_bwd_with("CAVS_UNFUSED_FWD_GATES"), 4)
         ablation["two_stream_lazy_products"] = round(fwd_bwd_with("CAVS_TWO_STREAM"), 4)
+        ablation["xcd_loop_off"] = round(fwd_bwd_with("CAVS_XCD_LOOP=0"), 4)
+        ablation["xcd_loop_on"] = round(fwd_bwd_with("CAVS_XCD_LOOP=1"), 4)
         ablation["unfused_gates_both"] = round(
             fwd_bwd_with("CAVS_UNFUSED_FWD_GATES", "CAVS_UNFUSED_BWD_GATES"), 4)
         if wl.prec == W.PREC_FP32:
