@@ -152,6 +152,43 @@ def cpu_model():
     return platform.processor() or "unknown"
 
 
+def measure_achievable(torch):
+    """Rates this device reaches outside the path, as context for the
+    roofline: a 1 GiB device-to-device copy (GB/s, read + write) and an
+    8192^3 fp32 GEMM through torch's library (TFLOP/s); best of 5 each."""
+    out = {}
+    a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = None
+    for _ in range(6):
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1)
+        best = t if best is None else min(best, t)
+    out["copy_gbs"] = round(2 * a.numel() * 4 / (best * 1e-3) / 1e9, 1)
+    del a, b
+    n = 8192
+    x = torch.randn(n, n, device="cuda")
+    y = torch.randn(n, n, device="cuda")
+    torch.backends.cuda.matmul.allow_tf32 = False
+    best = None
+    for _ in range(6):
+        e0.record()
+        z = x @ y
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1)
+        best = t if best is None else min(best, t)
+    out["fp32_gemm_tflops"] = round(2.0 * n ** 3 / (best * 1e-3) / 1e12, 1)
+    del x, y, z
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl, key):
     """The oracle as it stands, in its fp32 build (the same definitions the
     GPU path computes, in the GPU path's precision; bf16 workloads emulate
@@ -242,6 +279,17 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     fwdbwd_ms = e0.elapsed_time(e1) / args.steps
+    # per-pass distribution of forward + backward (an event pair per pass)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(max(args.steps, 1))]
+    for a, b in evs:
+        a.record(stream)
+        batch.forward()
+        batch.backward()
+        b.record(stream)
+    torch.cuda.synchronize()
+    per_pass = np.array([a.elapsed_time(b) for a, b in evs])
+    fwdbwd_pct = {q: round(float(np.percentile(per_pass, q)), 4) for q in (10, 50, 90)}
 
     # engine ablations (fwd+bwd per pass, HIP events): dU formed level by
     # level instead of lazily, the persistent loop for the small levels, and
@@ -416,6 +464,18 @@ def main():
     roof["algorithmic_per_launch"] = per_launch
 
     total_flops = sum(a[2] for a in agg.values()) / args.steps
+    # the whole step against the matrix peak of its precision (every
+    # workload here is bound by its products at the roofline), and the
+    # achievable rates measured on this device for context: a plain device
+    # copy and a large library fp32 GEMM (torch), neither part of the path
+    step_peak = PEAK_BF16_TFLOPS if wl.prec == W.PREC_BF16 else PEAK_FP32_TFLOPS
+    t_roof_us = total_flops / (step_peak * 1e12) * 1e6
+    achievable = measure_achievable(torch)
+    if roof["unit"] == "TFLOP/s" and roof["peak"] == PEAK_FP32_TFLOPS:
+        roof["frac_of_library_fp32_gemm"] = round(roof["achieved"] /
+                                                  achievable["fp32_gemm_tflops"], 4)
+    elif roof["unit"] == "GB/s":
+        roof["frac_of_copy"] = round(roof["achieved"] / achievable["copy_gbs"], 4)
     loss_desc = ("softmax CE at every vertex" if wl.loss == W.LOSS_CE and
                  (wl.push_idx >= 0).all() else
                  "softmax CE at the roots" if wl.loss == W.LOSS_CE else "L2 at the roots")
@@ -441,6 +501,11 @@ def main():
         "fwd_bwd_ms": round(fwdbwd_ms, 4),
         "fwd_bwd_vertices_per_s": wl.V / (fwdbwd_ms * 1e-3),
         "whole_step_tflops": round(total_flops / (wall_ms * 1e-3) / 1e12, 2),
+        "whole_step_roofline": {"bound": "mfma", "peak_tflops": step_peak,
+                                "t_roof_us": round(t_roof_us, 1),
+                                "frac": round(t_roof_us * 1e-3 / wall_ms, 4)},
+        "fwd_bwd_ms_p10_p50_p90": [fwdbwd_pct[10], fwdbwd_pct[50], fwdbwd_pct[90]],
+        "achievable": achievable,
         "algorithmic_gflop_per_step": round(total_flops / 1e9, 3),
         "kernels": kernels,
         "levels_us": {"columns": ["rows", "fwd", "bwd_gates", "bwd_gemm"], "rows": level_table},
