@@ -49,8 +49,8 @@
  *                                 the split-K reductions.
  *     One switch chooses an engine path that is on by default where it
  *     measured faster: child-sum Tree-LSTM at H = 512 whose small levels (at
- *     most 256 vertices each, at most 16384 in all) number 24 or more run
- *     them in one cooperative launch per direction, each XCD of the device
+ *     most 256 vertices each, at most 16384 in all) number 8 or more run
+ *     them in one launch per direction (one workgroup per CU), each XCD of the device
  *     taking the top levels of the trees rooted on it, with barriers among
  *     that XCD's workgroups only:
  *       CAVS_XCD_LOOP=0 / =1      never take it / take it wherever it applies
