@@ -541,6 +541,7 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
   n.h_out = h_out;
   n.c_out = p->cell == CAVS_TREE_LSTM ? c_out : nullptr;
   const int* lo = s->level_offsets_host;
+  ctx->xcd_owner = {};
   if (n.Ub && s->T > 1) lstm_round_u(n, str);   // bf16 weight operands of the level products
   if (p->cell == CAVS_TREE_LSTM && generic_mode(p, s)) {
     lstm_transpose_u(n, str);
@@ -558,17 +559,22 @@ static cavs_status run_forward(cavs_ctx* ctx, const cavs_params* p, const cavs_s
       lstm_fwd_gates(n, lo[t], lo[t + 1] - lo[t], true, str);
     }
   } else if (p->cell == CAVS_TREE_LSTM) {
+    const int tx = xcd_first_level(n, lo, s->T);
+    void* xws = (char*)ws + L.xcd;
     if ((s->T > 1 && lstm_tile_applies(n, lo[2] - lo[1])) || pull_tile_applies(n, s->n_pull))
       lstm_transpose_u(n, str);
     pull_gemm(n, s->n_pull, s->n_inner_input > 0, lo[1], str);
     // fp32: pulled leaves were finished by the pull product
     if (n.bf || s->n_leaf_noinput > 0) lstm_fwd_leaf(n, lo[0], lo[1] - lo[0], !n.bf, str);
-    const int tx = xcd_first_level(n, lo, s->T);
     const int ts = tx < s->T ? tx : persist_first_level(n, lo, s->T);
     for (int t = 1; t < ts; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
     int* bar = (int*)((char*)ws + L.bar);
     if (tx < s->T) {
-      if (!lstm_fwd_xcd(n, s->level_offsets, lo, tx, s->T, (char*)ws + L.xcd, str))
+      // the loop's owner array depends on the schedule alone: the matching
+      // backward reuses it
+      xcd_owner(n, lo, tx, xws, str);
+      ctx->xcd_owner = {ws, n.parent_pos, lo[tx], s->V};
+      if (!lstm_fwd_xcd(n, s->level_offsets, lo, tx, s->T, xws, true, str))
         for (int t = tx; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
     } else if (!lstm_fwd_persist(n, s->level_offsets, lo, ts, s->T, bar, str)) {
       for (int t = ts; t < s->T; ++t) lstm_fwd_level(n, lo[t], lo[t + 1] - lo[t], str);
@@ -661,7 +667,10 @@ cavs_status cavs_backward(cavs_ctx* ctx, const cavs_params* p, const cavs_sched*
     const int tx = eager ? T : xcd_first_level(n, lo, T);
     int ts = T;
     if (tx < T && tf <= tx) {
-      if (lstm_bwd_xcd(n, s->level_offsets, lo, tx, T, (char*)ws + L.xcd, str)) ts = tx;
+      const auto& o = ctx->xcd_owner;
+      const bool owned = o.ws == ws && o.parent_pos == n.parent_pos && o.base == lo[tx] &&
+                         o.V == s->V;
+      if (lstm_bwd_xcd(n, s->level_offsets, lo, tx, T, (char*)ws + L.xcd, owned, str)) ts = tx;
     } else {
       ts = eager ? T : persist_first_level(n, lo, T);
       if (ts < tf) ts = tf;

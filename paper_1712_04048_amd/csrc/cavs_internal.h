@@ -33,6 +33,13 @@ struct cavs_ctx {
   hipStream_t side = nullptr;             // the two-stream ablation's second stream and its
   hipEvent_t fork_ev = nullptr;           // fork / join events (created on first use)
   hipEvent_t join_ev = nullptr;
+  // The XCD loop's owner array that the last forward left in its workspace:
+  // valid for the matching backward (same workspace, schedule and suffix).
+  struct {
+    const void* ws = nullptr;
+    const int* parent_pos = nullptr;
+    int base = -1, V = -1;
+  } xcd_owner;
 };
 
 namespace cavs {

@@ -122,15 +122,19 @@ bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, i
                       hipStream_t s);
 // First level >= 1 small enough for the persistent loop (T if none).
 int persist_first_level(const Net& n, const int* lo_host, int T);
-// XCD-local small-level loop (CAVS_XCD_LOOP=1): the first level it would
-// take (T: none), its workspace, and the forward launch (false: nothing
-// suitable launched, run the levels one by one)
+// XCD-local small-level loop: the first level it takes (T: none), its
+// workspace, the owner computation of the suffix from level t0 (also clears
+// the loop's barrier words), and the two loops (false: nothing suitable
+// launched, run the levels one by one).  With owner_ready the caller has
+// already queued xcd_owner for this suffix and workspace, ordered before the
+// loop.
 int xcd_first_level(const Net& n, const int* lo_host, int T);
 size_t xcd_ws_bytes(int V);
+void xcd_owner(const Net& n, const int* lo_host, int t0, void* xws, hipStream_t s);
 bool lstm_fwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
-                  hipStream_t s);
+                  bool owner_ready, hipStream_t s);
 bool lstm_bwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
-                  hipStream_t s);
+                  bool owner_ready, hipStream_t s);
 // generic.hip
 // Forward gates of positions [off, off + M) from the pre-activation parts in
 // the saved-gate rows (has_product false: none, as for leaves).

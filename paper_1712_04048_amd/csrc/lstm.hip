@@ -1781,11 +1781,11 @@ const void* xcd_kernel(bool fwd, bool ws) {
 // Owner kernel, then the launch of the forward or backward loop
 // over levels [t0, T); false when none could be launched.
 bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t0, int T,
-                void* xws, hipStream_t s) {
+                void* xws, bool owner_ready, hipStream_t s) {
   if (t0 >= T) return true;
   int* words = (int*)xws;
   unsigned char* own = (unsigned char*)xws + (size_t)kXcdWords * 4;
-  const int base = lo_host[t0], S = n.V - base;
+  const int base = lo_host[t0];
   int dev = 0, ncu = 0, per = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -1800,8 +1800,7 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
   if (!fn || G < 8 ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, threads, 0) != hipSuccess || per < 1)
     return false;
-  CAVS_LAUNCH("k_xcd_owner", k_xcd_owner, dim3(1), dim3(1024), 0, s, n.parent_pos, base, S, own,
-              words);
+  if (!owner_ready) xcd_owner(n, lo_host, t0, xws, s);
   int spin = kXcdSpin;
   if (const char* e = getenv("CAVS_PERSIST_SPIN")) spin = atoi(e);
   XcdLoop xl{words, own, base, spin, t_active_ctx ? t_active_ctx->dev_err_dev : nullptr};
@@ -1829,14 +1828,20 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
 
 }  // namespace
 
+void xcd_owner(const Net& n, const int* lo_host, int t0, void* xws, hipStream_t s) {
+  const int base = lo_host[t0];
+  CAVS_LAUNCH("k_xcd_owner", k_xcd_owner, dim3(1), dim3(1024), 0, s, n.parent_pos, base,
+              n.V - base, (unsigned char*)xws + (size_t)kXcdWords * 4, (int*)xws);
+}
+
 bool lstm_fwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
-                  hipStream_t s) {
-  return xcd_launch(true, n, lo, lo_host, t0, T, xws, s);
+                  bool owner_ready, hipStream_t s) {
+  return xcd_launch(true, n, lo, lo_host, t0, T, xws, owner_ready, s);
 }
 
 bool lstm_bwd_xcd(const Net& n, const int* lo, const int* lo_host, int t0, int T, void* xws,
-                  hipStream_t s) {
-  return xcd_launch(false, n, lo, lo_host, t0, T, xws, s);
+                  bool owner_ready, hipStream_t s) {
+  return xcd_launch(false, n, lo, lo_host, t0, T, xws, owner_ready, s);
 }
 
 bool lstm_bwd_persist(const Net& n, const int* lo, const int* lo_host, int t0, int t1, int* bar,
