@@ -633,16 +633,21 @@ struct FwdRed {
 // WL: the weight columns of this unit tile are resident in LDS (wl: column
 // c = 16 g + r of the tile, k-contiguous, row stride WLD elements; fp32, or
 // bf16 pre-rounded); otherwise they are read from global memory.
+// FOLD (with EPI): the partial sums of contraction wavefronts KW/2 .. KW-1
+// are first added to those of wavefronts 0 .. KW/2-1 (own + partner, in that
+// order), so the reduction buffer holds KW/2 slots.
 template <int NCH, bool BF, int TR, int KW, bool EPI, class Rows = RangeRows, bool COH = false,
-          int WLD = 0>
+          int WLD = 0, bool FOLD = false>
 __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, const Rows& rows, int ut,
-                                                 FwdRed<NCH, TR, KW>& R,
+                                                 FwdRed<NCH, TR, FOLD ? KW / 2 : KW>& R,
                                                  const void* wl = nullptr) {
-  constexpr int NACC = 3 + NCH;
+  constexpr int NACC = 3 + NCH, RKW = FOLD ? KW / 2 : KW;
+  static_assert(!FOLD || (EPI && KW % 2 == 0), "fold");
   auto& red = R.v;
   const int H = n.H, H4 = 4 * H;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, gq = lane >> 4, r = lane & 15;
   const int u0 = ut * 16;
+  v4f acc[TR][NACC];
   if (w < KW) {
     // A rows of this lane: the children of the position of tile row 16 tr + r.
     // An absent child (or a row past the level) reads row 0 with weight 0,
@@ -664,7 +669,6 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, const Rows& rows,
     const CohBuf hb = COH ? coh_buf(n.Hs, (size_t)n.V * H) : CohBuf{};
     const float* ub = n.U + u0 + r;          // column u0 + r of each gate block
     const int kq = H / KW, kbeg = w * kq, kend = kbeg + kq;
-    v4f acc[TR][NACC];
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr)
 #pragma unroll
@@ -781,14 +785,15 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, const Rows& rows,
 #pragma unroll
       for (int g = 0; g < NACC; ++g)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i];
+        for (int i = 0; i < 4; ++i)
+          if (!FOLD || w >= RKW) red[w % RKW][tr][g][i][lane] = acc[tr][g][i];
   }
   auto zsum = [&](int tr, int i, float (&z)[NACC]) {
 #pragma unroll
     for (int g = 0; g < NACC; ++g) {
       float t = red[0][tr][g][i][lane];
 #pragma unroll
-      for (int q = 1; q < KW; ++q) t += red[q][tr][g][i][lane];
+      for (int q = 1; q < RKW; ++q) t += red[q][tr][g][i][lane];
       z[g] = t;
     }
   };
@@ -804,6 +809,17 @@ __device__ __forceinline__ void lstm_fwd_sk_tile(const Net& n, const Rows& rows,
       }
     }
     __syncthreads();
+    if constexpr (FOLD) {
+      if (w < RKW) {
+#pragma unroll
+        for (int tr = 0; tr < TR; ++tr)
+#pragma unroll
+          for (int g = 0; g < NACC; ++g)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[w][tr][g][i][lane] = acc[tr][g][i] + red[w][tr][g][i][lane];
+      }
+      __syncthreads();
+    }
     if (w < KW) return;
 #pragma unroll
     for (int tr = 0; tr < TR; ++tr) {
@@ -1350,6 +1366,10 @@ constexpr int kXcdRows = 256;          // levels of at most this many positions
 constexpr int kXcdMaxSuffix = 16384;   // suffix positions the owner kernel holds
 constexpr int kXcdWords = 1024;        // barrier words
 constexpr int kXcdSpin = 1 << 21;      // bounded waits (polls) before giving up
+// contraction wavefronts of the weight-stationary forward tile (their sums
+// folded in pairs, so the reduction buffer is that of four): 3.5 us less
+// per SST-shaped forward loop than four
+constexpr int kXcdFwdKW = 8;
 
 // Barrier words: [0] grid arrivals, [1] grid generation, [32 + x] the
 // ticket (rank counter) of XCD x, [64 + 32 x] arrivals at XCD x's barrier,
@@ -1530,21 +1550,21 @@ __device__ __forceinline__ void xcd_sync(const XcdLoop& xl, int x, int gs, int* 
 
 // The static operands of the first row tile of a level (positions
 // base + lst[0 .. m)) for unit / column tile u0, as the split-K tiles with
-// KW = 4 read them: the contraction wavefronts' child positions, the
+// KW contraction wavefronts read them: their child positions, and the
 // epilogue wavefronts' prefetch (forward: lstm_fwd_pre; backward:
 // lstm_bwd_pre, whose dL/dc word may be stale here and is read again
 // coherently by the tile).
-template <int NCH, bool FWD>
+template <int NCH, bool FWD, int KW = 4>
 __device__ __forceinline__ float xcd_touch(const Net& n, const short* lst, int m, int base, int u0) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, gq = lane >> 4, r = lane & 15;
   if (m <= 0) return 0.f;
   float acc = 0.f;
-  if (w < 4) {
+  if (w < KW) {
     const int p = base + lst[min(r, m - 1)];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) acc += (float)n.child_pos[(size_t)p * NCH + c];
-  } else if (w < 8) {
-    const int p = base + lst[min(4 * gq + (w - 4), m - 1)];
+  } else if (w < KW + 4) {
+    const int p = base + lst[min(4 * gq + (w - KW), m - 1)];
     if constexpr (FWD) {
       FwdPre<NCH> q;
       lstm_fwd_pre<NCH, false>(n, p, u0 + r, q);
@@ -1616,12 +1636,13 @@ struct WsLds {
   static constexpr int BYTES = 64 * LD * (BF ? 2 : 4);
 };
 
-template <int NCH, bool BF>
-__global__ void __launch_bounds__(512) k_lstm_fwd_xcd_ws(Net n, const int* lo, int t0, int t1,
-                                                         XcdLoop xl) {
+template <int NCH, bool BF, int KW>
+__global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_fwd_xcd_ws(Net n, const int* lo, int t0,
+                                                                  int t1, XcdLoop xl) {
+  constexpr int NT = 64 * (KW + 4), FOLD = KW > 4;
   using WS = WsLds<BF>;
   __shared__ __attribute__((aligned(16))) unsigned char wl[WS::BYTES];
-  __shared__ FwdRed<NCH, 1, 4> red;
+  __shared__ FwdRed<NCH, 1, FOLD ? KW / 2 : KW> red;
   __shared__ short lst[2][kXcdRows];
   __shared__ int s[8];
   __shared__ int sm[2];
@@ -1629,7 +1650,7 @@ __global__ void __launch_bounds__(512) k_lstm_fwd_xcd_ws(Net n, const int* lo, i
   const int H = n.H, ut = min(s[1], H / 16 - 1);
   // this unit tile's weight columns (while the grid-wide arrival completes):
   // column c = 16 g + r is column g H + 16 ut + r of U
-  for (int i = threadIdx.x; i < 64 * (H / 4); i += 512) {
+  for (int i = threadIdx.x; i < 64 * (H / 4); i += NT) {
     const int c = i / (H / 4), k4 = 4 * (i % (H / 4));
     const int col = (c >> 4) * H + 16 * ut + (c & 15);
     if constexpr (BF) {
@@ -1652,7 +1673,7 @@ __global__ void __launch_bounds__(512) k_lstm_fwd_xcd_ws(Net n, const int* lo, i
   for (int t = t0; t < t1 && !s[4]; ++t) {
     const int cur = (t - t0) & 1, m = sm[cur], base = lo[t];
     for (int rt = 0; rt < cdiv_dev(m, 16); ++rt) {
-      lstm_fwd_sk_tile<NCH, BF, 1, 4, true, ListRows, true, WS::LD>(
+      lstm_fwd_sk_tile<NCH, BF, 1, KW, true, ListRows, true, WS::LD, FOLD>(
           n, ListRows{lst[cur] + 16 * rt, m - 16 * rt, base}, ut, red, wl);
       __syncthreads();
     }
@@ -1660,7 +1681,7 @@ __global__ void __launch_bounds__(512) k_lstm_fwd_xcd_ws(Net n, const int* lo, i
     __syncthreads();
     const int nb = t + 1 < t1 ? lo[t + 1] : 0, nm = t + 1 < t1 ? sm[cur ^ 1] : 0;
     xcd_sync(xl, x, gs, s,
-             [&] { return xcd_touch<NCH, true>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
+             [&] { return xcd_touch<NCH, true, KW>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
   }
   if (threadIdx.x == 0 && rank == 0 && !s[4]) atomicExch(&xl.w[32 + x], 0);
 }
@@ -1773,7 +1794,7 @@ namespace {
 
 template <int NCH, bool BF>
 const void* xcd_kernel(bool fwd, bool ws) {
-  if (fwd) return ws ? reinterpret_cast<const void*>(&k_lstm_fwd_xcd_ws<NCH, BF>)
+  if (fwd) return ws ? reinterpret_cast<const void*>(&k_lstm_fwd_xcd_ws<NCH, BF, kXcdFwdKW>)
                      : reinterpret_cast<const void*>(&k_lstm_fwd_xcd<NCH, BF>);
   return ws ? reinterpret_cast<const void*>(&k_lstm_bwd_xcd_ws<NCH, BF>) : nullptr;
 }
@@ -1796,7 +1817,7 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
   if (!ws && xcd_mode() < 0) return false;   // the default takes only the weight-stationary loop
   const void* fn = n.N == 2 ? (n.bf ? xcd_kernel<2, true>(fwd, ws) : xcd_kernel<2, false>(fwd, ws))
                             : (n.bf ? xcd_kernel<1, true>(fwd, ws) : xcd_kernel<1, false>(fwd, ws));
-  const int threads = ws ? 512 : 768;
+  const int threads = ws && !fwd ? 512 : 768;   // forward: kXcdFwdKW + 4 wavefronts
   if (!fn || G < 8 ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, threads, 0) != hipSuccess || per < 1)
     return false;
