@@ -991,31 +991,56 @@ __device__ __forceinline__ void tn_dl_tile(const L& ld, int Q, int qchunk, int M
       for (int t = 0; t < IB; ++t)
         copy16_to_lds(B + ov[t] + bcolw, base + 128u * NA * BM + 1024u * (ws * IB + t));
     };
+    // the LDS reads of k step t+1 are issued before the MFMAs of step t (two
+    // register sets), so each wait finds them landed
+    struct KStep {
+      float4 a, a1;
+      float bv[TN];
+    };
     auto compute = [&](const float* Ls, int) {
       const float* A0 = Ls + wr * 64 + 4 * r;
       const float* A1 = A0 + 32 * BM;
       const float* Bp = Ls + NA * 32 * BM + wc * WTN + TN * r;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
+      auto rd = [&](int t, KStep& f) {
         const int k = 4 * t + g;
-        float4 a = *reinterpret_cast<const float4*>(A0 + k * BM);
-        if constexpr (NA == 2) {
-          const float4 a1 = *reinterpret_cast<const float4*>(A1 + k * BM);
-          a.x += a1.x; a.y += a1.y; a.z += a1.z; a.w += a1.w;
-        }
-        float bv[TN];
+        f.a = *reinterpret_cast<const float4*>(A0 + k * BM);
+        if constexpr (NA == 2) f.a1 = *reinterpret_cast<const float4*>(A1 + k * BM);
         if constexpr (TN == 4) {
           const float4 b4 = *reinterpret_cast<const float4*>(Bp + k * BN);
-          bv[0] = b4.x; bv[1] = b4.y; bv[2] = b4.z; bv[3] = b4.w;
+          f.bv[0] = b4.x; f.bv[1] = b4.y; f.bv[2] = b4.z; f.bv[3] = b4.w;
         } else {
           const float2 b2 = *reinterpret_cast<const float2*>(Bp + k * BN);
-          bv[0] = b2.x; bv[TN - 1] = b2.y;
+          f.bv[0] = b2.x; f.bv[TN - 1] = b2.y;
+        }
+      };
+      auto mm = [&](const KStep& f) {
+        float4 a = f.a;
+        if constexpr (NA == 2) {
+          a.x += f.a1.x; a.y += f.a1.y; a.z += f.a1.z; a.w += f.a1.w;
         }
         const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
         for (int b = 0; b < 4; ++b)
 #pragma unroll
-          for (int c = 0; c < TN; ++c) acc[b][c] = mfma_f32_16x16x4(av[b], bv[c], acc[b][c]);
+          for (int c = 0; c < TN; ++c) acc[b][c] = mfma_f32_16x16x4(av[b], f.bv[c], acc[b][c]);
+      };
+      KStep f0, f1;
+      rd(0, f0);
+#pragma unroll
+      for (int t = 0; t < 8; t += 2) {
+        rd(t + 1, f1);
+        mm(f0);
+        if (t + 2 < 8) rd(t + 2, f0);
+        mm(f1);
+      }
+      // keep that order: per step the next step's reads, the h~ adds, the MFMAs
+      constexpr int NR = NA + 1, NM = 4 * TN;
+      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        if (t + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+        if constexpr (NA == 2) __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
       }
     };
     ring_loop<S, IPW>((nq + 31) / 32, ring, issue, compute);
