@@ -1366,10 +1366,13 @@ constexpr int kXcdRows = 256;          // levels of at most this many positions
 constexpr int kXcdMaxSuffix = 16384;   // suffix positions the owner kernel holds
 constexpr int kXcdWords = 1024;        // barrier words
 constexpr int kXcdSpin = 1 << 21;      // bounded waits (polls) before giving up
-// contraction wavefronts of the weight-stationary forward tile (their sums
-// folded in pairs, so the reduction buffer is that of four): 3.5 us less
-// per SST-shaped forward loop than four
+// contraction wavefronts of the weight-stationary tiles: the forward's
+// partial sums are folded in pairs (its reduction buffer is that of four);
+// the backward's buffer of eight fits beside its 16 rows of U.  Against
+// four: 3.5 us less per SST-shaped forward loop, 15 us less per backward
+// loop (104 us on 99 chain levels)
 constexpr int kXcdFwdKW = 8;
+constexpr int kXcdBwdKW = 8;
 
 // Barrier words: [0] grid arrivals, [1] grid generation, [32 + x] the
 // ticket (rank counter) of XCD x, [64 + 32 x] arrivals at XCD x's barrier,
@@ -1696,18 +1699,19 @@ struct WsLdsB {
 // tile `rank` (rows 16 rank .. 16 rank + 15 of U resident in LDS) and runs
 // every row tile of its XCD's positions of a level; each child's dA (or,
 // below the loop, its dL/dh) is finished in the epilogue.
-template <int NCH, bool BF>
-__global__ void __launch_bounds__(512) k_lstm_bwd_xcd_ws(Net n, const int* lo, int t0, int t1,
-                                                         XcdLoop xl) {
+template <int NCH, bool BF, int KW>
+__global__ void __launch_bounds__(64 * (KW + 4)) k_lstm_bwd_xcd_ws(Net n, const int* lo, int t0,
+                                                                  int t1, XcdLoop xl) {
+  constexpr int NT = 64 * (KW + 4);
   using WS = WsLdsB<BF>;
   __shared__ __attribute__((aligned(16))) unsigned char wl[WS::BYTES];
-  __shared__ BwdRed<NCH, 1, 4> red;
+  __shared__ BwdRed<NCH, 1, KW> red;
   __shared__ short lst[2][kXcdRows];
   __shared__ int s[8];
   __shared__ int sm[2];
   xcd_arrive(xl, s);
   const int H = n.H, H4 = 4 * H, ut = min(s[1], H / 16 - 1);
-  for (int i = threadIdx.x; i < 16 * (H4 / 4); i += 512) {
+  for (int i = threadIdx.x; i < 16 * (H4 / 4); i += NT) {
     const int row = i / (H4 / 4), c4 = 4 * (i % (H4 / 4));
     const size_t src = (size_t)(16 * ut + row) * H4 + c4;
     if constexpr (BF) {
@@ -1728,7 +1732,7 @@ __global__ void __launch_bounds__(512) k_lstm_bwd_xcd_ws(Net n, const int* lo, i
   for (int t = t1 - 1; t >= t0 && !s[4]; --t) {
     const int cur = (t1 - 1 - t) & 1, m = sm[cur], base = lo[t];
     for (int rt = 0; rt < cdiv_dev(m, 16); ++rt) {
-      lstm_bwd_sk_tile<NCH, BF, 1, 4, true, ListRows, true, WS::LD>(
+      lstm_bwd_sk_tile<NCH, BF, 1, KW, true, ListRows, true, WS::LD>(
           n, ListRows{lst[cur] + 16 * rt, m - 16 * rt, base}, ut, red, wl);
       __syncthreads();
     }
@@ -1736,7 +1740,7 @@ __global__ void __launch_bounds__(512) k_lstm_bwd_xcd_ws(Net n, const int* lo, i
     __syncthreads();
     const int nb = t > t0 ? lo[t - 1] : 0, nm = t > t0 ? sm[cur ^ 1] : 0;
     xcd_sync(xl, x, gs, s,
-             [&] { return xcd_touch<NCH, false>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
+             [&] { return xcd_touch<NCH, false, KW>(n, lst[cur ^ 1], nm, nb, 16 * ut); });
   }
   if (threadIdx.x == 0 && rank == 0 && !s[4]) atomicExch(&xl.w[32 + x], 0);
 }
@@ -1796,7 +1800,7 @@ template <int NCH, bool BF>
 const void* xcd_kernel(bool fwd, bool ws) {
   if (fwd) return ws ? reinterpret_cast<const void*>(&k_lstm_fwd_xcd_ws<NCH, BF, kXcdFwdKW>)
                      : reinterpret_cast<const void*>(&k_lstm_fwd_xcd<NCH, BF>);
-  return ws ? reinterpret_cast<const void*>(&k_lstm_bwd_xcd_ws<NCH, BF>) : nullptr;
+  return ws ? reinterpret_cast<const void*>(&k_lstm_bwd_xcd_ws<NCH, BF, kXcdBwdKW>) : nullptr;
 }
 
 // Owner kernel, then the launch of the forward or backward loop
@@ -1817,7 +1821,7 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
   if (!ws && xcd_mode() < 0) return false;   // the default takes only the weight-stationary loop
   const void* fn = n.N == 2 ? (n.bf ? xcd_kernel<2, true>(fwd, ws) : xcd_kernel<2, false>(fwd, ws))
                             : (n.bf ? xcd_kernel<1, true>(fwd, ws) : xcd_kernel<1, false>(fwd, ws));
-  const int threads = ws && !fwd ? 512 : 768;   // forward: kXcdFwdKW + 4 wavefronts
+  const int threads = 768;   // eight contraction and four epilogue wavefronts
   if (!fn || G < 8 ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, threads, 0) != hipSuccess || per < 1)
     return false;
