@@ -1832,13 +1832,14 @@ bool xcd_launch(bool fwd, const Net& n, const int* lo, const int* lo_host, int t
   int a0 = t0, a1 = T;
   void* args[] = {(void*)&n, (void*)&lo, (void*)&a0, (void*)&a1, (void*)&xl};
   // timing names carry the template arguments, as the kernels' symbols do
+  static_assert(kXcdFwdKW == 8 && kXcdBwdKW == 8, "timing names below");
   static const char* const kNames[3][2][2] = {
       {{"k_lstm_fwd_xcd<1, false>", "k_lstm_fwd_xcd<1, true>"},
        {"k_lstm_fwd_xcd<2, false>", "k_lstm_fwd_xcd<2, true>"}},
-      {{"k_lstm_fwd_xcd_ws<1, false>", "k_lstm_fwd_xcd_ws<1, true>"},
-       {"k_lstm_fwd_xcd_ws<2, false>", "k_lstm_fwd_xcd_ws<2, true>"}},
-      {{"k_lstm_bwd_xcd_ws<1, false>", "k_lstm_bwd_xcd_ws<1, true>"},
-       {"k_lstm_bwd_xcd_ws<2, false>", "k_lstm_bwd_xcd_ws<2, true>"}}};
+      {{"k_lstm_fwd_xcd_ws<1, false, 8>", "k_lstm_fwd_xcd_ws<1, true, 8>"},
+       {"k_lstm_fwd_xcd_ws<2, false, 8>", "k_lstm_fwd_xcd_ws<2, true, 8>"}},
+      {{"k_lstm_bwd_xcd_ws<1, false, 8>", "k_lstm_bwd_xcd_ws<1, true, 8>"},
+       {"k_lstm_bwd_xcd_ws<2, false, 8>", "k_lstm_bwd_xcd_ws<2, true, 8>"}}};
   const char* name = kNames[fwd ? (ws ? 1 : 0) : 2][n.N == 2 ? 1 : 0][n.bf ? 1 : 0];
   TimedScope ts(name, s, lo_host[t0], lo_host[T] - lo_host[t0], /*bracket=*/true);
   // A plain launch: one workgroup per CU fits (checked above), and the

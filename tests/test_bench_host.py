@@ -58,5 +58,5 @@ def test_grouped_and_loop_launches_cost_what_their_parts_do():
     t0 = len(lo) - 4
     per_level = sum(cost("k_lstm_fwd_level_sk<2, false, 1, 8>", int(lo[t]), int(lo[t + 1] - lo[t]))
                     for t in range(t0, len(lo) - 1))
-    assert cost("k_lstm_fwd_xcd_ws<2, false>", int(lo[t0]), wl.V - int(lo[t0])) == per_level > 0
-    assert cost("k_lstm_bwd_xcd_ws<2, false>", int(lo[t0]), wl.V - int(lo[t0])) == per_level
+    assert cost("k_lstm_fwd_xcd_ws<2, false, 8>", int(lo[t0]), wl.V - int(lo[t0])) == per_level > 0
+    assert cost("k_lstm_bwd_xcd_ws<2, false, 8>", int(lo[t0]), wl.V - int(lo[t0])) == per_level
