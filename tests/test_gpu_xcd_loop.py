@@ -91,3 +91,19 @@ def test_xcd_barrier_timeout_reaches_the_caller(ctx, monkeypatch):
     ctx.sync()
     check_fp32(got, oracle_sharded(wl), oracle_sharded(wl, precision="f32"), ALL_KEYS,
                "xcd_after_timeout")
+
+
+def test_xcd_loop_bf16_at_h512(ctx, monkeypatch):
+    """bf16 products at H = 512 take the weight-stationary loop with the
+    rounded weights in LDS.  Loop on and off, each against the oracle that
+    rounds the same operands (normwise through the left-branching half,
+    whose deep chains move bf16 rounding points; see the bf16 parity tests)."""
+    from parity import check, oracle_sharded as osh
+    wl = W.config_treelstm_deep_bf16(3, K=8, D=300, H=512, lo=8, hi=40)
+    want = osh(wl, bf16=True)
+    for mode in ("1", "0"):
+        monkeypatch.setenv("CAVS_XCD_LOOP", mode)
+        print("xcd loop bf16 H=512 V=%d mode %s" % (wl.V, mode), flush=True)
+        got = Batch(wl, ctx).run()
+        ctx.sync()
+        check(got, want, ALL_KEYS, 2e-2, "xcd_bf16_h512_" + mode, floor=1.0)
