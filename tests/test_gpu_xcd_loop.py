@@ -40,6 +40,10 @@ def _cases():
     trees += [[[-1, -1], [0, -1], [-1, -1], [1, 2]]] * 9 + [W.chain(1)] * 5
     out["mixed_unary"] = lambda: W.make_workload("mixed_unary", trees, N=2, D=16, H=512, C=5,
                                                  sigma=0.2, rng=rng, labels="all")
+    # one tree only: seven of the eight XCDs own no position at any level
+    out["one_tree"] = lambda: W.make_workload("one_tree", [W.left_branching_tree(20)], N=2,
+                                              D=16, H=512, C=5, sigma=0.2, rng=rng,
+                                              labels="all")
     return out
 
 
