@@ -69,7 +69,7 @@ namespace {
 // the loss terms are kept: the saved gates and every gradient buffer take no
 // space.
 struct WsLayout {
-  size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, part, bpart, bar, total;
+  size_t P, UT, WxT, zrow, Hs, Cs, Gs, dZ, lossv, dHL, dHp, dCp, dA, dAb, part, bpart, bar, total;
   size_t part_floats;
   size_t gHt, gDt, gEh, gEc, gdAx, gpart;   // generic engine
   size_t WsT, dHLx;
@@ -147,6 +147,7 @@ WsLayout ws_layout(const cavs_params* p, const cavs_sched* s, bool train) {
   const bool ubf = lstm && !gen && p->prec == CAVS_BF16;
   L.Ub = take(ubf ? 2 * H * H : 0);    // 4 H^2 bf16 values each
   L.UTb = take(ubf ? 2 * H * H : 0);
+  L.dAb = take(ubf && tr ? V * GW / 2 : 0);   // V GW bf16 values
   if (lm && !gen) {
     L.gpart_floats = tr * gen_part_floats(p->D, p->H, (int)C);
     L.gpart = take(L.gpart_floats);
@@ -315,6 +316,7 @@ Net make_net(const cavs_params* p, const cavs_sched* s, const cavs_inputs* in, v
   const bool ubf = p->cell == CAVS_TREE_LSTM && p->prec == CAVS_BF16 && !generic_mode(p, s);
   n.Ub = ubf ? (unsigned short*)(base + L.Ub) : nullptr;
   n.UTb = ubf ? (unsigned short*)(base + L.UTb) : nullptr;
+  n.dAb = ubf && train ? (unsigned short*)(base + L.dAb) : nullptr;
   n.pack_elems = L.pack_elems;
   if (!train) {   // the kernels test these for null and skip what only backward reads
     if (!(p->cell == CAVS_TREE_LSTM && generic_mode(p, s))) n.Gs = nullptr;

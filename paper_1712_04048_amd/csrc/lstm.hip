@@ -61,12 +61,13 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int sk
 
 // dA of every position of a level below n.fuse_from (dL/dh, dL/dc stored by
 // the parent; zero at a root), four consecutive units per thread with
-// 16-byte accesses.  LEAF:
+// 16-byte accesses; with wb also its bf16 copy dAb (the operand rows of a
+// tiled bf16 backward product, rounded as that product rounds them).  LEAF:
 // the level is the leaves (no children).  Loads are unconditional (a root's
 // parent terms and an absent child's state read stale rows, masked by
 // selects), and each element's arithmetic is that of lstm_gates_fin.
 template <int NCH, bool LEAF>
-__global__ void __launch_bounds__(256) k_lstm_bwd_gates4(Net n, int off, int M) {
+__global__ void __launch_bounds__(256) k_lstm_bwd_gates4(Net n, int off, int M, int wb) {
   const int H = n.H, Hq = H / 4;
   const long idx = (long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long)M * Hq) return;
@@ -113,9 +114,18 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_gates4(Net n, int off, int M) 
   }
   auto f4 = [](const float (&x)[4]) { return make_float4(x[0], x[1], x[2], x[3]); };
   float* da = n.dA + (size_t)p * n.GW + j0;
-  st4(da, f4(di));
-  st4(da + 2 * H, f4(dO));
-  st4(da + 3 * H, f4(du));
+  unsigned short* db = wb ? n.dAb + (size_t)p * n.GW + j0 : nullptr;
+  auto st = [&](int col, const float (&x)[4]) {
+    st4(da + col, f4(x));
+    if (db) {
+      const unsigned lo = f2bf(x[0]) | ((unsigned)f2bf(x[1]) << 16);
+      const unsigned hi = f2bf(x[2]) | ((unsigned)f2bf(x[3]) << 16);
+      *reinterpret_cast<uint2*>(db + col) = make_uint2(lo, hi);
+    }
+  };
+  st(0, di);
+  st(2 * H, dO);
+  st(3 * H, du);
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const bool has = !LEAF && cp[k] >= 0;
@@ -125,7 +135,7 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_gates4(Net n, int off, int M) 
 #pragma unroll
         for (int e = 0; e < 4; ++e) z[e] = df[k][e];
       }
-      st4(da + (k == 0 ? H : 4 * H), f4(z));
+      st(k == 0 ? H : 4 * H, z);
     }
     if constexpr (!LEAF)
       if (has) st4(n.dCp + (size_t)cp[k] * H + j0, f4(dc[k]));
@@ -1230,11 +1240,13 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  // level 0 (off == 0) holds the leaves, which have no children
+  // level 0 (off == 0) holds the leaves, which have no children; a bf16 level
+  // that the tiled product takes next also gets the bf16 copy of its dA
   const dim3 g4(cdiv((long)M * (n.H / 4), 256));
+  const int wb = n.dAb && off > 0 && lstm_tile_applies(n, M);
 #define CAVS_G4(NCH, LEAF)                                                                   \
   CAVS_LAUNCH_ROWS("k_lstm_bwd_gates4<" #NCH ", " #LEAF ">", off, M,                          \
-                   (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), 0, s, n, off, M)
+                   (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), 0, s, n, off, M, wb)
   if (n.N == 2) {
     if (off == 0) CAVS_G4(2, true);
     else CAVS_G4(2, false);

@@ -208,7 +208,10 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
 // columns at each gate block, so one chunk feeds 3 + NCH MFMA blocks per
 // 16 x 16 output block:
 //   dL/dh~ += dA_i U_i^T + dA_o U_o^T + dA_u U_u^T,  dL/dh_k += dA_fk U_f^T
-// (one child: the f block joins the single accumulator).
+// (one child: the f block joins the single accumulator).  bf16: the operand
+// rows are staged already rounded (dAb, written by the gates kernel, and
+// Ub), so a 128-byte LDS row holds 64 k and a fragment's two 16-byte quads
+// are the operands of two bf16 MFMA steps, with no conversion.
 template <int NCH, bool BF, int BM, int BN, int S>
 __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TN = BN / 32;
@@ -249,16 +252,21 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
 #pragma unroll
   for (int t = 0; t < IPW; ++t) {
     const int row = (w * IPW + t) * 8 + (lane >> 3), qg = (lane & 7) ^ (row & 7);
-    const float* ptr;
+    size_t e;   // element offset of the row's k = 0
     if (row < AROWS) {
       const int a = row / BM, p = min(row0 + row % BM, rowend - 1);
       const int col = a == 0 ? 0 : a == 1 ? 2 * H : a == 2 ? 3 * H : a == 3 ? H : 4 * H;
-      ptr = n.dA + (size_t)p * GW + col;
+      e = (size_t)p * GW + col;
     } else {
       const int b = row - AROWS, g = b / BN, nn = n0 + b % BN;
-      ptr = n.U + (size_t)nn * H4 + (g == 0 ? G_I : g == 1 ? G_O : g == 2 ? G_U : G_F) * H;
+      e = (size_t)nn * H4 + (g == 0 ? G_I : g == 1 ? G_O : g == 2 ? G_U : G_F) * H;
     }
-    src[t] = ptr + 4 * qg;
+    if constexpr (BF) {   // 16-byte quad qg of bf16 values, addressed in floats' units
+      const unsigned short* base16 = row < AROWS ? n.dAb : n.Ub;
+      src[t] = reinterpret_cast<const float*>(base16 + e + 8 * qg);
+    } else {
+      src[t] = (row < AROWS ? n.dA : n.U) + e + 4 * qg;
+    }
   }
   const int wofs = __builtin_amdgcn_readfirstlane(w * IPW * 256);
 
@@ -289,31 +297,43 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) frag_sw(Ls, a * BM + wr * (BM / 2) + tm * 16 + r, gq, f.a[a][tm]);
   };
-  // A = weight fragment (columns), B = dA fragment (positions)
+  // A = weight fragment (columns), B = dA fragment (positions); bf16: the
+  // two quads of a fragment are two 32-deep steps
+  auto step = [&](const float (&w)[8], const float (&d)[8], v4f c) {
+    if constexpr (BF) {
+      const float4 w0 = make_float4(w[0], w[1], w[2], w[3]), w1 = make_float4(w[4], w[5], w[6], w[7]);
+      const float4 d0 = make_float4(d[0], d[1], d[2], d[3]), d1 = make_float4(d[4], d[5], d[6], d[7]);
+      c = mfma_bf16_16x16x32(__builtin_bit_cast(bf16x8, w0), __builtin_bit_cast(bf16x8, d0), c);
+      return mfma_bf16_16x16x32(__builtin_bit_cast(bf16x8, w1), __builtin_bit_cast(bf16x8, d1), c);
+    } else {
+      return mfma_chunk8<false>(w, d, c);
+    }
+  };
   auto mma = [&](const Frag& f) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         v4f h = acc[tm][tn][0];
-        h = mfma_chunk8<BF>(f.b[0][tn], f.a[0][tm], h);
-        h = mfma_chunk8<BF>(f.b[1][tn], f.a[1][tm], h);
-        h = mfma_chunk8<BF>(f.b[2][tn], f.a[2][tm], h);
+        h = step(f.b[0][tn], f.a[0][tm], h);
+        h = step(f.b[1][tn], f.a[1][tm], h);
+        h = step(f.b[2][tn], f.a[2][tm], h);
         if constexpr (NCH == 2) {
           acc[tm][tn][0] = h;
-          acc[tm][tn][1] = mfma_chunk8<BF>(f.b[3][tn], f.a[3][tm], acc[tm][tn][1]);
-          acc[tm][tn][2] = mfma_chunk8<BF>(f.b[3][tn], f.a[4][tm], acc[tm][tn][2]);
+          acc[tm][tn][1] = step(f.b[3][tn], f.a[3][tm], acc[tm][tn][1]);
+          acc[tm][tn][2] = step(f.b[3][tn], f.a[4][tm], acc[tm][tn][2]);
         } else {
-          acc[tm][tn][0] = mfma_chunk8<BF>(f.b[3][tn], f.a[3][tm], h);
+          acc[tm][tn][0] = step(f.b[3][tn], f.a[3][tm], h);
         }
       }
   };
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
     mma(cur);
-    interleave_reads<2 * (4 * TN + NGA * TM), TM * TN * (3 + NCH) * (BF ? 1 : 8)>();
+    interleave_reads<2 * (4 * TN + NGA * TM), TM * TN * (3 + NCH) * (BF ? 2 : 8)>();
   };
-  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+  // a chunk is 32 k in fp32, 64 in bf16 (128 bytes per LDS row either way)
+  ring_loop_db<S, IPW, Frag>(H / (BF ? 2 * kBK : kBK), ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
