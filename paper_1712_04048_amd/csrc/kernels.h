@@ -36,7 +36,8 @@ struct Net {
   unsigned short* Ub;           // LSTM bf16: U rounded to bf16, [H, 4H] (workspace; null in
   unsigned short* UTb;          // fp32) and U^T rounded to bf16, [4H, H]; written per pass
   unsigned short* dAb;          // LSTM bf16 training: dA rounded to bf16, [V, GW], written
-                                // for the rows of the tiled backward levels (their A operand)
+                                // with dA for internal positions (the backward products'
+                                // operand rows; null otherwise)
   float* zrow;                  // H zeros (workspace): the row an absent operand row reads;
                                 // cleared by the transpose kernel and by the loss kernel
   const float* b;

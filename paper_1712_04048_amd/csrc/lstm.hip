@@ -61,8 +61,8 @@ __global__ void __launch_bounds__(256) k_lstm_leaf(Net n, int off, int M, int sk
 
 // dA of every position of a level below n.fuse_from (dL/dh, dL/dc stored by
 // the parent; zero at a root), four consecutive units per thread with
-// 16-byte accesses; with wb also its bf16 copy dAb (the operand rows of a
-// tiled bf16 backward product, rounded as that product rounds them).  LEAF:
+// 16-byte accesses; with wb also its bf16 copy dAb (the operand rows of the
+// bf16 backward product, rounded as that product rounds them).  LEAF:
 // the level is the leaves (no children).  Loads are unconditional (a root's
 // parent terms and an absent child's state read stale rows, masked by
 // selects), and each element's arithmetic is that of lstm_gates_fin.
@@ -894,9 +894,17 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows,
       daoff[tr] = (size_t)rows.clamp(16 * tr + r) * GW;
       da[tr] = n.dA + daoff[tr];
     }
-    const CohBuf ab = COH ? coh_buf(n.dA, (size_t)n.V * GW) : CohBuf{};
-    auto lda = [&](int tr, int col, float (&v)[8]) {
-      if constexpr (COH) {
+    // bf16: dA's bf16 copy (written with dA, rounded as the product rounds
+    // it): eight values in one 16-byte load, no conversion
+    const CohBuf ab = !COH ? CohBuf{}
+                      : BF ? coh_buf(reinterpret_cast<const float*>(n.dAb), (size_t)n.V * GW / 2)
+                           : coh_buf(n.dA, (size_t)n.V * GW);
+    auto lda = [&](int tr, int col, float (&v)[BF ? 1 : 8], bf16x8& q) {
+      if constexpr (BF && COH) {
+        q = __builtin_bit_cast(bf16x8, coh_ld4(ab, (daoff[tr] + col) / 2));
+      } else if constexpr (BF) {
+        q = *reinterpret_cast<const bf16x8*>(n.dAb + daoff[tr] + col);
+      } else if constexpr (COH) {
         const float4 x = coh_ld4(ab, daoff[tr] + col), y = coh_ld4(ab, daoff[tr] + col + 4);
         v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
         v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
@@ -927,14 +935,14 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows,
       for (int g = 0; g < NACC; ++g) acc[tr][g] = v4f{0.f, 0.f, 0.f, 0.f};
     // phase 1: i|o|u columns (all four blocks with one child slot)
     struct F1 {
-      float a[TR][8], b[BF ? 1 : 8];
-      bf16x8 bq;
+      float a[TR][BF ? 1 : 8], b[BF ? 1 : 8];
+      bf16x8 aq[TR], bq;
     };
     const int K1 = NCH == 1 ? H4 : 3 * H, q1 = K1 / KW;
     auto load1 = [&](int c0, F1& f) {
       const int col = (NCH == 2 && c0 >= H ? c0 + H : c0) + 8 * gq;
 #pragma unroll
-      for (int tr = 0; tr < TR; ++tr) lda(tr, col, f.a[tr]);
+      for (int tr = 0; tr < TR; ++tr) lda(tr, col, f.a[tr], f.aq[tr]);
       float dummy[8];
       if constexpr (BF) ldu(col, dummy, f.bq);
       else ldu(col, f.b, f.bq);
@@ -942,7 +950,7 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows,
     auto comp1 = [&](const F1& f) {
 #pragma unroll
       for (int tr = 0; tr < TR; ++tr) {
-        if constexpr (BF) acc[tr][0] = mfma_bf16_16x16x32(to_bf8(f.a[tr]), f.bq, acc[tr][0]);
+        if constexpr (BF) acc[tr][0] = mfma_bf16_16x16x32(f.aq[tr], f.bq, acc[tr][0]);
         else acc[tr][0] = mfma_chunk8<BF>(f.a[tr], f.b, acc[tr][0]);
       }
     };
@@ -957,16 +965,16 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows,
     if constexpr (NCH == 2) {
       // the two phases' loads go out together: one memory latency per level
       struct F2 {
-        float a0[TR][8], a1[TR][8], b[BF ? 1 : 8];
-        bf16x8 bq;
+        float a0[TR][BF ? 1 : 8], a1[TR][BF ? 1 : 8], b[BF ? 1 : 8];
+        bf16x8 aq0[TR], aq1[TR], bq;
       };
       const int q2 = H / KW;
       auto load2 = [&](int c0, F2& f) {
         const int col = c0 + 8 * gq;
 #pragma unroll
         for (int tr = 0; tr < TR; ++tr) {
-          lda(tr, H + col, f.a0[tr]);
-          lda(tr, 4 * H + col, f.a1[tr]);
+          lda(tr, H + col, f.a0[tr], f.aq0[tr]);
+          lda(tr, 4 * H + col, f.a1[tr], f.aq1[tr]);
         }
         float dummy[8];
         if constexpr (BF) ldu(H + col, dummy, f.bq);
@@ -976,8 +984,8 @@ __device__ __forceinline__ void lstm_bwd_sk_tile(const Net& n, const Rows& rows,
 #pragma unroll
         for (int tr = 0; tr < TR; ++tr) {
           if constexpr (BF) {
-            acc[tr][1] = mfma_bf16_16x16x32(to_bf8(f.a0[tr]), f.bq, acc[tr][1]);
-            acc[tr][2] = mfma_bf16_16x16x32(to_bf8(f.a1[tr]), f.bq, acc[tr][2]);
+            acc[tr][1] = mfma_bf16_16x16x32(f.aq0[tr], f.bq, acc[tr][1]);
+            acc[tr][2] = mfma_bf16_16x16x32(f.aq1[tr], f.bq, acc[tr][2]);
           } else {
             acc[tr][1] = mfma_chunk8<BF>(f.a0[tr], f.b, acc[tr][1]);
             acc[tr][2] = mfma_chunk8<BF>(f.a1[tr], f.b, acc[tr][2]);
@@ -1240,10 +1248,10 @@ void lstm_fwd_level(const Net& n, int off, int M, hipStream_t s) {
 
 void lstm_bwd_gates(const Net& n, int off, int M, hipStream_t s) {
   if (M <= 0) return;
-  // level 0 (off == 0) holds the leaves, which have no children; a bf16 level
-  // that the tiled product takes next also gets the bf16 copy of its dA
+  // level 0 (off == 0) holds the leaves, which have no children; an internal
+  // bf16 level also gets the bf16 copy of its dA (its product's operand)
   const dim3 g4(cdiv((long)M * (n.H / 4), 256));
-  const int wb = n.dAb && off > 0 && lstm_tile_applies(n, M);
+  const int wb = n.dAb && off > 0;
 #define CAVS_G4(NCH, LEAF)                                                                   \
   CAVS_LAUNCH_ROWS("k_lstm_bwd_gates4<" #NCH ", " #LEAF ">", off, M,                          \
                    (k_lstm_bwd_gates4<NCH, LEAF>), g4, dim3(256), 0, s, n, off, M, wb)

@@ -314,11 +314,20 @@ __device__ __forceinline__ void lstm_gates_fin(const Net& n, int p, int j, float
       d_f = gc * q.ck[k] * q.fk[k] * (1.f - q.fk[k]);
       n.dCp[(size_t)q.cp[k] * H + j] = gc * q.fk[k];
     }
-    if (q.cp[k] >= 0 || p >= n.f_unread_below) da[(k == 0 ? H : 4 * H) + j] = d_f;
+    if (q.cp[k] >= 0 || p >= n.f_unread_below) {
+      da[(k == 0 ? H : 4 * H) + j] = d_f;
+      if (n.dAb) n.dAb[(size_t)p * n.GW + (k == 0 ? H : 4 * H) + j] = f2bf(d_f);
+    }
   }
   da[j] = d_i;
   da[2 * H + j] = d_o;
   da[3 * H + j] = d_u;
+  if (n.dAb) {   // bf16: the copy the backward products read, rounded as they round it
+    unsigned short* db = n.dAb + (size_t)p * n.GW;
+    db[j] = f2bf(d_i);
+    db[2 * H + j] = f2bf(d_o);
+    db[3 * H + j] = f2bf(d_u);
+  }
 }
 
 // dA of position p, unit j given the parent's contributions gh = dL/dh and
