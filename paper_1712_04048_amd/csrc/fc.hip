@@ -83,6 +83,9 @@ __global__ void __launch_bounds__(256) k_fc_transpose(const float* __restrict__ 
 template <int NCH, int BM, int BN, int S>
 __global__ void __launch_bounds__(256) k_fc_fwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TN = BN / 32;    // 16 x 16 blocks per wavefront
+  // copies interleaved with the MFMAs: measured faster for 64 x 64 tiles,
+  // slower for 32 x 32
+  constexpr bool ILV = BM >= 64 && S == 2;
   constexpr int AROWS = NCH * BM, ROWS = AROWS + NCH * BN;
   constexpr int IPW = ROWS / 32;               // copies per wavefront per chunk
   static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
@@ -139,9 +142,7 @@ __global__ void __launch_bounds__(256) k_fc_fwd_tile(Net n, int off, int M) {
     for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](auto sc, int c) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
-#pragma unroll
-    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+    ring_issue<IPW, ILV>(ring.at(sc), wofs, [&](int t) { return src[t] + c * kBK; });
   };
   struct Frag {
     float a[NCH][TM][8], b[NCH][TN][8];
@@ -169,9 +170,9 @@ __global__ void __launch_bounds__(256) k_fc_fwd_tile(Net n, int off, int M) {
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
     mma(cur);
-    interleave_reads<2 * NCH * (TN + TM), TM * TN * NCH * 8>();
+    ring_schedule<ILV, IPW, 2 * NCH * (TN + TM), TM * TN * NCH * 8>();
   };
-  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+  ring_loop_db<S, IPW, Frag, ILV>(H / kBK, ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
@@ -197,6 +198,7 @@ __global__ void __launch_bounds__(256) k_fc_fwd_tile(Net n, int off, int M) {
 template <int NCH, int BM, int BN, int S>
 __global__ void __launch_bounds__(256) k_fc_bwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TN = BN / 32;
+  constexpr bool ILV = BM >= 64 && S == 2;   // as in the forward tile
   constexpr int ROWS = BM + NCH * BN;
   constexpr int IPW = ROWS / 32;
   static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
@@ -245,9 +247,7 @@ __global__ void __launch_bounds__(256) k_fc_bwd_tile(Net n, int off, int M) {
       for (int k = 0; k < NCH; ++k) acc[tm][tn][k] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](auto sc, int c) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
-#pragma unroll
-    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+    ring_issue<IPW, ILV>(ring.at(sc), wofs, [&](int t) { return src[t] + c * kBK; });
   };
   struct Frag {
     float a[TM][8], b[NCH][TN][8];
@@ -273,9 +273,9 @@ __global__ void __launch_bounds__(256) k_fc_bwd_tile(Net n, int off, int M) {
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
     mma(cur);
-    interleave_reads<2 * (NCH * TN + TM), TM * TN * NCH * 8>();
+    ring_schedule<ILV, IPW, 2 * (NCH * TN + TM), TM * TN * NCH * 8>();
   };
-  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+  ring_loop_db<S, IPW, Frag, ILV>(H / kBK, ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)

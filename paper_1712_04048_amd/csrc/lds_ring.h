@@ -46,6 +46,13 @@ __device__ __forceinline__ void copy16_to_lds(const float* g, uint32_t lds_addr)
                :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
 
+// The same copy through the compiler's builtin, to LDS pointer `lds`
+// (wavefront-uniform): the scheduler sees a vector-memory load it may place
+// between MFMAs, where the inline-asm form stays where it is written.
+__device__ __forceinline__ void copy16_to_lds_s(const float* g, float* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 __device__ __forceinline__ uint32_t lds_addr_of(const float* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
 }
@@ -115,9 +122,17 @@ __device__ __forceinline__ void ring_loop(int nch, const RingT& ring, Issue&& is
 //   body(stage ptr of chunk c+1, F& cur, F& nxt, c): the LDS reads of chunk
 //     c+1 into nxt and the MFMAs of chunk c from cur (past the last chunk the
 //     reads see a stale stage: in bounds, never used).
-template <int S, int IPW, class F, class Issue, class Read0, class Body, class RingT>
+//   ALWAYS: every step issues a chunk (past the last one it copies the last
+//     chunk again, into a stage nothing reads any more), so the copies sit
+//     in the same basic block as the MFMAs and can be interleaved with
+//     them; the loop ends with every copy landed.  Two stages only: with
+//     three or four the compiler's own wait insertion makes some steps wait
+//     for the copy just issued before reading the other stage.
+template <int S, int IPW, class F, bool ALWAYS = false, class Issue, class Read0, class Body,
+          class RingT>
 __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&& issue,
                                              Read0&& read0, Body&& body) {
+  static_assert(!ALWAYS || S == 2, "interleaved builtin copies need a two-stage ring");
   issue(IC<0>{}, 0);
   if (1 < nch) issue(IC<1>{}, 1);
   if constexpr (S > 2) if (2 < nch) issue(IC<2>{}, 2);
@@ -132,7 +147,8 @@ __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&&
     if (c + S - 1 < nch) wait_vmcnt_lgkm0<(S - 2) * IPW>();
     else wait_vmcnt_lgkm0<0>();
     barrier_nofence();
-    if (c + S < nch) issue(IC<k>{}, c + S);
+    if constexpr (ALWAYS) issue(IC<k>{}, c + S < nch ? c + S : nch - 1);
+    else if (c + S < nch) issue(IC<k>{}, c + S);
     body(ring.at(IC<(k + 1) % S>{}), cur, nxt, c);
   };
   for (int c = 0; c < nch; c += 2 * S) {
@@ -149,6 +165,24 @@ __device__ __forceinline__ void ring_loop_db(int nch, const RingT& ring, Issue&&
       if (c + 7 < nch) step(IC<7 % S>{}, f1, f0, c + 7);
     }
   }
+  if constexpr (ALWAYS) wait_vmcnt<0>();
+}
+
+// The IPW copies of one chunk into `stage` (this wavefront's rows start
+// `wofs` floats in; copy t reads src(t)): through the builtin when they are
+// to be interleaved with the MFMAs (ILV, see ring_loop_db's ALWAYS), else the
+// inline-asm form, issued together ahead of them.
+template <int IPW, bool ILV, class Src>
+__device__ __forceinline__ void ring_issue(float* stage, int wofs, Src&& src) {
+  if constexpr (ILV) {
+    float* const base = stage + wofs;
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) copy16_to_lds_s(src(t), base + 256 * t);
+  } else {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(stage) + 4u * wofs);
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) copy16_to_lds(src(t), base + 1024u * t);
+  }
 }
 
 // sched_group_barrier sequence for one chunk: NR LDS reads spread evenly
@@ -162,6 +196,28 @@ __device__ __forceinline__ void interleave_reads() {
     __builtin_amdgcn_sched_group_barrier(0x008, PER, 0); // PER MFMAs
   }
   __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+}
+
+// The same with the chunk's NV ring copies (vector-memory loads) spread
+// over the first part of the MFMAs, ahead of the LDS reads.
+template <int NV, int NR, int NM>
+__device__ __forceinline__ void interleave_copies_reads() {
+  constexpr int NI = NV > NR ? NV : NR;
+  constexpr int PER = NM / NI > 0 ? NM / NI : 1;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one copy
+    if (i < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    __builtin_amdgcn_sched_group_barrier(0x008, PER, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+}
+
+// The schedule of one chunk's body to match ring_issue<IPW, ILV>.
+template <bool ILV, int IPW, int NR, int NM>
+__device__ __forceinline__ void ring_schedule() {
+  if constexpr (ILV) interleave_copies_reads<IPW, NR, NM>();
+  else interleave_reads<NR, NM>();
 }
 
 }  // namespace cavs

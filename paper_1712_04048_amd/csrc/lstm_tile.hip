@@ -80,6 +80,7 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   constexpr int TM = BM / 32, TU = BU / 32;   // 16 x 16 blocks per wavefront
   constexpr int NACC = 3 + NCH;
   constexpr int AROWS = NCH * BM, ROWS = AROWS + 4 * BU;
+  constexpr bool ILV = S == 2;   // copies interleaved with the MFMAs (measured faster)
   constexpr int IPW = ROWS / 32;               // copies per wavefront per chunk
   static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
@@ -145,9 +146,7 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
       for (int g = 0; g < NACC; ++g) acc[tm][tu][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](auto sc, int c) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
-#pragma unroll
-    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+    ring_issue<IPW, ILV>(ring.at(sc), wofs, [&](int t) { return src[t] + c * kBK; });
   };
   struct Frag {
     float a0[TM][8], a1[TM][8], b[4][TU][8];
@@ -186,9 +185,9 @@ __global__ void __launch_bounds__(256) k_lstm_fwd_tile(Net n, int off, int M) {
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
     mma(cur);
-    interleave_reads<2 * (4 * TU + NCH * TM), TM * TU * NACC * (BF ? 1 : 8)>();
+    ring_schedule<ILV, IPW, 2 * (4 * TU + NCH * TM), TM * TU * NACC * (BF ? 1 : 8)>();
   };
-  ring_loop_db<S, IPW, Frag>(H / kBK, ring, issue, read, body);
+  ring_loop_db<S, IPW, Frag, ILV>(H / kBK, ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
@@ -218,6 +217,9 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   constexpr int NGA = 3 + NCH;                 // dA blocks per chunk
   constexpr int NACC = NCH == 2 ? 3 : 1;
   constexpr int AROWS = NGA * BM, ROWS = AROWS + 4 * BN;
+  // copies interleaved with the MFMAs: measured faster in fp32, slower with
+  // bf16's half-length MFMA stream
+  constexpr bool ILV = !BF && S == 2;
   constexpr int IPW = ROWS / 32;
   static_assert(IPW * 32 == ROWS && S >= 2 && S <= 4, "tile shape");
   __shared__ __attribute__((aligned(1024))) float L0[ROWS * 32];
@@ -279,9 +281,7 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
       for (int g = 0; g < NACC; ++g) acc[tm][tn][g] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto issue = [&](auto sc, int c) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr_of(ring.at(sc)) + 4u * wofs);
-#pragma unroll
-    for (int t = 0; t < IPW; ++t) copy16_to_lds(src[t] + c * kBK, base + 1024u * t);
+    ring_issue<IPW, ILV>(ring.at(sc), wofs, [&](int t) { return src[t] + c * kBK; });
   };
   struct Frag {
     float a[NGA][TM][8], b[4][TN][8];
@@ -330,10 +330,10 @@ __global__ void __launch_bounds__(256) k_lstm_bwd_tile(Net n, int off, int M) {
   auto body = [&](const float* Lnext, Frag& cur, Frag& nxt, int) {
     read(Lnext, nxt);
     mma(cur);
-    interleave_reads<2 * (4 * TN + NGA * TM), TM * TN * (3 + NCH) * (BF ? 2 : 8)>();
+    ring_schedule<ILV, IPW, 2 * (4 * TN + NGA * TM), TM * TN * (3 + NCH) * (BF ? 2 : 8)>();
   };
   // a chunk is 32 k in fp32, 64 in bf16 (128 bytes per LDS row either way)
-  ring_loop_db<S, IPW, Frag>(H / (BF ? 2 * kBK : kBK), ring, issue, read, body);
+  ring_loop_db<S, IPW, Frag, ILV>(H / (BF ? 2 * kBK : kBK), ring, issue, read, body);
 
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
