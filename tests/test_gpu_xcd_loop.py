@@ -3,10 +3,10 @@
 256 positions near the roots run in one launch per direction, each XCD
 taking the tops of its own trees, with barriers among that XCD's
 workgroups only.  Its level products are the per-level split-K tiles (with
-the weight columns resident in LDS at H = 512, where the contraction is
-split over four wavefronts instead of eight), so every output must agree
-with the per-level launches to rounding, and the fp32 cases meet the
-oracle bar.
+the weight columns resident in LDS at H = 512), so the fp32 outputs must
+agree with the per-level launches to rounding, and meet the oracle bar.
+bf16 levels of 64 positions or more take another split of the contraction
+in the per-level launches, so there both sides are held to the oracle.
 """
 import numpy as np
 import pytest
@@ -59,11 +59,23 @@ def test_xcd_loop_equals_per_level_launches(ctx, monkeypatch, case):
     monkeypatch.setenv("CAVS_XCD_LOOP", "1")
     got = Batch(wl, ctx).run()
     ctx.sync()
+    if wl.prec == W.PREC_BF16:
+        # From 64 positions the per-level bf16 products give each workgroup
+        # two row tiles and split the contraction over four wavefronts (the
+        # loop: one row tile, eight), so their sums round in another order
+        # and the bf16 rounding of the states carries that on through the
+        # levels.  Both are held to the oracle that rounds the same operands
+        # (normwise, as in the bf16 parity tests).
+        from parity import check
+        want = oracle_sharded(wl, bf16=True)
+        check(base, want, ALL_KEYS, 2e-2, "xcd_" + case + "_off", floor=1.0)
+        check(got, want, ALL_KEYS, 2e-2, "xcd_" + case + "_on", floor=1.0)
+        return
     for k in base:
         a, b = np.asarray(got[k], np.float64), np.asarray(base[k], np.float64)
         scale = max(float(np.max(np.abs(b))), 1e-30)
         assert float(np.max(np.abs(a - b))) <= 1e-5 * scale, (case, k)
-    if wl.prec != W.PREC_BF16 and wl.V < 20000:
+    if wl.V < 20000:
         check_fp32(got, oracle_sharded(wl), oracle_sharded(wl, precision="f32"), ALL_KEYS,
                    "xcd_" + case)
 
