@@ -1508,7 +1508,7 @@ template <int MC>
 __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
   constexpr int NW = kLossWaves;
   __shared__ float zp[NW][16][17];
-  __shared__ float dzl[NW][16][17];
+  __shared__ float dzl[16][17];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
   const int p0 = blockIdx.x * 16;
   const int H = n.H, C = n.C, CP = n.CP, V = n.V;
@@ -1546,8 +1546,10 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
   for (int i = 0; i < 4; ++i) zp[w][4 * g + i][r] = acc[i];
   __syncthreads();
 
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  // wavefront i < 4 finishes row i of each lane group (16 lanes per row,
+  // one class per lane)
+  if (w < 4) {
+    const int i = w;
     const int p = p0 + 4 * g + i;
     float z = zp[0][4 * g + i][r];
 #pragma unroll
@@ -1568,21 +1570,19 @@ __global__ void __launch_bounds__(64 * kLossWaves) k_loss_ce(Net n) {
     float d = 0.f;
     if (q[i] >= 0 && cval)
       d = (float)((exp(zd - lse) - (r == q[i] ? 1.0 : 0.0)) * (double)n.inv_denom);
-    dzl[w][4 * g + i][r] = d;
-    if (w == 0 && p < V) {
+    dzl[4 * g + i][r] = d;
+    if (p < V) {
       if (r < CP && n.dZ) n.dZ[(size_t)p * CP + r] = d;
       if (q[i] < 0 && r == 0) n.lossv[p] = 0.f;
       if (q[i] >= 0 && r == q[i]) n.lossv[p] = (float)(lse - zd);
     }
   }
   if (!n.dHL) return;   // inference: no gradient of the head
-  // each wavefront re-reads only its own copy of dZ: its LDS operations
-  // complete in order
-  __builtin_amdgcn_wave_barrier();
+  __syncthreads();
   float a[4];
   const int KT = CP / 4;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) a[t] = t < KT ? dzl[w][r][4 * t + g] : 0.f;
+  for (int t = 0; t < 4; ++t) a[t] = t < KT ? dzl[r][4 * t + g] : 0.f;
   const int nb = H / 16;
   constexpr int MB = 4;
   for (int b0 = w; b0 < nb; b0 += NW * MB) {
