@@ -599,6 +599,24 @@ def test_parity_bf16_small_shapes(ctx):
     _parity_bf16(ctx, wl, "bf16_chains")
 
 
+def test_parity_bf16_two_row_split_k(ctx):
+    """bf16 levels of 64 positions or more below the tile threshold run the
+    split-K products with two 16-position row tiles per workgroup and four
+    contraction wavefronts; at H = 256 every level takes split-K (no tiles,
+    no XCD loop), for one and for two child slots.  Level sizes: trees
+    138 / 67 (the second row-tile pair ragged) / 2 / 2; chains 70 / 70 /
+    64 / 63 / 63 (both sides of the 64-position switch)."""
+    rng = np.random.Generator(np.random.PCG64(33))
+    trees = [W.complete_tree(2)] * 65 + [W.left_branching_tree(4)] * 2
+    wl = W.make_workload("bf16_two_rows_trees", trees, prec=W.PREC_BF16, N=2, D=32, H=256, C=5,
+                         sigma=0.2, rng=rng, labels="all")
+    _parity_bf16(ctx, wl, "bf16_two_rows_trees", elementwise=True)
+    chains = [W.chain(2)] * 6 + [W.chain(3)] + [W.chain(5)] * 63
+    wl = W.make_workload("bf16_two_rows_chains", chains, prec=W.PREC_BF16, N=1, D=32, H=256, C=5,
+                         sigma=0.2, rng=rng, inputs="all", labels="all")
+    _parity_bf16(ctx, wl, "bf16_two_rows_chains", elementwise=True)
+
+
 def test_full_size_bf16_states_on_sampled_graphs(ctx):
     """Config of 256 trees, H=1024, half left-branching (T=128), bf16 products:
     full batch on the GPU, states of eight sampled graphs (three
