@@ -135,7 +135,7 @@ def measured_traffic(workload, kernel):
 
 
 # graphs in the CPU-oracle samples: (one thread, all cores), chosen so the
-# baseline costs about 10-30 s of CPU time on the GPU machine
+# baseline costs about 10-30 s of CPU time on the host next to the GPU
 CPU_SAMPLE = {"sst": (48, 256), "tiny": (8, 8), "varlstm": (12, 64), "treefc": (12, 64),
               "deep_bf16": (2, 24)}
 
